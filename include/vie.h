@@ -1,0 +1,212 @@
+/*
+ * vie.h -- C ABI of libvie.so, an MI355X (gfx950) output head that treats
+ * "output projection + top-k token selection" as maximum inner product search
+ * over the rows of the output-embedding matrix W_out.
+ *
+ * Method: Loretz & Hochreiter, "Accelerating LLM Inference via Vector Index
+ * Based Output Embeddings", Section 3.  The logits are z = W_out h with
+ * z_i = <w_i, h>; top-k decoding only needs the k largest, which is exactly
+ * MIPS with query h.  An HNSW graph (Malkov & Yashunin 2018) built offline over
+ * the rows with inner product as the similarity answers it approximately; the
+ * retrieved logits are scattered into a full-vocabulary tensor that is -inf
+ * elsewhere.  The exact dense head (vie_dense_topk) is the baseline the paper
+ * compares against (Section 4.1).
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - Every function returns a vie_status; none throws or aborts.  On failure
+ *   vie_last_error() gives a detail string (thread-local, valid until the
+ *   next call on the same thread).
+ * - Device pointers are plain HIP device addresses on the current device;
+ *   the caller allocates and owns every device buffer.  The library owns only
+ *   a vie_index and the device copy of its graph.  W_out on the device is
+ *   borrowed, never copied.
+ * - Calls that take a stream (hipStream_t passed as void*, NULL = the null
+ *   stream) enqueue their kernels and return without waiting.  Argument errors
+ *   are reported synchronously, before anything is enqueued.  Device data
+ *   (ids, queries) is not validated by the host.
+ * - Layouts are row-major and densely packed.  W_out is [V][d] of the index
+ *   dtype; a batch of queries h is [B][d] of the same dtype.  bf16 values are
+ *   raw bit patterns (the top 16 bits of the fp32 value).
+ * - Returned top-k lists are ordered by logit descending; equal logits are
+ *   ordered by id ascending.  Logits are always fp32.
+ * - Sizes: 1 <= d <= 8192, 1 <= V < 2^31, 1 <= k <= min(V, 1024),
+ *   1 <= B <= 65535.
+ */
+#ifndef VIE_H
+#define VIE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    VIE_OK = 0,
+    VIE_EINVAL = 1,       /* bad argument (NULL, size, dtype, k > V, ...) */
+    VIE_ENOMEM = 2,       /* host or device allocation failed */
+    VIE_EHIP = 3,         /* a HIP runtime call or kernel launch failed */
+    VIE_EIO = 4,          /* file could not be opened, read or written */
+    VIE_EFORMAT = 5,      /* index file corrupt, truncated, or for another W */
+    VIE_ESTATE = 6,       /* index not on the device yet, or on another one */
+    VIE_EUNSUPPORTED = 7  /* valid request this build cannot serve */
+} vie_status;
+
+typedef enum { VIE_F32 = 0, VIE_BF16 = 1 } vie_dtype;
+
+typedef struct vie_index vie_index; /* opaque, library owned */
+
+/* HNSW construction parameters (Section 3: the index is built offline from
+ * the rows of W_out with inner product as the similarity; Section 4 uses
+ * M = 32, ef_construction = 5000). */
+typedef struct {
+    int32_t M;               /* neighbour cap on layers >= 1; 2 <= M <= 128 */
+    int32_t M0;              /* neighbour cap on layer 0; 0 selects 2*M (the
+                                |V|(4d + 8M) memory formula of Section 3);
+                                M <= M0 <= 256 */
+    int32_t ef_construction; /* candidate list size while inserting; >= 1 */
+    int32_t n_threads;       /* build threads; 0 = hardware concurrency.  With
+                                1 thread the graph is deterministic. */
+    uint64_t seed;           /* seeds the level of every node */
+    int32_t select;          /* 0 = neighbour-selection heuristic (Malkov &
+                                Yashunin Algorithm 4), 1 = the m nearest */
+} vie_build_params;
+
+/* Plain description of an index. */
+typedef struct {
+    int64_t V;
+    int32_t d;
+    int32_t dtype;           /* vie_dtype */
+    int32_t M, M0, ef_construction;
+    int32_t maxlevel;        /* top layer */
+    int32_t entry;           /* entry node (Section 2: the predefined entry node) */
+    int64_t n_upper_blocks;  /* sum over nodes of their level */
+    uint64_t seed;
+    uint64_t w_fingerprint;  /* see the file format below */
+    int32_t on_device;       /* 1 after vie_index_to_device */
+    int32_t device;          /* HIP device of the device copy, -1 if none */
+} vie_index_desc;
+
+/* ------------------------------------------------------------------------
+ * Index life cycle
+ * ------------------------------------------------------------------------ */
+
+/* Builds an HNSW graph over the V rows of W_host (host memory, [V][d] of
+ * dtype) on the CPU.  Rows are inserted in id order; the level of node i is
+ * floor(-ln(u_i) / ln M) with u_i = ((splitmix64(seed ^ i) >> 11) + 1) 2^-53,
+ * capped at 16.  W_host is only read during the call.  *out receives a new
+ * index that the caller releases with vie_index_free.
+ * Errors: VIE_EINVAL (NULL, sizes, params), VIE_ENOMEM. */
+vie_status vie_index_build(const void *W_host, vie_dtype dtype, int64_t V, int32_t d,
+                           const vie_build_params *params, vie_index **out);
+
+/* Writes the index file (format below).  Errors: VIE_EINVAL, VIE_EIO. */
+vie_status vie_index_save(const vie_index *index, const char *path);
+
+/* Reads and validates an index file (checksum, sizes, every id in range, no
+ * self loops or duplicates, degree caps, nested levels, entry on the top
+ * level).  If W_host is not NULL it must be the [V][d] matrix the index was
+ * built on: its fingerprint is compared with the stored one.
+ * Errors: VIE_EINVAL, VIE_EIO, VIE_EFORMAT, VIE_ENOMEM. */
+vie_status vie_index_load(const char *path, const void *W_host, vie_index **out);
+
+/* Copies the graph to the current HIP device and records W_dev, the device
+ * copy of W_out ([V][d] of the index dtype), which must stay allocated and
+ * unchanged while the index is used.  The copy is complete when the call
+ * returns.  May be called again to move the index or swap W_dev.
+ * Errors: VIE_EINVAL, VIE_ENOMEM, VIE_EHIP. */
+vie_status vie_index_to_device(vie_index *index, const void *W_dev, void *hip_stream);
+
+vie_status vie_index_info(const vie_index *index, vie_index_desc *out);
+
+/* Copies the graph into caller arrays: levels uint8[V], adj0 int32[V][M0],
+ * upper_off int32[V], upper int32[n_upper_blocks][M] (layout as in the file).
+ * Any pointer may be NULL to skip that array.  Errors: VIE_EINVAL. */
+vie_status vie_index_export(const vie_index *index, uint8_t *levels, int32_t *adj0,
+                            int32_t *upper_off, int32_t *upper);
+
+/* Releases the index and its device graph.  NULL is ignored. */
+void vie_index_free(vie_index *index);
+
+/* ------------------------------------------------------------------------
+ * Queries
+ * ------------------------------------------------------------------------ */
+
+/* HNSW k-NN search (Section 3; Malkov & Yashunin Algorithms 2 and 5) for B
+ * queries h_dev [B][d] (index dtype), one workgroup per query: greedy descent
+ * with a candidate list of 1 through layers maxlevel..1, then a candidate
+ * list of ef_eff = max(ef, k) on layer 0.  Writes ids_dev int32[B][k] and
+ * logits_dev fp32[B][k] (<w_id, h> accumulated in fp32); if fewer than k
+ * nodes are reachable the tail holds id -1 and logit -inf.  stats_dev, if
+ * not NULL, receives uint32[B][2] = (distance evaluations, expanded nodes)
+ * over all layers.  Needs vie_index_to_device on the current device first.
+ * Limits: ef_eff <= 1024, M0 <= 256, and the visited bitmap (V/8 bytes)
+ * must fit in one workgroup's LDS together with the beam.
+ * Errors: VIE_EINVAL, VIE_ESTATE, VIE_EUNSUPPORTED, VIE_EHIP. */
+vie_status vie_query(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                     int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+
+/* Bytes of device workspace vie_dense_topk needs for these sizes. */
+vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, size_t *bytes);
+
+/* Exact dense head: z = W_out h for B queries (fp32 accumulation over the
+ * stored values), fused with the selection of the k largest (Section 3 and
+ * the dense baseline of Section 4.1).  W_dev [V][d] and h_dev [B][d] of
+ * dtype; ids_dev int32[B][k], logits_dev fp32[B][k].  workspace_dev must
+ * hold at least vie_dense_topk_workspace() bytes, be 256-byte aligned and be
+ * zero-filled before its first use; each call leaves it ready for the next.
+ * Calls that share a workspace must not overlap in time.
+ * Errors: VIE_EINVAL, VIE_EHIP. */
+vie_status vie_dense_topk(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, const void *h_dev,
+                          int32_t B, int32_t k, int32_t *ids_dev, float *logits_dev, void *workspace_dev,
+                          size_t workspace_bytes, void *hip_stream);
+
+/* Reconstructs full-vocabulary logits (Section 3): out_dev fp32[B][V] is -inf
+ * everywhere except out[b][ids[b][j]] = logits[b][j].  Ids outside [0, V) are
+ * skipped (so -1 padding is harmless); ids within a row must be distinct.
+ * Errors: VIE_EINVAL, VIE_EHIP. */
+vie_status vie_scatter(const int32_t *ids_dev, const float *logits_dev, int32_t B, int32_t k, int64_t V,
+                       float *out_dev, void *hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Diagnostics
+ * ------------------------------------------------------------------------ */
+
+const char *vie_status_string(vie_status status);
+const char *vie_last_error(void);
+int32_t vie_version(void); /* 10000 * major + 100 * minor + patch */
+
+/* ------------------------------------------------------------------------
+ * Index file format (little endian), version 1
+ * ------------------------------------------------------------------------
+ *   0   char[8]  "VIEHNSW1"
+ *   8   u32      version = 1
+ *   12  u32      dtype (0 fp32, 1 bf16)
+ *   16  i64      V
+ *   24  i32      d
+ *   28  i32      M
+ *   32  i32      M0
+ *   36  i32      ef_construction
+ *   40  u64      seed
+ *   48  i32      maxlevel
+ *   52  i32      entry
+ *   56  i64      n_upper_blocks (nb)
+ *   64  u64      fingerprint of W
+ *   72  zero bytes up to 128
+ *   128 u8   levels[V], then zero bytes up to a multiple of 8
+ *       i32  adj0[V][M0]     layer-0 neighbours in stored order, -1 padded
+ *       i32  upper_off[V]    first upper block of a node, -1 at level 0
+ *       i32  upper[nb][M]    block upper_off[u] + l - 1 = level-l list of u
+ *       u64  FNV-1a-64 checksum of every preceding byte
+ * Fingerprint: FNV-1a-64 over V (8 bytes), d (4 bytes), dtype (4 bytes), then
+ * the bytes of rows 0, s, 2s, ... below V with s = max(1, V / 1024), then the
+ * bytes of row V - 1.
+ */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VIE_H */

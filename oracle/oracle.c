@@ -153,6 +153,21 @@ void oracle_pair_scores(const void *W, int dtype, int64_t V, int d, const void *
     free(x);
 }
 
+/* Sum of |w_ij h_j| for a list of (query, id) pairs: the scale of the
+ * rounding error of any fp32 evaluation of <w_i, h> (a length-d fp32 sum
+ * errs by at most about d * 2^-24 times this, whatever its order). */
+void oracle_pair_abs_scores(const void *W, int dtype, int64_t V, int d, const void *h, int64_t n,
+                            const int32_t *qidx, const int32_t *ids, double *out)
+{
+    for (int64_t t = 0; t < n; ++t) {
+        double s = 0.0;
+        if (ids[t] >= 0 && ids[t] < V)
+            for (int j = 0; j < d; ++j)
+                s += fabs(stored(W, dtype, (int64_t)ids[t] * d + j) * stored(h, dtype, (int64_t)qidx[t] * d + j));
+        out[t] = (ids[t] >= 0 && ids[t] < V) ? s : NAN;
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* O4: scatter (Section 3: unretrieved entries are -inf)                     */
 /* ------------------------------------------------------------------------ */

@@ -32,6 +32,7 @@ def lib() -> C.CDLL:
         L.oracle_topk.argtypes = [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp]
         L.oracle_topk.restype = i32
         L.oracle_pair_scores.argtypes = [vp, i32, i64, i32, vp, i64, vp, vp, vp]
+        L.oracle_pair_abs_scores.argtypes = [vp, i32, i64, i32, vp, i64, vp, vp, vp]
         L.oracle_scatter.argtypes = [vp, vp, i32, i32, i64, vp]
         L.oracle_levels.argtypes = [i64, i32, u64, vp]
         L.oracle_hnsw_build.argtypes = [vp, i32, i64, i32, i32, i32, i32, u64, i32]
@@ -113,6 +114,18 @@ def pair_scores(W: np.ndarray, dtype: int, h: np.ndarray, qidx: np.ndarray, ids:
     out = np.empty(ids.size, np.float64)
     lib().oracle_pair_scores(_p(W), dtype, W.shape[0], W.shape[1], _p(h), ids.size, _p(qidx), _p(ids),
                              _p(out))
+    return out
+
+
+def pair_abs_scores(W: np.ndarray, dtype: int, h: np.ndarray, qidx: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """sum_j |w_ids[t],j * h[qidx[t]],j| for a list of pairs (NaN for bad ids)."""
+    W = _check_w(W, dtype)
+    h = _check_h(h, dtype, W.shape[1])
+    qidx = np.ascontiguousarray(qidx, np.int32).ravel()
+    ids = np.ascontiguousarray(ids, np.int32).ravel()
+    out = np.empty(ids.size, np.float64)
+    lib().oracle_pair_abs_scores(_p(W), dtype, W.shape[0], W.shape[1], _p(h), ids.size, _p(qidx), _p(ids),
+                                 _p(out))
     return out
 
 

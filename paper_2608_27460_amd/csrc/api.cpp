@@ -1,0 +1,305 @@
+// C ABI of libvie (include/vie.h): argument checking, error reporting, index
+// ownership and dispatch to the CPU builder and the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "index.hpp"
+#include "vie.h"
+
+struct vie_index {
+    vie::Graph g;
+    vie::DeviceGraph dev;
+};
+
+namespace vie {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+void set_error(const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+}
+
+vie_status fail(vie_status s, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+namespace {
+
+vie_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(VIE_EHIP, "HIP error in %s: %s", what, hipGetErrorString(e));
+}
+
+vie_status check_dims(int64_t V, int32_t d, int32_t dtype)
+{
+    if (V < 1 || V >= (int64_t(1) << 31)) return fail(VIE_EINVAL, "V = %lld out of range", (long long)V);
+    if (d < 1 || d > kMaxD) return fail(VIE_EINVAL, "d = %d out of range [1, %d]", d, kMaxD);
+    if (dtype != VIE_F32 && dtype != VIE_BF16) return fail(VIE_EINVAL, "unknown dtype %d", dtype);
+    return VIE_OK;
+}
+
+vie_status check_k(int32_t k, int64_t V, int32_t B)
+{
+    if (B < 1 || B > 65535) return fail(VIE_EINVAL, "B = %d out of range [1, 65535]", B);
+    if (k < 1 || k > kMaxK || k > V) return fail(VIE_EINVAL, "k = %d out of range [1, min(V, %d)]", k, kMaxK);
+    return VIE_OK;
+}
+
+void free_device(DeviceGraph &d)
+{
+    if (d.device >= 0) {
+        int cur = 0;
+        (void)hipGetDevice(&cur);
+        (void)hipSetDevice(d.device);
+        (void)hipFree(d.adj0);
+        (void)hipFree(d.upper_off);
+        (void)hipFree(d.upper);
+        (void)hipSetDevice(cur);
+    }
+    d = DeviceGraph();
+}
+
+}  // namespace
+}  // namespace vie
+
+using namespace vie;
+
+extern "C" {
+
+const char *vie_status_string(vie_status s)
+{
+    switch (s) {
+    case VIE_OK: return "ok";
+    case VIE_EINVAL: return "invalid argument";
+    case VIE_ENOMEM: return "out of memory";
+    case VIE_EHIP: return "HIP runtime error";
+    case VIE_EIO: return "I/O error";
+    case VIE_EFORMAT: return "bad index file";
+    case VIE_ESTATE: return "index not ready on this device";
+    case VIE_EUNSUPPORTED: return "unsupported shape";
+    }
+    return "unknown status";
+}
+
+const char *vie_last_error(void) { return g_last_error.c_str(); }
+
+int32_t vie_version(void) { return 10000; }
+
+vie_status vie_index_build(const void *W_host, vie_dtype dtype, int64_t V, int32_t d, const vie_build_params *p,
+                           vie_index **out)
+{
+    g_last_error.clear();
+    if (!W_host || !p || !out) return fail(VIE_EINVAL, "NULL argument");
+    *out = nullptr;
+    if (vie_status s = check_dims(V, d, dtype)) return s;
+    const int M0 = p->M0 ? p->M0 : 2 * p->M;
+    if (p->M < 2 || p->M > kMaxM) return fail(VIE_EINVAL, "M = %d out of range [2, %d]", p->M, kMaxM);
+    if (M0 < p->M || M0 > kMaxM0) return fail(VIE_EINVAL, "M0 = %d out of range [M, %d]", M0, kMaxM0);
+    if (p->ef_construction < 1) return fail(VIE_EINVAL, "ef_construction = %d < 1", p->ef_construction);
+    if (p->n_threads < 0) return fail(VIE_EINVAL, "n_threads = %d < 0", p->n_threads);
+    if (p->select != 0 && p->select != 1) return fail(VIE_EINVAL, "select = %d is neither 0 nor 1", p->select);
+    vie_index *ix = new (std::nothrow) vie_index;
+    if (!ix) return fail(VIE_ENOMEM, "cannot allocate the index");
+    if (vie_status s = build_graph(W_host, dtype, V, d, *p, ix->g)) {
+        delete ix;
+        return s;
+    }
+    *out = ix;
+    return VIE_OK;
+}
+
+vie_status vie_index_save(const vie_index *ix, const char *path)
+{
+    g_last_error.clear();
+    if (!ix || !path) return fail(VIE_EINVAL, "NULL argument");
+    return save_graph(ix->g, path);
+}
+
+vie_status vie_index_load(const char *path, const void *W_host, vie_index **out)
+{
+    g_last_error.clear();
+    if (!path || !out) return fail(VIE_EINVAL, "NULL argument");
+    *out = nullptr;
+    vie_index *ix = new (std::nothrow) vie_index;
+    if (!ix) return fail(VIE_ENOMEM, "cannot allocate the index");
+    if (vie_status s = load_graph(path, ix->g)) {
+        delete ix;
+        return s;
+    }
+    if (W_host && w_fingerprint(W_host, ix->g.dtype, ix->g.V, ix->g.d) != ix->g.fingerprint) {
+        delete ix;
+        return fail(VIE_EFORMAT, "%s was built for another W_out (fingerprint mismatch)", path);
+    }
+    *out = ix;
+    return VIE_OK;
+}
+
+vie_status vie_index_to_device(vie_index *ix, const void *W_dev, void *hip_stream)
+{
+    g_last_error.clear();
+    if (!ix || !W_dev) return fail(VIE_EINVAL, "NULL argument");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    free_device(ix->dev);
+    const Graph &g = ix->g;
+    DeviceGraph d;
+    d.device = dev;
+    const size_t b0 = g.adj0.size() * 4, b1 = g.upper_off.size() * 4, b2 = std::max<size_t>(g.upper.size() * 4, 4);
+    if (hipMalloc(&d.adj0, b0) != hipSuccess || hipMalloc(&d.upper_off, b1) != hipSuccess ||
+        hipMalloc(&d.upper, b2) != hipSuccess) {
+        free_device(d);
+        (void)hipGetLastError();
+        return fail(VIE_ENOMEM, "cannot allocate %zu bytes of device graph", b0 + b1 + b2);
+    }
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    e = hipMemcpyAsync(d.adj0, g.adj0.data(), b0, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(d.upper_off, g.upper_off.data(), b1, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess && !g.upper.empty())
+        e = hipMemcpyAsync(d.upper, g.upper.data(), g.upper.size() * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        free_device(d);
+        return hip_fail(e, "graph upload");
+    }
+    d.W = W_dev;
+    ix->dev = d;
+    return VIE_OK;
+}
+
+vie_status vie_index_info(const vie_index *ix, vie_index_desc *out)
+{
+    g_last_error.clear();
+    if (!ix || !out) return fail(VIE_EINVAL, "NULL argument");
+    const Graph &g = ix->g;
+    out->V = g.V;
+    out->d = g.d;
+    out->dtype = g.dtype;
+    out->M = g.M;
+    out->M0 = g.M0;
+    out->ef_construction = g.efC;
+    out->maxlevel = g.maxlevel;
+    out->entry = g.entry;
+    out->n_upper_blocks = g.nb();
+    out->seed = g.seed;
+    out->w_fingerprint = g.fingerprint;
+    out->on_device = ix->dev.device >= 0;
+    out->device = ix->dev.device;
+    return VIE_OK;
+}
+
+vie_status vie_index_export(const vie_index *ix, uint8_t *levels, int32_t *adj0, int32_t *upper_off,
+                            int32_t *upper)
+{
+    g_last_error.clear();
+    if (!ix) return fail(VIE_EINVAL, "NULL index");
+    const Graph &g = ix->g;
+    if (levels) std::memcpy(levels, g.levels.data(), g.levels.size());
+    if (adj0) std::memcpy(adj0, g.adj0.data(), g.adj0.size() * 4);
+    if (upper_off) std::memcpy(upper_off, g.upper_off.data(), g.upper_off.size() * 4);
+    if (upper && !g.upper.empty()) std::memcpy(upper, g.upper.data(), g.upper.size() * 4);
+    return VIE_OK;
+}
+
+void vie_index_free(vie_index *ix)
+{
+    if (!ix) return;
+    free_device(ix->dev);
+    delete ix;
+}
+
+vie_status vie_query(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t *ids_dev,
+                     float *logits_dev, uint32_t *stats_dev, void *hip_stream)
+{
+    g_last_error.clear();
+    if (!ix || !h_dev || !ids_dev || !logits_dev) return fail(VIE_EINVAL, "NULL argument");
+    const Graph &g = ix->g;
+    if (vie_status s = check_k(k, g.V, B)) return s;
+    if (ef < 1) return fail(VIE_EINVAL, "ef = %d < 1", ef);
+    const int ef_eff = ef > k ? ef : k;
+    if (ef_eff > kMaxEf) return fail(VIE_EUNSUPPORTED, "max(ef, k) = %d above %d", ef_eff, kMaxEf);
+    if (ix->dev.device < 0) return fail(VIE_ESTATE, "index is not on a device (call vie_index_to_device)");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (ix->dev.device != dev)
+        return fail(VIE_ESTATE, "index lives on device %d, current device is %d", ix->dev.device, dev);
+    HnswLaunch a;
+    a.W = ix->dev.W;
+    a.dtype = g.dtype;
+    a.V = g.V;
+    a.d = g.d;
+    a.adj0 = ix->dev.adj0;
+    a.M0 = g.M0;
+    a.upper_off = ix->dev.upper_off;
+    a.upper = ix->dev.upper;
+    a.M = g.M;
+    a.maxlevel = g.maxlevel;
+    a.entry = g.entry;
+    a.h = h_dev;
+    a.B = B;
+    a.k = k;
+    a.ef_eff = ef_eff;
+    a.ids = ids_dev;
+    a.logits = logits_dev;
+    a.stats = stats_dev;
+    return launch_hnsw_search(a, static_cast<hipStream_t>(hip_stream));
+}
+
+vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, size_t *bytes)
+{
+    g_last_error.clear();
+    if (!bytes) return fail(VIE_EINVAL, "NULL argument");
+    if (vie_status s = check_dims(V, d, VIE_F32)) return s;
+    if (vie_status s = check_k(k, V, B)) return s;
+    *bytes = dense_workspace_bytes(V, d, B, k);
+    return VIE_OK;
+}
+
+vie_status vie_dense_topk(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, const void *h_dev, int32_t B,
+                          int32_t k, int32_t *ids_dev, float *logits_dev, void *ws, size_t ws_bytes,
+                          void *hip_stream)
+{
+    g_last_error.clear();
+    if (!W_dev || !h_dev || !ids_dev || !logits_dev || !ws) return fail(VIE_EINVAL, "NULL argument");
+    if (vie_status s = check_dims(V, d, dtype)) return s;
+    if (vie_status s = check_k(k, V, B)) return s;
+    if ((uintptr_t)ws % 256) return fail(VIE_EINVAL, "workspace is not 256-byte aligned");
+    const size_t need = dense_workspace_bytes(V, d, B, k);
+    if (ws_bytes < need) return fail(VIE_EINVAL, "workspace holds %zu bytes, needs %zu", ws_bytes, need);
+    return launch_dense_topk(W_dev, dtype, V, d, h_dev, B, k, ids_dev, logits_dev, ws,
+                             static_cast<hipStream_t>(hip_stream));
+}
+
+vie_status vie_scatter(const int32_t *ids_dev, const float *logits_dev, int32_t B, int32_t k, int64_t V,
+                       float *out_dev, void *hip_stream)
+{
+    g_last_error.clear();
+    if (!ids_dev || !logits_dev || !out_dev) return fail(VIE_EINVAL, "NULL argument");
+    if (V < 1 || V >= (int64_t(1) << 31)) return fail(VIE_EINVAL, "V = %lld out of range", (long long)V);
+    if (B < 1 || B > 65535) return fail(VIE_EINVAL, "B = %d out of range [1, 65535]", B);
+    if (k < 1 || k > kMaxK) return fail(VIE_EINVAL, "k = %d out of range [1, %d]", k, kMaxK);
+    return launch_scatter(ids_dev, logits_dev, B, k, V, out_dev, static_cast<hipStream_t>(hip_stream));
+}
+
+}  // extern "C"

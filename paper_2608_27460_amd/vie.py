@@ -1,0 +1,248 @@
+"""Python binding of libvie (include/vie.h): argument marshalling only.
+
+Every step of the head runs in the library's HIP kernels (or, for the offline
+index build, its C++ builder); torch only supplies device memory and the
+current HIP stream.  There is no fallback: if libvie.so is missing this module
+raises on import.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libvie.so")
+
+OK, EINVAL, ENOMEM, EHIP, EIO, EFORMAT, ESTATE, EUNSUPPORTED = range(8)
+F32, BF16 = 0, 1
+
+
+class VieError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s (status %d)" % (message, status))
+        self.status = status
+
+
+class BuildParams(C.Structure):
+    _fields_ = [("M", C.c_int32), ("M0", C.c_int32), ("ef_construction", C.c_int32), ("n_threads", C.c_int32),
+                ("seed", C.c_uint64), ("select", C.c_int32)]
+
+
+class IndexDesc(C.Structure):
+    _fields_ = [("V", C.c_int64), ("d", C.c_int32), ("dtype", C.c_int32), ("M", C.c_int32), ("M0", C.c_int32),
+                ("ef_construction", C.c_int32), ("maxlevel", C.c_int32), ("entry", C.c_int32),
+                ("n_upper_blocks", C.c_int64), ("seed", C.c_uint64), ("w_fingerprint", C.c_uint64),
+                ("on_device", C.c_int32), ("device", C.c_int32)]
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libvie.so is not built (%s); run `python -m paper_2608_27460_amd.build`" % LIB_PATH)
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    st = C.c_int
+    sig = {
+        "vie_index_build": (st, [vp, i32, i64, i32, C.POINTER(BuildParams), C.POINTER(vp)]),
+        "vie_index_save": (st, [vp, C.c_char_p]),
+        "vie_index_load": (st, [C.c_char_p, vp, C.POINTER(vp)]),
+        "vie_index_to_device": (st, [vp, vp, vp]),
+        "vie_index_info": (st, [vp, C.POINTER(IndexDesc)]),
+        "vie_index_export": (st, [vp, vp, vp, vp, vp]),
+        "vie_index_free": (None, [vp]),
+        "vie_query": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp]),
+        "vie_dense_topk_workspace": (st, [i64, i32, i32, i32, C.POINTER(sz)]),
+        "vie_dense_topk": (st, [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp, sz, vp]),
+        "vie_scatter": (st, [vp, vp, i32, i32, i64, vp, vp]),
+        "vie_status_string": (C.c_char_p, [st]),
+        "vie_last_error": (C.c_char_p, []),
+        "vie_version": (i32, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
+lib = _load()
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        msg = lib.vie_last_error().decode(errors="replace") or lib.vie_status_string(status).decode()
+        raise VieError(status, msg)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(t) -> C.c_void_p:
+    torch = _torch()
+    return C.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _dtype_of_tensor(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError("W_out / queries must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _dev_ptr(t, name: str):
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return C.c_void_p(t.data_ptr())
+
+
+def host_to_torch(W: np.ndarray, dtype: int):
+    """CPU torch tensor view of a synthetic matrix (fp32, or bf16 bit patterns)."""
+    torch = _torch()
+    W = np.ascontiguousarray(W)
+    if dtype == F32:
+        return torch.from_numpy(W.astype(np.float32, copy=False))
+    return torch.from_numpy(W.view(np.int16)).view(torch.bfloat16)
+
+
+class Index:
+    """An HNSW index over the rows of W_out (Section 3 of the paper)."""
+
+    def __init__(self, handle: C.c_void_p):
+        self._h = handle
+        self._W_dev = None
+
+    @classmethod
+    def build(cls, W: np.ndarray, dtype: int, M: int, ef_construction: int, seed: int = 0, n_threads: int = 0,
+              M0: int = 0, select: str = "heuristic") -> "Index":
+        W = np.ascontiguousarray(W)
+        want = np.float32 if dtype == F32 else np.uint16
+        if W.dtype != want or W.ndim != 2:
+            raise TypeError("W must be a 2-D %s array" % np.dtype(want).name)
+        p = BuildParams(M, M0, ef_construction, n_threads, seed, 0 if select == "heuristic" else 1)
+        h = C.c_void_p()
+        _check(lib.vie_index_build(W.ctypes.data_as(C.c_void_p), dtype, W.shape[0], W.shape[1], C.byref(p),
+                                   C.byref(h)))
+        return cls(h)
+
+    @classmethod
+    def load(cls, path: str, W: np.ndarray | None = None) -> "Index":
+        h = C.c_void_p()
+        wp = None if W is None else np.ascontiguousarray(W).ctypes.data_as(C.c_void_p)
+        _check(lib.vie_index_load(path.encode(), wp, C.byref(h)))
+        return cls(h)
+
+    def save(self, path: str) -> None:
+        _check(lib.vie_index_save(self._h, path.encode()))
+
+    def info(self) -> dict:
+        d = IndexDesc()
+        _check(lib.vie_index_info(self._h, C.byref(d)))
+        return {f: getattr(d, f) for f, _ in IndexDesc._fields_}
+
+    def export(self) -> dict:
+        i = self.info()
+        V, M, M0, nb = i["V"], i["M"], i["M0"], i["n_upper_blocks"]
+        out = {"levels": np.empty(V, np.uint8), "adj0": np.empty((V, M0), np.int32),
+               "upper_off": np.empty(V, np.int32), "upper": np.empty((nb, M), np.int32)}
+        _check(lib.vie_index_export(self._h, *(out[k].ctypes.data_as(C.c_void_p) if out[k].size else None
+                                               for k in ("levels", "adj0", "upper_off", "upper"))))
+        return out
+
+    def to_device(self, W_dev) -> None:
+        """Upload the graph to W_dev's device and borrow W_dev (kept alive here)."""
+        torch = _torch()
+        with torch.cuda.device(W_dev.device):
+            _check(lib.vie_index_to_device(self._h, _dev_ptr(W_dev, "W_dev"), _stream(W_dev)))
+        self._W_dev = W_dev
+
+    def query_into(self, h, k: int, ef: int, ids, logits, stats=None) -> None:
+        """HNSW top-k of h [B, d] into preallocated ids int32 [B, k], logits fp32 [B, k]
+        (and stats uint32-as-int32 [B, 2]) on the current stream."""
+        B = h.shape[0]
+        sp = None if stats is None else _dev_ptr(stats, "stats")
+        _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"), _dev_ptr(logits, "logits"),
+                             sp, _stream(h)))
+
+    def query(self, h, k: int, ef: int, stats: bool = False):
+        torch = _torch()
+        if h.dim() == 1:
+            h = h.unsqueeze(0)
+        B = h.shape[0]
+        ids = torch.empty((B, k), dtype=torch.int32, device=h.device)
+        lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
+        st = torch.empty((B, 2), dtype=torch.int32, device=h.device) if stats else None
+        self.query_into(h, k, ef, ids, lg, st)
+        return (ids, lg, st) if stats else (ids, lg)
+
+    def close(self) -> None:
+        if self._h:
+            lib.vie_index_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def dense_topk_workspace_bytes(V: int, d: int, B: int, k: int) -> int:
+    n = C.c_size_t()
+    _check(lib.vie_dense_topk_workspace(V, d, B, k, C.byref(n)))
+    return n.value
+
+
+def dense_topk_into(W, h, k: int, ids, logits, workspace) -> None:
+    """Exact top-k of W h on the current stream; workspace is a zero-initialised
+    uint8 device tensor of at least dense_topk_workspace_bytes() bytes."""
+    V, d = W.shape
+    dt = _dtype_of_tensor(W)
+    if _dtype_of_tensor(h) != dt:
+        raise TypeError("W and h must have the same dtype")
+    _check(lib.vie_dense_topk(_dev_ptr(W, "W"), dt, V, d, _dev_ptr(h, "h"), h.shape[0], k, _dev_ptr(ids, "ids"),
+                              _dev_ptr(logits, "logits"), _dev_ptr(workspace, "workspace"), workspace.numel(),
+                              _stream(h)))
+
+
+class DenseHead:
+    """Exact dense head over a device W_out with its own workspace."""
+
+    def __init__(self, W, max_batch: int = 8, max_k: int = 1024):
+        torch = _torch()
+        self.W = W
+        V, d = W.shape
+        nbytes = dense_topk_workspace_bytes(V, d, max_batch, min(max_k, V))
+        self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=W.device)
+
+    def __call__(self, h, k: int):
+        torch = _torch()
+        if h.dim() == 1:
+            h = h.unsqueeze(0)
+        B = h.shape[0]
+        ids = torch.empty((B, k), dtype=torch.int32, device=h.device)
+        lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
+        dense_topk_into(self.W, h, k, ids, lg, self.workspace)
+        return ids, lg
+
+
+def scatter_into(ids, logits, V: int, out) -> None:
+    B, k = ids.shape
+    _check(lib.vie_scatter(_dev_ptr(ids, "ids"), _dev_ptr(logits, "logits"), B, k, V, _dev_ptr(out, "out"),
+                           _stream(ids)))
+
+
+def scatter(ids, logits, V: int):
+    """Full-vocabulary logits [B, V]: -inf except at the retrieved ids (Section 3)."""
+    torch = _torch()
+    if ids.dim() == 1:
+        ids, logits = ids.unsqueeze(0), logits.unsqueeze(0)
+    out = torch.empty((ids.shape[0], V), dtype=torch.float32, device=ids.device)
+    scatter_into(ids, logits, V, out)
+    return out

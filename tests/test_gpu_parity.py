@@ -1,0 +1,229 @@
+"""GPU parity: every kernel, called through the C ABI, against the oracle on
+the same seeded inputs (and, for HNSW, the same graph file, entry point and
+ef).  Sizes span several tiles/workgroups with ragged tails; edge cases cover
+k = V, B above one pass, odd row widths, zero queries and ef >= |V|."""
+import os
+import sys
+import tempfile
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2608_27460_amd import synth
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import parity  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def vie():
+    assert torch.cuda.is_available(), "the gpu tests need an MI355X"
+    from paper_2608_27460_amd import vie as v
+    return v
+
+
+def dev_tensor(vie, a, dtype):
+    return vie.host_to_torch(a, dtype).cuda()
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+# ------------------------------------------------------------------ scatter
+
+@pytest.mark.parametrize("V,B,k", [(10000, 3, 50), (4096, 1, 7), (1, 1, 1), (4097, 2, 100), (151937, 2, 50)])
+def test_scatter_bitwise(vie, V, B, k):
+    say("scatter", V, B, k)
+    rng = np.random.default_rng(V + k)
+    k = min(k, V)
+    ids = np.stack([rng.choice(V, size=k, replace=False) for _ in range(B)]).astype(np.int32)
+    ids[:, ::7] = -1  # padding ids are skipped
+    lg = rng.standard_normal((B, k)).astype(np.float32)
+    out = vie.scatter(torch.from_numpy(ids).cuda(), torch.from_numpy(lg).cuda(), V)
+    torch.cuda.synchronize()
+    ref = O.scatter(ids, lg, V)
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+# --------------------------------------------------------------- dense head
+
+DENSE_CASES = [
+    (5000, 64, synth.F32, 1, 50),
+    (20011, 256, synth.BF16, 3, 100),
+    (3001, 37, synth.BF16, 2, 20),     # odd bf16 row: 2-byte loads
+    (2000, 5, synth.F32, 1, 16),       # 20-byte rows: 4-byte loads
+    (1000, 48, synth.F32, 9, 1000),    # two passes of queries, k = V
+    (777, 64, synth.BF16, 1, 777),     # k = V
+    (100000, 128, synth.BF16, 2, 50),
+    (262147, 96, synth.BF16, 1, 1),    # rows_per_wg > 512, k = 1
+]
+
+
+@pytest.mark.parametrize("V,d,dtype,B,k", DENSE_CASES)
+def test_dense_topk_matches_oracle(vie, V, d, dtype, B, k):
+    say("dense", V, d, dtype, B, k)
+    W = synth.make_w(V, d, dtype, 31 + V)
+    H, _ = synth.make_queries(W, dtype, B, 32 + V)
+    head = vie.DenseHead(dev_tensor(vie, W, dtype), max_batch=B, max_k=k)
+    ids, lg = head(dev_tensor(vie, H, dtype), k)
+    torch.cuda.synchronize()
+    ids, lg = ids.cpu().numpy(), lg.cpu().numpy()
+    oid, olg, osc = O.topk(W, dtype, H, k)
+    parity.check_logits(W, dtype, H, ids, lg, "dense")
+    parity.check_id_sets(W, dtype, H, ids, oid, osc[:, -1], what="dense")
+    # repeated calls reuse the workspace (its ticket counter must come back to 0)
+    for _ in range(2):
+        ids2, lg2 = head(dev_tensor(vie, H, dtype), k)
+        torch.cuda.synchronize()
+        assert np.array_equal(ids2.cpu().numpy(), ids) and np.array_equal(lg2.cpu().numpy(), lg)
+
+
+def test_dense_zero_query_orders_by_id(vie):
+    W = synth.make_w(30000, 64, synth.BF16, 5)
+    head = vie.DenseHead(dev_tensor(vie, W, synth.BF16), max_batch=1, max_k=64)
+    ids, lg = head(torch.zeros((1, 64), dtype=torch.bfloat16, device="cuda"), 64)
+    torch.cuda.synchronize()
+    assert ids.cpu().numpy()[0].tolist() == list(range(64))
+    assert np.all(lg.cpu().numpy() == 0)
+
+
+# --------------------------------------------------------------------- HNSW
+
+def _load_on_gpu(vie, g, W, dtype, tmp):
+    p = os.path.join(tmp, "g.vie")
+    O.save_graph(g, p, W)
+    ix = vie.Index.load(p, W)
+    ix.to_device(dev_tensor(vie, W, dtype))
+    return ix
+
+
+def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, max_diverge=0.05):
+    h = dev_tensor(vie, H, dtype)
+    ids, lg, st = ix.query(h, k, ef, stats=True)
+    torch.cuda.synchronize()
+    ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+    oid, olg, ost, _ = O.hnsw_search(W, dtype, g, H, k, ef, validate=False)
+    same = np.all(st == ost, axis=1)
+    ndiv = int((~same).sum())
+    parity.check_logits(W, dtype, H, ids, lg, what)
+    valid = oid[:, -1] >= 0
+    osk = np.where(valid, parity.exact_scores(W, dtype, H, np.where(oid >= 0, oid, 0))[:, -1], 0)
+    parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same & valid)[0], what=what)
+    assert ndiv <= max(1, int(max_diverge * len(H))), "%s: %d traversal divergences" % (what, ndiv)
+    return ids, st, ndiv
+
+
+@pytest.mark.parametrize("V,d,dtype,M,efC", [(3000, 64, synth.F32, 8, 60), (5000, 128, synth.BF16, 12, 80),
+                                             (2500, 40, synth.BF16, 6, 40)])
+def test_hnsw_matches_oracle_on_oracle_graph(vie, V, d, dtype, M, efC):
+    say("hnsw", V, d, dtype, M, efC)
+    W = synth.make_w(V, d, dtype, 41 + V)
+    H, _ = synth.make_queries(W, dtype, 48, 42 + V)
+    g = O.hnsw_build(W, dtype, M, efC, 7)
+    exact, _, _ = O.topk(W, dtype, H, 50)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, dtype, tmp)
+        for k, ef in [(1, 1), (10, 10), (10, 50), (50, 150), (50, 20)]:
+            ids, st, nd = _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "hnsw V=%d k=%d ef=%d" % (V, k, ef))
+            say("  k=%d ef=%d recall@k=%.3f divergent=%d mean n_dist=%.0f" %
+                (k, ef, parity.recall(ids, exact[:, :k]), nd, st[:, 0].mean()))
+        # one query per launch gives the same answers as the batch
+        ids_b, lg_b = ix.query(dev_tensor(vie, H, dtype), 10, 50)
+        for q in range(4):
+            i1, l1 = ix.query(dev_tensor(vie, H[q:q + 1], dtype), 10, 50)
+            assert np.array_equal(i1.cpu().numpy()[0], ids_b.cpu().numpy()[q])
+
+
+def test_hnsw_ef_at_least_v_is_exact(vie):
+    W = synth.make_w(400, 12, synth.F32, 121)
+    W = (W / np.linalg.norm(W, axis=1, keepdims=True)).astype(np.float32)
+    g = O.hnsw_build(W, synth.F32, 5, 40, 21)
+    H, _ = synth.make_queries(W, synth.F32, 16, 22)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.F32, tmp)
+        ids, lg = ix.query(dev_tensor(vie, H, synth.F32), 10, 400)
+    torch.cuda.synchronize()
+    oid, olg, osc = O.topk(W, synth.F32, H, 10)
+    parity.check_id_sets(W, synth.F32, H, ids.cpu().numpy(), oid, osc[:, -1], what="ef>=V")
+    parity.check_logits(W, synth.F32, H, ids.cpu().numpy(), lg.cpu().numpy(), "ef>=V")
+
+
+def test_hnsw_small_graph_pads_missing_results(vie):
+    # 6 nodes, k = 6: everything reachable is returned, the rest is -1 / -inf
+    W = synth.make_w(6, 4, synth.F32, 3)
+    g = O.hnsw_build(W, synth.F32, 2, 6, 1, M0=2, select="simple")
+    H, _ = synth.make_queries(W, synth.F32, 3, 4)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.F32, tmp)
+        ids, lg = ix.query(dev_tensor(vie, H, synth.F32), 6, 6)
+    oid, olg, _, _ = O.hnsw_search(W, synth.F32, g, H, 6, 6)
+    assert np.array_equal(ids.cpu().numpy(), oid)
+    assert np.array_equal(np.isneginf(lg.cpu().numpy()), np.isneginf(olg))
+
+
+# ------------------------------------------- full-size workload shapes
+
+def test_tiny_workload_full_size(vie):
+    """|V| = 32768, d = 256 fp32, M = 16, efC = 100, ef = 64, k = 50, 256 queries:
+    HNSW on the library-built graph against the oracle's search of that graph
+    (sampled), the dense head against the exact top-k (sampled), recall@50."""
+    wl = synth.WORKLOADS["tiny"]
+    W = wl.make_w()
+    H, _ = wl.make_queries(W)
+    ix = vie.Index.build(W, wl.dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=16)
+    e, info = ix.export(), ix.info()
+    g = O.Graph(wl.V, wl.d, wl.dtype, info["M"], info["M0"], wl.efC, wl.seed_levels, info["maxlevel"],
+                info["entry"], e["levels"], e["adj0"], e["upper_off"], e["upper"])
+    assert O.check_graph(g) == ""
+    Wd = dev_tensor(vie, W, wl.dtype)
+    ix.to_device(Wd)
+    sample = np.arange(0, wl.Q, 8)
+    ids, st, nd = _compare_hnsw(vie, ix, W, wl.dtype, g, H[sample], 50, 64, "tiny hnsw")
+    hid, _ = ix.query(dev_tensor(vie, H, wl.dtype), 50, 64)
+    head = vie.DenseHead(Wd, max_batch=1, max_k=50)
+    did = np.stack([head(dev_tensor(vie, H[q:q + 1], wl.dtype), 50)[0].cpu().numpy()[0] for q in sample])
+    oid, olg, osc = O.topk(W, wl.dtype, H[sample], 50)
+    parity.check_id_sets(W, wl.dtype, H[sample], did, oid, osc[:, -1], what="tiny dense")
+    say("tiny: recall@50 = %.4f, divergent = %d, mean n_dist = %.0f" %
+        (parity.recall(hid.cpu().numpy()[sample], oid), nd, st[:, 0].mean()))
+
+
+@pytest.mark.parametrize("name", ["qwen3-0.6b", "llama3.2-1b", "gemma3-270m", "llama3.2-3b"])
+def test_dense_full_size_sampled(vie, name):
+    wl = synth.WORKLOADS[name]
+    say("dense full", name)
+    W = wl.make_w()
+    H, _ = wl.make_queries(W, Q=2)
+    Wd = dev_tensor(vie, W, wl.dtype)
+    head = vie.DenseHead(Wd, max_batch=1, max_k=max(wl.k))
+    oid, olg, osc = O.topk(W, wl.dtype, H, max(wl.k))
+    for k in wl.k:
+        got = [head(dev_tensor(vie, H[q:q + 1], wl.dtype), k) for q in range(2)]
+        ids = np.stack([g[0].cpu().numpy()[0] for g in got])
+        lg = np.stack([g[1].cpu().numpy()[0] for g in got])
+        parity.check_logits(W, wl.dtype, H, ids, lg, name)
+        parity.check_id_sets(W, wl.dtype, H, ids, oid[:, :k], osc[:, k - 1], what=name)
+
+
+@pytest.mark.parametrize("name", ["qwen3-0.6b", "llama3.2-1b", "gemma3-270m", "llama3.2-3b"])
+def test_hnsw_row_shapes_of_each_workload(vie, name):
+    """The HNSW kernel at each workload's row width and dtype (and, for Gemma,
+    its hub rows) on a 12k-row slice with a quickly built graph."""
+    wl = synth.WORKLOADS[name]
+    say("hnsw shape", name)
+    V = 12000
+    W = synth.make_w(V, wl.d, wl.dtype, wl.seed_w, wl.hub_frac, seed_hub=wl.seed_hub)
+    H, _ = synth.make_queries(W, wl.dtype, 24, wl.seed_q)
+    ix = vie.Index.build(W, wl.dtype, 16, 40, seed=wl.seed_levels, n_threads=16)
+    e, info = ix.export(), ix.info()
+    g = O.Graph(V, wl.d, wl.dtype, info["M"], info["M0"], 40, wl.seed_levels, info["maxlevel"], info["entry"],
+                e["levels"], e["adj0"], e["upper_off"], e["upper"])
+    ix.to_device(dev_tensor(vie, W, wl.dtype))
+    for k in wl.k:
+        _compare_hnsw(vie, ix, W, wl.dtype, g, H, k, max(wl.ef), "%s k=%d" % (name, k))

@@ -424,3 +424,11 @@ def test_fingerprint_sees_sampled_rows():
     W2 = W.copy(); W2[0, 0] += 1
     W3 = W.copy(); W3[2999, 7] += 1
     assert O.fingerprint(W2, synth.F32) != f0 and O.fingerprint(W3, synth.F32) != f0
+
+
+def test_pair_abs_scores_matches_numpy():
+    W = synth.make_w(100, 9, synth.F32, 19)
+    H, _ = synth.make_queries(W, synth.F32, 2, 20)
+    got = O.pair_abs_scores(W, synth.F32, H, np.array([0, 1], np.int32), np.array([3, 99], np.int32))
+    ref = [np.abs(W[3].astype(np.float64) * H[0]).sum(), np.abs(W[99].astype(np.float64) * H[1]).sum()]
+    np.testing.assert_allclose(got, ref, rtol=1e-12)

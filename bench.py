@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the vector-index output head on one MI355X.
+
+Workload: the Qwen3-0.6B-shaped head (|V| = 151936, d = 1024, bf16 rows,
+fp32 accumulation), M = 32, ef_construction = 200, k = 50, 1024 seeded
+synthetic queries, each served at batch size 1.
+
+A step is one pass of the head over the 1024 queries, one call per query on
+one stream: HNSW search (greedy upper layers + layer-0 beam, ef = 128) and
+scatter of the 50 retrieved logits into a -inf-filled 151936-wide row.  The
+exact dense head (GEMV + fused top-k, then the same scatter) runs as the
+baseline leg in the same run, with the same protocol.  `value` is the HNSW
+head's queries per second; the dense leg, the ef sweep, recall@50 (against
+the exact dense head) and the per-kernel roofline figures are reported next
+to it.  The CPU baseline is the plain-C oracle's HNSW search on the same
+graph (one thread, a bounded sample of the same queries).
+
+    python bench.py [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "us/query and queries/s of top-k output head at B=1 (HNSW vs dense), %HBM peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="qwen3-0.6b")
+    ap.add_argument("--ef", type=int, default=128)
+    ap.add_argument("--k", type=int, default=50)
+    ap.add_argument("--queries", type=int, default=0, help="queries per step (default: the workload's)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cache", default=os.environ.get("VIE_CACHE", "/tmp/vie_cache"))
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the head is a single-GPU path (sharding it over several "
+              "GPUs is designed but not built), so --gpus %d is not supported." % args.gpus, file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2608_27460_amd import synth
+    from paper_2608_27460_amd import vie
+
+    if not torch.cuda.is_available():
+        print("bench.py needs an MI355X", file=sys.stderr)
+        return 2
+    wl = synth.WORKLOADS[args.workload]
+    Q = args.queries or wl.Q
+    k, ef = args.k, args.ef
+    s = wl.elem_bytes
+    dev = torch.device("cuda:0")
+
+    t0 = time.time()
+    W = wl.make_w()
+    H, _ = wl.make_queries(W, Q=Q)
+    log("[bench] inputs %s: %.1fs" % (wl.name, time.time() - t0))
+
+    os.makedirs(args.cache, exist_ok=True)
+    gpath = os.path.join(args.cache, "%s-M%d-efC%d-seed%d.vie" % (wl.name, wl.M, wl.efC, wl.seed_levels))
+    t0 = time.time()
+    ix = None
+    if os.path.exists(gpath):
+        try:
+            ix = vie.Index.load(gpath, W)
+            log("[bench] graph loaded from %s" % gpath)
+        except vie.VieError as e:
+            log("[bench] cached graph rejected (%s); rebuilding" % e)
+    if ix is None:
+        nt = min(16, os.cpu_count() or 1)
+        ix = vie.Index.build(W, wl.dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=nt)
+        ix.save(gpath)
+        log("[bench] graph built with %d threads in %.1fs" % (nt, time.time() - t0))
+    info = ix.info()
+
+    Wd = vie.host_to_torch(W, wl.dtype).to(dev)
+    Hd = vie.host_to_torch(H, wl.dtype).to(dev)
+    ix.to_device(Wd)
+    head = vie.DenseHead(Wd, max_batch=1, max_k=k)
+    ids = torch.empty((Q, k), dtype=torch.int32, device=dev)
+    lg = torch.empty((Q, k), dtype=torch.float32, device=dev)
+    st = torch.empty((Q, 2), dtype=torch.int32, device=dev)
+    dids = torch.empty((Q, k), dtype=torch.int32, device=dev)
+    dlg = torch.empty((Q, k), dtype=torch.float32, device=dev)
+    row = torch.empty((1, wl.V), dtype=torch.float32, device=dev)  # the step's full-vocab logits
+    hv = [Hd[q:q + 1] for q in range(Q)]
+    iv, lv, sv = [ids[q:q + 1] for q in range(Q)], [lg[q:q + 1] for q in range(Q)], [st[q:q + 1] for q in range(Q)]
+    div, dlv = [dids[q:q + 1] for q in range(Q)], [dlg[q:q + 1] for q in range(Q)]
+    stream = torch.cuda.current_stream(dev)
+
+    def hnsw_step(ev=None, ef_=ef):
+        for q in range(Q):
+            if ev is not None:
+                ev[0][q].record(stream)
+            ix.query_into(hv[q], k, ef_, iv[q], lv[q], sv[q])
+            if ev is not None:
+                ev[1][q].record(stream)
+            vie.scatter_into(iv[q], lv[q], wl.V, row)
+
+    def dense_step(ev=None):
+        for q in range(Q):
+            if ev is not None:
+                ev[0][q].record(stream)
+            vie.dense_topk_into(Wd, hv[q], k, div[q], dlv[q], head.workspace)
+            if ev is not None:
+                ev[1][q].record(stream)
+            vie.scatter_into(div[q], dlv[q], wl.V, row)
+
+    def timed(step, K, W_):
+        for _ in range(W_):
+            step()
+        torch.cuda.synchronize()
+        evs = [([torch.cuda.Event(enable_timing=True) for _ in range(Q)],
+                [torch.cuda.Event(enable_timing=True) for _ in range(Q)]) for _ in range(K)]
+        outer = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        outer[0].record(stream)
+        for i in range(K):
+            step(evs[i])
+        outer[1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t
+        ms = outer[0].elapsed_time(outer[1])
+        per_launch = np.array([[a.elapsed_time(b) for a, b in zip(*e)] for e in evs]) * 1e3  # us
+        return ms, wall, per_launch
+
+    # ---- HNSW head (the method) ----------------------------------------
+    log("[bench] HNSW head: %d steps x %d queries, ef=%d" % (args.steps, Q, ef))
+    h_ms, h_wall, h_launch = timed(hnsw_step, args.steps, args.warmup)
+    stats = st.cpu().numpy().astype(np.int64)
+    hnsw_ids = ids.cpu().numpy()
+    # ---- dense head (the baseline) -------------------------------------
+    log("[bench] dense head: %d steps x %d queries" % (args.steps, Q))
+    d_ms, d_wall, d_launch = timed(dense_step, args.steps, args.warmup)
+    exact_ids = dids.cpu().numpy()
+
+    def recall(a, b):
+        return float(np.mean([len(set(x.tolist()) & set(y.tolist())) / k for x, y in zip(a, b)]))
+
+    # ---- ef sweep (same protocol, one step each) -------------------------
+    sweep = {}
+    for e in sorted(set(wl.ef) | {ef}):
+        ms_e, _, _ = timed(lambda ev=None, e=e: hnsw_step(ev, e), 1, 1)
+        sweep[str(e)] = {"us_per_query": round(ms_e * 1e3 / Q, 2), "recall_at_k": round(recall(ids.cpu().numpy(),
+                                                                                                  exact_ids), 4),
+                         "mean_n_dist": float(st.cpu().numpy()[:, 0].mean())}
+    # ---- all queries in one launch (one workgroup each) -------------------
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ix.query_into(Hd, k, ef, ids, lg, st)
+    a.record(stream)
+    ix.query_into(Hd, k, ef, ids, lg, st)
+    b.record(stream)
+    torch.cuda.synchronize()
+    batched_qps = Q / (a.elapsed_time(b) * 1e-3)
+
+    # ---- roofline figures ----------------------------------------------------
+    n_dist, n_exp = stats[:, 0].astype(np.float64), stats[:, 1].astype(np.float64)
+    hnsw_bytes = n_dist * wl.d * s + n_exp * wl.M0 * 4 + wl.d * s + k * 8  # per launch (one query)
+    h_us = float(h_launch.mean())
+    hnsw_gbs = float(hnsw_bytes.mean()) / (h_us * 1e-6) / 1e9
+    dense_bytes = wl.V * wl.d * s + wl.d * s + k * 8
+    d_us = float(d_launch.mean())
+    dense_gbs = dense_bytes / (d_us * 1e-6) / 1e9
+
+    h_qps = Q * args.steps / (h_ms * 1e-3)
+    d_qps = Q * args.steps / (d_ms * 1e-3)
+
+    # ---- CPU baseline: the oracle on the host cores ----------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        g, _ = O.load_graph(gpath)
+        O.check_graph(g)
+        done, t = 0, time.perf_counter()
+        while time.perf_counter() - t < args.cpu_seconds and done < Q:
+            O.hnsw_search(W, wl.dtype, g, H[done:done + 8], k, ef, validate=False)
+            done += min(8, Q - done)
+        cpu_s = time.perf_counter() - t
+        t = time.perf_counter()
+        O.topk(W, wl.dtype, H[:1], k)
+        bf_s = time.perf_counter() - t
+        cpu = {"value": round(done / cpu_s, 2), "unit": "queries/s", "cores": 1, "kind": "oracle",
+               "sample": "HNSW search (ef=%d, k=%d) of the first %d of the %d queries on the same graph, one "
+                         "thread; exact brute-force top-k of 1 query: %.2f s" % (ef, k, done, Q, bf_s),
+               "brute_force_queries_per_s": round(1.0 / bf_s, 3)}
+
+    out = {
+        "metric": METRIC,
+        "value": round(h_qps, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(h_ms / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == synth.BF16 else "f32",
+        "data": "synthetic, seeded: rows N(0, I/d) x LogNormal(0, 0.25) norms, h = sum of 3 rows + N(0, 0.1/d)",
+        "config": {"workload": wl.name, "V": wl.V, "d": wl.d, "B": 1, "k": k, "ef": ef, "M": wl.M, "M0": wl.M0,
+                   "ef_construction": wl.efC, "queries_per_step": Q, "accumulate": "fp32",
+                   "graph": {"maxlevel": info["maxlevel"], "entry": info["entry"]}},
+        "hnsw": {"us_per_query": round(h_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(h_qps, 1),
+                 "kernel_us": round(h_us, 2), "recall_at_k": round(recall(hnsw_ids, exact_ids), 4),
+                 "mean_n_dist": float(n_dist.mean()), "mean_n_expand": float(n_exp.mean()),
+                 "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
+                 "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep},
+        "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
+                  "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
+        "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(hnsw_gbs / HBM_PEAK_GBS, 5), "traffic": None},
+        "roofline_dense": {"kernel": "dense_topk_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
+                           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dense_gbs / HBM_PEAK_GBS, 4),
+                           "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -6,9 +6,12 @@
 // follows Malkov & Yashunin Algorithm 1 (rows inserted in id order; entry
 // points of a layer are the result set of the layer above), neighbour choice
 // follows their Algorithm 4 heuristic without candidate extension or kept
-// pruned connections.  Distances are dist(a, b) = -<a, b>, accumulated in
-// float64 (the products of stored fp32/bf16 values are exact in float64), and
-// every tie between two nodes is broken by the smaller id.  The level of node
+// pruned connections.  Distances are dist(a, b) = -<a, b> and every tie
+// between two nodes is broken by the smaller id.  A single-thread build
+// accumulates them in float64 (the products of stored fp32/bf16 values are
+// exact there), so it makes the same decisions as a plain float64 reference;
+// a multi-thread build, whose result depends on the schedule anyway, uses
+// fp32 SIMD dot products (AVX-512 BF16 / FMA when the CPU has them).  The level of node
 // i is floor(-ln(u_i) / ln M), u_i = ((splitmix64(seed ^ i) >> 11) + 1) 2^-53.
 //
 // With several threads, nodes are taken in id order from a shared counter and
@@ -127,6 +130,58 @@ void widen_row(const void *W, int dtype, int d, int64_t row, double *out)
     }
 }
 
+// ---- fast <stored row a, stored row b> in fp32 (multi-thread builds) --------
+
+float fdot_scalar(const void *W, int dtype, int d, int64_t a, int64_t b)
+{
+    float s = 0.0f;
+    if (dtype == VIE_F32) {
+        const float *x = static_cast<const float *>(W) + a * d, *y = static_cast<const float *>(W) + b * d;
+        for (int j = 0; j < d; ++j) s += x[j] * y[j];
+    } else {
+        const uint16_t *x = static_cast<const uint16_t *>(W) + a * d, *y = static_cast<const uint16_t *>(W) + b * d;
+        for (int j = 0; j < d; ++j) {
+            uint32_t u = (uint32_t)x[j] << 16, v = (uint32_t)y[j] << 16;
+            float fu, fv;
+            std::memcpy(&fu, &u, 4);
+            std::memcpy(&fv, &v, 4);
+            s += fu * fv;
+        }
+    }
+    return s;
+}
+
+__attribute__((target("avx512f,avx512bf16"))) float fdot_avx512(const void *W, int dtype, int d, int64_t a,
+                                                                 int64_t b)
+{
+    __m512 acc0 = _mm512_setzero_ps(), acc1 = _mm512_setzero_ps();
+    int j = 0;
+    float t = 0.0f;
+    if (dtype == VIE_F32) {
+        const float *x = static_cast<const float *>(W) + a * d, *y = static_cast<const float *>(W) + b * d;
+        for (; j + 32 <= d; j += 32) {
+            acc0 = _mm512_fmadd_ps(_mm512_loadu_ps(x + j), _mm512_loadu_ps(y + j), acc0);
+            acc1 = _mm512_fmadd_ps(_mm512_loadu_ps(x + j + 16), _mm512_loadu_ps(y + j + 16), acc1);
+        }
+        for (; j < d; ++j) t += x[j] * y[j];
+    } else {
+        const uint16_t *x = static_cast<const uint16_t *>(W) + a * d, *y = static_cast<const uint16_t *>(W) + b * d;
+        for (; j + 64 <= d; j += 64) {
+            acc0 = _mm512_dpbf16_ps(acc0, (__m512bh)_mm512_loadu_si512(x + j), (__m512bh)_mm512_loadu_si512(y + j));
+            acc1 = _mm512_dpbf16_ps(acc1, (__m512bh)_mm512_loadu_si512(x + j + 32),
+                                    (__m512bh)_mm512_loadu_si512(y + j + 32));
+        }
+        for (; j < d; ++j) {
+            uint32_t u = (uint32_t)x[j] << 16, v = (uint32_t)y[j] << 16;
+            float fu, fv;
+            std::memcpy(&fu, &u, 4);
+            std::memcpy(&fv, &v, 4);
+            t += fu * fv;
+        }
+    }
+    return _mm512_reduce_add_ps(_mm512_add_ps(acc0, acc1)) + t;
+}
+
 // ---- shared build state ------------------------------------------------------
 
 struct Build {
@@ -136,7 +191,9 @@ struct Build {
     int M, M0, efC;
     bool heuristic;
     size_t row_bytes;
+    bool exact;  // float64 distances (single thread) or fp32 SIMD
     double (*dot)(const void *, int, int, int64_t, const double *);
+    float (*fdot)(const void *, int, int, int64_t, int64_t);
     std::vector<uint8_t> level;
     // Lists are blocks [count, id_0 .. id_cap] (one spare slot for the
     // append-then-shrink step).
@@ -160,21 +217,40 @@ struct Build {
     }
 };
 
+// A node whose distances to others are being evaluated: its row, widened
+// to float64 once when the build is exact.
+struct Probe {
+    int32_t row = -1;
+    std::vector<double> wide;
+};
+
 // Per-thread search state.
 struct Worker {
     Build &b;
     std::vector<uint32_t> seen;
     uint32_t tag = 0;
-    std::vector<double> q, xe;
+    Probe q, xe;
     std::vector<int32_t> nbuf;
     std::vector<Cand> res, sel, tmp;
 
-    explicit Worker(Build &bb)
-        : b(bb), seen(bb.V, 0), q(bb.d), xe(bb.d), nbuf(std::max(bb.M0, bb.M) + 2)
+    explicit Worker(Build &bb) : b(bb), seen(bb.V, 0), nbuf(std::max(bb.M0, bb.M) + 2)
     {
+        if (b.exact) {
+            q.wide.resize(b.d);
+            xe.wide.resize(b.d);
+        }
     }
 
-    double dist(const double *x, int32_t id) { return -b.dot(b.W, b.dtype, b.d, id, x); }
+    void set(Probe &p, int32_t row)
+    {
+        p.row = row;
+        if (b.exact) widen_row(b.W, b.dtype, b.d, row, p.wide.data());
+    }
+
+    double dist(const Probe &p, int32_t id)
+    {
+        return b.exact ? -b.dot(b.W, b.dtype, b.d, id, p.wide.data()) : -(double)b.fdot(b.W, b.dtype, b.d, p.row, id);
+    }
 
     // Snapshot of the level-l list of u under its lock.
     int read_list(int32_t u, int l)
@@ -221,7 +297,7 @@ struct Worker {
                 const int32_t e = nbuf[j];
                 if (seen[e] == tag) continue;
                 seen[e] = tag;
-                const Cand ce{dist(q.data(), e), e};
+                const Cand ce{dist(q, e), e};
                 if ((int)res.size() < ef || nearer(ce, res.front())) {
                     C.push_back(ce);
                     std::push_heap(C.begin(), C.end(), NearerFirst());
@@ -249,10 +325,10 @@ struct Worker {
         }
         size_t kept = 0;
         for (size_t i = 0; i < c.size() && (int)kept < m; ++i) {
-            widen_row(b.W, b.dtype, b.d, c[i].id, xe.data());
+            set(xe, c[i].id);
             bool good = true;
             for (size_t r = 0; r < kept; ++r)
-                if (!(c[i].dist < dist(xe.data(), c[r].id))) {
+                if (!(c[i].dist < dist(xe, c[r].id))) {
                     good = false;
                     break;
                 }
@@ -268,8 +344,8 @@ struct Worker {
         const int L = b.maxlevel.load();
         const int32_t ep0 = b.entry.load();
         if (l <= L) top.unlock();  // keep the global lock only when raising the top level
-        widen_row(b.W, b.dtype, b.d, i, q.data());
-        std::vector<Cand> ep{{dist(q.data(), ep0), ep0}};
+        set(q, i);
+        std::vector<Cand> ep{{dist(q, ep0), ep0}};
         for (int lc = L; lc > l; --lc) {
             search_layer(ep, 1, lc, i);
             ep.assign(1, *std::min_element(res.begin(), res.end(), nearer));
@@ -292,9 +368,9 @@ struct Worker {
                 el[1 + el[0]] = i;
                 el[0]++;
                 if (el[0] > cap) {
-                    widen_row(b.W, b.dtype, b.d, e, xe.data());
+                    set(xe, e);
                     tmp.resize(el[0]);
-                    for (int u = 0; u < el[0]; ++u) tmp[u] = Cand{dist(xe.data(), el[1 + u]), el[1 + u]};
+                    for (int u = 0; u < el[0]; ++u) tmp[u] = Cand{dist(xe, el[1 + u]), el[1 + u]};
                     select(tmp, cap);  // distances to e are in tmp; select() reuses xe
                     el[0] = (int32_t)tmp.size();
                     for (size_t u = 0; u < tmp.size(); ++u) el[1 + u] = tmp[u].id;
@@ -324,6 +400,7 @@ vie_status build_graph(const void *W, int dtype, int64_t V, int d, const vie_bui
     b.heuristic = p.select == 0;
     b.row_bytes = (size_t)d * elem_bytes(dtype);
     b.dot = __builtin_cpu_supports("avx2") && __builtin_cpu_supports("fma") ? dot_avx2 : dot_scalar;
+    b.fdot = __builtin_cpu_supports("avx512f") && __builtin_cpu_supports("avx512bf16") ? fdot_avx512 : fdot_scalar;
     int64_t nb = 0;
     try {
         b.level.resize(V);
@@ -344,6 +421,7 @@ vie_status build_graph(const void *W, int dtype, int64_t V, int d, const vie_bui
 
     unsigned nt = p.n_threads > 0 ? (unsigned)p.n_threads : std::max(1u, std::thread::hardware_concurrency());
     if ((int64_t)nt > V) nt = (unsigned)std::max<int64_t>(1, V);
+    b.exact = nt == 1;
     std::atomic<int64_t> next{1};
     std::atomic<bool> oom{false};
     auto run = [&]() {

@@ -155,9 +155,9 @@ vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, 
  * stored values), fused with the selection of the k largest (Section 3 and
  * the dense baseline of Section 4.1).  W_dev [V][d] and h_dev [B][d] of
  * dtype; ids_dev int32[B][k], logits_dev fp32[B][k].  workspace_dev must
- * hold at least vie_dense_topk_workspace() bytes, be 256-byte aligned and be
- * zero-filled before its first use; each call leaves it ready for the next.
- * Calls that share a workspace must not overlap in time.
+ * hold at least vie_dense_topk_workspace() bytes and be 256-byte aligned; it
+ * carries per-slab candidates between the call's two kernels and needs no
+ * initialisation.  Calls that share a workspace must not overlap in time.
  * Errors: VIE_EINVAL, VIE_EHIP. */
 vie_status vie_dense_topk(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, const void *h_dev,
                           int32_t B, int32_t k, int32_t *ids_dev, float *logits_dev, void *workspace_dev,

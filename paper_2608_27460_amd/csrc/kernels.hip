@@ -134,63 +134,6 @@ __device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t v, uint32_t *s
     return v + base;
 }
 
-// Radix selection of the `need` largest of `n` distinct 64-bit keys, produced
-// by key_at(i).  On return (every thread) s_sel->prefix / s_sel->shift
-// describe the threshold: key i is selected iff
-// (key >> shift) >= (prefix >> shift); exactly `need` keys qualify.
-struct SelState {
-    uint64_t prefix;
-    int shift;
-    int need;
-    int done;
-};
-
-template <int NT, typename KeyAt>
-__device__ void radix_select(int n, int need, KeyAt key_at, uint32_t *s_hist /*256*/, uint32_t *s_wave,
-                             SelState *s_sel)
-{
-    const int tid = threadIdx.x;
-    if (tid == 0) {
-        s_sel->prefix = 0;
-        s_sel->shift = 0;
-        s_sel->need = need;
-        s_sel->done = 0;
-    }
-    __syncthreads();
-    for (int shift = 56; shift >= 0; shift -= 8) {
-        const uint64_t prefix = s_sel->prefix;
-        const int want = s_sel->need;
-        const uint64_t hi_mask = shift == 56 ? 0ull : (~0ull << (shift + 8));
-        for (int b = tid; b < 256; b += NT) s_hist[b] = 0;
-        __syncthreads();
-        for (int i = tid; i < n; i += NT) {
-            const uint64_t key = key_at(i);
-            if ((key & hi_mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1u);
-        }
-        __syncthreads();
-        // suffix counts: digit 255 - t is handled by thread t
-        const uint32_t c = tid < 256 ? s_hist[255 - tid] : 0u;
-        const uint32_t incl = block_inclusive_scan<NT>(c, s_wave);
-        if (tid < 256) {
-            const uint32_t above = incl - c;  // keys with a larger digit
-            if (above < (uint32_t)want && (uint32_t)want <= incl) {
-                const uint32_t digit = 255 - tid;
-                s_sel->prefix = prefix | ((uint64_t)digit << shift);
-                s_sel->need = want - (int)above;
-                s_sel->shift = shift;
-                s_sel->done = (c == (uint32_t)(want - (int)above));
-            }
-        }
-        __syncthreads();
-        if (s_sel->done) break;
-    }
-}
-
-__device__ __forceinline__ bool selected(uint64_t key, const SelState &s)
-{
-    return (key >> s.shift) >= (s.prefix >> s.shift);
-}
-
 // ---------------------------------------------------------------------------
 // scatter
 // ---------------------------------------------------------------------------
@@ -229,48 +172,98 @@ __global__ __launch_bounds__(kScatterThreads) void scatter_kernel(const int32_t 
 }
 
 // ---------------------------------------------------------------------------
-// dense head: GEMV + fused top-k
+// dense head: GEMV + top-k
 // ---------------------------------------------------------------------------
 //
-// Workgroup w owns rows [w * rows_per_wg, ...) of W_out and streams them once
-// with 16-lane row groups (VEC-byte loads, fp32 accumulation), keeping the
-// logits of its rows in LDS.  It then radix-selects its own best
-// min(k, rows) keys per query into the workspace.  The last workgroup to
-// finish (ticket counter) selects the global top-k from those candidates,
-// orders it and writes ids/logits.  The counter is left at zero.
+// Two launches on the caller's stream.
+//
+// dense_slab_kernel: workgroup w owns a contiguous slab of rows and streams it
+// once.  Each wave takes U rows at a time; its 64 lanes read them with
+// VEC-byte loads (U loads in flight per lane), accumulate in fp32 and reduce
+// over the wave.  The slab writes its logits to the workspace and its
+// largest key.
+//
+// dense_merge_kernel: one workgroup per query.  Any T at or below the k-th
+// largest slab maximum is a lower bound of the k-th largest key overall (k
+// distinct elements are >= T), so every key of the answer is >= T, and only
+// the slabs whose maximum is >= T can hold one.  T comes from one radix pass
+// over the maxima; the kernel gathers those slabs' keys >= T (typically
+// little more than k) and orders them by rank.  The kernel boundary between the two launches is the only
+// cross-workgroup synchronisation: no atomics across workgroups, no fences.
 
-constexpr int kDenseThreads = 512;
-constexpr int kDenseGroup = 16;
-constexpr int kDenseWgs = 512;   // workgroups per launch (two per CU on MI355X)
-constexpr int kDenseMaxNB = 8;   // queries per pass
-constexpr int kDenseMaxRows = 2048;
+// Tuning knobs (compile-time; defaults measured on MI355X).
+#ifndef VIE_DENSE_UNROLL
+#define VIE_DENSE_UNROLL 1
+#endif
+#ifndef VIE_DENSE_ROWS
+#define VIE_DENSE_ROWS 4
+#endif
+#ifndef VIE_DENSE_WGS
+#define VIE_DENSE_WGS 1024
+#endif
+#ifndef VIE_DENSE_THREADS
+#define VIE_DENSE_THREADS 512
+#endif
 
-struct DenseShared {
-    uint32_t hist[256];
-    uint32_t wave[kDenseThreads / kWave];
-    SelState sel;
-    uint32_t count;
-    int last;
-};
+constexpr int kDenseThreads = VIE_DENSE_THREADS;
+constexpr int kDenseWaves = kDenseThreads / kWave;
+constexpr int kDenseMaxWgs = VIE_DENSE_WGS;
+constexpr int kDenseMaxNB = 8;        // queries per pass
+constexpr int kDenseMaxRows = 16384;  // rows per workgroup
+constexpr size_t kDenseLdsBudget = 96 * 1024;
+constexpr int kMergeThreads = 1024;
+constexpr int kMergeGather = 4096;    // gathered keys held in LDS
+static_assert(kDenseMaxWgs <= kMergeThreads, "the merge gives every slab maximum a thread");
 
-template <typename T>
-__device__ __forceinline__ T *align_up(char *p, size_t a)
+// Sums N values per lane over the 64 lanes of a wave.  The first log2(N)
+// steps halve the set each lane carries (lanes trade the half they give
+// away), the rest are plain xor steps; afterwards lane l holds the total of
+// value index l >> (6 - log2 N).
+template <int N>
+__device__ __forceinline__ float wave_sum_multi(float (&v)[N], int lane)
 {
-    return reinterpret_cast<T *>(((uintptr_t)p + a - 1) & ~(uintptr_t)(a - 1));
+#pragma unroll
+    for (int n = N, o = 32; n > 1; n >>= 1, o >>= 1) {
+        const bool upper = lane & o;
+#pragma unroll
+        for (int i = 0; i < n / 2; ++i) {
+            const float give = upper ? v[i] : v[i + n / 2];
+            const float keep = upper ? v[i + n / 2] : v[i];
+            v[i] = keep + __shfl_xor(give, o, kWave);
+        }
+    }
+    float a = v[0];
+#pragma unroll
+    for (int o = 32 / N; o >= 1; o >>= 1) a += __shfl_xor(a, o, kWave);
+    return a;
+}
+
+template <int N> struct Log2 { static constexpr int value = 1 + Log2<N / 2>::value; };
+template <> struct Log2<1> { static constexpr int value = 0; };
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t t = __shfl_xor(v, o, kWave);
+        v = t > v ? t : v;
+    }
+    return v;
 }
 
 template <int VEC, bool BF16, int NB>
-__global__ __launch_bounds__(kDenseThreads) void dense_topk_kernel(
-    const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq, int k,
-    int rows_per_wg, uint64_t *__restrict__ cand, uint32_t *__restrict__ counter, int32_t *__restrict__ ids,
-    float *__restrict__ logits)
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 8 : 4))) void
+dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
+                  int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ maxes)
 {
     extern __shared__ __align__(16) char smem[];
-    __shared__ DenseShared sh;
+    __shared__ unsigned long long s_max[kDenseMaxNB];
+    constexpr int U = NB >= 8 ? 2 : VIE_DENSE_ROWS;  // rows in flight per wave
+    constexpr int NV = NB * U;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int nwg = gridDim.x;
     const int hbytes = (row_bytes + 15) & ~15;
-    char *hs = smem;                                                  // [NB][hbytes]
+    char *hs = smem;                                                   // [NB][hbytes]
     float *z = reinterpret_cast<float *>(smem + (size_t)NB * hbytes);  // [NB][rows_per_wg]
 
     // queries into LDS (bytewise: rows need not be 4-byte aligned), zero padded
@@ -278,103 +271,206 @@ __global__ __launch_bounds__(kDenseThreads) void dense_topk_kernel(
         const int q = i / hbytes, c = i - q * hbytes;
         hs[i] = (q < nq && c < row_bytes) ? hq[(int64_t)q * row_bytes + c] : 0;
     }
+    if (tid < kDenseMaxNB) s_max[tid] = 0ull;
     __syncthreads();
 
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_wg;
     const int nrows = (int)max<int64_t>(0, min<int64_t>(rows_per_wg, V - r0));
-    const int gl = lane % kDenseGroup;
-    const int groups = kDenseThreads / kDenseGroup;
-    const int grp = wave * (kWave / kDenseGroup) + lane / kDenseGroup;
     const int nchunk = row_bytes / VEC;
     typedef typename Vec<VEC>::T TV;
-    for (int r = grp; r < nrows; r += groups) {
-        const TV *w = reinterpret_cast<const TV *>(W + (r0 + r) * (int64_t)row_bytes);
-        float acc[NB];
+    for (int rb = wave * U; rb < nrows; rb += kDenseWaves * U) {
+        const TV *wr[U];
 #pragma unroll
-        for (int q = 0; q < NB; ++q) acc[q] = 0.0f;
-#pragma unroll 4
-        for (int c = gl; c < nchunk; c += kDenseGroup) {
-            const TV wv = __builtin_nontemporal_load(w + c);
+        for (int u = 0; u < U; ++u)
+            wr[u] = reinterpret_cast<const TV *>(W + (r0 + min(rb + u, nrows - 1)) * (int64_t)row_bytes);
+        float acc[NV];
 #pragma unroll
-            for (int q = 0; q < NB; ++q)
-                acc[q] = dot_vec<VEC, BF16>(wv, reinterpret_cast<const TV *>(hs + q * hbytes)[c], acc[q]);
+        for (int v = 0; v < NV; ++v) acc[v] = 0.0f;
+#pragma unroll VIE_DENSE_UNROLL
+        for (int c = lane; c < nchunk; c += kWave) {
+            TV wv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) wv[u] = __builtin_nontemporal_load(wr[u] + c);
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const TV hv = reinterpret_cast<const TV *>(hs + q * hbytes)[c];
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[q * U + u] = dot_vec<VEC, BF16>(wv[u], hv, acc[q * U + u]);
+            }
         }
-#pragma unroll
-        for (int q = 0; q < NB; ++q) {
-            float a = acc[q];
-#pragma unroll
-            for (int m = kDenseGroup / 2; m >= 1; m >>= 1) a += __shfl_xor(a, m, kDenseGroup);
-            if (gl == 0) z[q * rows_per_wg + r] = a;
+        const float total = wave_sum_multi<NV>(acc, lane);
+        constexpr int lg = 6 - Log2<NV>::value;
+        if ((lane & ((1 << lg) - 1)) == 0) {
+            const int v = lane >> lg, q = v / U, u = v % U;
+            if (rb + u < nrows) z[q * rows_per_wg + rb + u] = total;
         }
     }
     __syncthreads();
 
-    // per-workgroup candidates: the best min(k, nrows) of its rows
-    const int kk = min(k, nrows);
+    // the slab's logits (coalesced) and its largest key, per query
     for (int q = 0; q < nq; ++q) {
-        uint64_t *out = cand + ((int64_t)q * nwg + blockIdx.x) * k;
         const float *zq = z + q * rows_per_wg;
-        auto key_at = [&](int i) { return make_key(zq[i], (int32_t)(r0 + i)); };
-        if (kk > 0) radix_select<kDenseThreads>(nrows, kk, key_at, sh.hist, sh.wave, &sh.sel);
-        if (tid == 0) sh.count = 0;
-        __syncthreads();
-        const SelState s = sh.sel;
-        for (int i = tid; i < nrows && kk > 0; i += kDenseThreads) {
-            const uint64_t key = key_at(i);
-            if (selected(key, s)) {
-                const uint32_t slot = atomicAdd(&sh.count, 1u);
-                if (slot < (uint32_t)kk) out[slot] = key;
-            }
+        float *oq = zout + (int64_t)q * V + r0;
+        uint64_t best = 0ull;
+        for (int i = tid; i < nrows; i += kDenseThreads) {
+            oq[i] = zq[i];
+            const uint64_t key = make_key(zq[i], (int32_t)(r0 + i));
+            best = key > best ? key : best;
         }
-        for (int i = kk + tid; i < k; i += kDenseThreads) out[i] = 0;  // empty slots
-        __syncthreads();
+        best = wave_max_u64(best);
+        if (lane == 0) atomicMax(&s_max[q], (unsigned long long)best);
     }
-
-    // ticket: the last workgroup merges
-    __threadfence();
     __syncthreads();
+    if (tid < nq) maxes[(int64_t)tid * nwg + blockIdx.x] = s_max[tid];
+}
+
+__global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float *__restrict__ zbuf,
+                                                                     const uint64_t *__restrict__ maxes, int64_t V,
+                                                                     int rows_per_wg, int nwg, int k,
+                                                                     int32_t *__restrict__ ids,
+                                                                     float *__restrict__ logits)
+{
+    __shared__ uint32_t hist[256];
+    __shared__ uint64_t gat[kMergeGather];
+    __shared__ int cand[kMergeThreads];
+    __shared__ uint32_t s_nc, s_n;
+    __shared__ unsigned long long s_T, s_and, s_or;
+    const int tid = threadIdx.x, q = blockIdx.x;
+    const float *zq = zbuf + (int64_t)q * V;
+
+    // 1. slab maxima and a lower bound T of their k-th largest: one radix
+    //    pass on the first 8 bits where the maxima differ; T is the lower
+    //    edge of the bucket that holds the k-th largest.  The slabs whose
+    //    maximum is >= T are the only ones that can hold an answer (fewer
+    //    than k slabs: T = 0, every slab).
+    const uint64_t m = tid < nwg ? maxes[(int64_t)q * nwg + tid] : 0ull;
+    if (tid < 256) hist[tid] = 0u;
     if (tid == 0) {
-        const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        sh.last = prev == (uint32_t)(nwg - 1);
+        s_nc = 0;
+        s_n = 0;
+        s_T = 0ull;
+        s_and = ~0ull;
+        s_or = 0ull;
     }
     __syncthreads();
-    if (!sh.last) return;
-    __threadfence();
-
-    uint64_t *sorted = reinterpret_cast<uint64_t *>(smem);  // reuse: [k] keys
-    const int n = nwg * k;
-    for (int q = 0; q < nq; ++q) {
-        const uint64_t *cq = cand + (int64_t)q * n;
-        auto key_at = [&](int i) { return __builtin_nontemporal_load(cq + i); };
-        radix_select<kDenseThreads>(n, k, key_at, sh.hist, sh.wave, &sh.sel);
-        if (tid == 0) sh.count = 0;
+    if (nwg >= k) {
+        uint64_t a = tid < nwg ? m : ~0ull, o = m;
+#pragma unroll
+        for (int x = 32; x >= 1; x >>= 1) {
+            a &= __shfl_xor(a, x, kWave);
+            o |= __shfl_xor(o, x, kWave);
+        }
+        if ((tid & (kWave - 1)) == 0) {
+            atomicAnd(&s_and, (unsigned long long)a);
+            atomicOr(&s_or, (unsigned long long)o);
+        }
         __syncthreads();
-        const SelState s = sh.sel;
-        uint64_t *pick = sorted + k;  // [k] unordered picks
-        for (int i = tid; i < n; i += kDenseThreads) {
-            const uint64_t key = key_at(i);
-            if (key != 0 && selected(key, s)) {
-                const uint32_t slot = atomicAdd(&sh.count, 1u);
-                if (slot < (uint32_t)k) pick[slot] = key;
+        const uint64_t common = s_and, diff = s_and ^ s_or;  // diff != 0: maxima are distinct
+        const int top = 63 - __clzll((long long)diff);
+        const int sh = top >= 7 ? top - 7 : 0;
+        if (tid < nwg) atomicAdd(&hist[(m >> sh) & 255u], 1u);
+        __syncthreads();
+        if (tid < kWave) {  // wave 0: the bucket holding the k-th largest
+            const int lane = tid;
+            uint32_t c[4], sum = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                c[j] = hist[255 - 4 * lane - j];
+                sum += c[j];
+            }
+            uint32_t incl = sum;
+#pragma unroll
+            for (int x = 1; x < kWave; x <<= 1) {
+                const uint32_t t = __shfl_up(incl, x, kWave);
+                if (lane >= x) incl += t;
+            }
+            uint32_t above = incl - sum;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (above < (uint32_t)k && (uint32_t)k <= above + c[j]) {
+                    const uint64_t hi = sh + 8 >= 64 ? 0ull : (common & (~0ull << (sh + 8)));
+                    s_T = hi | ((uint64_t)(255 - 4 * lane - j) << sh);
+                }
+                above += c[j];
             }
         }
         __syncthreads();
-        // rank sort (keys are distinct)
-        for (int t = tid; t < k; t += kDenseThreads) {
-            const uint64_t key = pick[t];
+    }
+    const uint64_t T = s_T;
+    if (tid < nwg && m >= T) cand[atomicAdd(&s_nc, 1u)] = tid;
+    __syncthreads();
+    const int nc = (int)s_nc;
+
+    // 2. gather the keys >= T of those slabs
+    for (int i = tid; i < nc * rows_per_wg; i += kMergeThreads) {
+        const int c = i / rows_per_wg;
+        const int64_t row = (int64_t)cand[c] * rows_per_wg + (i - c * rows_per_wg);
+        if (row < V) {
+            const uint64_t key = make_key(zq[row], (int32_t)row);
+            if (key >= T) {
+                const uint32_t slot = atomicAdd(&s_n, 1u);
+                if (slot < (uint32_t)kMergeGather) gat[slot] = key;
+            }
+        }
+    }
+    __syncthreads();
+    const int n = (int)s_n;
+
+    if (n <= kMergeGather) {
+        // 3. order by rank: key t lands at its rank if that is below k
+        for (int t = tid; t < n; t += kMergeThreads) {
+            const uint64_t key = gat[t];
             int rank = 0;
-            for (int j = 0; j < k; ++j) rank += pick[j] > key;
-            sorted[rank] = key;
+            for (int j = 0; j < n; ++j) rank += gat[j] > key;
+            if (rank < k) {
+                ids[(int64_t)q * k + rank] = key_id(key);
+                logits[(int64_t)q * k + rank] = key_logit(key);
+            }
         }
+        return;
+    }
+    // 3'. too many keys >= T (e.g. many equal logits): the k-th largest of
+    //     the gathered range by bisection on the key, then order by rank
+    //     among the ones above it (a slow path for degenerate inputs only).
+    __shared__ unsigned long long s_cnt;
+    uint64_t lo = T, hi = ~0ull;  // invariant: count(>= lo) >= k, count(>= hi + 1) < k
+    while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (tid == 0) s_cnt = 0;
         __syncthreads();
-        for (int t = tid; t < k; t += kDenseThreads) {
-            const uint64_t key = sorted[t];
-            ids[(int64_t)q * k + t] = key_id(key);
-            logits[(int64_t)q * k + t] = key_logit(key);
+        unsigned long long c = 0;
+        for (int i = tid; i < nc * rows_per_wg; i += kMergeThreads) {
+            const int cc = i / rows_per_wg;
+            const int64_t row = (int64_t)cand[cc] * rows_per_wg + (i - cc * rows_per_wg);
+            if (row < V && make_key(zq[row], (int32_t)row) >= mid) ++c;
         }
+        atomicAdd(&s_cnt, c);
+        __syncthreads();
+        if (s_cnt >= (unsigned long long)k) lo = mid; else hi = mid - 1;
         __syncthreads();
     }
-    if (tid == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) s_n = 0;
+    __syncthreads();
+    for (int i = tid; i < nc * rows_per_wg; i += kMergeThreads) {
+        const int c = i / rows_per_wg;
+        const int64_t row = (int64_t)cand[c] * rows_per_wg + (i - c * rows_per_wg);
+        if (row < V) {
+            const uint64_t key = make_key(zq[row], (int32_t)row);
+            if (key >= lo) {
+                const uint32_t slot = atomicAdd(&s_n, 1u);
+                if (slot < (uint32_t)kMergeGather) gat[slot] = key;
+            }
+        }
+    }
+    __syncthreads();
+    const int n2 = min((int)s_n, k);  // exactly k keys are >= lo
+    for (int t = tid; t < n2; t += kMergeThreads) {
+        const uint64_t key = gat[t];
+        int rank = 0;
+        for (int j = 0; j < n2; ++j) rank += gat[j] > key;
+        ids[(int64_t)q * k + rank] = key_id(key);
+        logits[(int64_t)q * k + rank] = key_logit(key);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -623,90 +719,116 @@ vie_status launch_scatter(const int32_t *ids, const float *logits, int B, int k,
     return launched(hipGetLastError(), "scatter launch");
 }
 
-size_t dense_workspace_bytes(int64_t V, int d, int B, int k)
-{
-    (void)V;
-    (void)d;
-    const int nb = B < kDenseMaxNB ? B : kDenseMaxNB;
-    return 256 + (size_t)nb * kDenseWgs * (size_t)k * 8;
-}
-
 namespace {
 
-size_t dense_lds(int nb, int row_bytes, int rows_per_wg, int k)
+// Grid size of the dense head: at most kDenseMaxWgs workgroups.
+int dense_grid(int64_t V)
+{
+    const int64_t nwg = V < kDenseMaxWgs ? V : kDenseMaxWgs;
+    return nwg < 1 ? 1 : (int)nwg;
+}
+
+struct DensePlan {
+    int nwg, rpw, nbmax;
+};
+
+size_t dense_lds(int nb, int row_bytes, int rows_per_wg)
 {
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
-    const size_t a = (size_t)nb * hbytes + (size_t)nb * rows_per_wg * 4;
-    const size_t b = (size_t)k * 16;  // final merge reuse
-    return a > b ? a : b;
+    return (size_t)nb * (hbytes + (size_t)rows_per_wg * 4);
+}
+
+// Slab size, grid and queries per pass; a slab's logits and the queries of
+// one pass must fit the LDS budget.
+bool dense_plan(int64_t V, int row_bytes, DensePlan &p)
+{
+    const int nwg = dense_grid(V);
+    const int rpw = (int)((V + nwg - 1) / nwg);
+    if (rpw > kDenseMaxRows) return false;
+    int nb = kDenseMaxNB;
+    while (nb > 1 && dense_lds(nb, row_bytes, rpw) > kDenseLdsBudget) nb >>= 1;
+    if (dense_lds(nb, row_bytes, rpw) > kDenseLdsBudget) return false;
+    p.nwg = (int)((V + rpw - 1) / rpw);
+    p.rpw = rpw;
+    p.nbmax = nb;
+    return true;
 }
 
 template <int VEC, bool BF16, int NB>
-hipError_t dense_launch(const void *W, int64_t V, int row_bytes, const char *h, int nq, int k, int rpw, int nwg,
-                        uint64_t *cand, uint32_t *counter, int32_t *ids, float *logits, hipStream_t s)
+hipError_t dense_launch(const void *W, int64_t V, int row_bytes, const char *h, int nq, int k, const DensePlan &p,
+                        float *zbuf, uint64_t *maxes, int32_t *ids, float *logits, hipStream_t s)
 {
-    const size_t lds = dense_lds(NB, row_bytes, rpw, k);
-    auto kern = dense_topk_kernel<VEC, BF16, NB>;
+    const size_t lds = dense_lds(NB, row_bytes, p.rpw);
+    auto kern = dense_slab_kernel<VEC, BF16, NB>;
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    kern<<<nwg, kDenseThreads, lds, s>>>(static_cast<const char *>(W), V, row_bytes, h, nq, k, rpw, cand, counter,
-                                          ids, logits);
+    kern<<<p.nwg, kDenseThreads, lds, s>>>(static_cast<const char *>(W), V, row_bytes, h, nq, p.rpw, zbuf, maxes);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, maxes, V, p.rpw, p.nwg, k, ids, logits);
     return hipGetLastError();
 }
 
 template <int VEC, bool BF16>
-hipError_t dense_launch_nb(int nb, const void *W, int64_t V, int row_bytes, const char *h, int nq, int k, int rpw,
-                           int nwg, uint64_t *cand, uint32_t *counter, int32_t *ids, float *logits, hipStream_t s)
+hipError_t dense_launch_nb(int nb, const void *W, int64_t V, int row_bytes, const char *h, int nq, int k,
+                           const DensePlan &p, float *zbuf, uint64_t *maxes, int32_t *ids, float *logits,
+                           hipStream_t s)
 {
     switch (nb) {
-    case 1: return dense_launch<VEC, BF16, 1>(W, V, row_bytes, h, nq, k, rpw, nwg, cand, counter, ids, logits, s);
-    case 2: return dense_launch<VEC, BF16, 2>(W, V, row_bytes, h, nq, k, rpw, nwg, cand, counter, ids, logits, s);
-    case 4: return dense_launch<VEC, BF16, 4>(W, V, row_bytes, h, nq, k, rpw, nwg, cand, counter, ids, logits, s);
-    default: return dense_launch<VEC, BF16, 8>(W, V, row_bytes, h, nq, k, rpw, nwg, cand, counter, ids, logits, s);
+    case 1: return dense_launch<VEC, BF16, 1>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
+    case 2: return dense_launch<VEC, BF16, 2>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
+    case 4: return dense_launch<VEC, BF16, 4>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
+    default: return dense_launch<VEC, BF16, 8>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
     }
 }
 
 }  // namespace
 
+// Workspace: the logits [min(B, 8)][V] fp32 (256-byte padded), then the slab
+// maxima [min(B, 8)][slabs] u64.
+size_t dense_workspace_bytes(int64_t V, int d, int B, int k)
+{
+    (void)d;
+    (void)k;
+    const int nb = B < kDenseMaxNB ? B : kDenseMaxNB;
+    return (((size_t)nb * V * 4 + 255) & ~(size_t)255) + (size_t)nb * dense_grid(V) * 8;
+}
+
 vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const void *h, int B, int k, int32_t *ids,
                              float *logits, void *ws, hipStream_t s)
 {
     const int row_bytes = d * elem_bytes(dtype);
-    const int hbytes = (row_bytes + 15) & ~15;
-    // queries per pass: at most 8, and their rows must fit in 48 KB of LDS
-    int nbmax = kDenseMaxNB;
-    while (nbmax > 1 && (size_t)nbmax * hbytes > 48 * 1024) nbmax >>= 1;
-    int nwg = kDenseWgs;
-    int rpw = (int)((V + nwg - 1) / nwg);
-    if (rpw > kDenseMaxRows)
-        return fail(VIE_EUNSUPPORTED, "V = %lld needs more than %d rows per workgroup", (long long)V, kDenseMaxRows);
-    if (rpw < 1) rpw = 1;
-    nwg = (int)((V + rpw - 1) / rpw);
-    uint32_t *counter = static_cast<uint32_t *>(ws);
-    uint64_t *cand = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 256);
+    DensePlan p;
+    if (!dense_plan(V, row_bytes, p))
+        return fail(VIE_EUNSUPPORTED, "dense top-k: V = %lld rows of %d bytes exceed one pass's slab", (long long)V,
+                    row_bytes);
+    const int nbw = B < kDenseMaxNB ? B : kDenseMaxNB;
+    float *zbuf = static_cast<float *>(ws);
+    uint64_t *maxes = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) +
+                                                   (((size_t)nbw * V * 4 + 255) & ~(size_t)255));
     const char *hb = static_cast<const char *>(h);
     const int vec = pick_vec(row_bytes, W);
-    for (int q0 = 0; q0 < B; q0 += nbmax) {
-        const int nq = B - q0 < nbmax ? B - q0 : nbmax;
+    const bool bf = dtype == VIE_BF16;
+    for (int q0 = 0; q0 < B; q0 += p.nbmax) {
+        const int nq = B - q0 < p.nbmax ? B - q0 : p.nbmax;
         const int nb = nq == 1 ? 1 : nq == 2 ? 2 : nq <= 4 ? 4 : 8;
         const char *hp = hb + (int64_t)q0 * row_bytes;
         int32_t *ip = ids + (int64_t)q0 * k;
         float *lp = logits + (int64_t)q0 * k;
         hipError_t e;
-        const bool bf = dtype == VIE_BF16;
         if (vec == 16)
-            e = bf ? dense_launch_nb<16, true>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s)
-                   : dense_launch_nb<16, false>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s);
+            e = bf ? dense_launch_nb<16, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s)
+                   : dense_launch_nb<16, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
         else if (vec == 8)
-            e = bf ? dense_launch_nb<8, true>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s)
-                   : dense_launch_nb<8, false>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s);
+            e = bf ? dense_launch_nb<8, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s)
+                   : dense_launch_nb<8, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
         else if (vec == 4)
-            e = bf ? dense_launch_nb<4, true>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s)
-                   : dense_launch_nb<4, false>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s);
+            e = bf ? dense_launch_nb<4, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s)
+                   : dense_launch_nb<4, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
         else
-            e = dense_launch_nb<2, true>(nb, W, V, row_bytes, hp, nq, k, rpw, nwg, cand, counter, ip, lp, s);
+            e = dense_launch_nb<2, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
         if (e != hipSuccess) return launched(e, "dense top-k launch");
     }
     return VIE_OK;

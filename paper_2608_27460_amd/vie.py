@@ -13,7 +13,7 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "lib", "libvie.so")
+LIB_PATH = os.environ.get("VIE_LIB") or os.path.join(_HERE, "lib", "libvie.so")
 
 OK, EINVAL, ENOMEM, EHIP, EIO, EFORMAT, ESTATE, EUNSUPPORTED = range(8)
 F32, BF16 = 0, 1
@@ -200,8 +200,8 @@ def dense_topk_workspace_bytes(V: int, d: int, B: int, k: int) -> int:
 
 
 def dense_topk_into(W, h, k: int, ids, logits, workspace) -> None:
-    """Exact top-k of W h on the current stream; workspace is a zero-initialised
-    uint8 device tensor of at least dense_topk_workspace_bytes() bytes."""
+    """Exact top-k of W h on the current stream; workspace is a uint8 device
+    tensor of at least dense_topk_workspace_bytes() bytes."""
     V, d = W.shape
     dt = _dtype_of_tensor(W)
     if _dtype_of_tensor(h) != dt:
@@ -219,7 +219,7 @@ class DenseHead:
         self.W = W
         V, d = W.shape
         nbytes = dense_topk_workspace_bytes(V, d, max_batch, min(max_k, V))
-        self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=W.device)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
 
     def __call__(self, h, k: int):
         torch = _torch()

@@ -77,19 +77,23 @@ def test_dense_topk_matches_oracle(vie, V, d, dtype, B, k):
     oid, olg, osc = O.topk(W, dtype, H, k)
     parity.check_logits(W, dtype, H, ids, lg, "dense")
     parity.check_id_sets(W, dtype, H, ids, oid, osc[:, -1], what="dense")
-    # repeated calls reuse the workspace (its ticket counter must come back to 0)
+    # repeated calls reuse the workspace
     for _ in range(2):
         ids2, lg2 = head(dev_tensor(vie, H, dtype), k)
         torch.cuda.synchronize()
         assert np.array_equal(ids2.cpu().numpy(), ids) and np.array_equal(lg2.cpu().numpy(), lg)
 
 
-def test_dense_zero_query_orders_by_id(vie):
-    W = synth.make_w(30000, 64, synth.BF16, 5)
-    head = vie.DenseHead(dev_tensor(vie, W, synth.BF16), max_batch=1, max_k=64)
-    ids, lg = head(torch.zeros((1, 64), dtype=torch.bfloat16, device="cuda"), 64)
+@pytest.mark.parametrize("V,k", [(30000, 64), (200000, 100)])
+def test_dense_zero_query_orders_by_id(vie, V, k):
+    # every logit is 0, so the answer is ids 0..k-1 (ties go to the smaller
+    # id); the second case has more tied keys at the threshold than the
+    # merge holds in LDS, which takes its bisection path
+    W = synth.make_w(V, 32, synth.BF16, 5)
+    head = vie.DenseHead(dev_tensor(vie, W, synth.BF16), max_batch=1, max_k=k)
+    ids, lg = head(torch.zeros((1, 32), dtype=torch.bfloat16, device="cuda"), k)
     torch.cuda.synchronize()
-    assert ids.cpu().numpy()[0].tolist() == list(range(64))
+    assert ids.cpu().numpy()[0].tolist() == list(range(k))
     assert np.all(lg.cpu().numpy() == 0)
 
 

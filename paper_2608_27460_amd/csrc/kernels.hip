@@ -481,26 +481,33 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
 // set of 1) through layers maxlevel..1, then a sorted beam of ef_eff keys on
 // layer 0.  Each step expands the best unexpanded beam entry: its neighbour
 // list is read by one thread per slot, unseen ids are claimed in the LDS
-// visited bitmap, their rows are dotted with h by 16-lane groups, and the new
-// keys are merged into the beam (which keeps the best ef_eff).  The search
-// ends when every beam entry is expanded.  This visits, scores and expands
-// exactly the nodes the sequential algorithm does (a node evicted from the
-// result set is worse than all of it and would only be popped to stop the
-// search), so the distance and expansion counts match it.
-
-constexpr int kHnswThreads = 256;
-constexpr int kHnswGroup = 16;
+// visited bitmap, and their rows are dotted with h by G-lane groups (every
+// chunk of a row is loaded before the first is used, so one memory round
+// trip covers all the new rows of a step).  New keys that cannot enter a full
+// beam are dropped; the rest are ordered and merged in (the beam keeps the
+// best ef_eff).  The search ends when every beam entry is expanded.  This
+// visits, scores and expands exactly the nodes the sequential algorithm
+// does: a node evicted from the result set is worse than all of it and would
+// only be popped to stop the search.  So the distance and expansion counts
+// match it.
+//
+// Latency hiding that keeps those semantics: the next step expands either
+// the entry that is now second best among the unexpanded ones, or the best
+// node this step inserts.  Both layer-0 lists are fetched during this step's
+// row loads (the second with spare threads, each new node's by the group
+// that scores its row), so the next step finds its list in LDS.  The beam is
+// double buffered (merge from one buffer into the other).
 
 struct HnswShared {
-    uint64_t best;
-    uint32_t nnew;
-    uint32_t first;  // first unexpanded beam slot
-    uint32_t nbeam;
+    unsigned long long best;
+    uint32_t nnew, nkeep;
+    uint32_t first, second, nbeam;
+    int32_t pfa_id, pfb_id;  // nodes whose layer-0 lists sit in pfa[] / pfb[]
 };
 
 __device__ __forceinline__ void clear_bits(uint32_t *vis, int words)
 {
-    for (int i = threadIdx.x; i < words; i += kHnswThreads) vis[i] = 0u;
+    for (int i = threadIdx.x; i < words; i += blockDim.x) vis[i] = 0u;
 }
 
 // Returns true if id was not yet marked (and marks it).
@@ -510,8 +517,45 @@ __device__ __forceinline__ bool claim(uint32_t *vis, int32_t id)
     return (atomicOr(&vis[id >> 5], bit) & bit) == 0u;
 }
 
-template <int VEC, bool BF16>
-__global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
+// Row chunks per lane held in registers (fp32 rows: 4, which avoids the
+// register spills 8 causes there).
+template <bool BF16> struct RowCpl { static constexpr int value = BF16 ? 8 : 4; };
+
+// <row, h> by the G lanes of a group (lane gl of the group covers chunks gl,
+// gl + G, ...): up to RowCpl chunks per lane are loaded before any is used.
+// Every lane of the group returns the sum.
+template <int VEC, bool BF16, int G>
+__device__ __forceinline__ float row_dot(const char *__restrict__ W, int64_t row, int row_bytes, const char *hs,
+                                         int gl)
+{
+    typedef typename Vec<VEC>::T T;
+    const T *w = reinterpret_cast<const T *>(W + row * (int64_t)row_bytes);
+    const T *h = reinterpret_cast<const T *>(hs);
+    const int nchunk = row_bytes / VEC;
+    constexpr int CPL = RowCpl<BF16>::value;
+    T buf[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) buf[i] = w[c];
+    }
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) acc = dot_vec<VEC, BF16>(buf[i], h[c], acc);
+    }
+    for (int c = gl + CPL * G; c < nchunk; c += G) acc = dot_vec<VEC, BF16>(w[c], h[c], acc);
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, G);
+    return acc;
+}
+
+constexpr int kPfbPerLane = 4;       // a new node's list is prefetched when M0 <= 4 * G
+constexpr int kHnswWideBatch = 256;  // batches below this get 1024-thread workgroups
+
+template <int NT, int VEC, bool BF16, int G>
+__global__ __launch_bounds__(NT) void hnsw_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
     const char *__restrict__ hq, int k, int ef, int32_t *__restrict__ ids, float *__restrict__ logits,
@@ -519,11 +563,13 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
 {
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    constexpr int kGroups = NT / G;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int q = blockIdx.x;
     const int hbytes = (row_bytes + 15) & ~15;
     const int vwords = (int)((V + 31) / 32);
     const int maxdeg = M0 > M ? M0 : M;
+    const bool pfb_on = M0 <= kPfbPerLane * G;
     // LDS carve-up (sizes mirror hnsw_lds_bytes)
     char *p = smem;
     char *hs = p;
@@ -538,6 +584,10 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
     p += (size_t)maxdeg * 8;
     int32_t *cid = reinterpret_cast<int32_t *>(p);
     p += (size_t)maxdeg * 4;
+    int32_t *pfa = reinterpret_cast<int32_t *>(p);
+    p += (size_t)M0 * 4;
+    int32_t *pfb = reinterpret_cast<int32_t *>(p);
+    p += (size_t)M0 * 4;
     uint8_t *flag = reinterpret_cast<uint8_t *>(p);
     p += (size_t)ef;
     uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
@@ -545,19 +595,21 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
     uint32_t *vis = reinterpret_cast<uint32_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);
 
     const char *h = hq + (int64_t)q * row_bytes;
-    for (int i = tid; i < hbytes; i += kHnswThreads) hs[i] = i < row_bytes ? h[i] : 0;
+    for (int i = tid; i < hbytes; i += NT) hs[i] = i < row_bytes ? h[i] : 0;
+    if (tid == 0) {
+        sh.best = 0;
+        sh.pfa_id = -1;
+        sh.pfb_id = -1;
+    }
     __syncthreads();
 
-    const int gl = lane % kHnswGroup;
-    const int grp = wave * (kWave / kHnswGroup) + lane / kHnswGroup;
-    const int ngroups = kHnswThreads / kHnswGroup;
+    const int gl = tid % G;
+    const int grp = tid / G;
     uint32_t n_dist = 0, n_expand = 0;
 
     // score the entry point
-    if (tid == 0) sh.best = 0;
-    __syncthreads();
     if (grp == 0) {
-        const float s = group_row_dot<VEC, BF16, kHnswGroup>(W, entry, row_bytes, hs, gl);
+        const float s = row_dot<VEC, BF16, G>(W, entry, row_bytes, hs, gl);
         if (gl == 0) sh.best = make_key(s, entry);
     }
     __syncthreads();
@@ -575,16 +627,15 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
             __syncthreads();
             ++n_expand;
             const int32_t *lst = upper + ((int64_t)upper_off[c] + lc - 1) * M;
-            if (tid < M) {
-                const int32_t e = lst[tid];
+            for (int t = tid; t < M; t += NT) {
+                const int32_t e = lst[t];
                 if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
             }
             __syncthreads();
             const int nn = (int)sh.nnew;
-            for (int j = grp; j < nn; j += ngroups) {
-                const float s = group_row_dot<VEC, BF16, kHnswGroup>(W, cid[j], row_bytes, hs, gl);
-                if (gl == 0) atomicMax(reinterpret_cast<unsigned long long *>(&sh.best),
-                                       (unsigned long long)make_key(s, cid[j]));
+            for (int j = grp; j < nn; j += kGroups) {
+                const float s = row_dot<VEC, BF16, G>(W, cid[j], row_bytes, hs, gl);
+                if (gl == 0) atomicMax(&sh.best, (unsigned long long)make_key(s, cid[j]));
             }
             __syncthreads();
             n_dist += nn;
@@ -595,7 +646,8 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
         }
     }
 
-    // layer 0: beam of ef keys, sorted descending, with expanded flags
+    // layer 0: beam of ef keys, sorted descending, with expanded flags,
+    // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...)
     clear_bits(vis, vwords);
     __syncthreads();
     if (tid == 0) {
@@ -610,37 +662,87 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
         const uint32_t first = sh.first, nbeam = sh.nbeam;
         if (first >= nbeam) break;
         const int32_t c = key_id(beam[first]);
+        const int32_t *lst = sh.pfa_id == c ? pfa : (sh.pfb_id == c ? pfb : nullptr);
         __syncthreads();
         if (tid == 0) {
             flag[first] = 1;
             sh.nnew = 0;
+            sh.nkeep = 0;
+            sh.second = 0xFFFFFFFFu;
+            sh.best = 0;
         }
         ++n_expand;
         __syncthreads();
-        const int32_t *lst = adj0 + (int64_t)c * M0;
-        for (int t = tid; t < M0; t += kHnswThreads) {
-            const int32_t e = lst[t];
+        // claim the unseen neighbours; find the next unexpanded entry after first
+        for (int t = tid; t < M0; t += NT) {
+            const int32_t e = lst ? lst[t] : adj0[(int64_t)c * M0 + t];
             if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
+        }
+        for (int i0 = (int)first + 1 + (tid & ~(kWave - 1)); i0 < (int)nbeam; i0 += NT) {
+            const int i = i0 + lane;
+            const uint64_t ball = __ballot(i < (int)nbeam && !flag[i]);
+            if (ball && lane == 0) atomicMin(&sh.second, (uint32_t)(i0 + __ffsll((long long)ball) - 1));
         }
         __syncthreads();
         const int nn = (int)sh.nnew;
         n_dist += nn;
-        for (int j = grp; j < nn; j += ngroups) {
-            const float s = group_row_dot<VEC, BF16, kHnswGroup>(W, cid[j], row_bytes, hs, gl);
-            if (gl == 0) ckey[j] = make_key(s, cid[j]);
+        const uint32_t second = sh.second;
+        const int32_t ida = second < nbeam ? key_id(beam[second]) : -1;
+        // spare threads fetch the second entry's list while the rows load
+        int32_t pfv = -1;
+        const int pft = tid - (NT - M0);  // the last M0 threads
+        if (ida >= 0 && pft >= 0) pfv = adj0[(int64_t)ida * M0 + pft];
+        const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
+        uint64_t gbest = 0ull;  // best key this group scored, and its node's list
+        int32_t glist[kPfbPerLane];
+        for (int j = grp; j < nn; j += kGroups) {
+            const int32_t e = cid[j];
+            int32_t l[kPfbPerLane];
+            if (pfb_on) {
+#pragma unroll
+                for (int u = 0; u < kPfbPerLane; ++u) {
+                    const int t = gl + u * G;
+                    l[u] = t < M0 ? adj0[(int64_t)e * M0 + t] : -1;
+                }
+            }
+            const float s = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
+            const uint64_t key = make_key(s, e);
+            if (gl == 0 && key > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = key;
+            if (key > gbest) {
+                gbest = key;
+#pragma unroll
+                for (int u = 0; u < kPfbPerLane; ++u) glist[u] = l[u];
+            }
         }
+        if (gl == 0 && gbest > worst) atomicMax(&sh.best, (unsigned long long)gbest);
         __syncthreads();
-        // order the new keys (rank sort; keys are distinct)
-        for (int j = tid; j < nn; j += kHnswThreads) {
+        if (ida >= 0 && pft >= 0) pfa[pft] = pfv;
+        const uint64_t bestnew = sh.best;
+        if (pfb_on && bestnew != 0ull && gbest == bestnew) {
+#pragma unroll
+            for (int u = 0; u < kPfbPerLane; ++u) {
+                const int t = gl + u * G;
+                if (t < M0) pfb[t] = glist[u];
+            }
+        }
+        if (tid == 0) {
+            sh.pfa_id = ida;
+            sh.pfb_id = pfb_on && bestnew != 0ull ? key_id(bestnew) : -1;
+            sh.first = 0xFFFFFFFFu;
+        }
+        const int nk = (int)sh.nkeep;
+        // order the kept keys (rank sort; keys are distinct)
+        for (int j = tid; j < nk; j += NT) {
             const uint64_t key = ckey[j];
             int rank = 0;
-            for (int t = 0; t < nn; ++t) rank += ckey[t] > key;
+            for (int t = 0; t < nk; ++t) rank += ckey[t] > key;
             csort[rank] = key;
         }
         __syncthreads();
-        // merge beam (nbeam) and csort (nn) into beam2, keep the best ef
-        const int total = min((int)nbeam + nn, ef);
-        for (int j = tid; j < nn; j += kHnswThreads) {
+        // merge beam (nbeam) and csort (nk) into beam2, keep the best ef; the
+        // new first unexpanded entry is the best kept key or the old second
+        const int total = min((int)nbeam + nk, ef);
+        for (int j = tid; j < nk; j += NT) {
             const uint64_t key = csort[j];
             int lo = 0, hi = (int)nbeam;  // count beam keys > key
             while (lo < hi) {
@@ -651,11 +753,12 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
             if (pos < total) {
                 beam2[pos] = key;
                 flag2[pos] = 0;
+                if (j == 0) atomicMin(&sh.first, (uint32_t)pos);
             }
         }
-        for (int i = tid; i < (int)nbeam; i += kHnswThreads) {
+        for (int i = tid; i < (int)nbeam; i += NT) {
             const uint64_t key = beam[i];
-            int lo = 0, hi = nn;  // count new keys > key
+            int lo = 0, hi = nk;  // count new keys > key
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
                 if (csort[mid] > key) lo = mid + 1; else hi = mid;
@@ -664,21 +767,21 @@ __global__ __launch_bounds__(kHnswThreads) void hnsw_kernel(
             if (pos < total) {
                 beam2[pos] = key;
                 flag2[pos] = flag[i];
+                if (i == (int)second) atomicMin(&sh.first, (uint32_t)pos);
             }
-        }
-        if (tid == 0) sh.first = 0xFFFFFFFFu;
-        __syncthreads();
-        for (int i = tid; i < total; i += kHnswThreads) {
-            beam[i] = beam2[i];
-            flag[i] = flag2[i];
-            if (!flag2[i]) atomicMin(&sh.first, (uint32_t)i);
         }
         if (tid == 0) sh.nbeam = (uint32_t)total;
         __syncthreads();
+        uint64_t *tb = beam;
+        beam = beam2;
+        beam2 = tb;
+        uint8_t *tf = flag;
+        flag = flag2;
+        flag2 = tf;
     }
 
     const int nb = (int)sh.nbeam;
-    for (int t = tid; t < k; t += kHnswThreads) {
+    for (int t = tid; t < k; t += NT) {
         ids[(int64_t)q * k + t] = t < nb ? key_id(beam[t]) : -1;
         logits[(int64_t)q * k + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
     }
@@ -839,7 +942,7 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t maxdeg = (size_t)(M0 > M ? M0 : M);
-    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + maxdeg * (8 + 8 + 4) + (size_t)ef_eff * 2;
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + maxdeg * (8 + 8 + 4) + (size_t)M0 * 8 + (size_t)ef_eff * 2;
     n = (n + 15) & ~(size_t)15;
     return n + (size_t)((V + 31) / 32) * 4;
 }
@@ -854,18 +957,35 @@ size_t hnsw_lds_limit()
 }
 
 namespace {
-template <int VEC, bool BF16>
+template <int NT, int VEC, bool BF16, int G>
 hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
 {
-    auto kern = hnsw_kernel<VEC, BF16>;
+    auto kern = hnsw_kernel<NT, VEC, BF16, G>;
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    kern<<<a.B, kHnswThreads, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0,
-                                         a.M0, a.upper_off, a.upper, a.M, a.maxlevel, a.entry,
-                                         static_cast<const char *>(a.h), a.k, a.ef_eff, a.ids, a.logits, a.stats);
+    kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
+                               a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h), a.k,
+                               a.ef_eff, a.ids, a.logits, a.stats);
     return hipGetLastError();
+}
+
+// Lanes per row: the fewest (16, 32 or 64) that cover a row in the
+// register-held chunks per lane, so as many rows as possible load at once.
+// Workgroup size: 1024 threads (the most rows in flight for one query) for
+// small batches; 256 when the batch alone fills the GPU.
+template <int VEC, bool BF16>
+hipError_t hnsw_launch_g(const HnswLaunch &a, size_t lds, hipStream_t s)
+{
+    const int nchunk = a.d * elem_bytes(a.dtype) / VEC;
+    constexpr int CPL = RowCpl<BF16>::value;
+    const bool wide = a.B < kHnswWideBatch;
+    if (nchunk <= 16 * CPL)
+        return wide ? hnsw_launch<1024, VEC, BF16, 16>(a, lds, s) : hnsw_launch<256, VEC, BF16, 16>(a, lds, s);
+    if (nchunk <= 32 * CPL)
+        return wide ? hnsw_launch<1024, VEC, BF16, 32>(a, lds, s) : hnsw_launch<256, VEC, BF16, 32>(a, lds, s);
+    return wide ? hnsw_launch<1024, VEC, BF16, 64>(a, lds, s) : hnsw_launch<256, VEC, BF16, 64>(a, lds, s);
 }
 }  // namespace
 
@@ -876,14 +996,15 @@ vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
     if (lds > lim)
         return fail(VIE_EUNSUPPORTED, "HNSW search needs %zu bytes of LDS per workgroup; the device allows %zu", lds,
                     lim);
+    if (a.M0 > 256 || a.M > 256) return fail(VIE_EUNSUPPORTED, "HNSW search: degree caps above 256");
     const int row_bytes = a.d * elem_bytes(a.dtype);
     const int vec = pick_vec(row_bytes, a.W);
     const bool bf = a.dtype == VIE_BF16;
     hipError_t e;
-    if (vec == 16) e = bf ? hnsw_launch<16, true>(a, lds, s) : hnsw_launch<16, false>(a, lds, s);
-    else if (vec == 8) e = bf ? hnsw_launch<8, true>(a, lds, s) : hnsw_launch<8, false>(a, lds, s);
-    else if (vec == 4) e = bf ? hnsw_launch<4, true>(a, lds, s) : hnsw_launch<4, false>(a, lds, s);
-    else e = hnsw_launch<2, true>(a, lds, s);
+    if (vec == 16) e = bf ? hnsw_launch_g<16, true>(a, lds, s) : hnsw_launch_g<16, false>(a, lds, s);
+    else if (vec == 8) e = bf ? hnsw_launch_g<8, true>(a, lds, s) : hnsw_launch_g<8, false>(a, lds, s);
+    else if (vec == 4) e = bf ? hnsw_launch_g<4, true>(a, lds, s) : hnsw_launch_g<4, false>(a, lds, s);
+    else e = hnsw_launch_g<2, true>(a, lds, s);
     return launched(e, "HNSW search launch");
 }
 

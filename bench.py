@@ -29,6 +29,28 @@ import numpy as np
 
 METRIC = "us/query and queries/s of top-k output head at B=1 (HNSW vs dense), %HBM peak"
 HBM_PEAK_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_27460_amd", "csrc", "kernels.hip")
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch from the committed counter summary of this workload
+    (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading of a
+    plain device copy of known size).  None when no summary exists or when the
+    kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.txt" % workload)
+    if not os.path.exists(path):
+        return {}
+    sha = hashlib.sha1(open(KERNEL_SRC, "rb").read()).hexdigest()
+    out, src = {}, None
+    for line in open(path):
+        f = line.split()
+        if len(f) == 2 and f[0] == "source_sha1":
+            src = f[1]
+        elif len(f) == 3 and f[0] == "traffic_bytes":
+            out[f[1]] = float(f[2])
+    return out if src == sha else {}
 
 
 def log(*a):
@@ -47,6 +69,11 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cache", default=os.environ.get("VIE_CACHE", "/tmp/vie_cache"))
+    ap.add_argument("--sweep-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024, 2048, 4096],
+                    help="extra beam widths of the ef sweep (comma separated)")
+    ap.add_argument("--sweep-queries", type=int, default=128, help="queries per extra sweep point")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="finish with a device copy of this many MiB (a known-size reference for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the head is a single-GPU path (sharding it over several "
@@ -122,12 +149,12 @@ def main() -> int:
                 ev[1][q].record(stream)
             vie.scatter_into(div[q], dlv[q], wl.V, row)
 
-    def timed(step, K, W_):
+    def timed(step, K, W_, n=Q):
         for _ in range(W_):
             step()
         torch.cuda.synchronize()
-        evs = [([torch.cuda.Event(enable_timing=True) for _ in range(Q)],
-                [torch.cuda.Event(enable_timing=True) for _ in range(Q)]) for _ in range(K)]
+        evs = [([torch.cuda.Event(enable_timing=True) for _ in range(n)],
+                [torch.cuda.Event(enable_timing=True) for _ in range(n)]) for _ in range(K)]
         outer = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
         torch.cuda.synchronize()
         t = time.perf_counter()
@@ -154,13 +181,26 @@ def main() -> int:
     def recall(a, b):
         return float(np.mean([len(set(x.tolist()) & set(y.tolist())) / k for x, y in zip(a, b)]))
 
-    # ---- ef sweep (same protocol, one step each) -------------------------
+    # ---- ef sweep (same protocol; one warm-up and one timed pass each) ----
+    # Beams wider than the workload's own ef values run on the first
+    # --sweep-queries queries only.
     sweep = {}
-    for e in sorted(set(wl.ef) | {ef}):
-        ms_e, _, _ = timed(lambda ev=None, e=e: hnsw_step(ev, e), 1, 1)
-        sweep[str(e)] = {"us_per_query": round(ms_e * 1e3 / Q, 2), "recall_at_k": round(recall(ids.cpu().numpy(),
-                                                                                                  exact_ids), 4),
-                         "mean_n_dist": float(st.cpu().numpy()[:, 0].mean())}
+    for e in sorted(set(wl.ef) | {ef} | set(args.sweep_ef)):
+        nq = Q if e <= max(max(wl.ef), ef) else min(Q, args.sweep_queries)
+
+        def step_e(ev=None, e=e, nq=nq):
+            for q in range(nq):
+                if ev is not None:
+                    ev[0][q].record(stream)
+                ix.query_into(hv[q], k, e, iv[q], lv[q], sv[q])
+                if ev is not None:
+                    ev[1][q].record(stream)
+                vie.scatter_into(iv[q], lv[q], wl.V, row)
+
+        ms_e, _, _ = timed(step_e, 1, 1, nq)
+        sweep[str(e)] = {"us_per_query": round(ms_e * 1e3 / nq, 2), "queries": nq,
+                         "recall_at_k": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq]), 4),
+                         "mean_n_dist": float(st.cpu().numpy()[:nq, 0].mean())}
     # ---- all queries in one launch (one workgroup each) -------------------
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -180,6 +220,7 @@ def main() -> int:
     d_us = float(d_launch.mean())
     dense_gbs = dense_bytes / (d_us * 1e-6) / 1e9
 
+    traffic = measured_traffic(args.workload)
     h_qps = Q * args.steps / (h_ms * 1e-3)
     d_qps = Q * args.steps / (d_ms * 1e-3)
 
@@ -226,13 +267,20 @@ def main() -> int:
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(hnsw_gbs / HBM_PEAK_GBS, 5), "traffic": None},
-        "roofline_dense": {"kernel": "dense_topk_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
+                     "unit": "GB/s", "frac": round(hnsw_gbs / HBM_PEAK_GBS, 5),
+                     "traffic": traffic.get("hnsw_kernel")},
+        "roofline_dense": {"kernel": "dense_slab_kernel+dense_merge_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dense_gbs / HBM_PEAK_GBS, 4),
-                           "traffic": None},
+                           "traffic": traffic.get("dense_head")},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
     return 0
 
 

@@ -16,7 +16,7 @@ constexpr int kMaxLevel = 16;     // level cap of the level draw
 constexpr int kMaxM = 128;        // cap on M (upper layers)
 constexpr int kMaxM0 = 256;       // cap on M0 (layer 0)
 constexpr int kMaxK = 1024;       // largest k of any query
-constexpr int kMaxEf = 1024;      // largest beam of the HNSW kernel
+constexpr int kMaxEf = 8192;      // largest beam of the HNSW kernel (LDS permitting)
 constexpr int kMaxD = 8192;       // largest row width
 
 inline int elem_bytes(int dtype) { return dtype == VIE_F32 ? 4 : 2; }

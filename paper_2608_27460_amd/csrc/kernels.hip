@@ -1,11 +1,13 @@
 // gfx950 (CDNA4) kernels of the vector-index output head.
 //
-//   scatter_kernel     Section 3: full-vocabulary logits, -inf except the
-//                      retrieved ids.
-//   dense_topk_kernel  exact head z = W_out h fused with top-k (Section 3;
-//                      the dense baseline of Section 4.1).
-//   hnsw_kernel        HNSW k-NN search (Sections 2-3; Malkov & Yashunin
-//                      Algorithms 2 and 5), one workgroup per query.
+//   scatter_kernel      Section 3: full-vocabulary logits, -inf except the
+//                       retrieved ids.
+//   dense_slab_kernel,  exact head z = W_out h fused with top-k (Section 3;
+//   dense_mfma_kernel,  the dense baseline of Section 4.1): slab logits on
+//   dense_merge_kernel  the vector ALUs (one to a few queries) or the matrix
+//                       cores (batches), then the top k from slab summaries.
+//   hnsw_kernel         HNSW k-NN search (Sections 2-3; Malkov & Yashunin
+//                       Algorithms 2 and 5), one workgroup per query.
 //
 // Ordering: a candidate is the 64-bit key (ord(logit) << 32) | ~id, where
 // ord() maps fp32 to an unsigned integer of the same order.  A larger key is
@@ -13,6 +15,7 @@
 // That is the (dist, id) order of the search with dist = -logit.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "index.hpp"
@@ -186,9 +189,12 @@ __global__ __launch_bounds__(kScatterThreads) void scatter_kernel(const int32_t 
 // dense_merge_kernel: one workgroup per query.  Any T at or below the k-th
 // largest slab maximum is a lower bound of the k-th largest key overall (k
 // distinct elements are >= T), so every key of the answer is >= T, and only
-// the slabs whose maximum is >= T can hold one.  T comes from one radix pass
-// over the maxima; the kernel gathers those slabs' keys >= T (typically
-// little more than k) and orders them by rank.  The kernel boundary between the two launches is the only
+// the slabs whose maximum is >= T can hold one.  T is found by a radix
+// select over the maxima (8 bits per pass, from the first bit where they
+// differ, until the bucket of the k-th largest is taken whole), so exactly
+// k slabs qualify; the kernel gathers their keys >= T (typically little more
+// than k, with several row loads in flight per thread) and orders them by
+// rank.  The kernel boundary between the two launches is the only
 // cross-workgroup synchronisation: no atomics across workgroups, no fences.
 
 // Tuning knobs (compile-time; defaults measured on MI355X).
@@ -241,14 +247,33 @@ __device__ __forceinline__ float wave_sum_multi(float (&v)[N], int lane)
 template <int N> struct Log2 { static constexpr int value = 1 + Log2<N / 2>::value; };
 template <> struct Log2<1> { static constexpr int value = 0; };
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
+// The two largest of a set of distinct keys, (b1 > b2), 0 for "none".
+__device__ __forceinline__ void top2_insert(uint64_t key, uint64_t &b1, uint64_t &b2)
+{
+    // selects only: branches here make the compiler keep (b1, b2) in scratch
+    const uint64_t hi = key > b1 ? key : b1, lo = key > b1 ? b1 : key;
+    b2 = lo > b2 ? lo : b2;
+    b1 = hi;
+}
+
+__device__ __forceinline__ void top2_merge(uint64_t o1, uint64_t o2, uint64_t &b1, uint64_t &b2)
+{
+    const uint64_t hi = o1 > b1 ? o1 : b1, lo = o1 > b1 ? b1 : o1;
+    const uint64_t r2 = o2 > b2 ? o2 : b2;
+    b1 = hi;
+    b2 = lo > r2 ? lo : r2;
+}
+
+// Top two over the lanes whose index differs in the bits of `span` (xor
+// steps from span down to 1); every such lane ends with the result.
+template <int SPAN>
+__device__ __forceinline__ void top2_reduce(uint64_t &b1, uint64_t &b2)
 {
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const uint64_t t = __shfl_xor(v, o, kWave);
-        v = t > v ? t : v;
+    for (int o = SPAN; o >= 1; o >>= 1) {
+        const uint64_t o1 = __shfl_xor(b1, o, kWave), o2 = __shfl_xor(b2, o, kWave);
+        top2_merge(o1, o2, b1, b2);
     }
-    return v;
 }
 
 template <int VEC, bool BF16, int NB>
@@ -257,7 +282,7 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
                   int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ maxes)
 {
     extern __shared__ __align__(16) char smem[];
-    __shared__ unsigned long long s_max[kDenseMaxNB];
+    __shared__ uint64_t s_top[NB][kDenseWaves][2];
     constexpr int U = NB >= 8 ? 2 : VIE_DENSE_ROWS;  // rows in flight per wave
     constexpr int NV = NB * U;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -271,7 +296,6 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
         const int q = i / hbytes, c = i - q * hbytes;
         hs[i] = (q < nq && c < row_bytes) ? hq[(int64_t)q * row_bytes + c] : 0;
     }
-    if (tid < kDenseMaxNB) s_max[tid] = 0ull;
     __syncthreads();
 
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_wg;
@@ -307,117 +331,257 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
     }
     __syncthreads();
 
-    // the slab's logits (coalesced) and its largest key, per query
+    // the slab's logits (coalesced) and its two largest keys, per query
     for (int q = 0; q < nq; ++q) {
         const float *zq = z + q * rows_per_wg;
         float *oq = zout + (int64_t)q * V + r0;
-        uint64_t best = 0ull;
+        uint64_t b1 = 0ull, b2 = 0ull;
         for (int i = tid; i < nrows; i += kDenseThreads) {
             oq[i] = zq[i];
-            const uint64_t key = make_key(zq[i], (int32_t)(r0 + i));
-            best = key > best ? key : best;
+            top2_insert(make_key(zq[i], (int32_t)(r0 + i)), b1, b2);
         }
-        best = wave_max_u64(best);
-        if (lane == 0) atomicMax(&s_max[q], (unsigned long long)best);
+        top2_reduce<32>(b1, b2);
+        if (lane == 0) {
+            s_top[q][wave][0] = b1;
+            s_top[q][wave][1] = b2;
+        }
     }
     __syncthreads();
-    if (tid < nq) maxes[(int64_t)tid * nwg + blockIdx.x] = s_max[tid];
+    if (tid < nq) {
+        uint64_t b1 = 0ull, b2 = 0ull;
+        for (int w = 0; w < kDenseWaves; ++w) top2_merge(s_top[tid][w][0], s_top[tid][w][1], b1, b2);
+        maxes[((int64_t)tid * nwg + blockIdx.x) * 2] = b1;
+        maxes[((int64_t)tid * nwg + blockIdx.x) * 2 + 1] = b2;
+    }
+}
+
+constexpr int kGatherBatch = 8;  // row loads in flight per thread while gathering
+constexpr int kMergeWaves = kMergeThreads / kWave;
+
+// Sorts one key per lane of a wave, largest first (bitonic network over xor
+// partners).
+__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t key, int lane)
+{
+#pragma unroll
+    for (int size = 2; size <= kWave; size <<= 1)
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            const uint64_t other = __shfl_xor(key, stride, kWave);
+            const bool keep_max = ((lane & stride) == 0) == ((lane & size) == 0);
+            key = keep_max ? (other > key ? other : key) : (other < key ? other : key);
+        }
+    return key;
+}
+
+// Sorts a bitonic sequence held one key per lane, largest first.
+__device__ __forceinline__ uint64_t wave_bitonic_merge_desc(uint64_t key, int lane)
+{
+#pragma unroll
+    for (int stride = kWave / 2; stride > 0; stride >>= 1) {
+        const uint64_t other = __shfl_xor(key, stride, kWave);
+        key = (lane & stride) == 0 ? (other > key ? other : key) : (other < key ? other : key);
+    }
+    return key;
+}
+
+// Adds the keys >= T of rows [row0, row0 + nrows) (clamped to V) of zq to
+// gat; the whole workgroup takes part, kGatherBatch loads in flight per
+// thread.  Element i is row i % rows_per of listed slab i / rows_per.
+__device__ __forceinline__ void gather_slabs(const float *__restrict__ zq, int64_t V, const int *slabs, int nslab,
+                                             int rows_per, uint64_t T, uint64_t *gat, uint32_t *s_n)
+{
+    const int tid = threadIdx.x;
+    const int total = nslab * rows_per;
+    const int step_c = kMergeThreads / rows_per, step_r = kMergeThreads % rows_per;
+    for (int base = 0; base < total; base += kMergeThreads * kGatherBatch) {
+        float z[kGatherBatch];
+        int64_t row[kGatherBatch];
+        int c = (base + tid) / rows_per, rr = (base + tid) - c * rows_per;
+#pragma unroll
+        for (int j = 0; j < kGatherBatch; ++j) {
+            row[j] = -1;
+            z[j] = 0.0f;
+            if (c < nslab) {
+                const int64_t r = (int64_t)slabs[c] * rows_per + rr;
+                if (r < V) {
+                    row[j] = r;
+                    z[j] = zq[r];
+                }
+            }
+            c += step_c;
+            rr += step_r;
+            if (rr >= rows_per) {
+                rr -= rows_per;
+                ++c;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kGatherBatch; ++j) {
+            if (row[j] >= 0) {
+                const uint64_t key = make_key(z[j], (int32_t)row[j]);
+                if (key >= T) {
+                    const uint32_t slot = atomicAdd(s_n, 1u);
+                    if (slot < (uint32_t)kMergeGather) gat[slot] = key;
+                }
+            }
+        }
+    }
 }
 
 __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float *__restrict__ zbuf,
-                                                                     const uint64_t *__restrict__ maxes, int64_t V,
+                                                                     const uint64_t *__restrict__ tops, int64_t V,
                                                                      int rows_per_wg, int nwg, int k,
                                                                      int32_t *__restrict__ ids,
                                                                      float *__restrict__ logits)
 {
     __shared__ uint32_t hist[256];
     __shared__ uint64_t gat[kMergeGather];
-    __shared__ int cand[kMergeThreads];
-    __shared__ uint32_t s_nc, s_n;
-    __shared__ unsigned long long s_T, s_and, s_or;
-    const int tid = threadIdx.x, q = blockIdx.x;
+    __shared__ uint64_t lists[kMergeWaves][kWave];
+    __shared__ int cand[kMergeThreads], scan[kWave];
+    __shared__ uint64_t second[kMergeThreads];
+    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count;
+    __shared__ unsigned long long s_prefix, s_and, s_or, s_T;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave, q = blockIdx.x;
     const float *zq = zbuf + (int64_t)q * V;
+    const uint64_t *tq = tops + (int64_t)q * nwg * 2;  // (largest, second largest) key per slab
 
-    // 1. slab maxima and a lower bound T of their k-th largest: one radix
-    //    pass on the first 8 bits where the maxima differ; T is the lower
-    //    edge of the bucket that holds the k-th largest.  The slabs whose
-    //    maximum is >= T are the only ones that can hold an answer (fewer
-    //    than k slabs: T = 0, every slab).
-    const uint64_t m = tid < nwg ? maxes[(int64_t)q * nwg + tid] : 0ull;
-    if (tid < 256) hist[tid] = 0u;
+    uint64_t m = 0ull, m2 = 0ull;
+    if (tid < nwg) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(tq + 2 * tid);
+        m = ((uint64_t)v.y << 32) | v.x;
+        m2 = ((uint64_t)v.w << 32) | v.z;
+    }
+    second[tid] = m2;
     if (tid == 0) {
         s_nc = 0;
         s_n = 0;
-        s_T = 0ull;
+        s_nscan = 0;
         s_and = ~0ull;
         s_or = 0ull;
     }
-    __syncthreads();
-    if (nwg >= k) {
-        uint64_t a = tid < nwg ? m : ~0ull, o = m;
+    if (k <= kWave && nwg >= k) {
+        // 1. T = the k-th largest slab maximum, exactly: every wave sorts its
+        //    64 maxima, then pairs of sorted lists merge (keeping the larger
+        //    64) in four rounds until wave 0 holds the largest 64.
+        uint64_t key = wave_sort_desc(m, lane);
 #pragma unroll
-        for (int x = 32; x >= 1; x >>= 1) {
-            a &= __shfl_xor(a, x, kWave);
-            o |= __shfl_xor(o, x, kWave);
+        for (int span = 1; span < kMergeWaves; span <<= 1) {
+            if ((wave & (2 * span - 1)) == span) lists[wave][lane] = key;
+            __syncthreads();
+            if ((wave & (2 * span - 1)) == 0) {
+                const uint64_t other = lists[wave + span][kWave - 1 - lane];
+                key = wave_bitonic_merge_desc(other > key ? other : key, lane);
+            }
         }
-        if ((tid & (kWave - 1)) == 0) {
-            atomicAnd(&s_and, (unsigned long long)a);
-            atomicOr(&s_or, (unsigned long long)o);
+        // 2. the k slabs whose maximum is >= T hold every key >= T; a slab's
+        //    maximum is its only such key unless its second largest is >= T
+        //    too, and only those slabs are read again
+        if (wave == 0) {
+            const uint64_t T = __shfl(key, k - 1, kWave);
+            if (lane < k) {
+                const int slab = (int)(key_id(key) / rows_per_wg);
+                cand[lane] = slab;
+                if (second[slab] >= T) scan[atomicAdd(&s_nscan, 1u)] = slab;
+                else gat[atomicAdd(&s_n, 1u)] = key;
+            }
+            if (lane == 0) {
+                s_T = T;
+                s_nc = (uint32_t)k;
+            }
         }
         __syncthreads();
-        const uint64_t common = s_and, diff = s_and ^ s_or;  // diff != 0: maxima are distinct
-        const int top = 63 - __clzll((long long)diff);
-        const int sh = top >= 7 ? top - 7 : 0;
-        if (tid < nwg) atomicAdd(&hist[(m >> sh) & 255u], 1u);
+        gather_slabs(zq, V, scan, (int)s_nscan, rows_per_wg, s_T, gat, &s_n);
+    } else {
+        // 1'. any k, or fewer slabs than k: T by radix select over the
+        //     maxima, 8 bits per pass from the first bit where they differ,
+        //     until the bucket of the k-th largest is taken whole (T = 0 with
+        //     fewer slabs than k: every slab); every slab with maximum >= T
+        //     is read
         __syncthreads();
-        if (tid < kWave) {  // wave 0: the bucket holding the k-th largest
-            const int lane = tid;
-            uint32_t c[4], sum = 0;
+        uint64_t T = 0ull;
+        if (nwg >= k) {
+            uint64_t a = tid < nwg ? m : ~0ull, o = m;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                c[j] = hist[255 - 4 * lane - j];
-                sum += c[j];
+            for (int x = 32; x >= 1; x >>= 1) {
+                a &= __shfl_xor(a, x, kWave);
+                o |= __shfl_xor(o, x, kWave);
             }
-            uint32_t incl = sum;
-#pragma unroll
-            for (int x = 1; x < kWave; x <<= 1) {
-                const uint32_t t = __shfl_up(incl, x, kWave);
-                if (lane >= x) incl += t;
+            if (lane == 0) {
+                atomicAnd(&s_and, (unsigned long long)a);
+                atomicOr(&s_or, (unsigned long long)o);
             }
-            uint32_t above = incl - sum;
+            __syncthreads();
+            const uint64_t diff = s_and ^ s_or;
+            uint64_t prefix = s_and;
+            if (diff != 0ull) {
+                // bits >= hi are known (in prefix); each pass decides bits [lo, hi)
+                int hi = 64 - __clzll((long long)diff);
+                prefix &= hi >= 64 ? 0ull : (~0ull << hi);
+                uint32_t want = (uint32_t)k;
+                for (;;) {
+                    const int lo = hi > 8 ? hi - 8 : 0;
+                    const uint64_t known = hi >= 64 ? 0ull : (~0ull << hi);
+                    const uint64_t dmask = (1ull << (hi - lo)) - 1ull;
+                    if (tid < 256) hist[tid] = 0u;
+                    __syncthreads();
+                    if (tid < nwg && (m & known) == prefix) atomicAdd(&hist[(m >> lo) & dmask], 1u);
+                    __syncthreads();
+                    if (tid < kWave) {  // wave 0: the bucket holding the want-th largest
+                        uint32_t c[4], sum = 0;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (above < (uint32_t)k && (uint32_t)k <= above + c[j]) {
-                    const uint64_t hi = sh + 8 >= 64 ? 0ull : (common & (~0ull << (sh + 8)));
-                    s_T = hi | ((uint64_t)(255 - 4 * lane - j) << sh);
+                        for (int j = 0; j < 4; ++j) {
+                            c[j] = hist[255 - 4 * lane - j];
+                            sum += c[j];
+                        }
+                        uint32_t incl = sum;
+#pragma unroll
+                        for (int x = 1; x < kWave; x <<= 1) {
+                            const uint32_t t = __shfl_up(incl, x, kWave);
+                            if (lane >= x) incl += t;
+                        }
+                        uint32_t above = incl - sum;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            if (above < want && want <= above + c[j]) {
+                                s_prefix = prefix | ((uint64_t)(255 - 4 * lane - j) << lo);
+                                s_want = want - above;
+                                s_count = c[j];
+                            }
+                            above += c[j];
+                        }
+                    }
+                    __syncthreads();
+                    prefix = s_prefix;
+                    want = s_want;
+                    if (s_count == want || lo == 0) break;  // uniform: shared values after a barrier
+                    hi = lo;
                 }
-                above += c[j];
             }
+            T = prefix;
         }
+        if (tid < nwg && m >= T) cand[atomicAdd(&s_nc, 1u)] = tid;
+        if (tid == 0) s_T = T;
         __syncthreads();
+        gather_slabs(zq, V, cand, (int)s_nc, rows_per_wg, T, gat, &s_n);
     }
+    __syncthreads();
     const uint64_t T = s_T;
-    if (tid < nwg && m >= T) cand[atomicAdd(&s_nc, 1u)] = tid;
-    __syncthreads();
     const int nc = (int)s_nc;
-
-    // 2. gather the keys >= T of those slabs
-    for (int i = tid; i < nc * rows_per_wg; i += kMergeThreads) {
-        const int c = i / rows_per_wg;
-        const int64_t row = (int64_t)cand[c] * rows_per_wg + (i - c * rows_per_wg);
-        if (row < V) {
-            const uint64_t key = make_key(zq[row], (int32_t)row);
-            if (key >= T) {
-                const uint32_t slot = atomicAdd(&s_n, 1u);
-                if (slot < (uint32_t)kMergeGather) gat[slot] = key;
-            }
-        }
-    }
-    __syncthreads();
     const int n = (int)s_n;
 
+    if (n <= kWave) {
+        // 3. one wave sorts the (typically little more than k) keys >= T
+        if (tid < kWave) {
+            const uint64_t key = wave_sort_desc(tid < n ? gat[tid] : 0ull, lane);
+            if (tid < k && tid < n) {
+                ids[(int64_t)q * k + tid] = key_id(key);
+                logits[(int64_t)q * k + tid] = key_logit(key);
+            }
+        }
+        return;
+    }
     if (n <= kMergeGather) {
-        // 3. order by rank: key t lands at its rank if that is below k
+        // 3'. more keys: order by rank, key t lands at its rank if that is below k
         for (int t = tid; t < n; t += kMergeThreads) {
             const uint64_t key = gat[t];
             int rank = 0;
@@ -429,9 +593,9 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
         }
         return;
     }
-    // 3'. too many keys >= T (e.g. many equal logits): the k-th largest of
-    //     the gathered range by bisection on the key, then order by rank
-    //     among the ones above it (a slow path for degenerate inputs only).
+    // 3''. too many keys >= T (e.g. many equal logits): the k-th largest of
+    //      the candidate slabs by bisection on the key, then order by rank
+    //      among the ones above it (a slow path for degenerate inputs only).
     __shared__ unsigned long long s_cnt;
     uint64_t lo = T, hi = ~0ull;  // invariant: count(>= lo) >= k, count(>= hi + 1) < k
     while (lo < hi) {
@@ -470,6 +634,211 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
         for (int j = 0; j < n2; ++j) rank += gat[j] > key;
         ids[(int64_t)q * k + rank] = key_id(key);
         logits[(int64_t)q * k + rank] = key_logit(key);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dense head, batched bf16: skinny GEMM on the matrix cores
+// ---------------------------------------------------------------------------
+//
+// For several queries at once the slab logits come from
+// v_mfma_f32_16x16x32_bf16 (16 rows of W_out times 16 queries per
+// instruction, fp32 accumulation).  Workgroup w owns a slab of rows; each of
+// its four waves takes 32 rows at a time against all the queries of the pass
+// (NQT 16-query tiles) and walks the row width in stages of KC columns.
+//
+// The operand layout of the instruction wants 16 different rows per load,
+// which scatters a wave's accesses over 16 rows; streamed that way W_out
+// reaches barely half of the HBM bandwidth.  So each wave stages its rows
+// through its own slice of LDS: a stage is read with non-temporal loads that
+// cover whole contiguous row segments (the next stage is loaded while the
+// current one is multiplied), written to LDS and read back in operand
+// layout.  The reduction index is free to permute, so lane (r, g) =
+// (lane % 16, lane / 16) takes columns 32 t + 8 g .. + 7 of step t for its
+// row r and the same columns of its query.  The queries' columns of a stage
+// are staged in LDS once for the four waves (read with the row stage, one
+// stage ahead), which keeps the registers for loads in flight.  The slab's
+// logits and two largest keys per query go to the workspace in the layout
+// of the single-query path, and dense_merge_kernel selects the top k.
+
+#ifndef VIE_MFMA_MIN_B
+#define VIE_MFMA_MIN_B 3
+#endif
+#ifndef VIE_MFMA_MAX_WGS
+#define VIE_MFMA_MAX_WGS 1024
+#endif
+#ifndef VIE_MFMA_KC4
+#define VIE_MFMA_KC4 128
+#endif
+#ifndef VIE_MFMA_KC12
+#define VIE_MFMA_KC12 256
+#endif
+
+constexpr int kMfmaWaves = 4;
+constexpr int kMfmaThreads = kMfmaWaves * kWave;
+constexpr int kMfmaMaxNB = 64;                    // queries per pass
+constexpr int kMfmaMinB = VIE_MFMA_MIN_B;
+constexpr int kMfmaMaxWgs = VIE_MFMA_MAX_WGS;
+constexpr int kMfmaRowsPerWave = 32;              // two 16-row tiles
+constexpr int kMfmaRowsPerIter = kMfmaWaves * kMfmaRowsPerWave;
+static_assert(kMfmaMaxWgs <= kMergeThreads, "the merge gives every slab maximum a thread");
+
+constexpr int mfma_pitch(int KC) { return KC * 2 + 16; }  // LDS bytes per staged row (padded)
+constexpr size_t mfma_lds(int NQT, int KC)
+{
+    return (size_t)(kMfmaWaves * kMfmaRowsPerWave + 16 * NQT) * mfma_pitch(KC);
+}
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+}
+
+template <int NQT, int KC>
+__global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t *__restrict__ W, int64_t V, int d,
+                                                                   const uint16_t *__restrict__ hq, int nq,
+                                                                   int rows_per_wg, float *__restrict__ zout,
+                                                                   uint64_t *__restrict__ maxes)
+{
+    extern __shared__ __align__(16) char smem[];
+    __shared__ uint64_t s_top[16 * NQT][kMfmaWaves][2];
+    constexpr int kPitch = mfma_pitch(KC);
+    constexpr int kSteps = KC / 32;                     // MFMA steps per stage
+    constexpr int kLanesPerRow = KC / 8;                // 16-byte pieces per staged row
+    constexpr int kRowsPerLoad = kWave / kLanesPerRow;
+    constexpr int kLoads = kMfmaRowsPerWave / kRowsPerLoad;  // W stage loads per lane
+    constexpr int kHLoads = 16 * NQT * kLanesPerRow / kMfmaThreads;  // query stage loads per thread
+    static_assert(kRowsPerLoad >= 1 && kMfmaRowsPerWave % kRowsPerLoad == 0, "stage shape");
+    static_assert(kHLoads >= 1 && (16 * NQT * kLanesPerRow) % kMfmaThreads == 0, "query stage shape");
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int r = lane & 15, g = lane >> 4;
+    char *slice = smem + (size_t)wave * kMfmaRowsPerWave * kPitch;
+    char *hsl = smem + (size_t)kMfmaWaves * kMfmaRowsPerWave * kPitch;  // [16 NQT][kPitch]
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_wg;
+    const int nrows = (int)max<int64_t>(0, min<int64_t>(rows_per_wg, V - r0));
+    const int nstage = (d + KC - 1) / KC;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    // W staging: load j of a lane covers row kRowsPerLoad j + srow, 16 bytes
+    // at column scol of the stage
+    const int srow = lane / kLanesPerRow, scol = 8 * (lane % kLanesPerRow);
+
+    // query staging: load j of a thread covers query row L / kLanesPerRow
+    // (padding rows repeat the last query), column hcol[j]
+    const uint16_t *hrowp[kHLoads];
+    int hoff[kHLoads], hcol[kHLoads];
+#pragma unroll
+    for (int j = 0; j < kHLoads; ++j) {
+        const int L = j * kMfmaThreads + tid;
+        const int row = L / kLanesPerRow;
+        hcol[j] = 8 * (L % kLanesPerRow);
+        hrowp[j] = hq + (int64_t)min(row, nq - 1) * d;
+        hoff[j] = row * kPitch + hcol[j] * 2;
+    }
+
+    uint64_t best[NQT], best2[NQT];
+#pragma unroll
+    for (int n = 0; n < NQT; ++n) best[n] = best2[n] = 0ull;
+
+    // every wave runs the same number of iterations (the workgroup barriers
+    // need it); rows past the slab are clamped and discarded
+    for (int rb0 = 0; rb0 < nrows; rb0 += kMfmaRowsPerIter) {
+        const int rb = rb0 + wave * kMfmaRowsPerWave;
+        const uint16_t *wrow[kLoads];
+#pragma unroll
+        for (int j = 0; j < kLoads; ++j)
+            wrow[j] = W + (r0 + min(rb + kRowsPerLoad * j + srow, nrows - 1)) * (int64_t)d;
+        u32x4 pre[kLoads];
+#pragma unroll
+        for (int j = 0; j < kLoads; ++j)
+            pre[j] = scol + 8 <= d ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + scol)) : zero;
+        u32x4 hpre[kHLoads];
+#pragma unroll
+        for (int j = 0; j < kHLoads; ++j)
+            hpre[j] = hcol[j] + 8 <= d ? *reinterpret_cast<const u32x4 *>(hrowp[j] + hcol[j]) : zero;
+        f32x4 acc[2][NQT];
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int n = 0; n < NQT; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        for (int st = 0; st < nstage; ++st) {
+            const int c0 = st * KC;
+            __syncthreads();  // every wave is done with the previous query stage
+            // this stage into LDS, then the next stage's loads
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j)
+                *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) = pre[j];
+#pragma unroll
+            for (int j = 0; j < kHLoads; ++j) *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = hpre[j];
+            if (st + 1 < nstage) {
+                const int c = c0 + KC + scol;
+#pragma unroll
+                for (int j = 0; j < kLoads; ++j)
+                    pre[j] = c + 8 <= d ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + c))
+                                        : zero;
+#pragma unroll
+                for (int j = 0; j < kHLoads; ++j) {
+                    const int ch = c0 + KC + hcol[j];
+                    hpre[j] = ch + 8 <= d ? *reinterpret_cast<const u32x4 *>(hrowp[j] + ch) : zero;
+                }
+            }
+            __syncthreads();  // the query stage is complete
+#pragma unroll
+            for (int t = 0; t < kSteps; ++t) {
+                u32x4 a[2];
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+                    a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                for (int n = 0; n < NQT; ++n) {
+                    const u32x4 bv =
+                        *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                    for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+        // lane (r, g) holds rows 4 g + i of each 16-row tile for query 16 n + r
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int n = 0; n < NQT; ++n) {
+                const int q = n * 16 + r;
+                const int lr = rb + m * 16 + 4 * g;
+                if (q < nq) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (lr + i < nrows) {
+                            const float z = acc[m][n][i];
+                            zout[(int64_t)q * V + r0 + lr + i] = z;
+                            top2_insert(make_key(z, (int32_t)(r0 + lr + i)), best[n], best2[n]);
+                        }
+                }
+            }
+    }
+    // per query: the two largest over the four lane groups, then over the waves
+#pragma unroll
+    for (int n = 0; n < NQT; ++n) {
+        uint64_t b1 = best[n], b2 = best2[n];
+        for (int o = 16; o <= 32; o <<= 1) {
+            const uint64_t o1 = __shfl_xor(b1, o, kWave), o2 = __shfl_xor(b2, o, kWave);
+            top2_merge(o1, o2, b1, b2);
+        }
+        if (g == 0) {
+            s_top[n * 16 + r][wave][0] = b1;
+            s_top[n * 16 + r][wave][1] = b2;
+        }
+    }
+    __syncthreads();
+    if (tid < nq) {
+        uint64_t b1 = 0ull, b2 = 0ull;
+        for (int w = 0; w < kMfmaWaves; ++w) top2_merge(s_top[tid][w][0], s_top[tid][w][1], b1, b2);
+        maxes[((int64_t)tid * gridDim.x + blockIdx.x) * 2] = b1;
+        maxes[((int64_t)tid * gridDim.x + blockIdx.x) * 2 + 1] = b2;
     }
 }
 
@@ -889,14 +1258,60 @@ hipError_t dense_launch_nb(int nb, const void *W, int64_t V, int row_bytes, cons
 
 }  // namespace
 
-// Workspace: the logits [min(B, 8)][V] fp32 (256-byte padded), then the slab
-// maxima [min(B, 8)][slabs] u64.
+namespace {
+
+// Matrix-core plan: slabs of whole workgroup iterations, at most
+// kDenseMaxWgs of them (the merge gives every slab maximum a thread).
+DensePlan mfma_plan(int64_t V)
+{
+    const int64_t iters = (V + kMfmaRowsPerIter - 1) / kMfmaRowsPerIter;
+    const int64_t per = (iters + kMfmaMaxWgs - 1) / kMfmaMaxWgs;
+    DensePlan p;
+    p.rpw = (int)(per * kMfmaRowsPerIter);
+    p.nwg = (int)((V + p.rpw - 1) / p.rpw);
+    p.nbmax = kMfmaMaxNB;
+    return p;
+}
+
+bool use_mfma(int dtype, int d, int B, const void *W, const void *h)
+{
+    return dtype == VIE_BF16 && B >= kMfmaMinB && d % 8 == 0 && (uintptr_t)W % 16 == 0 && (uintptr_t)h % 16 == 0;
+}
+
+// Queries per pass of either path.
+int dense_pass(int B) { return B >= kMfmaMinB ? kMfmaMaxNB : kDenseMaxNB; }
+
+template <int NQT, int KC>
+hipError_t mfma_launch(const void *W, int64_t V, int d, const char *h, int nq, int k, const DensePlan &p,
+                       float *zbuf, uint64_t *maxes, int32_t *ids, float *logits, hipStream_t s)
+{
+    auto kern = dense_mfma_kernel<NQT, KC>;
+    constexpr size_t lds = mfma_lds(NQT, KC);
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    kern<<<p.nwg, kMfmaThreads, lds, s>>>(static_cast<const uint16_t *>(W), V, d,
+                                           reinterpret_cast<const uint16_t *>(h), nq, p.rpw, zbuf, maxes);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, maxes, V, p.rpw, p.nwg, k, ids, logits);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// Workspace: the logits [nb][V] fp32 (256-byte padded), then the two
+// largest keys of every slab [nb][slabs][2] u64, nb = the queries of one pass (at most 8 on the vector
+// path, 64 on the matrix-core path, never more than B).
 size_t dense_workspace_bytes(int64_t V, int d, int B, int k)
 {
     (void)d;
     (void)k;
-    const int nb = B < kDenseMaxNB ? B : kDenseMaxNB;
-    return (((size_t)nb * V * 4 + 255) & ~(size_t)255) + (size_t)nb * dense_grid(V) * 8;
+    const int pass = dense_pass(B);
+    const int nb = B < pass ? B : pass;
+    const int slabs = std::max(dense_grid(V), mfma_plan(V).nwg);
+    return (((size_t)nb * V * 4 + 255) & ~(size_t)255) + (size_t)nb * slabs * 16;
 }
 
 vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const void *h, int B, int k, int32_t *ids,
@@ -907,11 +1322,26 @@ vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const v
     if (!dense_plan(V, row_bytes, p))
         return fail(VIE_EUNSUPPORTED, "dense top-k: V = %lld rows of %d bytes exceed one pass's slab", (long long)V,
                     row_bytes);
-    const int nbw = B < kDenseMaxNB ? B : kDenseMaxNB;
+    const int pass = dense_pass(B);
+    const int nbw = B < pass ? B : pass;
     float *zbuf = static_cast<float *>(ws);
     uint64_t *maxes = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) +
                                                    (((size_t)nbw * V * 4 + 255) & ~(size_t)255));
     const char *hb = static_cast<const char *>(h);
+    if (use_mfma(dtype, d, B, W, h)) {
+        const DensePlan mp = mfma_plan(V);
+        for (int q0 = 0; q0 < B; q0 += kMfmaMaxNB) {
+            const int nq = B - q0 < kMfmaMaxNB ? B - q0 : kMfmaMaxNB;
+            const char *hp = hb + (int64_t)q0 * row_bytes;
+            int32_t *ip = ids + (int64_t)q0 * k;
+            float *lp = logits + (int64_t)q0 * k;
+            hipError_t e = nq <= 16   ? mfma_launch<1, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, maxes, ip, lp, s)
+                           : nq <= 32 ? mfma_launch<2, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, maxes, ip, lp, s)
+                                      : mfma_launch<4, VIE_MFMA_KC4>(W, V, d, hp, nq, k, mp, zbuf, maxes, ip, lp, s);
+            if (e != hipSuccess) return launched(e, "dense top-k (matrix cores) launch");
+        }
+        return VIE_OK;
+    }
     const int vec = pick_vec(row_bytes, W);
     const bool bf = dtype == VIE_BF16;
     for (int q0 = 0; q0 < B; q0 += p.nbmax) {

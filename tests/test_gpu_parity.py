@@ -62,6 +62,15 @@ DENSE_CASES = [
     (777, 64, synth.BF16, 1, 777),     # k = V
     (100000, 128, synth.BF16, 2, 50),
     (262147, 96, synth.BF16, 1, 1),    # rows_per_wg > 512, k = 1
+    # batched bf16 on the matrix cores
+    (20011, 256, synth.BF16, 16, 50),  # one 16-query tile, ragged slab tail
+    (9000, 1000, synth.BF16, 33, 64),  # three query tiles padded to four, column tail
+    (2500, 40, synth.BF16, 20, 5),     # a row shorter than one 128-column step
+    (3000, 64, synth.BF16, 130, 10),   # passes of 64, 64 and 2 queries
+    (262147, 64, synth.BF16, 16, 20),  # several row blocks per slab
+    (777, 37, synth.BF16, 17, 30),     # odd row: batched on the vector path
+    (4000, 96, synth.F32, 24, 40),     # fp32 batch: vector path, passes of 8
+    (1000, 64, synth.BF16, 16, 50),    # fewer slabs than k on the matrix-core path
 ]
 
 
@@ -82,6 +91,30 @@ def test_dense_topk_matches_oracle(vie, V, d, dtype, B, k):
         ids2, lg2 = head(dev_tensor(vie, H, dtype), k)
         torch.cuda.synchronize()
         assert np.array_equal(ids2.cpu().numpy(), ids) and np.array_equal(lg2.cpu().numpy(), lg)
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_dense_clustered_top_keys(vie, B):
+    # the best rows sit next to each other, so several slabs hold many of
+    # the top k and must be read again (not just their largest key)
+    V, d, k = 20000, 128, 50
+    W = synth.make_w(V, d, synth.BF16, 77)
+    H, _ = synth.make_queries(W, synth.BF16, B, 78)
+    Wf = synth.bf16_bits_to_f32(W).copy()
+    hf = synth.bf16_bits_to_f32(H)
+    rng = np.random.default_rng(3)
+    for b in range(B):
+        rows = np.arange(1000 * b, 1000 * b + 120)
+        Wf[rows] = hf[b] * (0.02 + rng.random((120, 1)))
+    W = synth.f32_to_bf16_bits(Wf)
+    head = vie.DenseHead(dev_tensor(vie, W, synth.BF16), max_batch=B, max_k=k)
+    ids, lg = head(dev_tensor(vie, H, synth.BF16), k)
+    torch.cuda.synchronize()
+    ids, lg = ids.cpu().numpy(), lg.cpu().numpy()
+    oid, olg, osc = O.topk(W, synth.BF16, H, k)
+    parity.check_logits(W, synth.BF16, H, ids, lg, "clustered")
+    parity.check_id_sets(W, synth.BF16, H, ids, oid, osc[:, -1], what="clustered")
+    assert all(np.isin(ids[b], np.arange(1000 * b, 1000 * b + 120)).sum() >= 40 for b in range(B))
 
 
 @pytest.mark.parametrize("V,k", [(30000, 64), (200000, 100)])
@@ -142,6 +175,24 @@ def test_hnsw_matches_oracle_on_oracle_graph(vie, V, d, dtype, M, efC):
         for q in range(4):
             i1, l1 = ix.query(dev_tensor(vie, H[q:q + 1], dtype), 10, 50)
             assert np.array_equal(i1.cpu().numpy()[0], ids_b.cpu().numpy()[q])
+
+
+def test_hnsw_wide_beams_match_oracle(vie):
+    """Beams of 2048 and 4096 entries (LDS above 64 KiB) follow the oracle's
+    traversal exactly, and recall does not drop as the beam grows."""
+    V, d = 20000, 64
+    W = synth.make_w(V, d, synth.BF16, 555)
+    H, _ = synth.make_queries(W, synth.BF16, 12, 556)
+    g = O.hnsw_build(W, synth.BF16, 8, 40, 9)
+    exact, _, _ = O.topk(W, synth.BF16, H, 50)
+    rec = []
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
+        for ef in (2048, 4096):
+            ids, st, nd = _compare_hnsw(vie, ix, W, synth.BF16, g, H, 50, ef, "hnsw ef=%d" % ef)
+            rec.append(parity.recall(ids, exact))
+            say("  ef=%d recall@50=%.3f divergent=%d mean n_dist=%.0f" % (ef, rec[-1], nd, st[:, 0].mean()))
+    assert rec[1] >= rec[0] - 1e-9
 
 
 def test_hnsw_ef_at_least_v_is_exact(vie):
@@ -213,6 +264,15 @@ def test_dense_full_size_sampled(vie, name):
         lg = np.stack([g[1].cpu().numpy()[0] for g in got])
         parity.check_logits(W, wl.dtype, H, ids, lg, name)
         parity.check_id_sets(W, wl.dtype, H, ids, oid[:, :k], osc[:, k - 1], what=name)
+    # a batch of 64 (matrix-core path) whose first two queries are the ones above
+    HB, _ = wl.make_queries(W, Q=64)
+    assert np.array_equal(HB[:2], H)
+    bhead = vie.DenseHead(Wd, max_batch=64, max_k=max(wl.k))
+    k = max(wl.k)
+    ids, lg = bhead(dev_tensor(vie, HB, wl.dtype), k)
+    ids, lg = ids.cpu().numpy()[:2], lg.cpu().numpy()[:2]
+    parity.check_logits(W, wl.dtype, H, ids, lg, name + " B=64")
+    parity.check_id_sets(W, wl.dtype, H, ids, oid[:, :k], osc[:, k - 1], what=name + " B=64")
 
 
 @pytest.mark.parametrize("name", ["qwen3-0.6b", "llama3.2-1b", "gemma3-270m", "llama3.2-3b"])

@@ -15,7 +15,13 @@ the exact dense head) and the per-kernel roofline figures are reported next
 to it.  The CPU baseline is the plain-C oracle's HNSW search on the same
 graph (one thread, a bounded sample of the same queries).
 
-    python bench.py [--steps K] [--warmup W]
+The other workloads (--workload tiny | llama3.2-1b | gemma3-270m |
+llama3.2-3b) run the same protocol at their own shapes, ef and k; the Gemma
+shape adds a k sweep (20, 50, 100) and the Llama-3.2-3B shape a sweep of
+queries per call (1, 4, 16, 64: HNSW with one workgroup per query against
+the dense head, which switches to the matrix cores from 3 queries on).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
 """
 from __future__ import annotations
 
@@ -63,8 +69,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="qwen3-0.6b")
-    ap.add_argument("--ef", type=int, default=128)
-    ap.add_argument("--k", type=int, default=50)
+    ap.add_argument("--ef", type=int, default=0, help="beam width (default: the workload's middle ef)")
+    ap.add_argument("--k", type=int, default=0, help="results per query (default: the workload's middle k)")
     ap.add_argument("--queries", type=int, default=0, help="queries per step (default: the workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -90,7 +96,8 @@ def main() -> int:
         return 2
     wl = synth.WORKLOADS[args.workload]
     Q = args.queries or wl.Q
-    k, ef = args.k, args.ef
+    k = args.k or wl.k[len(wl.k) // 2]
+    ef = args.ef or wl.ef[len(wl.ef) // 2]
     s = wl.elem_bytes
     dev = torch.device("cuda:0")
 
@@ -178,8 +185,9 @@ def main() -> int:
     d_ms, d_wall, d_launch = timed(dense_step, args.steps, args.warmup)
     exact_ids = dids.cpu().numpy()
 
-    def recall(a, b):
-        return float(np.mean([len(set(x.tolist()) & set(y.tolist())) / k for x, y in zip(a, b)]))
+    def recall(a, b, kk=None):
+        kk = kk or a.shape[1]
+        return float(np.mean([len(set(x[:kk].tolist()) & set(y[:kk].tolist())) / kk for x, y in zip(a, b)]))
 
     # ---- ef sweep (same protocol; one warm-up and one timed pass each) ----
     # Beams wider than the workload's own ef values run on the first
@@ -200,6 +208,7 @@ def main() -> int:
         ms_e, _, _ = timed(step_e, 1, 1, nq)
         sweep[str(e)] = {"us_per_query": round(ms_e * 1e3 / nq, 2), "queries": nq,
                          "recall_at_k": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq]), 4),
+                         "recall_at_2": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq], 2), 4),
                          "mean_n_dist": float(st.cpu().numpy()[:nq, 0].mean())}
     # ---- all queries in one launch (one workgroup each) -------------------
     torch.cuda.synchronize()
@@ -210,6 +219,59 @@ def main() -> int:
     b.record(stream)
     torch.cuda.synchronize()
     batched_qps = Q / (a.elapsed_time(b) * 1e-3)
+
+    def per_call_us(fn, n_calls):
+        # mean event-timed duration of n_calls back-to-back calls (after one warm-up call)
+        fn(0)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for c in range(n_calls):
+            fn(c)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n_calls
+
+    # ---- k sweep (workloads quoted at several k; B = 1, first 256 queries) --
+    k_sweep = {}
+    if len(wl.k) > 1:
+        nq = min(Q, 256)
+        for kk in wl.k:
+            ik = torch.empty((nq, kk), dtype=torch.int32, device=dev)
+            lk = torch.empty((nq, kk), dtype=torch.float32, device=dev)
+            dk = torch.empty((nq, kk), dtype=torch.int32, device=dev)
+            dlk = torch.empty((nq, kk), dtype=torch.float32, device=dev)
+            hk = vie.DenseHead(Wd, max_batch=1, max_k=kk)
+            h_us_k = per_call_us(lambda c: ix.query_into(hv[c], kk, ef, ik[c:c + 1], lk[c:c + 1]), nq)
+            d_us_k = per_call_us(lambda c: vie.dense_topk_into(Wd, hv[c], kk, dk[c:c + 1], dlk[c:c + 1],
+                                                               hk.workspace), nq)
+            k_sweep[str(kk)] = {"hnsw_us_per_query": round(h_us_k, 2), "dense_us_per_query": round(d_us_k, 2),
+                                "recall_at_k": round(recall(ik.cpu().numpy(), dk.cpu().numpy()), 4),
+                                "queries": nq}
+            del hk
+
+    # ---- batch sweep (queries per call; HNSW: one workgroup per query) ----
+    b_sweep = {}
+    if len(wl.B) > 1:
+        bdense = vie.DenseHead(Wd, max_batch=max(wl.B), max_k=k)
+        for Bc in wl.B:
+            ncall = Q // Bc
+            bi = torch.empty((ncall * Bc, k), dtype=torch.int32, device=dev)
+            bl = torch.empty((ncall * Bc, k), dtype=torch.float32, device=dev)
+            di = torch.empty((ncall * Bc, k), dtype=torch.int32, device=dev)
+            dl = torch.empty((ncall * Bc, k), dtype=torch.float32, device=dev)
+            hs = [Hd[c * Bc:(c + 1) * Bc] for c in range(ncall)]
+            h_call = per_call_us(lambda c: ix.query_into(hs[c], k, ef, bi[c * Bc:(c + 1) * Bc],
+                                                         bl[c * Bc:(c + 1) * Bc]), ncall)
+            d_call = per_call_us(lambda c: vie.dense_topk_into(Wd, hs[c], k, di[c * Bc:(c + 1) * Bc],
+                                                               dl[c * Bc:(c + 1) * Bc], bdense.workspace), ncall)
+            b_sweep[str(Bc)] = {"hnsw_us_per_call": round(h_call, 2), "dense_us_per_call": round(d_call, 2),
+                                "hnsw_queries_per_s": round(Bc * 1e6 / h_call, 1),
+                                "dense_queries_per_s": round(Bc * 1e6 / d_call, 1),
+                                "dense_hbm_frac": round(wl.V * wl.d * s / (d_call * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                                "recall_at_k": round(recall(bi.cpu().numpy(), di.cpu().numpy()), 4),
+                                "calls": ncall}
+        del bdense
 
     # ---- roofline figures ----------------------------------------------------
     n_dist, n_exp = stats[:, 0].astype(np.float64), stats[:, 1].astype(np.float64)
@@ -261,9 +323,11 @@ def main() -> int:
                    "graph": {"maxlevel": info["maxlevel"], "entry": info["entry"]}},
         "hnsw": {"us_per_query": round(h_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(h_qps, 1),
                  "kernel_us": round(h_us, 2), "recall_at_k": round(recall(hnsw_ids, exact_ids), 4),
+                 "recall_at_2": round(recall(hnsw_ids, exact_ids, 2), 4),
                  "mean_n_dist": float(n_dist.mean()), "mean_n_expand": float(n_exp.mean()),
                  "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
-                 "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep},
+                 "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
+                 "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None},
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,

@@ -144,7 +144,7 @@ void vie_index_free(vie_index *index);
  * over all layers.  Needs vie_index_to_device on the current device first.
  * Limits: ef_eff <= 8192, M0 <= 256, and one workgroup's LDS must hold the
  * query, the beam twice (16 bytes + 2 flag bytes per entry), the visited
- * bitmap (V/8 bytes) and per-step lists of about 28 bytes per layer-0 slot
+ * bitmap (V/8 bytes) and per-step lists of about 20 bytes per layer-0 slot
  * (160 KiB on gfx950: ef_eff = 4096 fits next to a 262144-row bitmap).
  * Errors: VIE_EINVAL, VIE_ESTATE, VIE_EUNSUPPORTED, VIE_EHIP. */
 vie_status vie_query(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,

@@ -949,8 +949,6 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     p += (size_t)ef * 8;
     uint64_t *ckey = reinterpret_cast<uint64_t *>(p);
     p += (size_t)maxdeg * 8;
-    uint64_t *csort = reinterpret_cast<uint64_t *>(p);
-    p += (size_t)maxdeg * 8;
     int32_t *cid = reinterpret_cast<int32_t *>(p);
     p += (size_t)maxdeg * 4;
     int32_t *pfa = reinterpret_cast<int32_t *>(p);
@@ -1016,7 +1014,10 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     }
 
     // layer 0: beam of ef keys, sorted descending, with expanded flags,
-    // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...)
+    // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...).  Three
+    // workgroup barriers per expansion: after the claim, after the row
+    // scores, after the merge.  Every shared counter is reset by thread 0 in
+    // a phase where no other thread reads or updates it.
     clear_bits(vis, vwords);
     __syncthreads();
     if (tid == 0) {
@@ -1025,6 +1026,8 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         flag[0] = 0;
         sh.nbeam = 1;
         sh.first = 0;
+        sh.nnew = 0;
+        sh.second = 0xFFFFFFFFu;
     }
     __syncthreads();
     for (;;) {
@@ -1032,16 +1035,12 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         if (first >= nbeam) break;
         const int32_t c = key_id(beam[first]);
         const int32_t *lst = sh.pfa_id == c ? pfa : (sh.pfb_id == c ? pfb : nullptr);
-        __syncthreads();
         if (tid == 0) {
-            flag[first] = 1;
-            sh.nnew = 0;
-            sh.nkeep = 0;
-            sh.second = 0xFFFFFFFFu;
+            flag[first] = 1;  // read again only after the next barrier
+            sh.nkeep = 0;     // last read before the previous merge
             sh.best = 0;
         }
         ++n_expand;
-        __syncthreads();
         // claim the unseen neighbours; find the next unexpanded entry after first
         for (int t = tid; t < M0; t += NT) {
             const int32_t e = lst ? lst[t] : adj0[(int64_t)c * M0 + t];
@@ -1084,6 +1083,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             }
         }
         if (gl == 0 && gbest > worst) atomicMax(&sh.best, (unsigned long long)gbest);
+        if (tid == 0) sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
         __syncthreads();
         if (ida >= 0 && pft >= 0) pfa[pft] = pfv;
         const uint64_t bestnew = sh.best;
@@ -1094,52 +1094,47 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
                 if (t < M0) pfb[t] = glist[u];
             }
         }
-        if (tid == 0) {
-            sh.pfa_id = ida;
-            sh.pfb_id = pfb_on && bestnew != 0ull ? key_id(bestnew) : -1;
-            sh.first = 0xFFFFFFFFu;
-        }
         const int nk = (int)sh.nkeep;
-        // order the kept keys (rank sort; keys are distinct)
-        for (int j = tid; j < nk; j += NT) {
-            const uint64_t key = ckey[j];
-            int rank = 0;
-            for (int t = 0; t < nk; ++t) rank += ckey[t] > key;
-            csort[rank] = key;
-        }
-        __syncthreads();
-        // merge beam (nbeam) and csort (nk) into beam2, keep the best ef; the
-        // new first unexpanded entry is the best kept key or the old second
+        // merge the beam (nbeam, sorted) and the kept keys (nk, unordered,
+        // distinct) into beam2, keeping the best ef: a kept key lands at
+        // (kept keys above it) + (beam keys above it), a beam key at its
+        // index + (kept keys above it).  The new first unexpanded entry is
+        // the best kept key or the old second.
         const int total = min((int)nbeam + nk, ef);
         for (int j = tid; j < nk; j += NT) {
-            const uint64_t key = csort[j];
+            const uint64_t key = ckey[j];
+            int above = 0;
+            for (int t = 0; t < nk; ++t) above += ckey[t] > key;
             int lo = 0, hi = (int)nbeam;  // count beam keys > key
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
                 if (beam[mid] > key) lo = mid + 1; else hi = mid;
             }
-            const int pos = lo + j;
+            const int pos = lo + above;
             if (pos < total) {
                 beam2[pos] = key;
                 flag2[pos] = 0;
-                if (j == 0) atomicMin(&sh.first, (uint32_t)pos);
+                if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
             }
         }
         for (int i = tid; i < (int)nbeam; i += NT) {
             const uint64_t key = beam[i];
-            int lo = 0, hi = nk;  // count new keys > key
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (csort[mid] > key) lo = mid + 1; else hi = mid;
-            }
-            const int pos = lo + i;
+            int above = 0;
+            for (int t = 0; t < nk; ++t) above += ckey[t] > key;
+            const int pos = i + above;
             if (pos < total) {
                 beam2[pos] = key;
                 flag2[pos] = flag[i];
                 if (i == (int)second) atomicMin(&sh.first, (uint32_t)pos);
             }
         }
-        if (tid == 0) sh.nbeam = (uint32_t)total;
+        if (tid == 0) {
+            sh.nbeam = (uint32_t)total;
+            sh.pfa_id = ida;
+            sh.pfb_id = pfb_on && bestnew != 0ull ? key_id(bestnew) : -1;
+            sh.nnew = 0;  // read after the claim barrier only
+            sh.second = 0xFFFFFFFFu;
+        }
         __syncthreads();
         uint64_t *tb = beam;
         beam = beam2;
@@ -1372,7 +1367,7 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t maxdeg = (size_t)(M0 > M ? M0 : M);
-    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + maxdeg * (8 + 8 + 4) + (size_t)M0 * 8 + (size_t)ef_eff * 2;
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + maxdeg * (8 + 4) + (size_t)M0 * 8 + (size_t)ef_eff * 2;
     n = (n + 15) & ~(size_t)15;
     return n + (size_t)((V + 31) / 32) * 4;
 }

@@ -679,6 +679,127 @@ done:
 }
 
 /* ------------------------------------------------------------------------ */
+/* O3': layer-0 search expanding several beam entries per step               */
+/* ------------------------------------------------------------------------ */
+
+/* A variant of SEARCH-LAYER for wide hardware (it is not in either paper; the
+ * library's batched traversal follows it).  The result set R is kept sorted
+ * by (dist, id) with an "expanded" flag per entry.  Each step takes the P
+ * best unexpanded entries of R and marks them expanded; their lists are
+ * scanned in that order, each list in stored order, and every neighbour not
+ * visited yet is marked visited and its distance evaluated.  All of them are
+ * then inserted into R, which keeps its ef nearest.  The search ends when
+ * every entry of R is expanded.  With P = 1 this visits, scores and expands
+ * the same nodes as SEARCH-LAYER: an entry dropped from R is worse than all
+ * of R and would only have been popped to end the search. */
+typedef struct {
+    cand c;
+    int expanded;
+} bentry;
+
+static int by_bentry(const void *a, const void *b)
+{
+    return by_dist_asc(&((const bentry *)a)->c, &((const bentry *)b)->c);
+}
+
+static int beam_multi(searcher *s, const ograph *g, const double *q, cand ep, int ef, int P, cand *out)
+{
+    if (++s->tag == 0) {
+        memset(s->seen, 0, sizeof(uint32_t) * (size_t)s->V);
+        s->tag = 1;
+    }
+    const int cap = ef + P * g->M0 + 1;
+    bentry *R = malloc(sizeof(bentry) * (size_t)cap);
+    int *pick = malloc(sizeof(int) * (size_t)P);
+    if (!R || !pick) {
+        free(R);
+        free(pick);
+        return -1;
+    }
+    int nR = 1;
+    R[0].c = ep;
+    R[0].expanded = 0;
+    s->seen[ep.id] = s->tag;
+    for (;;) {
+        int np = 0;
+        for (int i = 0; i < nR && np < P; ++i)
+            if (!R[i].expanded) pick[np++] = i;
+        if (np == 0) break;
+        int n = nR;
+        for (int t = 0; t < np; ++t) {
+            R[pick[t]].expanded = 1;
+            s->n_expand++;
+            const int32_t *lst = olist(g, R[pick[t]].c.id, 0);
+            for (int j = 0; j < lst[0]; ++j) {
+                const int32_t e = lst[1 + j];
+                if (s->seen[e] == s->tag) continue;
+                s->seen[e] = s->tag;
+                R[n].c.dist = qdist(s, q, e);
+                R[n].c.id = e;
+                R[n].expanded = 0;
+                ++n;
+            }
+        }
+        qsort(R, (size_t)n, sizeof(bentry), by_bentry);
+        nR = n < ef ? n : ef;
+    }
+    for (int i = 0; i < nR; ++i) out[i] = R[i].c;
+    free(R);
+    free(pick);
+    return nR;
+}
+
+/* K-NN-SEARCH with the layer-0 step above (expand_width = P >= 1); the upper
+ * layers are the greedy descent of MY18 Algorithm 5.  Same outputs and
+ * return value as oracle_hnsw_search. */
+int oracle_hnsw_search_multi(const void *W, int dtype, int64_t V, int d, int M, int M0, int maxlevel,
+                             int32_t entry, const uint8_t *levels, const int32_t *adj0, const int32_t *upper_off,
+                             const int32_t *upper, const void *h, int B, int k, int ef, int expand_width,
+                             int32_t *ids, float *logits, uint32_t *stats)
+{
+    if (V < 1 || d < 1 || B < 1 || k < 1 || k > V || ef < 1 || entry < 0 || entry >= V || expand_width < 1)
+        return -1;
+    ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
+    int efe = ef > k ? ef : k;
+    searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0 };
+    cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
+    double *q = malloc(sizeof(double) * (size_t)d);
+    int rc = 0;
+    if (!g || !s.seen || !s.C || !s.R || !out || !q) { rc = -1; goto done; }
+    for (int b = 0; b < B; ++b) {
+        s.n_dist = s.n_expand = 0;
+        widen(h, dtype, d, b, q);
+        cand ep = { qdist(&s, q, entry), entry };
+        for (int lc = maxlevel; lc >= 1; --lc) {
+            int n = search_layer(&s, g, q, &ep, 1, 1, lc, out);
+            int best = 0;
+            for (int t = 1; t < n; ++t)
+                if (nearer(out[t], out[best])) best = t;
+            ep = out[best];
+        }
+        int n = beam_multi(&s, g, q, ep, efe, expand_width, out);
+        if (n < 0) { rc = -1; goto done; }
+        for (int j = 0; j < k; ++j) {
+            ids[(int64_t)b * k + j] = j < n ? out[j].id : -1;
+            logits[(int64_t)b * k + j] = j < n ? (float)(-out[j].dist) : -INFINITY;
+        }
+        if (stats) {
+            stats[2 * b] = (uint32_t)s.n_dist;
+            stats[2 * b + 1] = (uint32_t)s.n_expand;
+        }
+    }
+done:
+    ograph_free(g);
+    free(s.seen);
+    free(s.C);
+    free(s.R);
+    free(out);
+    free(q);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
 /* index file (the on-disk form of the precomputed index of Section 3)      */
 /* ------------------------------------------------------------------------ */
 

@@ -45,6 +45,9 @@ def lib() -> C.CDLL:
         L.oracle_hnsw_search.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                          i32, i32, i32, vp, vp, vp, vp]
         L.oracle_hnsw_search.restype = i32
+        L.oracle_hnsw_search_multi.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
+                                               i32, i32, i32, i32, vp, vp, vp]
+        L.oracle_hnsw_search_multi.restype = i32
         L.oracle_w_fingerprint.argtypes = [vp, i32, i64, i32]
         L.oracle_w_fingerprint.restype = u64
         L.oracle_file_write.argtypes = [C.c_char_p, i32, i64, i32, i32, i32, i32, u64, i32, i32, i64, u64,
@@ -229,6 +232,30 @@ def hnsw_search(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int, ef: 
     if rc != 0:
         raise ValueError("oracle_hnsw_search: bad arguments")
     return ids, lg, st, l0
+
+
+def hnsw_search_multi(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int, ef: int,
+                      expand_width: int, validate: bool = True):
+    """K-NN-SEARCH whose layer-0 step expands the expand_width best
+    unexpanded beam entries at once: ids [B,k], logits [B,k], stats [B,2]."""
+    W = _check_w(W, dtype)
+    h = _check_h(h, dtype, W.shape[1])
+    if validate:
+        err = check_graph(g)
+        if err:
+            raise ValueError("invalid graph: " + err)
+    B = h.shape[0]
+    ids = np.empty((B, k), np.int32)
+    lg = np.empty((B, k), np.float32)
+    st = np.empty((B, 2), np.uint32)
+    up = np.ascontiguousarray(g.upper, np.int32)
+    rc = lib().oracle_hnsw_search_multi(_p(W), dtype, W.shape[0], W.shape[1], g.M, g.M0, g.maxlevel, g.entry,
+                                        _p(np.ascontiguousarray(g.levels)), _p(np.ascontiguousarray(g.adj0)),
+                                        _p(np.ascontiguousarray(g.upper_off)), _p(up) if up.size else None,
+                                        _p(h), B, k, ef, expand_width, _p(ids), _p(lg), _p(st))
+    if rc != 0:
+        raise ValueError("oracle_hnsw_search_multi: bad arguments")
+    return ids, lg, st
 
 
 def fingerprint(W: np.ndarray, dtype: int) -> int:

@@ -291,6 +291,65 @@ def test_search_golden_chain_trace():
         assert st[0].tolist() == [nd, ne], (ef, st)
 
 
+def _tree_case():
+    lines = [l.split() for l in open(os.path.join(GOLDEN, "multi_expand_tree.txt")) if l.strip() and l[0] != "#"]
+    vals = next(l for l in lines if l[0] == "values")[1:]
+    edges = next(l for l in lines if l[0] == "edges")[1:]
+    V = len(vals)
+    W = np.array([[float(v)] for v in vals], np.float32)
+    nbr = [[] for _ in range(V)]
+    for e in edges:
+        a, b = (int(x) for x in e.split("-"))
+        nbr[a].append(b)
+        nbr[b].append(a)
+    adj0 = -np.ones((V, 3), np.int32)
+    for u in range(V):
+        s = sorted(nbr[u])
+        adj0[u, :len(s)] = s
+    g = O.Graph(V, 1, synth.F32, 2, 3, 1, 0, 0, 0, np.zeros(V, np.uint8), adj0, -np.ones(V, np.int32),
+                np.zeros((0, 2), np.int32))
+    cases = []
+    for l in lines:
+        if l[0] == "case":
+            kv = dict(x.split("=") for x in l[1:])
+            cases.append((int(kv["P"]), int(kv["ef"]), int(kv["k"]), [int(x) for x in kv["ids"].split(",")],
+                          int(kv["n_dist"]), int(kv["n_expand"])))
+    return W, g, cases
+
+
+def test_multi_expansion_golden_tree_trace():
+    W, g, cases = _tree_case()
+    assert O.check_graph(g) == ""
+    for P, ef, k, ids, nd, ne in cases:
+        got, lg, st = O.hnsw_search_multi(W, synth.F32, g, np.ones((1, 1), np.float32), k, ef, P)
+        assert got[0].tolist() == ids, (P, ef, got)
+        assert st[0].tolist() == [nd, ne], (P, ef, st)
+
+
+@pytest.mark.parametrize("seed", [4, 5])
+def test_multi_expansion_with_width_one_is_the_search(seed):
+    V, d = 1500, 16
+    W = synth.make_w(V, d, synth.BF16, 60 + seed)
+    H, _ = synth.make_queries(W, synth.BF16, 20, 70 + seed)
+    g = O.hnsw_build(W, synth.BF16, 6, 30, seed)
+    a = O.hnsw_search(W, synth.BF16, g, H, 10, 40)
+    b = O.hnsw_search_multi(W, synth.BF16, g, H, 10, 40, 1)
+    for x, y in zip(a[:3], b):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("P", [2, 3, 8])
+def test_multi_expansion_with_ef_at_least_v_is_exact(P):
+    W = synth.make_w(300, 8, synth.F32, 123)
+    W = (W / np.linalg.norm(W, axis=1, keepdims=True)).astype(np.float32)
+    g = O.hnsw_build(W, synth.F32, 5, 40, 3)
+    H, _ = synth.make_queries(W, synth.F32, 12, 124)
+    ids, lg, st = O.hnsw_search_multi(W, synth.F32, g, H, 10, 300, P)
+    oid, olg, _ = O.topk(W, synth.F32, H, 10)
+    assert np.array_equal(ids, oid)
+    assert np.array_equal(lg, olg)
+
+
 def _beam_search_reformulated(W, dtype, g, h, k, ef):
     """Independent restatement: keep one beam sorted by (dist, id) with
     'expanded' flags; repeatedly expand the best unexpanded entry, scoring all

@@ -78,6 +78,8 @@ def main() -> int:
     ap.add_argument("--sweep-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024, 2048, 4096],
                     help="extra beam widths of the ef sweep (comma separated)")
     ap.add_argument("--sweep-queries", type=int, default=128, help="queries per extra sweep point")
+    ap.add_argument("--widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[2, 4, 8],
+                    help="expansion widths of the vie_query_ex sweep (comma separated)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="finish with a device copy of this many MiB (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -232,6 +234,20 @@ def main() -> int:
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / n_calls
 
+    # ---- expansion-width sweep (vie_query_ex; B = 1, first 256 queries) ---
+    w_sweep = {}
+    for wd in args.widths:
+        nq = min(Q, 256)
+        wi = torch.empty((nq, k), dtype=torch.int32, device=dev)
+        wlg = torch.empty((nq, k), dtype=torch.float32, device=dev)
+        ws = torch.empty((nq, 2), dtype=torch.int32, device=dev)
+        w_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, wi[c:c + 1], wlg[c:c + 1], ws[c:c + 1], wd), nq)
+        wst = ws.cpu().numpy().astype(np.int64)
+        w_sweep[str(wd)] = {"us_per_query": round(w_us, 2), "queries": nq,
+                            "recall_at_k": round(recall(wi.cpu().numpy(), exact_ids[:nq]), 4),
+                            "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
+                            "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean())}
+
     # ---- k sweep (workloads quoted at several k; B = 1, first 256 queries) --
     k_sweep = {}
     if len(wl.k) > 1:
@@ -327,7 +343,7 @@ def main() -> int:
                  "mean_n_dist": float(n_dist.mean()), "mean_n_expand": float(n_exp.mean()),
                  "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
                  "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
-                 "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None},
+                 "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None},
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,

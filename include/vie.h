@@ -150,6 +150,27 @@ void vie_index_free(vie_index *index);
 vie_status vie_query(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
 
+/* Options of vie_query_ex. */
+typedef struct {
+    int32_t expand_width; /* beam entries expanded per layer-0 step, 1..8 */
+} vie_search_params;
+
+/* vie_query with a layer-0 step that expands the expand_width best
+ * unexpanded beam entries at once (their unvisited neighbours are scored
+ * together and merged into the beam, which keeps its ef_eff best; the search
+ * ends when every beam entry is expanded).  expand_width = 1 is exactly
+ * vie_query.  Wider steps trade extra distance evaluations for fewer
+ * dependent steps, which is what a GPU pays for (the paper names the
+ * sequential traversal as the obstacle to GPU execution, Section 5).  The
+ * results follow the same rule on any hardware; the test oracle implements
+ * it independently.  Limits as vie_query, and LDS must also hold about
+ * 16 bytes per claimed neighbour (expand_width * M0 of them).
+ * Errors: as vie_query; VIE_EINVAL also for params NULL or expand_width
+ * outside 1..8. */
+vie_status vie_query_ex(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                        const vie_search_params *params, int32_t *ids_dev, float *logits_dev,
+                        uint32_t *stats_dev, void *hip_stream);
+
 /* Bytes of device workspace vie_dense_topk needs for these sizes. */
 vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, size_t *bytes);
 

@@ -228,10 +228,33 @@ void vie_index_free(vie_index *ix)
     delete ix;
 }
 
+namespace {
+vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
+                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+}  // namespace
+
 vie_status vie_query(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t *ids_dev,
                      float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     g_last_error.clear();
+    return query_impl(ix, h_dev, B, k, ef, 1, ids_dev, logits_dev, stats_dev, hip_stream);
+}
+
+vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                        const vie_search_params *params, int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev,
+                        void *hip_stream)
+{
+    g_last_error.clear();
+    if (!params) return fail(VIE_EINVAL, "NULL argument");
+    if (params->expand_width < 1 || params->expand_width > 8)
+        return fail(VIE_EINVAL, "expand_width = %d outside 1..8", params->expand_width);
+    return query_impl(ix, h_dev, B, k, ef, params->expand_width, ids_dev, logits_dev, stats_dev, hip_stream);
+}
+
+namespace {
+vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
+                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream)
+{
     if (!ix || !h_dev || !ids_dev || !logits_dev) return fail(VIE_EINVAL, "NULL argument");
     const Graph &g = ix->g;
     if (vie_status s = check_k(k, g.V, B)) return s;
@@ -263,8 +286,10 @@ vie_status vie_query(const vie_index *ix, const void *h_dev, int32_t B, int32_t 
     a.ids = ids_dev;
     a.logits = logits_dev;
     a.stats = stats_dev;
+    a.width = width;
     return launch_hnsw_search(a, static_cast<hipStream_t>(hip_stream));
 }
+}  // namespace
 
 vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, size_t *bytes)
 {

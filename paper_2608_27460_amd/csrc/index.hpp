@@ -75,6 +75,7 @@ struct HnswLaunch {
     int32_t entry;
     const void *h;
     int B, k, ef_eff;
+    int width;  // beam entries expanded per layer-0 step (1 = the sequential algorithm)
     int32_t *ids;
     float *logits;
     uint32_t *stats;

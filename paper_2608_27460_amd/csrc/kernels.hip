@@ -920,6 +920,56 @@ __device__ __forceinline__ float row_dot(const char *__restrict__ W, int64_t row
     return acc;
 }
 
+// Scores the entry point, then SEARCH-LAYER with a result set of one
+// (greedy) through layers maxlevel..1; returns the key of the layer-0 entry
+// point.  cid holds at least M ids; counts go to n_dist / n_expand.
+template <int NT, int VEC, bool BF16, int G>
+__device__ uint64_t descend_upper(const char *__restrict__ W, int64_t V, int row_bytes,
+                                  const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M,
+                                  int maxlevel, int32_t entry, const char *hs, int32_t *cid, uint32_t *vis,
+                                  HnswShared &sh, uint32_t &n_dist, uint32_t &n_expand)
+{
+    constexpr int kGroups = NT / G;
+    const int tid = threadIdx.x, gl = tid % G, grp = tid / G;
+    const int vwords = (int)((V + 31) / 32);
+    if (grp == 0) {
+        const float s = row_dot<VEC, BF16, G>(W, entry, row_bytes, hs, gl);
+        if (gl == 0) sh.best = make_key(s, entry);
+    }
+    __syncthreads();
+    uint64_t cur = sh.best;
+    n_dist = 1;
+    for (int lc = maxlevel; lc >= 1; --lc) {
+        clear_bits(vis, vwords);
+        __syncthreads();
+        if (tid == 0) vis[key_id(cur) >> 5] |= 1u << (key_id(cur) & 31);
+        for (;;) {
+            const int32_t c = key_id(cur);
+            if (tid == 0) sh.nnew = 0;
+            __syncthreads();
+            ++n_expand;
+            const int32_t *lst = upper + ((int64_t)upper_off[c] + lc - 1) * M;
+            for (int t = tid; t < M; t += NT) {
+                const int32_t e = lst[t];
+                if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
+            }
+            __syncthreads();
+            const int nn = (int)sh.nnew;
+            for (int j = grp; j < nn; j += kGroups) {
+                const float s = row_dot<VEC, BF16, G>(W, cid[j], row_bytes, hs, gl);
+                if (gl == 0) atomicMax(&sh.best, (unsigned long long)make_key(s, cid[j]));
+            }
+            __syncthreads();
+            n_dist += nn;
+            const uint64_t best = sh.best;
+            __syncthreads();
+            if (best <= cur) break;
+            cur = best;
+        }
+    }
+    return cur;
+}
+
 constexpr int kPfbPerLane = 4;       // a new node's list is prefetched when M0 <= 4 * G
 constexpr int kHnswWideBatch = 256;  // batches below this get 1024-thread workgroups
 
@@ -974,44 +1024,8 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     const int grp = tid / G;
     uint32_t n_dist = 0, n_expand = 0;
 
-    // score the entry point
-    if (grp == 0) {
-        const float s = row_dot<VEC, BF16, G>(W, entry, row_bytes, hs, gl);
-        if (gl == 0) sh.best = make_key(s, entry);
-    }
-    __syncthreads();
-    uint64_t cur = sh.best;
-    n_dist = 1;
-
-    // upper layers: SEARCH-LAYER with a result set of one (greedy)
-    for (int lc = maxlevel; lc >= 1; --lc) {
-        clear_bits(vis, vwords);
-        __syncthreads();
-        if (tid == 0) vis[key_id(cur) >> 5] |= 1u << (key_id(cur) & 31);
-        for (;;) {
-            const int32_t c = key_id(cur);
-            if (tid == 0) sh.nnew = 0;
-            __syncthreads();
-            ++n_expand;
-            const int32_t *lst = upper + ((int64_t)upper_off[c] + lc - 1) * M;
-            for (int t = tid; t < M; t += NT) {
-                const int32_t e = lst[t];
-                if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
-            }
-            __syncthreads();
-            const int nn = (int)sh.nnew;
-            for (int j = grp; j < nn; j += kGroups) {
-                const float s = row_dot<VEC, BF16, G>(W, cid[j], row_bytes, hs, gl);
-                if (gl == 0) atomicMax(&sh.best, (unsigned long long)make_key(s, cid[j]));
-            }
-            __syncthreads();
-            n_dist += nn;
-            const uint64_t best = sh.best;
-            __syncthreads();
-            if (best <= cur) break;
-            cur = best;
-        }
-    }
+    uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
+                                                   vis, sh, n_dist, n_expand);
 
     // layer 0: beam of ef keys, sorted descending, with expanded flags,
     // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...).  Three
@@ -1134,6 +1148,288 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             sh.pfb_id = pfb_on && bestnew != 0ull ? key_id(bestnew) : -1;
             sh.nnew = 0;  // read after the claim barrier only
             sh.second = 0xFFFFFFFFu;
+        }
+        __syncthreads();
+        uint64_t *tb = beam;
+        beam = beam2;
+        beam2 = tb;
+        uint8_t *tf = flag;
+        flag = flag2;
+        flag2 = tf;
+    }
+
+    const int nb = (int)sh.nbeam;
+    for (int t = tid; t < k; t += NT) {
+        ids[(int64_t)q * k + t] = t < nb ? key_id(beam[t]) : -1;
+        logits[(int64_t)q * k + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
+    }
+    if (stats && tid == 0) {
+        stats[2 * q] = n_dist;
+        stats[2 * q + 1] = n_expand;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// HNSW search, several expansions per step
+// ---------------------------------------------------------------------------
+//
+// The batched traversal: every step expands the `width` best unexpanded beam
+// entries at once (their lists are claimed together, all the new rows are
+// scored in one pass, and the new keys are merged in as above).  It follows
+// the oracle's multi-expansion search exactly (width 1 is the sequential
+// algorithm), trading a few more distance evaluations for width times fewer
+// dependent steps.
+//
+// Picks: every wave finds the same picks on its own (ballots over the
+// expanded flags, from the best unexpanded entry on), so no barrier publishes
+// them; the picked entries are marked expanded when the beam is merged into
+// its other buffer.  Lists: the groups that score the best `width` new rows
+// keep those rows' lists in a small LDS cache, so the next step reads most
+// of its lists there; the rest come from HBM.  Rows: each group keeps two
+// rows' loads in flight.
+
+constexpr int kMaxWidth = 8;        // widest expansion step
+constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
+
+// <row a, h> and <row b, h> (b < 0: only a) with both rows' chunks loaded
+// before either is used.
+template <int VEC, bool BF16, int G>
+__device__ __forceinline__ void row_dot2(const char *__restrict__ W, int64_t ra, int64_t rb, int row_bytes,
+                                         const char *hs, int gl, float &sa, float &sb)
+{
+    typedef typename Vec<VEC>::T T;
+    const T *wa = reinterpret_cast<const T *>(W + ra * (int64_t)row_bytes);
+    const T *wb = reinterpret_cast<const T *>(W + (rb >= 0 ? rb : ra) * (int64_t)row_bytes);
+    const T *h = reinterpret_cast<const T *>(hs);
+    const int nchunk = row_bytes / VEC;
+    constexpr int CPL = RowCpl<BF16>::value;
+    T ba[CPL], bb[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) {
+            ba[i] = wa[c];
+            if (rb >= 0) bb[i] = wb[c];
+        }
+    }
+    float xa = 0.0f, xb = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) {
+            xa = dot_vec<VEC, BF16>(ba[i], h[c], xa);
+            if (rb >= 0) xb = dot_vec<VEC, BF16>(bb[i], h[c], xb);
+        }
+    }
+    for (int c = gl + CPL * G; c < nchunk; c += G) {
+        xa = dot_vec<VEC, BF16>(wa[c], h[c], xa);
+        if (rb >= 0) xb = dot_vec<VEC, BF16>(wb[c], h[c], xb);
+    }
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1) {
+        xa += __shfl_xor(xa, m, G);
+        xb += __shfl_xor(xb, m, G);
+    }
+    sa = xa;
+    sb = xb;
+}
+
+template <int NT, int VEC, bool BF16, int G>
+__global__ __launch_bounds__(NT) void hnsw_multi_kernel(
+    const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
+    const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
+    const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits,
+    uint32_t *__restrict__ stats)
+{
+    extern __shared__ __align__(16) char smem[];
+    __shared__ HnswShared sh;
+    __shared__ int32_t lc_id[kMaxWidth];  // nodes whose lists sit in the cache
+    constexpr int kGroups = NT / G;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int q = blockIdx.x;
+    const int hbytes = (row_bytes + 15) & ~15;
+    const int vwords = (int)((V + 31) / 32);
+    const int cap = width * M0;  // most nodes claimed in one step
+    const int nid = cap > M ? cap : M;
+    const bool cache_on = M0 <= kPfbPerLane * G;
+    // LDS carve-up (sizes mirror hnsw_multi_lds_bytes)
+    char *p = smem;
+    char *hs = p;
+    p += hbytes;
+    uint64_t *beam = reinterpret_cast<uint64_t *>(p);
+    p += (size_t)ef * 8;
+    uint64_t *beam2 = reinterpret_cast<uint64_t *>(p);
+    p += (size_t)ef * 8;
+    uint64_t *ckey = reinterpret_cast<uint64_t *>(p);
+    p += (size_t)cap * 8;
+    int32_t *cid = reinterpret_cast<int32_t *>(p);
+    p += (size_t)nid * 4;
+    int32_t *lcache = reinterpret_cast<int32_t *>(p);
+    p += (size_t)cap * 4;
+    uint8_t *flag = reinterpret_cast<uint8_t *>(p);
+    p += (size_t)ef;
+    uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
+    p += (size_t)ef;
+    uint32_t *vis = reinterpret_cast<uint32_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);
+
+    const char *h = hq + (int64_t)q * row_bytes;
+    for (int i = tid; i < hbytes; i += NT) hs[i] = i < row_bytes ? h[i] : 0;
+    if (tid == 0) sh.best = 0;
+    if (tid < kMaxWidth) lc_id[tid] = -1;
+    __syncthreads();
+
+    const int gl = tid % G;
+    const int grp = tid / G;
+    uint32_t n_dist = 0, n_expand = 0;
+    uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
+                                                   vis, sh, n_dist, n_expand);
+
+    clear_bits(vis, vwords);
+    __syncthreads();
+    if (tid == 0) {
+        vis[key_id(cur) >> 5] |= 1u << (key_id(cur) & 31);
+        beam[0] = cur;
+        flag[0] = 0;
+        sh.nbeam = 1;
+        sh.first = 0;
+        sh.nnew = 0;
+    }
+    __syncthreads();
+    for (;;) {
+        const uint32_t first = sh.first, nbeam = sh.nbeam;
+        if (first >= nbeam) break;  // no unexpanded entry (first is ~0 then)
+        // the picks (up to width unexpanded entries from `first` on) and the
+        // next unexpanded entry after them, the same in every wave
+        int pick[kMaxWidth];
+#pragma unroll
+        for (int t = 0; t < kMaxWidth; ++t) pick[t] = -1;
+        int np = 0, after = -1;
+        for (int i0 = (int)first; i0 < (int)nbeam && after < 0; i0 += kWave) {
+            uint64_t ball = __ballot(i0 + lane < (int)nbeam && !flag[i0 + lane]);
+#pragma unroll
+            for (int t = 0; t < kMaxWidth; ++t)
+                if (t < width && pick[t] < 0 && ball) {
+                    pick[t] = i0 + __ffsll((long long)ball) - 1;
+                    ball &= ball - 1;
+                    ++np;
+                }
+            if (np == width && ball && after < 0) after = i0 + __ffsll((long long)ball) - 1;
+        }
+        if (np == 0) break;
+        if (tid == 0) sh.nkeep = 0;  // last read before the previous merge
+        n_expand += np;
+        // claim the unseen neighbours of the picks (node t / M0, slot t % M0)
+        for (int t = tid; t < np * M0; t += NT) {
+            const int j = t / M0, slot = t - j * M0;
+            int pj = pick[0];
+#pragma unroll
+            for (int u = 1; u < kMaxWidth; ++u)
+                if (u == j) pj = pick[u];
+            const int32_t c = key_id(beam[pj]);
+            int src = -1;
+#pragma unroll
+            for (int u = 0; u < kMaxWidth; ++u)
+                if (u < width && lc_id[u] == c) src = u;
+            const int32_t e = src >= 0 ? lcache[src * M0 + slot] : adj0[(int64_t)c * M0 + slot];
+            if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
+        }
+        __syncthreads();
+        const int nn = (int)sh.nnew;
+        n_dist += nn;
+        const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
+        // score the new rows, two per group at a time; keep the keys that
+        // can enter the beam, and the lists of a group's first rows
+        uint64_t rk[kMultiHeld];
+        int32_t rl[kMultiHeld][kPfbPerLane];
+#pragma unroll
+        for (int r = 0; r < kMultiHeld; ++r) rk[r] = 0ull;
+        int r = 0;
+        for (int j = grp; j < nn; j += 2 * kGroups, r += 2) {
+            const int32_t ea = cid[j];
+            const int32_t eb = j + kGroups < nn ? cid[j + kGroups] : -1;
+            int32_t la[kPfbPerLane], lb[kPfbPerLane];
+            if (cache_on && r < kMultiHeld) {
+#pragma unroll
+                for (int u = 0; u < kPfbPerLane; ++u) {
+                    const int t = gl + u * G;
+                    la[u] = t < M0 ? adj0[(int64_t)ea * M0 + t] : -1;
+                    lb[u] = t < M0 && eb >= 0 ? adj0[(int64_t)eb * M0 + t] : -1;
+                }
+            }
+            float sa, sb;
+            row_dot2<VEC, BF16, G>(W, ea, eb, row_bytes, hs, gl, sa, sb);
+            const uint64_t ka = make_key(sa, ea), kb = eb >= 0 ? make_key(sb, eb) : 0ull;
+            if (gl == 0 && ka > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = ka;
+            if (gl == 0 && eb >= 0 && kb > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = kb;
+#pragma unroll
+            for (int x = 0; x + 1 < kMultiHeld; x += 2)
+                if (x == r) {
+                    rk[x] = ka > worst ? ka : 0ull;
+                    rk[x + 1] = kb > worst ? kb : 0ull;
+#pragma unroll
+                    for (int u = 0; u < kPfbPerLane; ++u) {
+                        rl[x][u] = la[u];
+                        rl[x + 1][u] = lb[u];
+                    }
+                }
+        }
+        if (tid == 0) sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
+        __syncthreads();
+        const int nk = (int)sh.nkeep;
+        // the lists of the best `width` new nodes into the cache, by rank
+        if (cache_on) {
+#pragma unroll
+            for (int x = 0; x < kMultiHeld; ++x)
+                if (rk[x] != 0ull) {
+                    int above = 0;
+                    for (int t = 0; t < nk; ++t) above += ckey[t] > rk[x];
+                    if (above < width) {
+#pragma unroll
+                        for (int u = 0; u < kPfbPerLane; ++u) {
+                            const int t = gl + u * G;
+                            if (t < M0) lcache[above * M0 + t] = rl[x][u];
+                        }
+                        if (gl == 0) lc_id[above] = key_id(rk[x]);
+                    }
+                }
+        }
+        // merge the beam and the kept keys (as in the sequential kernel); the
+        // picks are marked expanded, and the new first unexpanded entry is
+        // the best kept key or the entry after the picks
+        const int total = min((int)nbeam + nk, ef);
+        for (int j = tid; j < nk; j += NT) {
+            const uint64_t key = ckey[j];
+            int above = 0;
+            for (int t = 0; t < nk; ++t) above += ckey[t] > key;
+            int lo = 0, hi = (int)nbeam;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (beam[mid] > key) lo = mid + 1; else hi = mid;
+            }
+            const int pos = lo + above;
+            if (pos < total) {
+                beam2[pos] = key;
+                flag2[pos] = 0;
+                if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
+            }
+        }
+        for (int i = tid; i < (int)nbeam; i += NT) {
+            const uint64_t key = beam[i];
+            int above = 0;
+            for (int t = 0; t < nk; ++t) above += ckey[t] > key;
+            const int pos = i + above;
+            if (pos < total) {
+                bool picked = false;
+#pragma unroll
+                for (int u = 0; u < kMaxWidth; ++u) picked |= pick[u] == i;
+                beam2[pos] = key;
+                flag2[pos] = picked ? 1 : flag[i];
+                if (i == after) atomicMin(&sh.first, (uint32_t)pos);
+            }
+        }
+        if (tid == 0) {
+            sh.nbeam = (uint32_t)total;
+            sh.nnew = 0;  // read after the claim barrier only
         }
         __syncthreads();
         uint64_t *tb = beam;
@@ -1372,6 +1668,16 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
+size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width)
+{
+    const int row_bytes = d * elem_bytes(dtype);
+    const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
+    const size_t cap = (size_t)width * M0, nid = cap > (size_t)M ? cap : (size_t)M;
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + cap * 8 + nid * 4 + cap * 4 + (size_t)ef_eff * 2;
+    n = (n + 15) & ~(size_t)15;
+    return n + (size_t)((V + 31) / 32) * 4;
+}
+
 size_t hnsw_lds_limit()
 {
     int dev = 0, v = 0;
@@ -1385,6 +1691,18 @@ namespace {
 template <int NT, int VEC, bool BF16, int G>
 hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
 {
+    if (a.width > 1) {
+        auto kern = hnsw_multi_kernel<NT, VEC, BF16, G>;
+        if (lds > 64 * 1024) {
+            hipError_t e =
+                hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+        }
+        kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
+                                   a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h),
+                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.stats);
+        return hipGetLastError();
+    }
     auto kern = hnsw_kernel<NT, VEC, BF16, G>;
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1416,7 +1734,10 @@ hipError_t hnsw_launch_g(const HnswLaunch &a, size_t lds, hipStream_t s)
 
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
 {
-    const size_t lds = hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
+    if (a.width < 1 || a.width > kMaxWidth)
+        return fail(VIE_EUNSUPPORTED, "HNSW search: expansion width %d outside 1..%d", a.width, kMaxWidth);
+    const size_t lds = a.width > 1 ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width)
+                                   : hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
     const size_t lim = hnsw_lds_limit();
     if (lds > lim)
         return fail(VIE_EUNSUPPORTED, "HNSW search needs %zu bytes of LDS per workgroup; the device allows %zu", lds,

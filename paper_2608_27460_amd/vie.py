@@ -25,6 +25,10 @@ class VieError(RuntimeError):
         self.status = status
 
 
+class SearchParams(C.Structure):
+    _fields_ = [("expand_width", C.c_int32)]
+
+
 class BuildParams(C.Structure):
     _fields_ = [("M", C.c_int32), ("M0", C.c_int32), ("ef_construction", C.c_int32), ("n_threads", C.c_int32),
                 ("seed", C.c_uint64), ("select", C.c_int32)]
@@ -52,6 +56,7 @@ def _load() -> C.CDLL:
         "vie_index_export": (st, [vp, vp, vp, vp, vp]),
         "vie_index_free": (None, [vp]),
         "vie_query": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp]),
+        "vie_query_ex": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]),
         "vie_dense_topk_workspace": (st, [i64, i32, i32, i32, C.POINTER(sz)]),
         "vie_dense_topk": (st, [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp, sz, vp]),
         "vie_scatter": (st, [vp, vp, i32, i32, i64, vp, vp]),
@@ -162,15 +167,21 @@ class Index:
             _check(lib.vie_index_to_device(self._h, _dev_ptr(W_dev, "W_dev"), _stream(W_dev)))
         self._W_dev = W_dev
 
-    def query_into(self, h, k: int, ef: int, ids, logits, stats=None) -> None:
+    def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1) -> None:
         """HNSW top-k of h [B, d] into preallocated ids int32 [B, k], logits fp32 [B, k]
-        (and stats uint32-as-int32 [B, 2]) on the current stream."""
+        (and stats uint32-as-int32 [B, 2]) on the current stream; width > 1
+        expands that many beam entries per layer-0 step (vie_query_ex)."""
         B = h.shape[0]
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"), _dev_ptr(logits, "logits"),
-                             sp, _stream(h)))
+        if width == 1:
+            _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"),
+                                 _dev_ptr(logits, "logits"), sp, _stream(h)))
+        else:
+            prm = SearchParams(width)
+            _check(lib.vie_query_ex(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), _dev_ptr(ids, "ids"),
+                                    _dev_ptr(logits, "logits"), sp, _stream(h)))
 
-    def query(self, h, k: int, ef: int, stats: bool = False):
+    def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1):
         torch = _torch()
         if h.dim() == 1:
             h = h.unsqueeze(0)
@@ -178,7 +189,7 @@ class Index:
         ids = torch.empty((B, k), dtype=torch.int32, device=h.device)
         lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
         st = torch.empty((B, 2), dtype=torch.int32, device=h.device) if stats else None
-        self.query_into(h, k, ef, ids, lg, st)
+        self.query_into(h, k, ef, ids, lg, st, width)
         return (ids, lg, st) if stats else (ids, lg)
 
     def close(self) -> None:

@@ -177,6 +177,33 @@ def test_hnsw_matches_oracle_on_oracle_graph(vie, V, d, dtype, M, efC):
             assert np.array_equal(i1.cpu().numpy()[0], ids_b.cpu().numpy()[q])
 
 
+@pytest.mark.parametrize("width", [2, 3, 4, 8])
+def test_hnsw_multi_expansion_matches_oracle(vie, width):
+    """Several expansions per step follow the oracle's multi-expansion search
+    (same visits and counts), with the list cache and ragged picks."""
+    V, d = 6000, 96
+    W = synth.make_w(V, d, synth.BF16, 880)
+    H, _ = synth.make_queries(W, synth.BF16, 32, 881)
+    g = O.hnsw_build(W, synth.BF16, 8, 40, 5)
+    exact, _, _ = O.topk(W, synth.BF16, H, 50)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
+        for k, ef in [(10, 10), (50, 64), (50, 200)]:
+            h = dev_tensor(vie, H, synth.BF16)
+            ids, lg, st = ix.query(h, k, ef, stats=True, width=width)
+            torch.cuda.synchronize()
+            ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+            oid, olg, ost = O.hnsw_search_multi(W, synth.BF16, g, H, k, ef, width, validate=False)
+            same = np.all(st == ost, axis=1)
+            what = "multi width=%d k=%d ef=%d" % (width, k, ef)
+            parity.check_logits(W, synth.BF16, H, ids, lg, what)
+            osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
+            parity.check_id_sets(W, synth.BF16, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
+            assert int((~same).sum()) <= max(1, len(H) // 20), what
+            say("  %s recall@k=%.3f mean n_dist=%.0f n_expand=%.1f" %
+                (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
+
+
 def test_hnsw_wide_beams_match_oracle(vie):
     """Beams of 2048 and 4096 entries (LDS above 64 KiB) follow the oracle's
     traversal exactly, and recall does not drop as the beam grows."""

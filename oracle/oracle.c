@@ -800,6 +800,55 @@ done:
 }
 
 /* ------------------------------------------------------------------------ */
+/* O6: forced-inclusion tokens (Section 3)                                   */
+/* ------------------------------------------------------------------------ */
+
+/* Section 3 computes the logits of a fixed set of tokens (special tokens,
+ * punctuation, structural words) explicitly, so that they are never missing
+ * from the reconstructed logits.  For query b: the union of the search
+ * result ids_in[b][0..k) (entries < 0 ignored) and the forced ids, each id
+ * once, every logit fp32 of its exact fp64 score, ordered by (score desc,
+ * id asc); out_ids / out_logits [B][k + n] are padded with -1 / -inf.
+ * Returns 0, or -1 on bad arguments. */
+int oracle_forced_merge(const void *W, int dtype, int64_t V, int d, const void *h, int B, int k,
+                        const int32_t *ids_in, int n, const int32_t *forced, int32_t *out_ids, float *out_logits)
+{
+    if (V < 1 || d < 1 || B < 1 || k < 0 || n < 0) return -1;
+    for (int i = 0; i < n; ++i)
+        if (forced[i] < 0 || forced[i] >= V) return -1;
+    const int w = k + n;
+    scored *c = malloc(sizeof(scored) * (size_t)(w > 0 ? w : 1));
+    double *q = malloc(sizeof(double) * (size_t)d);
+    if (!c || !q) {
+        free(c);
+        free(q);
+        return -1;
+    }
+    for (int b = 0; b < B; ++b) {
+        widen(h, dtype, d, b, q);
+        int m = 0;
+        for (int j = 0; j < k + n; ++j) {
+            const int32_t id = j < k ? ids_in[(int64_t)b * k + j] : forced[j - k];
+            if (id < 0) continue;
+            int dup = 0;
+            for (int t = 0; t < m && !dup; ++t) dup = c[t].id == id;
+            if (dup) continue;
+            c[m].id = id;
+            c[m].s = dot_row(W, dtype, d, id, q);
+            ++m;
+        }
+        qsort(c, (size_t)m, sizeof(scored), by_score_desc);
+        for (int j = 0; j < w; ++j) {
+            out_ids[(int64_t)b * w + j] = j < m ? c[j].id : -1;
+            out_logits[(int64_t)b * w + j] = j < m ? (float)c[j].s : -INFINITY;
+        }
+    }
+    free(c);
+    free(q);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* index file (the on-disk form of the precomputed index of Section 3)      */
 /* ------------------------------------------------------------------------ */
 

@@ -48,6 +48,8 @@ def lib() -> C.CDLL:
         L.oracle_hnsw_search_multi.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
                                                i32, i32, i32, i32, vp, vp, vp]
         L.oracle_hnsw_search_multi.restype = i32
+        L.oracle_forced_merge.argtypes = [vp, i32, i64, i32, vp, i32, i32, vp, i32, vp, vp, vp]
+        L.oracle_forced_merge.restype = i32
         L.oracle_w_fingerprint.argtypes = [vp, i32, i64, i32]
         L.oracle_w_fingerprint.restype = u64
         L.oracle_file_write.argtypes = [C.c_char_p, i32, i64, i32, i32, i32, i32, u64, i32, i32, i64, u64,
@@ -256,6 +258,24 @@ def hnsw_search_multi(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int
     if rc != 0:
         raise ValueError("oracle_hnsw_search_multi: bad arguments")
     return ids, lg, st
+
+
+def forced_merge(W: np.ndarray, dtype: int, h: np.ndarray, ids_in: np.ndarray, forced: np.ndarray):
+    """Search results ids_in [B,k] joined with the forced ids (Section 3):
+    ids [B,k+n], logits [B,k+n] by exact score, each id once, -1/-inf padded."""
+    W = _check_w(W, dtype)
+    h = _check_h(h, dtype, W.shape[1])
+    ids_in = np.ascontiguousarray(np.atleast_2d(ids_in), np.int32)
+    forced = np.ascontiguousarray(forced, np.int32).reshape(-1)
+    B, k = ids_in.shape
+    n = forced.size
+    ids = np.empty((B, k + n), np.int32)
+    lg = np.empty((B, k + n), np.float32)
+    rc = lib().oracle_forced_merge(_p(W), dtype, W.shape[0], W.shape[1], _p(h), B, k, _p(ids_in), n,
+                                   _p(forced) if n else None, _p(ids), _p(lg))
+    if rc != 0:
+        raise ValueError("oracle_forced_merge: bad arguments")
+    return ids, lg
 
 
 def fingerprint(W: np.ndarray, dtype: int) -> int:

@@ -350,6 +350,34 @@ def test_multi_expansion_with_ef_at_least_v_is_exact(P):
     assert np.array_equal(lg, olg)
 
 
+def test_forced_merge_golden_hand_example():
+    lines = {l.split()[0]: l.split()[1:] for l in open(os.path.join(GOLDEN, "forced_hand.txt"))
+             if l.strip() and l[0] != "#"}
+    W = np.array([[float(x) for x in r.split(",")] for r in lines["rows"]], np.float32)
+    h = np.array([[float(x) for x in lines["h"][0].split(",")]], np.float32)
+    search = np.array([[int(x) for x in lines["search"][0].split(",")]], np.int32)
+    forced = np.array([int(x) for x in lines["forced"][0].split(",")], np.int32)
+    kv = dict(x.split("=") for x in lines["expect"])
+    ids, lg = O.forced_merge(W, synth.F32, h, search, forced)
+    assert ids[0].tolist() == [int(x) for x in kv["ids"].split(",")]
+    assert lg[0].tolist() == [float(x) for x in kv["logits"].split(",")]
+
+
+def test_forced_merge_special_cases():
+    W = synth.make_w(400, 16, synth.BF16, 9)
+    H, _ = synth.make_queries(W, synth.BF16, 5, 10)
+    g = O.hnsw_build(W, synth.BF16, 6, 30, 2)
+    ids, lg, _, _ = O.hnsw_search(W, synth.BF16, g, H, 10, 20)
+    # no forced ids: the search result itself
+    fi, fl = O.forced_merge(W, synth.BF16, H, ids, np.zeros(0, np.int32))
+    assert np.array_equal(fi, ids) and np.array_equal(fl, lg)
+    # every id forced: the exact order of the whole vocabulary, then k pads
+    fi, fl = O.forced_merge(W, synth.BF16, H, ids, np.arange(400, dtype=np.int32)[::-1].copy())
+    oid, olg, _ = O.topk(W, synth.BF16, H, 400)
+    assert np.array_equal(fi[:, :400], oid) and np.array_equal(fl[:, :400], olg)
+    assert np.all(fi[:, 400:] == -1) and np.all(np.isneginf(fl[:, 400:]))
+
+
 def _beam_search_reformulated(W, dtype, g, h, k, ef):
     """Independent restatement: keep one beam sorted by (dist, id) with
     'expanded' flags; repeatedly expand the best unexpanded entry, scoring all

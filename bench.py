@@ -78,6 +78,8 @@ def main() -> int:
     ap.add_argument("--sweep-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024, 2048, 4096],
                     help="extra beam widths of the ef sweep (comma separated)")
     ap.add_argument("--sweep-queries", type=int, default=128, help="queries per extra sweep point")
+    ap.add_argument("--forced", type=int, default=64,
+                    help="forced-inclusion tokens of the forced leg (ids 0..n-1 stand in for special tokens)")
     ap.add_argument("--widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[2, 4, 8],
                     help="expansion widths of the vie_query_ex sweep (comma separated)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -248,6 +250,18 @@ def main() -> int:
                             "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
                             "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean())}
 
+    # ---- forced-inclusion tokens (stand-in: the first 64 ids; B = 1) -------
+    forced = None
+    if args.forced:
+        nq = min(Q, 256)
+        fids = torch.arange(args.forced, dtype=torch.int32, device=dev)
+        fi = torch.empty((nq, k + args.forced), dtype=torch.int32, device=dev)
+        fl = torch.empty((nq, k + args.forced), dtype=torch.float32, device=dev)
+        f_us = per_call_us(lambda c: ix.query_forced_into(hv[c], k, ef, fids, fi[c:c + 1], fl[c:c + 1]), nq)
+        p_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, iv[c], lv[c]), nq)
+        forced = {"n": args.forced, "ids": "0..%d" % (args.forced - 1), "queries": nq,
+                  "us_per_query": round(f_us, 2), "search_only_us_per_query": round(p_us, 2)}
+
     # ---- k sweep (workloads quoted at several k; B = 1, first 256 queries) --
     k_sweep = {}
     if len(wl.k) > 1:
@@ -343,7 +357,8 @@ def main() -> int:
                  "mean_n_dist": float(n_dist.mean()), "mean_n_expand": float(n_exp.mean()),
                  "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
                  "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
-                 "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None},
+                 "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None,
+                 "forced": forced},
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,

@@ -171,6 +171,21 @@ vie_status vie_query_ex(const vie_index *index, const void *h_dev, int32_t B, in
                         const vie_search_params *params, int32_t *ids_dev, float *logits_dev,
                         uint32_t *stats_dev, void *hip_stream);
 
+/* vie_query_ex (params NULL: expand_width 1) followed by the forced-inclusion
+ * tokens of Section 3, whose logits are computed explicitly so that they are
+ * never missing from the reconstructed logits.  forced_dev int32[n_forced]
+ * (device; distinct ids, ids outside [0, V) are skipped) is caller owned.
+ * ids_dev / logits_dev are [B][k + n_forced]: the union of the search's
+ * top k and the forced ids, each id once, ordered by logit descending (ties:
+ * id ascending), padded with -1 / -inf where an id occurred in both.  Forced
+ * logits are computed like the search's (fp32 accumulation).
+ * Limits: 0 <= n_forced <= 1024 and as vie_query_ex.
+ * Errors: as vie_query_ex; VIE_EINVAL also for n_forced out of range or
+ * forced_dev NULL with n_forced > 0. */
+vie_status vie_query_forced(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                            const vie_search_params *params, const int32_t *forced_dev, int32_t n_forced,
+                            int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+
 /* Bytes of device workspace vie_dense_topk needs for these sizes. */
 vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, size_t *bytes);
 

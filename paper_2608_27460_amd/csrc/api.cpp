@@ -230,14 +230,15 @@ void vie_index_free(vie_index *ix)
 
 namespace {
 vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
-                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+                      const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev, float *logits_dev,
+                      uint32_t *stats_dev, void *hip_stream);
 }  // namespace
 
 vie_status vie_query(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t *ids_dev,
                      float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     g_last_error.clear();
-    return query_impl(ix, h_dev, B, k, ef, 1, ids_dev, logits_dev, stats_dev, hip_stream);
+    return query_impl(ix, h_dev, B, k, ef, 1, nullptr, 0, ids_dev, logits_dev, stats_dev, hip_stream);
 }
 
 vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
@@ -248,12 +249,28 @@ vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32
     if (!params) return fail(VIE_EINVAL, "NULL argument");
     if (params->expand_width < 1 || params->expand_width > 8)
         return fail(VIE_EINVAL, "expand_width = %d outside 1..8", params->expand_width);
-    return query_impl(ix, h_dev, B, k, ef, params->expand_width, ids_dev, logits_dev, stats_dev, hip_stream);
+    return query_impl(ix, h_dev, B, k, ef, params->expand_width, nullptr, 0, ids_dev, logits_dev, stats_dev,
+                      hip_stream);
+}
+
+vie_status vie_query_forced(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                            const vie_search_params *params, const int32_t *forced_dev, int32_t n_forced,
+                            int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream)
+{
+    g_last_error.clear();
+    const int width = params ? params->expand_width : 1;
+    if (width < 1 || width > 8) return fail(VIE_EINVAL, "expand_width = %d outside 1..8", width);
+    if (n_forced < 0 || n_forced > kMaxForced)
+        return fail(VIE_EINVAL, "n_forced = %d outside 0..%d", n_forced, kMaxForced);
+    if (n_forced > 0 && !forced_dev) return fail(VIE_EINVAL, "NULL argument");
+    return query_impl(ix, h_dev, B, k, ef, width, forced_dev, n_forced, ids_dev, logits_dev, stats_dev,
+                      hip_stream);
 }
 
 namespace {
 vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
-                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream)
+                      const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev, float *logits_dev,
+                      uint32_t *stats_dev, void *hip_stream)
 {
     if (!ix || !h_dev || !ids_dev || !logits_dev) return fail(VIE_EINVAL, "NULL argument");
     const Graph &g = ix->g;
@@ -287,7 +304,10 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
     a.logits = logits_dev;
     a.stats = stats_dev;
     a.width = width;
-    return launch_hnsw_search(a, static_cast<hipStream_t>(hip_stream));
+    a.ldo = k + n_forced;
+    hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    if (vie_status r = launch_hnsw_search(a, st)) return r;
+    return n_forced > 0 ? launch_forced(a, forced_dev, n_forced, st) : VIE_OK;
 }
 }  // namespace
 

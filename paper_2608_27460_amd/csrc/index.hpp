@@ -76,6 +76,7 @@ struct HnswLaunch {
     const void *h;
     int B, k, ef_eff;
     int width;  // beam entries expanded per layer-0 step (1 = the sequential algorithm)
+    int ldo;    // row stride of ids / logits (k, or k + forced tokens)
     int32_t *ids;
     float *logits;
     uint32_t *stats;
@@ -84,6 +85,8 @@ struct HnswLaunch {
 // VIE_EHIP for a failed launch; the detail goes to set_error().
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s);
 size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M);
+constexpr int kMaxForced = 1024;  // forced-inclusion tokens per query
+vie_status launch_forced(const HnswLaunch &a, const int32_t *forced, int n, hipStream_t s);
 size_t hnsw_lds_limit();
 
 size_t dense_workspace_bytes(int64_t V, int d, int B, int k);

@@ -977,7 +977,7 @@ template <int NT, int VEC, bool BF16, int G>
 __global__ __launch_bounds__(NT) void hnsw_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
-    const char *__restrict__ hq, int k, int ef, int32_t *__restrict__ ids, float *__restrict__ logits,
+    const char *__restrict__ hq, int k, int ef, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
     uint32_t *__restrict__ stats)
 {
     extern __shared__ __align__(16) char smem[];
@@ -1160,8 +1160,8 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 
     const int nb = (int)sh.nbeam;
     for (int t = tid; t < k; t += NT) {
-        ids[(int64_t)q * k + t] = t < nb ? key_id(beam[t]) : -1;
-        logits[(int64_t)q * k + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
+        ids[(int64_t)q * ldo + t] = t < nb ? key_id(beam[t]) : -1;
+        logits[(int64_t)q * ldo + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
     }
     if (stats && tid == 0) {
         stats[2 * q] = n_dist;
@@ -1238,7 +1238,7 @@ template <int NT, int VEC, bool BF16, int G>
 __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
-    const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits,
+    const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
     uint32_t *__restrict__ stats)
 {
     extern __shared__ __align__(16) char smem[];
@@ -1442,12 +1442,73 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
 
     const int nb = (int)sh.nbeam;
     for (int t = tid; t < k; t += NT) {
-        ids[(int64_t)q * k + t] = t < nb ? key_id(beam[t]) : -1;
-        logits[(int64_t)q * k + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
+        ids[(int64_t)q * ldo + t] = t < nb ? key_id(beam[t]) : -1;
+        logits[(int64_t)q * ldo + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
     }
     if (stats && tid == 0) {
         stats[2 * q] = n_dist;
         stats[2 * q + 1] = n_expand;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// forced-inclusion tokens (Section 3)
+// ---------------------------------------------------------------------------
+//
+// One workgroup per query: the search result (the first k entries of the
+// query's output row) and the logits of the forced ids, computed exactly
+// like the search's (G-lane row dots, fp32), are joined with each id once
+// and written back over the row (k + n entries) by rank, padded with -1 /
+// -inf.  The row is read into LDS before anything is written.
+
+constexpr int kForcedThreads = 256;
+
+template <int VEC, bool BF16, int G>
+__global__ __launch_bounds__(kForcedThreads) void forced_kernel(const char *__restrict__ W, int64_t V, int row_bytes,
+                                                                const char *__restrict__ hq,
+                                                                const int32_t *__restrict__ forced, int n, int k,
+                                                                int32_t *__restrict__ ids, float *__restrict__ logits)
+{
+    extern __shared__ __align__(16) char smem[];
+    __shared__ uint32_t s_m;
+    constexpr int kGroups = kForcedThreads / G;
+    const int tid = threadIdx.x, q = blockIdx.x;
+    const int w = k + n;
+    const int hbytes = (row_bytes + 15) & ~15;
+    char *hs = smem;
+    int32_t *sid = reinterpret_cast<int32_t *>(smem + hbytes);        // [k] search ids
+    uint64_t *keys = reinterpret_cast<uint64_t *>(smem + hbytes + (((size_t)k * 4 + 7) & ~(size_t)7));  // [k + n]
+    const char *h = hq + (int64_t)q * row_bytes;
+    for (int i = tid; i < hbytes; i += kForcedThreads) hs[i] = i < row_bytes ? h[i] : 0;
+    if (tid == 0) s_m = 0;
+    __syncthreads();
+    for (int j = tid; j < k; j += kForcedThreads) {
+        const int32_t id = ids[(int64_t)q * w + j];
+        sid[j] = id;
+        if (id >= 0) keys[atomicAdd(&s_m, 1u)] = make_key(logits[(int64_t)q * w + j], id);
+    }
+    __syncthreads();
+    const int gl = tid % G, grp = tid / G;
+    for (int i = grp; i < n; i += kGroups) {
+        const int32_t f = forced[i];
+        if (f < 0 || f >= V) continue;
+        bool dup = false;
+        for (int j = 0; j < k; ++j) dup |= sid[j] == f;
+        const float sc = row_dot<VEC, BF16, G>(W, f, row_bytes, hs, gl);
+        if (!dup && gl == 0) keys[atomicAdd(&s_m, 1u)] = make_key(sc, f);
+    }
+    __syncthreads();
+    const int m = (int)s_m;
+    for (int t = tid; t < m; t += kForcedThreads) {
+        const uint64_t key = keys[t];
+        int rank = 0;
+        for (int j = 0; j < m; ++j) rank += keys[j] > key;
+        ids[(int64_t)q * w + rank] = key_id(key);
+        logits[(int64_t)q * w + rank] = key_logit(key);
+    }
+    for (int t = m + tid; t < w; t += kForcedThreads) {
+        ids[(int64_t)q * w + t] = -1;
+        logits[(int64_t)q * w + t] = -__builtin_inff();
     }
 }
 
@@ -1700,7 +1761,7 @@ hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
         }
         kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
                                    a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h),
-                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.stats);
+                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.ldo, a.stats);
         return hipGetLastError();
     }
     auto kern = hnsw_kernel<NT, VEC, BF16, G>;
@@ -1710,7 +1771,7 @@ hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
     }
     kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
                                a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h), a.k,
-                               a.ef_eff, a.ids, a.logits, a.stats);
+                               a.ef_eff, a.ids, a.logits, a.ldo, a.stats);
     return hipGetLastError();
 }
 
@@ -1731,6 +1792,44 @@ hipError_t hnsw_launch_g(const HnswLaunch &a, size_t lds, hipStream_t s)
     return wide ? hnsw_launch<1024, VEC, BF16, 64>(a, lds, s) : hnsw_launch<256, VEC, BF16, 64>(a, lds, s);
 }
 }  // namespace
+
+namespace {
+template <int VEC, bool BF16>
+hipError_t forced_launch_g(const HnswLaunch &a, const int32_t *forced, int n, size_t lds, hipStream_t s)
+{
+    const int row_bytes = a.d * elem_bytes(a.dtype);
+    const int nchunk = row_bytes / VEC;
+    constexpr int CPL = RowCpl<BF16>::value;
+    const char *W = static_cast<const char *>(a.W);
+    const char *h = static_cast<const char *>(a.h);
+    if (nchunk <= 16 * CPL)
+        forced_kernel<VEC, BF16, 16><<<a.B, kForcedThreads, lds, s>>>(W, a.V, row_bytes, h, forced, n, a.k, a.ids,
+                                                                        a.logits);
+    else if (nchunk <= 32 * CPL)
+        forced_kernel<VEC, BF16, 32><<<a.B, kForcedThreads, lds, s>>>(W, a.V, row_bytes, h, forced, n, a.k, a.ids,
+                                                                        a.logits);
+    else
+        forced_kernel<VEC, BF16, 64><<<a.B, kForcedThreads, lds, s>>>(W, a.V, row_bytes, h, forced, n, a.k, a.ids,
+                                                                        a.logits);
+    return hipGetLastError();
+}
+}  // namespace
+
+vie_status launch_forced(const HnswLaunch &a, const int32_t *forced, int n, hipStream_t s)
+{
+    const int row_bytes = a.d * elem_bytes(a.dtype);
+    const size_t lds = (size_t)((row_bytes + 15) & ~15) + (((size_t)a.k * 4 + 7) & ~(size_t)7) +
+                       (size_t)(a.k + n) * 8;
+    if (lds > 64 * 1024) return fail(VIE_EUNSUPPORTED, "forced tokens: k + n too large for one workgroup");
+    const int vec = pick_vec(row_bytes, a.W);
+    const bool bf = a.dtype == VIE_BF16;
+    hipError_t e;
+    if (vec == 16) e = bf ? forced_launch_g<16, true>(a, forced, n, lds, s) : forced_launch_g<16, false>(a, forced, n, lds, s);
+    else if (vec == 8) e = bf ? forced_launch_g<8, true>(a, forced, n, lds, s) : forced_launch_g<8, false>(a, forced, n, lds, s);
+    else if (vec == 4) e = bf ? forced_launch_g<4, true>(a, forced, n, lds, s) : forced_launch_g<4, false>(a, forced, n, lds, s);
+    else e = forced_launch_g<2, true>(a, forced, n, lds, s);
+    return launched(e, "forced-token launch");
+}
 
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
 {

@@ -57,6 +57,7 @@ def _load() -> C.CDLL:
         "vie_index_free": (None, [vp]),
         "vie_query": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp]),
         "vie_query_ex": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]),
+        "vie_query_forced": (st, [vp, vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp]),
         "vie_dense_topk_workspace": (st, [i64, i32, i32, i32, C.POINTER(sz)]),
         "vie_dense_topk": (st, [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp, sz, vp]),
         "vie_scatter": (st, [vp, vp, i32, i32, i64, vp, vp]),
@@ -179,6 +180,17 @@ class Index:
         else:
             prm = SearchParams(width)
             _check(lib.vie_query_ex(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), _dev_ptr(ids, "ids"),
+                                    _dev_ptr(logits, "logits"), sp, _stream(h)))
+
+    def query_forced_into(self, h, k: int, ef: int, forced, ids, logits, stats=None, width: int = 1) -> None:
+        """Search plus the forced-inclusion ids (int32 device tensor [n]):
+        ids int32 [B, k + n], logits fp32 [B, k + n] (vie_query_forced)."""
+        B = h.shape[0]
+        n = int(forced.numel())
+        sp = None if stats is None else _dev_ptr(stats, "stats")
+        prm = SearchParams(width)
+        fp = _dev_ptr(forced, "forced") if n else None
+        _check(lib.vie_query_forced(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), fp, n, _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
     def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1):

@@ -204,6 +204,49 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
                 (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
 
 
+@pytest.mark.parametrize("case", ["first64", "overlap", "max", "width4", "none"])
+def test_forced_tokens_match_oracle(vie, case):
+    """Search plus forced-inclusion ids against the oracle's search joined
+    with the same ids (each id once, by exact score, -1/-inf padding)."""
+    V, d, k, ef = 5000, 64, 20, 40
+    W = synth.make_w(V, d, synth.BF16, 990)
+    H, _ = synth.make_queries(W, synth.BF16, 24, 991)
+    g = O.hnsw_build(W, synth.BF16, 8, 40, 6)
+    width = 4 if case == "width4" else 1
+    if width == 1:
+        oid, olg, ost, _ = O.hnsw_search(W, synth.BF16, g, H, k, ef, validate=False)
+    else:
+        oid, olg, ost = O.hnsw_search_multi(W, synth.BF16, g, H, k, ef, width, validate=False)
+    rng = np.random.default_rng(7)
+    if case in ("first64", "width4"):
+        forced = np.arange(64, dtype=np.int32)
+    elif case == "overlap":  # half of them are found by the search of query 0
+        forced = np.unique(np.concatenate([oid[0, :10], rng.choice(V, 30, replace=False)])).astype(np.int32)
+    elif case == "max":
+        forced = rng.choice(V, 1024, replace=False).astype(np.int32)
+    else:
+        forced = np.zeros(0, np.int32)
+    n = forced.size
+    fid, flg = O.forced_merge(W, synth.BF16, H, oid, forced)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
+        ids = torch.empty((len(H), k + n), dtype=torch.int32, device="cuda")
+        lg = torch.empty((len(H), k + n), dtype=torch.float32, device="cuda")
+        st = torch.empty((len(H), 2), dtype=torch.int32, device="cuda")
+        ix.query_forced_into(dev_tensor(vie, H, synth.BF16), k, ef, torch.from_numpy(forced).cuda(), ids, lg, st,
+                             width)
+        torch.cuda.synchronize()
+    ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+    same = np.all(st == ost, axis=1)
+    assert int((~same).sum()) <= 1, case
+    parity.check_logits(W, synth.BF16, H, ids, lg, "forced " + case)
+    osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
+    parity.check_id_sets(W, synth.BF16, H, ids, fid, osk, queries=np.nonzero(same)[0], what="forced " + case)
+    for q in np.nonzero(same)[0]:
+        assert set(forced.tolist()) <= set(ids[q].tolist()), case  # every forced id is present
+        assert (ids[q] >= 0).sum() == (fid[q] >= 0).sum(), case     # the same number of distinct ids
+
+
 def test_hnsw_wide_beams_match_oracle(vie):
     """Beams of 2048 and 4096 entries (LDS above 64 KiB) follow the oracle's
     traversal exactly, and recall does not drop as the beam grows."""

@@ -152,6 +152,10 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, None, fake, fake, None, None) == vie.EINVAL
     prm = vie.SearchParams(4)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.ESTATE
+    assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, fake, -1, fake, fake, None, None) == vie.EINVAL
+    assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, fake, 1025, fake, fake, None, None) == vie.EINVAL
+    assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, None, 5, fake, fake, None, None) == vie.EINVAL
+    assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, fake, 5, fake, fake, None, None) == vie.ESTATE
     n = C.c_size_t()
     assert L.vie_dense_topk_workspace(1000, 64, 1, 50, C.byref(n)) == vie.OK and n.value > 0
     assert L.vie_dense_topk_workspace(10, 64, 1, 50, C.byref(n)) == vie.EINVAL  # k > V

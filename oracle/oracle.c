@@ -304,12 +304,32 @@ typedef struct {
     cand *C;        /* candidate set, capacity V */
     cand *R;        /* result set W of MY18, capacity ef + 1 */
     uint64_t n_dist, n_expand;
+    /* int8 rows (O7), used only by beam_multi when approx is set */
+    const int8_t *qw;
+    const float *qscale;
+    const int8_t *qh;
+    float sh;
 } searcher;
 
 static double qdist(searcher *s, const double *q, int32_t id)
 {
     s->n_dist++;
     return -dot_row(s->W, s->dtype, s->d, id, q);
+}
+
+/* O7: approximate distance from int8 rows: the integer dot product of the
+ * quantized row and query (exact), converted to fp32 and multiplied by the
+ * row scale, then by the query scale, each product rounded to fp32. */
+static double qdist8(searcher *s, int32_t id)
+{
+    s->n_dist++;
+    const int8_t *r = s->qw + (int64_t)id * s->d;
+    int64_t acc = 0;
+    for (int j = 0; j < s->d; ++j) acc += (int64_t)r[j] * (int64_t)s->qh[j];
+    float a = (float)acc;
+    a = a * s->qscale[id];
+    a = a * s->sh;
+    return -(double)a;
 }
 
 /* SEARCH-LAYER(q, ep, ef, lc): ep[0..nep) hold entry points with their
@@ -410,7 +430,7 @@ void *oracle_hnsw_build(const void *W, int dtype, int64_t V, int d, int M, int M
     free(lv);
     obuilt *ob = calloc(1, sizeof *ob);
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0,
-                   malloc(sizeof(cand) * (size_t)V), malloc(sizeof(cand) * (size_t)(efC + 2)), 0, 0 };
+                   malloc(sizeof(cand) * (size_t)V), malloc(sizeof(cand) * (size_t)(efC + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
     int capmax = efC + M0 + M + 4; /* search result, or a selection plus an over-full list */
     cand *Wc = malloc(sizeof(cand) * (size_t)capmax);
     cand *ep = malloc(sizeof(cand) * (size_t)capmax);
@@ -640,7 +660,7 @@ int oracle_hnsw_search(const void *W, int dtype, int64_t V, int d, int M, int M0
     ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
     int efe = ef > k ? ef : k; /* ef < k is read as ef = k */
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
-                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0 };
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
     cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
     double *q = malloc(sizeof(double) * (size_t)d);
     int rc = 0;
@@ -702,7 +722,8 @@ static int by_bentry(const void *a, const void *b)
     return by_dist_asc(&((const bentry *)a)->c, &((const bentry *)b)->c);
 }
 
-static int beam_multi(searcher *s, const ograph *g, const double *q, cand ep, int ef, int P, cand *out)
+static int beam_multi(searcher *s, const ograph *g, const double *q, cand ep, int ef, int P, int approx,
+                      cand *out)
 {
     if (++s->tag == 0) {
         memset(s->seen, 0, sizeof(uint32_t) * (size_t)s->V);
@@ -734,7 +755,7 @@ static int beam_multi(searcher *s, const ograph *g, const double *q, cand ep, in
                 const int32_t e = lst[1 + j];
                 if (s->seen[e] == s->tag) continue;
                 s->seen[e] = s->tag;
-                R[n].c.dist = qdist(s, q, e);
+                R[n].c.dist = approx ? qdist8(s, e) : qdist(s, q, e);
                 R[n].c.id = e;
                 R[n].expanded = 0;
                 ++n;
@@ -762,7 +783,7 @@ int oracle_hnsw_search_multi(const void *W, int dtype, int64_t V, int d, int M, 
     ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
     int efe = ef > k ? ef : k;
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
-                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0 };
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
     cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
     double *q = malloc(sizeof(double) * (size_t)d);
     int rc = 0;
@@ -778,7 +799,7 @@ int oracle_hnsw_search_multi(const void *W, int dtype, int64_t V, int d, int M, 
                 if (nearer(out[t], out[best])) best = t;
             ep = out[best];
         }
-        int n = beam_multi(&s, g, q, ep, efe, expand_width, out);
+        int n = beam_multi(&s, g, q, ep, efe, expand_width, 0, out);
         if (n < 0) { rc = -1; goto done; }
         for (int j = 0; j < k; ++j) {
             ids[(int64_t)b * k + j] = j < n ? out[j].id : -1;
@@ -796,6 +817,106 @@ done:
     free(s.R);
     free(out);
     free(q);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* O7: int8 rows for the traversal, exact re-rank of the beam                */
+/* ------------------------------------------------------------------------ */
+
+/* Quantized data types are the paper's stated future work (Section 5).  Our
+ * definition, per vector (a row of W_out or a query) of stored values x:
+ * scale = fp32(max_j |x_j| / 127) (an fp32 division of the fp32 maximum) and
+ * q_j = rint(fp32(x_j / scale)) clamped to [-127, 127] (round half to even);
+ * a vector of zeros has scale 0 and q = 0. */
+static float quantize_vec(const void *base, int dtype, int d, int64_t row, int8_t *q)
+{
+    float mx = 0.0f;
+    for (int j = 0; j < d; ++j) {
+        const float v = fabsf((float)stored(base, dtype, row * d + j));
+        if (v > mx) mx = v;
+    }
+    const float scale = mx / 127.0f;
+    for (int j = 0; j < d; ++j) {
+        if (scale == 0.0f) {
+            q[j] = 0;
+            continue;
+        }
+        float r = rintf((float)stored(base, dtype, row * d + j) / scale);
+        if (r > 127.0f) r = 127.0f;
+        if (r < -127.0f) r = -127.0f;
+        q[j] = (int8_t)r;
+    }
+    return scale;
+}
+
+void oracle_quantize_rows(const void *W, int dtype, int64_t V, int d, int8_t *q, float *scale)
+{
+    for (int64_t i = 0; i < V; ++i) scale[i] = quantize_vec(W, dtype, d, i, q + i * d);
+}
+
+/* K-NN-SEARCH whose layer-0 step (expand_width P, as O3') scores nodes with
+ * qdist8 over the int8 rows qw / qscale (from oracle_quantize_rows) and the
+ * query quantized the same way; the upper layers use exact distances.  The
+ * layer-0 entry point is scored again with qdist8 (one more evaluation).  The
+ * final result set is then ranked by exact score and its first k returned
+ * with fp32 exact logits (the re-rank is not counted in n_dist). */
+int oracle_hnsw_search_q(const void *W, int dtype, int64_t V, int d, int M, int M0, int maxlevel, int32_t entry,
+                         const uint8_t *levels, const int32_t *adj0, const int32_t *upper_off, const int32_t *upper,
+                         const int8_t *qw, const float *qscale, const void *h, int B, int k, int ef,
+                         int expand_width, int32_t *ids, float *logits, uint32_t *stats)
+{
+    if (V < 1 || d < 1 || B < 1 || k < 1 || k > V || ef < 1 || entry < 0 || entry >= V || expand_width < 1)
+        return -1;
+    ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
+    int efe = ef > k ? ef : k;
+    searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, qw, qscale, NULL, 0.0f };
+    cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
+    scored *ex = malloc(sizeof(scored) * (size_t)(efe + 2));
+    double *q = malloc(sizeof(double) * (size_t)d);
+    int8_t *qh = malloc((size_t)d);
+    int rc = 0;
+    if (!g || !s.seen || !s.C || !s.R || !out || !ex || !q || !qh) { rc = -1; goto done; }
+    s.qh = qh;
+    for (int b = 0; b < B; ++b) {
+        s.n_dist = s.n_expand = 0;
+        widen(h, dtype, d, b, q);
+        s.sh = quantize_vec(h, dtype, d, b, qh);
+        cand ep = { qdist(&s, q, entry), entry };
+        for (int lc = maxlevel; lc >= 1; --lc) {
+            int n = search_layer(&s, g, q, &ep, 1, 1, lc, out);
+            int best = 0;
+            for (int t = 1; t < n; ++t)
+                if (nearer(out[t], out[best])) best = t;
+            ep = out[best];
+        }
+        ep.dist = qdist8(&s, ep.id);
+        int n = beam_multi(&s, g, q, ep, efe, expand_width, 1, out);
+        if (n < 0) { rc = -1; goto done; }
+        for (int t = 0; t < n; ++t) {
+            ex[t].id = out[t].id;
+            ex[t].s = dot_row(W, dtype, d, out[t].id, q);
+        }
+        qsort(ex, (size_t)n, sizeof(scored), by_score_desc);
+        for (int j = 0; j < k; ++j) {
+            ids[(int64_t)b * k + j] = j < n ? ex[j].id : -1;
+            logits[(int64_t)b * k + j] = j < n ? (float)ex[j].s : -INFINITY;
+        }
+        if (stats) {
+            stats[2 * b] = (uint32_t)s.n_dist;
+            stats[2 * b + 1] = (uint32_t)s.n_expand;
+        }
+    }
+done:
+    ograph_free(g);
+    free(s.seen);
+    free(s.C);
+    free(s.R);
+    free(out);
+    free(ex);
+    free(q);
+    free(qh);
     return rc;
 }
 

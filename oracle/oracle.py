@@ -50,6 +50,10 @@ def lib() -> C.CDLL:
         L.oracle_hnsw_search_multi.restype = i32
         L.oracle_forced_merge.argtypes = [vp, i32, i64, i32, vp, i32, i32, vp, i32, vp, vp, vp]
         L.oracle_forced_merge.restype = i32
+        L.oracle_quantize_rows.argtypes = [vp, i32, i64, i32, vp, vp]
+        L.oracle_hnsw_search_q.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                           i32, i32, i32, i32, vp, vp, vp]
+        L.oracle_hnsw_search_q.restype = i32
         L.oracle_w_fingerprint.argtypes = [vp, i32, i64, i32]
         L.oracle_w_fingerprint.restype = u64
         L.oracle_file_write.argtypes = [C.c_char_p, i32, i64, i32, i32, i32, i32, u64, i32, i32, i64, u64,
@@ -276,6 +280,42 @@ def forced_merge(W: np.ndarray, dtype: int, h: np.ndarray, ids_in: np.ndarray, f
     if rc != 0:
         raise ValueError("oracle_forced_merge: bad arguments")
     return ids, lg
+
+
+def quantize_rows(W: np.ndarray, dtype: int):
+    """int8 rows [V,d] and fp32 scales [V] (per-row symmetric, O7)."""
+    W = _check_w(W, dtype)
+    V, d = W.shape
+    q = np.empty((V, d), np.int8)
+    sc = np.empty(V, np.float32)
+    lib().oracle_quantize_rows(_p(W), dtype, V, d, _p(q), _p(sc))
+    return q, sc
+
+
+def hnsw_search_q(W: np.ndarray, dtype: int, g: Graph, qw: np.ndarray, qscale: np.ndarray, h: np.ndarray, k: int,
+                  ef: int, expand_width: int = 1, validate: bool = True):
+    """K-NN-SEARCH with int8 layer-0 distances and an exact re-rank of the
+    final beam: ids [B,k], logits [B,k], stats [B,2]."""
+    W = _check_w(W, dtype)
+    h = _check_h(h, dtype, W.shape[1])
+    if validate:
+        err = check_graph(g)
+        if err:
+            raise ValueError("invalid graph: " + err)
+    qw = np.ascontiguousarray(qw, np.int8)
+    qscale = np.ascontiguousarray(qscale, np.float32)
+    B = h.shape[0]
+    ids = np.empty((B, k), np.int32)
+    lg = np.empty((B, k), np.float32)
+    st = np.empty((B, 2), np.uint32)
+    up = np.ascontiguousarray(g.upper, np.int32)
+    rc = lib().oracle_hnsw_search_q(_p(W), dtype, W.shape[0], W.shape[1], g.M, g.M0, g.maxlevel, g.entry,
+                                    _p(np.ascontiguousarray(g.levels)), _p(np.ascontiguousarray(g.adj0)),
+                                    _p(np.ascontiguousarray(g.upper_off)), _p(up) if up.size else None, _p(qw),
+                                    _p(qscale), _p(h), B, k, ef, expand_width, _p(ids), _p(lg), _p(st))
+    if rc != 0:
+        raise ValueError("oracle_hnsw_search_q: bad arguments")
+    return ids, lg, st
 
 
 def fingerprint(W: np.ndarray, dtype: int) -> int:

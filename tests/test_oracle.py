@@ -378,6 +378,58 @@ def test_forced_merge_special_cases():
     assert np.all(fi[:, 400:] == -1) and np.all(np.isneginf(fl[:, 400:]))
 
 
+def test_int8_quantization_closed_forms():
+    rng = np.random.default_rng(3)
+    ints = rng.integers(-127, 128, size=(6, 40)).astype(np.float32)
+    ints[:, 0] = 127.0                       # max |x| = 127: scale exactly 1 (times the power of two below)
+    W = np.concatenate([ints, ints * 0.25, np.zeros((1, 40), np.float32),
+                        np.array([[127.0, 2.5, 3.5, -2.5, -3.5, 0.5] + [0.0] * 34], np.float32)])
+    q, sc = O.quantize_rows(W, synth.F32)
+    assert np.array_equal(sc[:6], np.ones(6, np.float32)) and np.array_equal(q[:6], ints.astype(np.int8))
+    assert np.array_equal(sc[6:12], np.full(6, 0.25, np.float32)) and np.array_equal(q[6:12], ints.astype(np.int8))
+    assert sc[12] == 0.0 and not q[12].any()
+    assert q[13, :6].tolist() == [127, 2, 4, -2, -4, 0]    # ties round to even
+    Wr = synth.make_w(300, 64, synth.BF16, 17)
+    q, sc = O.quantize_rows(Wr, synth.BF16)
+    x = synth.bf16_bits_to_f32(Wr).astype(np.float64)
+    err = np.abs(q.astype(np.float64) * sc[:, None] - x)
+    # half a step, plus the fp32 rounding of x / scale and of scale (each at most 127 * 2^-24 steps)
+    assert np.all(err <= sc[:, None] * (0.5 + 2 * 127 * 2.0 ** -24))
+    assert np.all(np.abs(q).max(axis=1) == 127)
+    assert np.all(np.abs(q[np.arange(300), np.abs(x).argmax(axis=1)]) == 127)
+
+
+def test_int8_search_with_exact_integer_data_is_the_multi_search():
+    # rows and query are integers with max 127: every int8 score is exact, so
+    # the traversal is the unquantized one (plus the re-scored entry point)
+    rng = np.random.default_rng(11)
+    V, d = 800, 12
+    W = rng.integers(-20, 21, size=(V, d)).astype(np.float32)
+    W[:, 0] = 127.0
+    H = rng.integers(-30, 31, size=(6, d)).astype(np.float32)
+    H[:, 1] = 127.0
+    g = O.hnsw_build(W, synth.F32, 6, 30, 4)
+    q, sc = O.quantize_rows(W, synth.F32)
+    for P in (1, 3):
+        a = O.hnsw_search_multi(W, synth.F32, g, H, 10, 30, P)
+        b = O.hnsw_search_q(W, synth.F32, g, q, sc, H, 10, 30, P)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+        assert np.array_equal(a[2][:, 0] + 1, b[2][:, 0]) and np.array_equal(a[2][:, 1], b[2][:, 1])
+
+
+@pytest.mark.parametrize("P", [1, 4])
+def test_int8_search_with_ef_at_least_v_is_exact(P):
+    W = synth.make_w(300, 8, synth.BF16, 125)
+    Wf = synth.bf16_bits_to_f32(W)
+    W = synth.f32_to_bf16_bits(Wf / np.linalg.norm(Wf, axis=1, keepdims=True))
+    g = O.hnsw_build(W, synth.BF16, 5, 40, 3)
+    H, _ = synth.make_queries(W, synth.BF16, 12, 126)
+    q, sc = O.quantize_rows(W, synth.BF16)
+    ids, lg, st = O.hnsw_search_q(W, synth.BF16, g, q, sc, H, 10, 300, P)
+    oid, olg, _ = O.topk(W, synth.BF16, H, 10)
+    assert np.array_equal(ids, oid) and np.array_equal(lg, olg)
+
+
 def _beam_search_reformulated(W, dtype, g, h, k, ef):
     """Independent restatement: keep one beam sorted by (dist, id) with
     'expanded' flags; repeatedly expand the best unexpanded entry, scoring all

@@ -78,6 +78,8 @@ def main() -> int:
     ap.add_argument("--sweep-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024, 2048, 4096],
                     help="extra beam widths of the ef sweep (comma separated)")
     ap.add_argument("--sweep-queries", type=int, default=128, help="queries per extra sweep point")
+    ap.add_argument("--int8-widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[1, 4, 8],
+                    help="expansion widths of the int8-row sweep (comma separated; empty: skip)")
     ap.add_argument("--forced", type=int, default=64,
                     help="forced-inclusion tokens of the forced leg (ids 0..n-1 stand in for special tokens)")
     ap.add_argument("--widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[2, 4, 8],
@@ -250,6 +252,27 @@ def main() -> int:
                             "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
                             "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean())}
 
+    # ---- int8 rows for layer 0, exact re-rank (B = 1, first 256 queries) ----
+    q_sweep = {}
+    if args.int8_widths and wl.d % 16 == 0:
+        qrows, qscale = vie.quantize_rows(Wd, wl.dtype)
+        ix.attach_int8(qrows, qscale)
+        for wd in args.int8_widths:
+            nq = min(Q, 256)
+            wi = torch.empty((nq, k), dtype=torch.int32, device=dev)
+            wlg = torch.empty((nq, k), dtype=torch.float32, device=dev)
+            ws = torch.empty((nq, 2), dtype=torch.int32, device=dev)
+            w_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, wi[c:c + 1], wlg[c:c + 1], ws[c:c + 1], wd,
+                                                       True), nq)
+            wst = ws.cpu().numpy().astype(np.int64)
+            q_sweep[str(wd)] = {"us_per_query": round(w_us, 2), "queries": nq,
+                                "recall_at_k": round(recall(wi.cpu().numpy(), exact_ids[:nq]), 4),
+                                "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
+                                "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean()),
+                                "row_bytes_per_query": float(wst[:, 0].mean() * wl.d)}
+        ix.attach_int8(None, None)
+        del qrows, qscale
+
     # ---- forced-inclusion tokens (stand-in: the first 64 ids; B = 1) -------
     forced = None
     if args.forced:
@@ -358,7 +381,7 @@ def main() -> int:
                  "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
                  "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
                  "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None,
-                 "forced": forced},
+                 "int8_sweep": q_sweep or None, "forced": forced},
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,

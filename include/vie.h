@@ -150,9 +150,12 @@ void vie_index_free(vie_index *index);
 vie_status vie_query(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
 
-/* Options of vie_query_ex. */
+/* Options of vie_query_ex and vie_query_forced. */
 typedef struct {
     int32_t expand_width; /* beam entries expanded per layer-0 step, 1..8 */
+    int32_t int8_rows;    /* 1: layer-0 scores from the int8 rows attached with
+                             vie_index_attach_int8, final beam re-ranked on
+                             the stored rows; 0: stored rows throughout */
 } vie_search_params;
 
 /* vie_query with a layer-0 step that expands the expand_width best
@@ -185,6 +188,27 @@ vie_status vie_query_ex(const vie_index *index, const void *h_dev, int32_t B, in
 vie_status vie_query_forced(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
                             const vie_search_params *params, const int32_t *forced_dev, int32_t n_forced,
                             int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+
+/* int8 copy of W_out for the traversal (quantized data types are the
+ * paper's future work, Section 5).  Per row: scale = max_j |w_j| / 127 as an
+ * fp32 division, q_j = rint(w_j / scale) (fp32 division, ties to even)
+ * clamped to [-127, 127]; a row of zeros gets scale 0 and q = 0.  W_dev [V][d]
+ * of dtype; q_dev int8[V][d] and scale_dev fp32[V] are caller-owned device
+ * buffers.  Enqueued on the stream.  Errors: VIE_EINVAL, VIE_EHIP. */
+vie_status vie_quantize_rows(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, int8_t *q_dev,
+                             float *scale_dev, void *hip_stream);
+
+/* Lets searches with int8_rows = 1 use q_dev / scale_dev (as written by
+ * vie_quantize_rows for the index's W_dev; borrowed, must stay allocated and
+ * unchanged while used; both NULL detaches).  With int8 rows, layer 0 is
+ * walked on int8 scores: the query is quantized by the same rule, a score is
+ * fp32(integer dot) times the row scale, times the query scale, each product
+ * rounded to fp32; the layer-0 entry point is scored again that way.  The
+ * upper layers use the stored rows, and the final beam is ranked again on
+ * the stored rows (fp32 accumulation), so returned logits are exact-path
+ * logits.  vie_index_to_device detaches.  Needs d divisible by 16.
+ * Errors: VIE_EINVAL, VIE_ESTATE (not on a device), VIE_EUNSUPPORTED. */
+vie_status vie_index_attach_int8(vie_index *index, const int8_t *q_dev, const float *scale_dev);
 
 /* Bytes of device workspace vie_dense_topk needs for these sizes. */
 vie_status vie_dense_topk_workspace(int64_t V, int32_t d, int32_t B, int32_t k, size_t *bytes);

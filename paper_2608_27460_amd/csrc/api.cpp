@@ -230,15 +230,48 @@ void vie_index_free(vie_index *ix)
 
 namespace {
 vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
-                      const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev, float *logits_dev,
-                      uint32_t *stats_dev, void *hip_stream);
+                      bool int8_rows, const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev,
+                      float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+
+vie_status check_params(const vie_search_params *params)
+{
+    if (!params) return VIE_OK;
+    if (params->expand_width < 1 || params->expand_width > 8)
+        return fail(VIE_EINVAL, "expand_width = %d outside 1..8", params->expand_width);
+    if (params->int8_rows != 0 && params->int8_rows != 1)
+        return fail(VIE_EINVAL, "int8_rows = %d is neither 0 nor 1", params->int8_rows);
+    return VIE_OK;
+}
 }  // namespace
+
+vie_status vie_quantize_rows(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, int8_t *q_dev,
+                             float *scale_dev, void *hip_stream)
+{
+    g_last_error.clear();
+    if (!W_dev || !q_dev || !scale_dev) return fail(VIE_EINVAL, "NULL argument");
+    if (dtype != VIE_F32 && dtype != VIE_BF16) return fail(VIE_EINVAL, "dtype %d", (int)dtype);
+    if (V < 1 || V >= ((int64_t)1 << 31)) return fail(VIE_EINVAL, "V = %lld", (long long)V);
+    if (d < 1 || d > kMaxD) return fail(VIE_EINVAL, "d = %d", d);
+    return launch_quantize_rows(W_dev, dtype, V, d, q_dev, scale_dev, static_cast<hipStream_t>(hip_stream));
+}
+
+vie_status vie_index_attach_int8(vie_index *ix, const int8_t *q_dev, const float *scale_dev)
+{
+    g_last_error.clear();
+    if (!ix) return fail(VIE_EINVAL, "NULL argument");
+    if ((q_dev == nullptr) != (scale_dev == nullptr)) return fail(VIE_EINVAL, "NULL argument");
+    if (ix->dev.device < 0) return fail(VIE_ESTATE, "index is not on a device (call vie_index_to_device)");
+    if (q_dev && ix->g.d % 16 != 0) return fail(VIE_EUNSUPPORTED, "int8 rows need d divisible by 16");
+    ix->dev.q8 = q_dev;
+    ix->dev.q8scale = scale_dev;
+    return VIE_OK;
+}
 
 vie_status vie_query(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t *ids_dev,
                      float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     g_last_error.clear();
-    return query_impl(ix, h_dev, B, k, ef, 1, nullptr, 0, ids_dev, logits_dev, stats_dev, hip_stream);
+    return query_impl(ix, h_dev, B, k, ef, 1, false, nullptr, 0, ids_dev, logits_dev, stats_dev, hip_stream);
 }
 
 vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
@@ -247,10 +280,9 @@ vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32
 {
     g_last_error.clear();
     if (!params) return fail(VIE_EINVAL, "NULL argument");
-    if (params->expand_width < 1 || params->expand_width > 8)
-        return fail(VIE_EINVAL, "expand_width = %d outside 1..8", params->expand_width);
-    return query_impl(ix, h_dev, B, k, ef, params->expand_width, nullptr, 0, ids_dev, logits_dev, stats_dev,
-                      hip_stream);
+    if (vie_status r = check_params(params)) return r;
+    return query_impl(ix, h_dev, B, k, ef, params->expand_width, params->int8_rows != 0, nullptr, 0, ids_dev,
+                      logits_dev, stats_dev, hip_stream);
 }
 
 vie_status vie_query_forced(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
@@ -258,19 +290,20 @@ vie_status vie_query_forced(const vie_index *ix, const void *h_dev, int32_t B, i
                             int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     g_last_error.clear();
+    if (vie_status r = check_params(params)) return r;
     const int width = params ? params->expand_width : 1;
-    if (width < 1 || width > 8) return fail(VIE_EINVAL, "expand_width = %d outside 1..8", width);
+    const bool int8_rows = params && params->int8_rows != 0;
     if (n_forced < 0 || n_forced > kMaxForced)
         return fail(VIE_EINVAL, "n_forced = %d outside 0..%d", n_forced, kMaxForced);
     if (n_forced > 0 && !forced_dev) return fail(VIE_EINVAL, "NULL argument");
-    return query_impl(ix, h_dev, B, k, ef, width, forced_dev, n_forced, ids_dev, logits_dev, stats_dev,
+    return query_impl(ix, h_dev, B, k, ef, width, int8_rows, forced_dev, n_forced, ids_dev, logits_dev, stats_dev,
                       hip_stream);
 }
 
 namespace {
 vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
-                      const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev, float *logits_dev,
-                      uint32_t *stats_dev, void *hip_stream)
+                      bool int8_rows, const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev,
+                      float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     if (!ix || !h_dev || !ids_dev || !logits_dev) return fail(VIE_EINVAL, "NULL argument");
     const Graph &g = ix->g;
@@ -305,6 +338,11 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
     a.stats = stats_dev;
     a.width = width;
     a.ldo = k + n_forced;
+    if (int8_rows) {
+        if (!ix->dev.q8) return fail(VIE_ESTATE, "no int8 rows attached (call vie_index_attach_int8)");
+        a.q8 = ix->dev.q8;
+        a.q8scale = ix->dev.q8scale;
+    }
     hipStream_t st = static_cast<hipStream_t>(hip_stream);
     if (vie_status r = launch_hnsw_search(a, st)) return r;
     return n_forced > 0 ? launch_forced(a, forced_dev, n_forced, st) : VIE_OK;

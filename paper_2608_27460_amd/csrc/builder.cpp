@@ -365,6 +365,10 @@ struct Worker {
                 const int32_t e = s.id;
                 std::lock_guard<std::mutex> g(b.locks[e]);
                 int32_t *el = b.list(e, lc);
+                // a concurrent insertion of e may have listed i already
+                bool present = false;
+                for (int u = 0; u < el[0]; ++u) present |= el[1 + u] == i;
+                if (present) continue;
                 el[1 + el[0]] = i;
                 el[0]++;
                 if (el[0] > cap) {

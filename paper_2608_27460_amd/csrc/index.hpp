@@ -45,6 +45,8 @@ struct DeviceGraph {
     int32_t *adj0 = nullptr;
     int32_t *upper_off = nullptr;
     int32_t *upper = nullptr;
+    const int8_t *q8 = nullptr;     // borrowed int8 rows [V][d] (vie_index_attach_int8)
+    const float *q8scale = nullptr; // borrowed row scales [V]
 };
 
 // Thread-local error detail returned by vie_last_error().
@@ -77,6 +79,8 @@ struct HnswLaunch {
     int B, k, ef_eff;
     int width;  // beam entries expanded per layer-0 step (1 = the sequential algorithm)
     int ldo;    // row stride of ids / logits (k, or k + forced tokens)
+    const int8_t *q8 = nullptr;      // int8 rows for layer-0 scores (nullptr: exact rows)
+    const float *q8scale = nullptr;
     int32_t *ids;
     float *logits;
     uint32_t *stats;
@@ -86,6 +90,7 @@ struct HnswLaunch {
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s);
 size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M);
 constexpr int kMaxForced = 1024;  // forced-inclusion tokens per query
+vie_status launch_quantize_rows(const void *W, int dtype, int64_t V, int d, int8_t *q, float *scale, hipStream_t s);
 vie_status launch_forced(const HnswLaunch &a, const int32_t *forced, int n, hipStream_t s);
 size_t hnsw_lds_limit();
 

@@ -843,6 +843,48 @@ __global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t
 }
 
 // ---------------------------------------------------------------------------
+// int8 rows
+// ---------------------------------------------------------------------------
+//
+// Quantized storage is the paper's future work (Section 5).  Per vector (a
+// row of W_out, or a query inside the search): scale = max |x| / 127 as an
+// fp32 division, q = rint(x / scale) (fp32 division, ties to even) clamped to
+// [-127, 127]; a vector of zeros has scale 0 and q = 0.  One wave per row.
+
+constexpr int kQuantWaves = 4;
+
+template <bool BF16>
+__device__ __forceinline__ float stored_at(const void *base, int64_t i)
+{
+    if constexpr (BF16) return __uint_as_float((uint32_t) static_cast<const uint16_t *>(base)[i] << 16);
+    else return static_cast<const float *>(base)[i];
+}
+
+__device__ __forceinline__ int8_t quantize_one(float x, float scale)
+{
+    if (scale == 0.0f) return 0;
+    const float r = rintf(__fdiv_rn(x, scale));
+    return (int8_t)fminf(fmaxf(r, -127.0f), 127.0f);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kQuantWaves *kWave) void quantize_kernel(const void *__restrict__ W, int64_t V, int d,
+                                                                      int8_t *__restrict__ q,
+                                                                      float *__restrict__ scale)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t row = (int64_t)blockIdx.x * kQuantWaves + threadIdx.x / kWave;
+    if (row >= V) return;
+    float mx = 0.0f;
+    for (int j = lane; j < d; j += kWave) mx = fmaxf(mx, fabsf(stored_at<BF16>(W, row * d + j)));
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    const float sc = __fdiv_rn(mx, 127.0f);
+    for (int j = lane; j < d; j += kWave) q[row * d + j] = quantize_one(stored_at<BF16>(W, row * d + j), sc);
+    if (lane == 0) scale[row] = sc;
+}
+
+// ---------------------------------------------------------------------------
 // HNSW search, one workgroup per query
 // ---------------------------------------------------------------------------
 //
@@ -1234,16 +1276,86 @@ __device__ __forceinline__ void row_dot2(const char *__restrict__ W, int64_t ra,
     sb = xb;
 }
 
-template <int NT, int VEC, bool BF16, int G>
+// Integer <q_a, hq> and <q_b, hq> over int8 rows of d bytes (d % 16 == 0;
+// b < 0: only a), both rows' chunks loaded before either is used.
+template <int G>
+__device__ __forceinline__ void row_dot2_q8(const int8_t *__restrict__ Q, int64_t ra, int64_t rb, int d,
+                                            const int8_t *hq, int gl, int &ia, int &ib)
+{
+    const u32x4 *qa = reinterpret_cast<const u32x4 *>(Q + ra * (int64_t)d);
+    const u32x4 *qb = reinterpret_cast<const u32x4 *>(Q + (rb >= 0 ? rb : ra) * (int64_t)d);
+    const u32x4 *h = reinterpret_cast<const u32x4 *>(hq);
+    const int nchunk = d / 16;
+    constexpr int CPL = 8;
+    u32x4 ba[CPL], bb[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) {
+            ba[i] = qa[c];
+            if (rb >= 0) bb[i] = qb[c];
+        }
+    }
+    int xa = 0, xb = 0;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) {
+            const u32x4 hv = h[c];
+            xa = __builtin_amdgcn_sdot4((int)ba[i].x, (int)hv.x, xa, false);
+            xa = __builtin_amdgcn_sdot4((int)ba[i].y, (int)hv.y, xa, false);
+            xa = __builtin_amdgcn_sdot4((int)ba[i].z, (int)hv.z, xa, false);
+            xa = __builtin_amdgcn_sdot4((int)ba[i].w, (int)hv.w, xa, false);
+            if (rb >= 0) {
+                xb = __builtin_amdgcn_sdot4((int)bb[i].x, (int)hv.x, xb, false);
+                xb = __builtin_amdgcn_sdot4((int)bb[i].y, (int)hv.y, xb, false);
+                xb = __builtin_amdgcn_sdot4((int)bb[i].z, (int)hv.z, xb, false);
+                xb = __builtin_amdgcn_sdot4((int)bb[i].w, (int)hv.w, xb, false);
+            }
+        }
+    }
+    for (int c = gl + CPL * G; c < nchunk; c += G) {
+        const u32x4 hv = h[c], wa = qa[c];
+        xa = __builtin_amdgcn_sdot4((int)wa.x, (int)hv.x, xa, false);
+        xa = __builtin_amdgcn_sdot4((int)wa.y, (int)hv.y, xa, false);
+        xa = __builtin_amdgcn_sdot4((int)wa.z, (int)hv.z, xa, false);
+        xa = __builtin_amdgcn_sdot4((int)wa.w, (int)hv.w, xa, false);
+        if (rb >= 0) {
+            const u32x4 wb = qb[c];
+            xb = __builtin_amdgcn_sdot4((int)wb.x, (int)hv.x, xb, false);
+            xb = __builtin_amdgcn_sdot4((int)wb.y, (int)hv.y, xb, false);
+            xb = __builtin_amdgcn_sdot4((int)wb.z, (int)hv.z, xb, false);
+            xb = __builtin_amdgcn_sdot4((int)wb.w, (int)hv.w, xb, false);
+        }
+    }
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1) {
+        xa += __shfl_xor(xa, m, G);
+        xb += __shfl_xor(xb, m, G);
+    }
+    ia = xa;
+    ib = xb;
+}
+
+// Layer-0 score from int8 rows: fp32(integer dot) * row scale * query scale,
+// each product rounded to fp32 (no fused operations).
+__device__ __forceinline__ float q8_score(int acc, float row_scale, float query_scale)
+{
+    const float a = __fmul_rn((float)acc, row_scale);
+    return __fmul_rn(a, query_scale);
+}
+
+template <int NT, int VEC, bool BF16, int G, bool Q8>
 __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
     const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
-    uint32_t *__restrict__ stats)
+    uint32_t *__restrict__ stats, const int8_t *__restrict__ q8, const float *__restrict__ q8scale)
 {
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
     __shared__ int32_t lc_id[kMaxWidth];  // nodes whose lists sit in the cache
+    __shared__ uint32_t s_hmax;           // Q8: bits of max |h|
     constexpr int kGroups = NT / G;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int q = blockIdx.x;
@@ -1252,6 +1364,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int cap = width * M0;  // most nodes claimed in one step
     const int nid = cap > M ? cap : M;
     const bool cache_on = M0 <= kPfbPerLane * G;
+    const int d = row_bytes / (BF16 ? 2 : 4);
+    const int d8 = Q8 ? (d + 15) & ~15 : 0;
     // LDS carve-up (sizes mirror hnsw_multi_lds_bytes)
     char *p = smem;
     char *hs = p;
@@ -1270,13 +1384,26 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)ef;
     uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
     p += (size_t)ef;
+    int8_t *hq8 = reinterpret_cast<int8_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);  // Q8: the int8 query
+    p = reinterpret_cast<char *>(hq8) + d8;
     uint32_t *vis = reinterpret_cast<uint32_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);
 
     const char *h = hq + (int64_t)q * row_bytes;
     for (int i = tid; i < hbytes; i += NT) hs[i] = i < row_bytes ? h[i] : 0;
-    if (tid == 0) sh.best = 0;
+    if (tid == 0) {
+        sh.best = 0;
+        s_hmax = 0;
+    }
     if (tid < kMaxWidth) lc_id[tid] = -1;
     __syncthreads();
+    float hscale = 0.0f;
+    if constexpr (Q8) {  // the query quantized like the rows
+        for (int j = tid; j < d; j += NT) atomicMax(&s_hmax, __float_as_uint(fabsf(stored_at<BF16>(hs, j))));
+        __syncthreads();
+        hscale = __fdiv_rn(__uint_as_float(s_hmax), 127.0f);
+        for (int j = tid; j < d8; j += NT) hq8[j] = j < d ? quantize_one(stored_at<BF16>(hs, j), hscale) : 0;
+        __syncthreads();
+    }
 
     const int gl = tid % G;
     const int grp = tid / G;
@@ -1284,6 +1411,16 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
                                                    vis, sh, n_dist, n_expand);
 
+    if constexpr (Q8) {  // the layer-0 entry point scored again on its int8 row
+        if (grp == 0) {
+            int ia, ib;
+            row_dot2_q8<G>(q8, key_id(cur), -1, d, hq8, gl, ia, ib);
+            if (gl == 0) sh.best = make_key(q8_score(ia, q8scale[key_id(cur)], hscale), key_id(cur));
+        }
+        __syncthreads();
+        cur = sh.best;
+        ++n_dist;
+    }
     clear_bits(vis, vwords);
     __syncthreads();
     if (tid == 0) {
@@ -1357,7 +1494,15 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 }
             }
             float sa, sb;
-            row_dot2<VEC, BF16, G>(W, ea, eb, row_bytes, hs, gl, sa, sb);
+            if constexpr (Q8) {
+                const float ca = q8scale[ea], cb = eb >= 0 ? q8scale[eb] : 0.0f;
+                int ia, ib;
+                row_dot2_q8<G>(q8, ea, eb, d, hq8, gl, ia, ib);
+                sa = q8_score(ia, ca, hscale);
+                sb = q8_score(ib, cb, hscale);
+            } else {
+                row_dot2<VEC, BF16, G>(W, ea, eb, row_bytes, hs, gl, sa, sb);
+            }
             const uint64_t ka = make_key(sa, ea), kb = eb >= 0 ? make_key(sb, eb) : 0ull;
             if (gl == 0 && ka > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = ka;
             if (gl == 0 && eb >= 0 && kb > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = kb;
@@ -1441,9 +1586,32 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     }
 
     const int nb = (int)sh.nbeam;
-    for (int t = tid; t < k; t += NT) {
-        ids[(int64_t)q * ldo + t] = t < nb ? key_id(beam[t]) : -1;
-        logits[(int64_t)q * ldo + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
+    if constexpr (Q8) {
+        // exact re-rank of the final beam: exact keys into beam2, then by rank
+        for (int j = grp; j < nb; j += kGroups) {
+            const int32_t e = key_id(beam[j]);
+            const float sc = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
+            if (gl == 0) beam2[j] = make_key(sc, e);
+        }
+        __syncthreads();
+        for (int t = tid; t < nb; t += NT) {
+            const uint64_t key = beam2[t];
+            int rank = 0;
+            for (int j = 0; j < nb; ++j) rank += beam2[j] > key;
+            if (rank < k) {
+                ids[(int64_t)q * ldo + rank] = key_id(key);
+                logits[(int64_t)q * ldo + rank] = key_logit(key);
+            }
+        }
+        for (int t = nb + tid; t < k; t += NT) {
+            ids[(int64_t)q * ldo + t] = -1;
+            logits[(int64_t)q * ldo + t] = -__builtin_inff();
+        }
+    } else {
+        for (int t = tid; t < k; t += NT) {
+            ids[(int64_t)q * ldo + t] = t < nb ? key_id(beam[t]) : -1;
+            logits[(int64_t)q * ldo + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
+        }
     }
     if (stats && tid == 0) {
         stats[2 * q] = n_dist;
@@ -1729,13 +1897,14 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
-size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width)
+size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width, bool q8)
 {
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t cap = (size_t)width * M0, nid = cap > (size_t)M ? cap : (size_t)M;
     size_t n = hbytes + (size_t)ef_eff * 8 * 2 + cap * 8 + nid * 4 + cap * 4 + (size_t)ef_eff * 2;
     n = (n + 15) & ~(size_t)15;
+    if (q8) n += (size_t)((d + 15) & ~15);
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
@@ -1752,8 +1921,8 @@ namespace {
 template <int NT, int VEC, bool BF16, int G>
 hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
 {
-    if (a.width > 1) {
-        auto kern = hnsw_multi_kernel<NT, VEC, BF16, G>;
+    if (a.width > 1 || a.q8) {
+        auto kern = a.q8 ? hnsw_multi_kernel<NT, VEC, BF16, G, true> : hnsw_multi_kernel<NT, VEC, BF16, G, false>;
         if (lds > 64 * 1024) {
             hipError_t e =
                 hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1761,7 +1930,7 @@ hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
         }
         kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
                                    a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h),
-                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.ldo, a.stats);
+                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.ldo, a.stats, a.q8, a.q8scale);
         return hipGetLastError();
     }
     auto kern = hnsw_kernel<NT, VEC, BF16, G>;
@@ -1831,17 +2000,27 @@ vie_status launch_forced(const HnswLaunch &a, const int32_t *forced, int n, hipS
     return launched(e, "forced-token launch");
 }
 
+vie_status launch_quantize_rows(const void *W, int dtype, int64_t V, int d, int8_t *q, float *scale, hipStream_t s)
+{
+    const unsigned grid = (unsigned)((V + kQuantWaves - 1) / kQuantWaves);
+    if (dtype == VIE_BF16) quantize_kernel<true><<<grid, kQuantWaves * kWave, 0, s>>>(W, V, d, q, scale);
+    else quantize_kernel<false><<<grid, kQuantWaves * kWave, 0, s>>>(W, V, d, q, scale);
+    return launched(hipGetLastError(), "row quantization launch");
+}
+
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
 {
     if (a.width < 1 || a.width > kMaxWidth)
         return fail(VIE_EUNSUPPORTED, "HNSW search: expansion width %d outside 1..%d", a.width, kMaxWidth);
-    const size_t lds = a.width > 1 ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width)
-                                   : hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
+    const bool multi = a.width > 1 || a.q8;
+    const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8)
+                             : hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
     const size_t lim = hnsw_lds_limit();
     if (lds > lim)
         return fail(VIE_EUNSUPPORTED, "HNSW search needs %zu bytes of LDS per workgroup; the device allows %zu", lds,
                     lim);
     if (a.M0 > 256 || a.M > 256) return fail(VIE_EUNSUPPORTED, "HNSW search: degree caps above 256");
+    if (a.q8 && a.d % 16 != 0) return fail(VIE_EUNSUPPORTED, "int8 rows need d divisible by 16 (d = %d)", a.d);
     const int row_bytes = a.d * elem_bytes(a.dtype);
     const int vec = pick_vec(row_bytes, a.W);
     const bool bf = a.dtype == VIE_BF16;

@@ -26,7 +26,7 @@ class VieError(RuntimeError):
 
 
 class SearchParams(C.Structure):
-    _fields_ = [("expand_width", C.c_int32)]
+    _fields_ = [("expand_width", C.c_int32), ("int8_rows", C.c_int32)]
 
 
 class BuildParams(C.Structure):
@@ -58,6 +58,8 @@ def _load() -> C.CDLL:
         "vie_query": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp]),
         "vie_query_ex": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]),
         "vie_query_forced": (st, [vp, vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp]),
+        "vie_quantize_rows": (st, [vp, i32, i64, i32, vp, vp, vp]),
+        "vie_index_attach_int8": (st, [vp, vp, vp]),
         "vie_dense_topk_workspace": (st, [i64, i32, i32, i32, C.POINTER(sz)]),
         "vie_dense_topk": (st, [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp, sz, vp]),
         "vie_scatter": (st, [vp, vp, i32, i32, i64, vp, vp]),
@@ -167,33 +169,45 @@ class Index:
         with torch.cuda.device(W_dev.device):
             _check(lib.vie_index_to_device(self._h, _dev_ptr(W_dev, "W_dev"), _stream(W_dev)))
         self._W_dev = W_dev
+        self._q8 = None  # the library detaches int8 rows on every move
 
-    def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1) -> None:
+    def attach_int8(self, q, scale) -> None:
+        """Layer-0 scores from these int8 rows (see quantize_rows); None detaches."""
+        if q is None:
+            _check(lib.vie_index_attach_int8(self._h, None, None))
+            self._q8 = None
+            return
+        _check(lib.vie_index_attach_int8(self._h, _dev_ptr(q, "q"), _dev_ptr(scale, "scale")))
+        self._q8 = (q, scale)
+
+    def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1, int8: bool = False) -> None:
         """HNSW top-k of h [B, d] into preallocated ids int32 [B, k], logits fp32 [B, k]
         (and stats uint32-as-int32 [B, 2]) on the current stream; width > 1
-        expands that many beam entries per layer-0 step (vie_query_ex)."""
+        expands that many beam entries per layer-0 step, int8 walks layer 0 on
+        the attached int8 rows (vie_query_ex)."""
         B = h.shape[0]
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        if width == 1:
+        if width == 1 and not int8:
             _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"),
                                  _dev_ptr(logits, "logits"), sp, _stream(h)))
         else:
-            prm = SearchParams(width)
+            prm = SearchParams(width, int(int8))
             _check(lib.vie_query_ex(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
-    def query_forced_into(self, h, k: int, ef: int, forced, ids, logits, stats=None, width: int = 1) -> None:
+    def query_forced_into(self, h, k: int, ef: int, forced, ids, logits, stats=None, width: int = 1,
+                          int8: bool = False) -> None:
         """Search plus the forced-inclusion ids (int32 device tensor [n]):
         ids int32 [B, k + n], logits fp32 [B, k + n] (vie_query_forced)."""
         B = h.shape[0]
         n = int(forced.numel())
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        prm = SearchParams(width)
+        prm = SearchParams(width, int(int8))
         fp = _dev_ptr(forced, "forced") if n else None
         _check(lib.vie_query_forced(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), fp, n, _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
-    def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1):
+    def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1, int8: bool = False):
         torch = _torch()
         if h.dim() == 1:
             h = h.unsqueeze(0)
@@ -201,7 +215,7 @@ class Index:
         ids = torch.empty((B, k), dtype=torch.int32, device=h.device)
         lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
         st = torch.empty((B, 2), dtype=torch.int32, device=h.device) if stats else None
-        self.query_into(h, k, ef, ids, lg, st, width)
+        self.query_into(h, k, ef, ids, lg, st, width, int8)
         return (ids, lg, st) if stats else (ids, lg)
 
     def close(self) -> None:
@@ -214,6 +228,16 @@ class Index:
             self.close()
         except Exception:
             pass
+
+
+def quantize_rows(W, dtype: int):
+    """int8 rows [V, d] and fp32 scales [V] of the device matrix W (vie_quantize_rows)."""
+    torch = _torch()
+    V, d = W.shape
+    q = torch.empty((V, d), dtype=torch.int8, device=W.device)
+    sc = torch.empty((V,), dtype=torch.float32, device=W.device)
+    _check(lib.vie_quantize_rows(_dev_ptr(W, "W"), dtype, V, d, _dev_ptr(q, "q"), _dev_ptr(sc, "scale"), _stream(W)))
+    return q, sc
 
 
 def dense_topk_workspace_bytes(V: int, d: int, B: int, k: int) -> int:

@@ -247,6 +247,47 @@ def test_forced_tokens_match_oracle(vie, case):
         assert (ids[q] >= 0).sum() == (fid[q] >= 0).sum(), case     # the same number of distinct ids
 
 
+@pytest.mark.parametrize("V,d,dtype", [(3000, 64, synth.BF16), (1000, 48, synth.F32), (500, 3072, synth.BF16),
+                                       (777, 256, synth.F32)])
+def test_int8_rows_bitwise(vie, V, d, dtype):
+    W = synth.make_w(V, d, dtype, 400 + d)
+    if dtype == synth.F32:
+        W[::97] = 0.0  # rows of zeros: scale 0
+    q, sc = vie.quantize_rows(dev_tensor(vie, W, dtype), dtype)
+    torch.cuda.synchronize()
+    oq, osc = O.quantize_rows(W, dtype)
+    assert np.array_equal(q.cpu().numpy(), oq)
+    assert np.array_equal(sc.cpu().numpy().view(np.uint32), osc.view(np.uint32))
+
+
+@pytest.mark.parametrize("width", [1, 4])
+def test_int8_search_matches_oracle(vie, width):
+    """Layer 0 on int8 scores (integer dot, fp32 scale products) walks exactly
+    the oracle's path; the re-ranked result matches within the tolerances."""
+    V, d = 6000, 128
+    W = synth.make_w(V, d, synth.BF16, 1234)
+    H, _ = synth.make_queries(W, synth.BF16, 32, 1235)
+    g = O.hnsw_build(W, synth.BF16, 8, 40, 8)
+    oq, osc = O.quantize_rows(W, synth.BF16)
+    exact, _, _ = O.topk(W, synth.BF16, H, 50)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
+        q, sc = vie.quantize_rows(ix._W_dev, synth.BF16)
+        ix.attach_int8(q, sc)
+        for k, ef in [(10, 40), (50, 100)]:
+            ids, lg, st = ix.query(dev_tensor(vie, H, synth.BF16), k, ef, stats=True, width=width, int8=True)
+            torch.cuda.synchronize()
+            ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+            oid, olg, ost = O.hnsw_search_q(W, synth.BF16, g, oq, osc, H, k, ef, width, validate=False)
+            what = "int8 width=%d k=%d ef=%d" % (width, k, ef)
+            same = np.all(st == ost, axis=1)
+            assert int((~same).sum()) == 0, "%s: %d traversal divergences" % (what, int((~same).sum()))
+            parity.check_logits(W, synth.BF16, H, ids, lg, what)
+            osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
+            parity.check_id_sets(W, synth.BF16, H, ids, oid, osk, what=what)
+            say("  %s recall@k=%.3f mean n_dist=%.0f" % (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean()))
+
+
 def test_hnsw_wide_beams_match_oracle(vie):
     """Beams of 2048 and 4096 entries (LDS above 64 KiB) follow the oracle's
     traversal exactly, and recall does not drop as the beam grows."""

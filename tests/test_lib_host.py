@@ -156,6 +156,14 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, fake, 1025, fake, fake, None, None) == vie.EINVAL
     assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, None, 5, fake, fake, None, None) == vie.EINVAL
     assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, fake, 5, fake, fake, None, None) == vie.ESTATE
+    prm = vie.SearchParams(1, 2)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # int8_rows
+    assert L.vie_index_attach_int8(ix._h, fake, fake) == vie.ESTATE  # not on a device
+    assert L.vie_index_attach_int8(ix._h, fake, None) == vie.EINVAL
+    assert L.vie_quantize_rows(fake, 0, 0, 8, fake, fake, None) == vie.EINVAL     # V
+    assert L.vie_quantize_rows(fake, 0, 10, 0, fake, fake, None) == vie.EINVAL    # d
+    assert L.vie_quantize_rows(fake, 3, 10, 8, fake, fake, None) == vie.EINVAL    # dtype
+    assert L.vie_quantize_rows(None, 0, 10, 8, fake, fake, None) == vie.EINVAL
     n = C.c_size_t()
     assert L.vie_dense_topk_workspace(1000, 64, 1, 50, C.byref(n)) == vie.OK and n.value > 0
     assert L.vie_dense_topk_workspace(10, 64, 1, 50, C.byref(n)) == vie.EINVAL  # k > V
@@ -175,7 +183,7 @@ def test_calls_fail_synchronously_before_any_hip_call():
 def test_parallel_build_never_breaks_invariants():
     # concurrent inserts race on neighbour lists; every run must stay valid
     W = synth.make_w(2500, 16, synth.BF16, 91)
-    for rep in range(4):
+    for rep in range(12):
         ix = vie.Index.build(W, synth.BF16, 6, 30, seed=rep, n_threads=8)
         e, info = ix.export(), ix.info()
         g = O.Graph(2500, 16, synth.BF16, info["M"], info["M0"], 30, rep, info["maxlevel"], info["entry"],

@@ -1286,7 +1286,7 @@ __device__ __forceinline__ void row_dot2_q8(const int8_t *__restrict__ Q, int64_
     const u32x4 *qb = reinterpret_cast<const u32x4 *>(Q + (rb >= 0 ? rb : ra) * (int64_t)d);
     const u32x4 *h = reinterpret_cast<const u32x4 *>(hq);
     const int nchunk = d / 16;
-    constexpr int CPL = 8;
+    constexpr int CPL = 4;  // int8 rows are at most half a stored row: G lanes cover them in 4 chunks
     u32x4 ba[CPL], bb[CPL];
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
@@ -1521,13 +1521,40 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (tid == 0) sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
         __syncthreads();
         const int nk = (int)sh.nkeep;
+        // with more than 64 kept keys, each wave sorts a run of 64 of them, so
+        // that a key's rank among the kept keys is a sum of binary searches
+        const int nrun = (nk + kWave - 1) / kWave;
+        if (nk > kWave) {
+            for (int r = tid / kWave; r < nrun; r += NT / kWave) {
+                const int j = r * kWave + lane;
+                const uint64_t key = wave_sort_desc(j < nk ? ckey[j] : 0ull, lane);
+                if (j < nk) ckey[j] = key;  // the run's real keys are its largest
+            }
+            __syncthreads();
+        }
+        auto kept_above = [&](uint64_t key) -> int {  // kept keys larger than key
+            int above = 0;
+            if (nk <= kWave) {
+                for (int t = 0; t < nk; ++t) above += ckey[t] > key;
+                return above;
+            }
+            for (int r = 0; r < nrun; ++r) {
+                const uint64_t *run = ckey + r * kWave;
+                int lo = 0, hi = min(kWave, nk - r * kWave);
+                while (lo < hi) {
+                    const int mid = (lo + hi) >> 1;
+                    if (run[mid] > key) lo = mid + 1; else hi = mid;
+                }
+                above += lo;
+            }
+            return above;
+        };
         // the lists of the best `width` new nodes into the cache, by rank
         if (cache_on) {
 #pragma unroll
             for (int x = 0; x < kMultiHeld; ++x)
                 if (rk[x] != 0ull) {
-                    int above = 0;
-                    for (int t = 0; t < nk; ++t) above += ckey[t] > rk[x];
+                    const int above = kept_above(rk[x]);
                     if (above < width) {
 #pragma unroll
                         for (int u = 0; u < kPfbPerLane; ++u) {
@@ -1544,8 +1571,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         const int total = min((int)nbeam + nk, ef);
         for (int j = tid; j < nk; j += NT) {
             const uint64_t key = ckey[j];
-            int above = 0;
-            for (int t = 0; t < nk; ++t) above += ckey[t] > key;
+            const int above = kept_above(key);
             int lo = 0, hi = (int)nbeam;
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
@@ -1560,9 +1586,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         }
         for (int i = tid; i < (int)nbeam; i += NT) {
             const uint64_t key = beam[i];
-            int above = 0;
-            for (int t = 0; t < nk; ++t) above += ckey[t] > key;
-            const int pos = i + above;
+            const int pos = i + kept_above(key);
             if (pos < total) {
                 bool picked = false;
 #pragma unroll

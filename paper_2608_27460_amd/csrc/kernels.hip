@@ -439,7 +439,7 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
     __shared__ uint64_t lists[kMergeWaves][kWave];
     __shared__ int cand[kMergeThreads], scan[kWave];
     __shared__ uint64_t second[kMergeThreads];
-    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count;
+    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count, s_done;
     __shared__ unsigned long long s_prefix, s_and, s_or, s_T;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave, q = blockIdx.x;
     const float *zq = zbuf + (int64_t)q * V;
@@ -456,6 +456,7 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
         s_nc = 0;
         s_n = 0;
         s_nscan = 0;
+        s_done = 0;
         s_and = ~0ull;
         s_or = 0ull;
     }
@@ -478,10 +479,18 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
         //    too, and only those slabs are read again
         if (wave == 0) {
             const uint64_t T = __shfl(key, k - 1, kWave);
-            if (lane < k) {
-                const int slab = (int)(key_id(key) / rows_per_wg);
+            const int slab = lane < k ? (int)(key_id(key) / rows_per_wg) : 0;
+            const bool rescan = lane < k && second[slab] >= T;
+            if (__ballot(rescan) == 0ull) {
+                // no slab holds a second key >= T: the answer is these k maxima, already in order
+                if (lane < k) {
+                    ids[(int64_t)q * k + lane] = key_id(key);
+                    logits[(int64_t)q * k + lane] = key_logit(key);
+                }
+                if (lane == 0) s_done = 1u;
+            } else if (lane < k) {
                 cand[lane] = slab;
-                if (second[slab] >= T) scan[atomicAdd(&s_nscan, 1u)] = slab;
+                if (rescan) scan[atomicAdd(&s_nscan, 1u)] = slab;
                 else gat[atomicAdd(&s_n, 1u)] = key;
             }
             if (lane == 0) {
@@ -490,6 +499,7 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
             }
         }
         __syncthreads();
+        if (s_done) return;
         gather_slabs(zq, V, scan, (int)s_nscan, rows_per_wg, s_T, gat, &s_n);
     } else {
         // 1'. any k, or fewer slabs than k: T by radix select over the

@@ -224,7 +224,11 @@ def main() -> int:
     ix.query_into(Hd, k, ef, ids, lg, st)
     b.record(stream)
     torch.cuda.synchronize()
-    batched_qps = Q / (a.elapsed_time(b) * 1e-3)
+    batched_s = a.elapsed_time(b) * 1e-3
+    batched_qps = Q / batched_s
+    bst = st.cpu().numpy().astype(np.float64)
+    batched_bytes = float((bst[:, 0] * wl.d * s + bst[:, 1] * wl.M0 * 4 + wl.d * s + k * 8).sum())
+    batched_gbs = batched_bytes / batched_s / 1e9
 
     def per_call_us(fn, n_calls):
         # mean event-timed duration of n_calls back-to-back calls (after one warm-up call)
@@ -270,6 +274,15 @@ def main() -> int:
                                 "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
                                 "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean()),
                                 "row_bytes_per_query": float(wst[:, 0].mean() * wl.d)}
+        wb = max(args.int8_widths)
+        torch.cuda.synchronize()
+        ix.query_into(Hd, k, ef, ids, lg, st, wb, True)
+        a.record(stream)
+        ix.query_into(Hd, k, ef, ids, lg, st, wb, True)
+        b.record(stream)
+        torch.cuda.synchronize()
+        q_sweep["batched_width_%d" % wb] = {"queries_per_s": round(Q / (a.elapsed_time(b) * 1e-3), 1),
+                                             "recall_at_k": round(recall(ids.cpu().numpy(), exact_ids), 4)}
         ix.attach_int8(None, None)
         del qrows, qscale
 
@@ -387,6 +400,9 @@ def main() -> int:
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(hnsw_gbs / HBM_PEAK_GBS, 5),
                      "traffic": traffic.get("hnsw_kernel")},
+        "roofline_batched": {"kernel": "hnsw_kernel, all %d queries in one launch" % Q, "bound": "hbm",
+                             "achieved": round(batched_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": round(batched_gbs / HBM_PEAK_GBS, 4), "traffic": None},
         "roofline_dense": {"kernel": "dense_slab_kernel+dense_merge_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dense_gbs / HBM_PEAK_GBS, 4),
                            "traffic": traffic.get("dense_head")},

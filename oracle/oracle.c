@@ -821,6 +821,106 @@ done:
 }
 
 /* ------------------------------------------------------------------------ */
+/* O8: batch construction of a single-layer graph                            */
+/* ------------------------------------------------------------------------ */
+
+/* The library's GPU build (a batch construction in the spirit of CAGRA,
+ * which Section 3 considered; GPU indices are the future work of Section 5).
+ * Our definition:
+ *   1. cand(i): the K nodes nearest to i (dist = -<w_i, w_j>, j != i),
+ *      ordered by (dist, id);
+ *   2. fwd(i) = SELECT(i, cand(i), M0) with the MY18 Algorithm 4 heuristic;
+ *   3. rev(j): every i with j in fwd(i), i ascending;
+ *   4. the list of j is fwd(j) followed by the nodes of rev(j) not in fwd(j);
+ *      if that is more than M0 nodes, it becomes SELECT(j, its first K after
+ *      ordering by (dist to j, id), M0);
+ *   5. one layer; the entry point is the row of largest squared norm (ties:
+ *      smaller id).
+ * adj0 [V][M0] (-1 padded) and *entry are written.  Returns 0 or -1. */
+int oracle_knn_graph(const void *W, int dtype, int64_t V, int d, int K, int M0, int32_t *adj0, int32_t *entry)
+{
+    if (V < 2 || d < 1 || K < 1 || K > V - 1 || M0 < 1) return -1;
+    cand *all = malloc(sizeof(cand) * (size_t)V);
+    cand *c = malloc(sizeof(cand) * (size_t)(V + M0));
+    int32_t *fwd = malloc(sizeof(int32_t) * (size_t)V * M0);
+    int *nf = calloc((size_t)V, sizeof(int));
+    int *nr = calloc((size_t)V, sizeof(int));
+    double *q = malloc(sizeof(double) * (size_t)d), *xa = malloc(sizeof(double) * (size_t)d);
+    int rc = 0;
+    if (!all || !c || !fwd || !nf || !nr || !q || !xa) { rc = -1; goto done; }
+    /* 1 + 2 */
+    for (int64_t i = 0; i < V; ++i) {
+        widen(W, dtype, d, i, q);
+        int n = 0;
+        for (int64_t j = 0; j < V; ++j)
+            if (j != i) {
+                all[n].dist = -dot_row(W, dtype, d, j, q);
+                all[n].id = (int32_t)j;
+                ++n;
+            }
+        qsort(all, (size_t)n, sizeof(cand), by_dist_asc);
+        const int kept = select_neighbors(W, dtype, d, all, K, M0, 1, xa);
+        nf[i] = kept;
+        for (int t = 0; t < kept; ++t) fwd[i * M0 + t] = all[t].id;
+        for (int t = 0; t < kept; ++t) nr[all[t].id]++;
+    }
+    /* 3 + 4: reverse lists (i ascending), then the final lists */
+    int64_t *roff = malloc(sizeof(int64_t) * (size_t)(V + 1));
+    int32_t *rev = NULL;
+    if (!roff) { rc = -1; goto done; }
+    roff[0] = 0;
+    for (int64_t j = 0; j < V; ++j) roff[j + 1] = roff[j] + nr[j];
+    rev = malloc(sizeof(int32_t) * (size_t)(roff[V] > 0 ? roff[V] : 1));
+    if (!rev) { free(roff); rc = -1; goto done; }
+    memset(nr, 0, sizeof(int) * (size_t)V);
+    for (int64_t i = 0; i < V; ++i)
+        for (int t = 0; t < nf[i]; ++t) {
+            const int32_t j = fwd[i * M0 + t];
+            rev[roff[j] + nr[j]++] = (int32_t)i;
+        }
+    for (int64_t j = 0; j < V; ++j) {
+        int n = 0;
+        for (int t = 0; t < nf[j]; ++t) c[n++].id = fwd[j * M0 + t];
+        for (int t = 0; t < nr[j]; ++t) {
+            const int32_t u = rev[roff[j] + t];
+            int dup = 0;
+            for (int x = 0; x < nf[j] && !dup; ++x) dup = fwd[j * M0 + x] == u;
+            if (!dup) c[n++].id = u;
+        }
+        int m = n;
+        if (n > M0) {
+            widen(W, dtype, d, j, q);
+            for (int t = 0; t < n; ++t) c[t].dist = -dot_row(W, dtype, d, c[t].id, q);
+            qsort(c, (size_t)n, sizeof(cand), by_dist_asc);
+            m = select_neighbors(W, dtype, d, c, n < K ? n : K, M0, 1, xa);
+        }
+        for (int t = 0; t < M0; ++t) adj0[j * M0 + t] = t < m ? c[t].id : -1;
+    }
+    free(roff);
+    free(rev);
+    /* 5 */
+    double best = -1.0;
+    for (int64_t i = 0; i < V; ++i) {
+        widen(W, dtype, d, i, q);
+        double s2 = 0.0;
+        for (int j = 0; j < d; ++j) s2 += q[j] * q[j];
+        if (s2 > best) {
+            best = s2;
+            *entry = (int32_t)i;
+        }
+    }
+done:
+    free(all);
+    free(c);
+    free(fwd);
+    free(nf);
+    free(nr);
+    free(q);
+    free(xa);
+    return rc;
+}
+
+/* ------------------------------------------------------------------------ */
 /* O7: int8 rows for the traversal, exact re-rank of the beam                */
 /* ------------------------------------------------------------------------ */
 

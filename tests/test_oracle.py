@@ -430,6 +430,51 @@ def test_int8_search_with_ef_at_least_v_is_exact(P):
     assert np.array_equal(ids, oid) and np.array_equal(lg, olg)
 
 
+def test_knn_graph_golden_star():
+    lines = [l.split() for l in open(os.path.join(GOLDEN, "knn_graph_star.txt")) if l.strip() and l[0] != "#"]
+    vals = next(l for l in lines if l[0] == "values")[1:]
+    K = int(next(l for l in lines if l[0] == "K")[1])
+    M0 = int(next(l for l in lines if l[0] == "M0")[1])
+    W = np.array([[float(v)] for v in vals], np.float32)
+    g = O.knn_graph(W, synth.F32, K, M0)
+    assert O.check_graph(g) == ""
+    for l in lines:
+        if l[0] == "list":
+            got = [int(x) for x in g.adj0[int(l[1])] if x >= 0]
+            assert got == [int(x) for x in l[2].split(",")], (l, got)
+    assert g.entry == int(next(l for l in lines if l[0] == "entry")[1])
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_knn_graph_properties(dtype):
+    V, d, K, M0 = 700, 16, 24, 12
+    W = synth.make_w(V, d, dtype, 31)
+    g = O.knn_graph(W, dtype, K, M0)
+    assert O.check_graph(g) == ""
+    Wf = synth.stored_values_f32(W, dtype).astype(np.float64)
+    G = Wf @ Wf.T
+    np.fill_diagonal(G, -np.inf)
+    nearest = np.lexsort((np.arange(V)[None, :].repeat(V, 0), -G), axis=1)[:, 0]
+    # every node keeps its nearest other node (the heuristic keeps the first candidate)
+    assert all(nearest[i] in g.adj0[i] for i in range(V))
+    assert g.entry == int(np.argmax((Wf * Wf).sum(1)))
+    # the search on this graph with ef >= |V| is exact over the nodes reachable from the entry
+    H, _ = synth.make_queries(W, dtype, 8, 32)
+    ids, _, _, _ = O.hnsw_search(W, dtype, g, H, 10, V)
+    seen, todo = {g.entry}, [g.entry]
+    while todo:
+        u = todo.pop()
+        for v in g.adj0[u]:
+            if v >= 0 and v not in seen:
+                seen.add(int(v))
+                todo.append(int(v))
+    reach = np.array(sorted(seen))
+    sc = synth.stored_values_f32(H, dtype).astype(np.float64) @ Wf[reach].T
+    for q in range(len(H)):
+        order = reach[np.lexsort((reach, -sc[q]))][:10]
+        assert ids[q].tolist() == order.tolist()
+
+
 def _beam_search_reformulated(W, dtype, g, h, k, ef):
     """Independent restatement: keep one beam sorted by (dist, id) with
     'expanded' flags; repeatedly expand the best unexpanded entry, scoring all

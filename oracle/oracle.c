@@ -830,14 +830,16 @@ done:
  *   1. cand(i): the K nodes nearest to i (dist = -<w_i, w_j>, j != i),
  *      ordered by (dist, id);
  *   2. fwd(i) = SELECT(i, cand(i), M0) with the MY18 Algorithm 4 heuristic;
- *   3. rev(j): every i with j in fwd(i), i ascending;
- *   4. the list of j is fwd(j) followed by the nodes of rev(j) not in fwd(j);
- *      if that is more than M0 nodes, it becomes SELECT(j, its first K after
- *      ordering by (dist to j, id), M0);
+ *   3. rev(j): every i with j in fwd(i);
+ *   4. the list of j is fwd(j) followed by the nodes of rev(j) that are not
+ *      in fwd(j), ordered by (dist to j, id), cut at M0 entries (reverse
+ *      edges fill the slots the heuristic left free, nearest first);
  *   5. one layer; the entry point is the row of largest squared norm (ties:
  *      smaller id).
- * adj0 [V][M0] (-1 padded) and *entry are written.  Returns 0 or -1. */
-int oracle_knn_graph(const void *W, int dtype, int64_t V, int d, int K, int M0, int32_t *adj0, int32_t *entry)
+ * adj0 [V][M0] (-1 padded) and *entry are written, and fwd(i) to fwd_out
+ * [V][M0] (-1 padded) if it is not NULL.  Returns 0 or -1. */
+int oracle_knn_graph(const void *W, int dtype, int64_t V, int d, int K, int M0, int32_t *adj0, int32_t *entry,
+                     int32_t *fwd_out)
 {
     if (V < 2 || d < 1 || K < 1 || K > V - 1 || M0 < 1) return -1;
     cand *all = malloc(sizeof(cand) * (size_t)V);
@@ -863,6 +865,8 @@ int oracle_knn_graph(const void *W, int dtype, int64_t V, int d, int K, int M0, 
         nf[i] = kept;
         for (int t = 0; t < kept; ++t) fwd[i * M0 + t] = all[t].id;
         for (int t = 0; t < kept; ++t) nr[all[t].id]++;
+        if (fwd_out)
+            for (int t = 0; t < M0; ++t) fwd_out[i * M0 + t] = t < kept ? all[t].id : -1;
     }
     /* 3 + 4: reverse lists (i ascending), then the final lists */
     int64_t *roff = malloc(sizeof(int64_t) * (size_t)(V + 1));
@@ -879,22 +883,22 @@ int oracle_knn_graph(const void *W, int dtype, int64_t V, int d, int K, int M0, 
             rev[roff[j] + nr[j]++] = (int32_t)i;
         }
     for (int64_t j = 0; j < V; ++j) {
+        const int f = nf[j];
         int n = 0;
-        for (int t = 0; t < nf[j]; ++t) c[n++].id = fwd[j * M0 + t];
+        for (int t = 0; t < f; ++t) c[n++].id = fwd[j * M0 + t];
+        widen(W, dtype, d, j, q);
         for (int t = 0; t < nr[j]; ++t) {
             const int32_t u = rev[roff[j] + t];
             int dup = 0;
-            for (int x = 0; x < nf[j] && !dup; ++x) dup = fwd[j * M0 + x] == u;
-            if (!dup) c[n++].id = u;
+            for (int x = 0; x < f && !dup; ++x) dup = fwd[j * M0 + x] == u;
+            if (!dup) {
+                c[n].id = u;
+                c[n].dist = -dot_row(W, dtype, d, u, q);
+                ++n;
+            }
         }
-        int m = n;
-        if (n > M0) {
-            widen(W, dtype, d, j, q);
-            for (int t = 0; t < n; ++t) c[t].dist = -dot_row(W, dtype, d, c[t].id, q);
-            qsort(c, (size_t)n, sizeof(cand), by_dist_asc);
-            m = select_neighbors(W, dtype, d, c, n < K ? n : K, M0, 1, xa);
-        }
-        for (int t = 0; t < M0; ++t) adj0[j * M0 + t] = t < m ? c[t].id : -1;
+        qsort(c + f, (size_t)(n - f), sizeof(cand), by_dist_asc);
+        for (int t = 0; t < M0; ++t) adj0[j * M0 + t] = t < n ? c[t].id : -1;
     }
     free(roff);
     free(rev);

@@ -51,7 +51,7 @@ def lib() -> C.CDLL:
         L.oracle_forced_merge.argtypes = [vp, i32, i64, i32, vp, i32, i32, vp, i32, vp, vp, vp]
         L.oracle_forced_merge.restype = i32
         L.oracle_quantize_rows.argtypes = [vp, i32, i64, i32, vp, vp]
-        L.oracle_knn_graph.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
+        L.oracle_knn_graph.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp, vp]
         L.oracle_knn_graph.restype = i32
         L.oracle_hnsw_search_q.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
                                            i32, i32, i32, i32, vp, vp, vp]
@@ -320,18 +320,21 @@ def hnsw_search_q(W: np.ndarray, dtype: int, g: Graph, qw: np.ndarray, qscale: n
     return ids, lg, st
 
 
-def knn_graph(W: np.ndarray, dtype: int, K: int, M0: int, seed: int = 0) -> Graph:
-    """Single-layer graph of the batch construction (O8) as a Graph."""
+def knn_graph(W: np.ndarray, dtype: int, K: int, M0: int, seed: int = 0, with_forward: bool = False):
+    """Single-layer graph of the batch construction (O8) as a Graph (and the
+    forward lists [V, M0] if with_forward)."""
     W = _check_w(W, dtype)
     V, d = W.shape
     adj0 = np.empty((V, M0), np.int32)
+    fwd = np.empty((V, M0), np.int32)
     entry = C.c_int32(0)
-    rc = lib().oracle_knn_graph(_p(W), dtype, V, d, K, M0, _p(adj0), C.byref(entry))
+    rc = lib().oracle_knn_graph(_p(W), dtype, V, d, K, M0, _p(adj0), C.byref(entry), _p(fwd))
     if rc != 0:
         raise ValueError("oracle_knn_graph: bad arguments")
     M = max(2, M0 // 2)
-    return Graph(V, d, dtype, M, M0, K, seed, 0, int(entry.value), np.zeros(V, np.uint8), adj0,
-                 -np.ones(V, np.int32), np.zeros((0, M), np.int32))
+    g = Graph(V, d, dtype, M, M0, K, seed, 0, int(entry.value), np.zeros(V, np.uint8), adj0,
+              -np.ones(V, np.int32), np.zeros((0, M), np.int32))
+    return (g, fwd) if with_forward else g
 
 
 def fingerprint(W: np.ndarray, dtype: int) -> int:

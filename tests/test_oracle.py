@@ -475,6 +475,35 @@ def test_knn_graph_properties(dtype):
         assert ids[q].tolist() == order.tolist()
 
 
+def test_knn_graph_forward_and_reverse_edges():
+    V, d, K, M0 = 500, 8, 20, 10
+    W = synth.make_w(V, d, synth.F32, 41)
+    g, fwd = O.knn_graph(W, synth.F32, K, M0, with_forward=True)
+    Wf = W.astype(np.float64)
+    G = Wf @ Wf.T
+    rev = [[] for _ in range(V)]
+    for i in range(V):
+        f = [int(x) for x in fwd[i] if x >= 0]
+        # fwd(i) follows the heuristic over the exact K nearest: every kept e beats all kept before it,
+        # every skipped candidate (before M0 kept) loses to one of them
+        order = sorted((j for j in range(V) if j != i), key=lambda j: (-G[i, j], j))[:K]
+        kept = []
+        for e in order:
+            if len(kept) == M0:
+                break
+            if all(G[e, i] > G[e, r] for r in kept):
+                kept.append(e)
+        assert f == kept, i
+        assert [int(x) for x in g.adj0[i][:len(f)]] == f  # forward edges come first
+        for j in f:
+            rev[j].append(i)
+    for j in range(V):
+        lst = [int(x) for x in g.adj0[j] if x >= 0]
+        f = [int(x) for x in fwd[j] if x >= 0]
+        extra = sorted(set(rev[j]) - set(f), key=lambda i: (-G[j, i], i))
+        assert lst == (f + extra)[:M0], j  # free slots filled by reverse edges, nearest first
+
+
 def _beam_search_reformulated(W, dtype, g, h, k, ef):
     """Independent restatement: keep one beam sorted by (dist, id) with
     'expanded' flags; repeatedly expand the best unexpanded entry, scoring all

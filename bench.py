@@ -144,52 +144,56 @@ def main() -> int:
     div, dlv = [dids[q:q + 1] for q in range(Q)], [dlg[q:q + 1] for q in range(Q)]
     stream = torch.cuda.current_stream(dev)
 
-    def hnsw_step(ev=None, ef_=ef):
+    def hnsw_step(ef_=ef):
         for q in range(Q):
-            if ev is not None:
-                ev[0][q].record(stream)
             ix.query_into(hv[q], k, ef_, iv[q], lv[q], sv[q])
-            if ev is not None:
-                ev[1][q].record(stream)
             vie.scatter_into(iv[q], lv[q], wl.V, row)
 
-    def dense_step(ev=None):
+    def dense_step():
         for q in range(Q):
-            if ev is not None:
-                ev[0][q].record(stream)
             vie.dense_topk_into(Wd, hv[q], k, div[q], dlv[q], head.workspace)
-            if ev is not None:
-                ev[1][q].record(stream)
             vie.scatter_into(div[q], dlv[q], wl.V, row)
 
-    def timed(step, K, W_, n=Q):
+    def timed(step, K, W_):
+        # K steps between two events on the launch stream (nothing else recorded inside)
         for _ in range(W_):
             step()
         torch.cuda.synchronize()
-        evs = [([torch.cuda.Event(enable_timing=True) for _ in range(n)],
-                [torch.cuda.Event(enable_timing=True) for _ in range(n)]) for _ in range(K)]
         outer = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-        torch.cuda.synchronize()
         t = time.perf_counter()
         outer[0].record(stream)
         for i in range(K):
-            step(evs[i])
+            step()
         outer[1].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t
-        ms = outer[0].elapsed_time(outer[1])
-        per_launch = np.array([[a.elapsed_time(b) for a, b in zip(*e)] for e in evs]) * 1e3  # us
-        return ms, wall, per_launch
+        return outer[0].elapsed_time(outer[1]), wall
+
+    def per_call_us(fn, n_calls):
+        # mean event-timed duration of n_calls back-to-back calls (after one warm-up call)
+        fn(0)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for c in range(n_calls):
+            fn(c)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n_calls
 
     # ---- HNSW head (the method) ----------------------------------------
     log("[bench] HNSW head: %d steps x %d queries, ef=%d" % (args.steps, Q, ef))
-    h_ms, h_wall, h_launch = timed(hnsw_step, args.steps, args.warmup)
+    h_ms, h_wall = timed(hnsw_step, args.steps, args.warmup)
     stats = st.cpu().numpy().astype(np.int64)
     hnsw_ids = ids.cpu().numpy()
     # ---- dense head (the baseline) -------------------------------------
     log("[bench] dense head: %d steps x %d queries" % (args.steps, Q))
-    d_ms, d_wall, d_launch = timed(dense_step, args.steps, args.warmup)
+    d_ms, d_wall = timed(dense_step, args.steps, args.warmup)
     exact_ids = dids.cpu().numpy()
+    # ---- per-launch kernel time: Q back-to-back calls between two events ----
+    # (the roofline figures; the kernels alone, no scatter and no events in between)
+    h_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, iv[c], lv[c], sv[c]), Q)
+    d_us = per_call_us(lambda c: vie.dense_topk_into(Wd, hv[c], k, div[c], dlv[c], head.workspace), Q)
 
     def recall(a, b, kk=None):
         kk = kk or a.shape[1]
@@ -202,16 +206,12 @@ def main() -> int:
     for e in sorted(set(wl.ef) | {ef} | set(args.sweep_ef)):
         nq = Q if e <= max(max(wl.ef), ef) else min(Q, args.sweep_queries)
 
-        def step_e(ev=None, e=e, nq=nq):
+        def step_e(e=e, nq=nq):
             for q in range(nq):
-                if ev is not None:
-                    ev[0][q].record(stream)
                 ix.query_into(hv[q], k, e, iv[q], lv[q], sv[q])
-                if ev is not None:
-                    ev[1][q].record(stream)
                 vie.scatter_into(iv[q], lv[q], wl.V, row)
 
-        ms_e, _, _ = timed(step_e, 1, 1, nq)
+        ms_e, _ = timed(step_e, 1, 1)
         sweep[str(e)] = {"us_per_query": round(ms_e * 1e3 / nq, 2), "queries": nq,
                          "recall_at_k": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq]), 4),
                          "recall_at_2": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq], 2), 4),
@@ -229,18 +229,6 @@ def main() -> int:
     bst = st.cpu().numpy().astype(np.float64)
     batched_bytes = float((bst[:, 0] * wl.d * s + bst[:, 1] * wl.M0 * 4 + wl.d * s + k * 8).sum())
     batched_gbs = batched_bytes / batched_s / 1e9
-
-    def per_call_us(fn, n_calls):
-        # mean event-timed duration of n_calls back-to-back calls (after one warm-up call)
-        fn(0)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for c in range(n_calls):
-            fn(c)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / n_calls
 
     # ---- expansion-width sweep (vie_query_ex; B = 1, first 256 queries) ---
     w_sweep = {}
@@ -342,10 +330,8 @@ def main() -> int:
     # ---- roofline figures ----------------------------------------------------
     n_dist, n_exp = stats[:, 0].astype(np.float64), stats[:, 1].astype(np.float64)
     hnsw_bytes = n_dist * wl.d * s + n_exp * wl.M0 * 4 + wl.d * s + k * 8  # per launch (one query)
-    h_us = float(h_launch.mean())
     hnsw_gbs = float(hnsw_bytes.mean()) / (h_us * 1e-6) / 1e9
     dense_bytes = wl.V * wl.d * s + wl.d * s + k * 8
-    d_us = float(d_launch.mean())
     dense_gbs = dense_bytes / (d_us * 1e-6) / 1e9
 
     traffic = measured_traffic(args.workload)
@@ -403,7 +389,7 @@ def main() -> int:
         "roofline_batched": {"kernel": "hnsw_kernel, all %d queries in one launch" % Q, "bound": "hbm",
                              "achieved": round(batched_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": round(batched_gbs / HBM_PEAK_GBS, 4), "traffic": None},
-        "roofline_dense": {"kernel": "dense_slab_kernel+dense_merge_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
+        "roofline_dense": {"kernel": "dense_stream_kernel+dense_merge_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dense_gbs / HBM_PEAK_GBS, 4),
                            "traffic": traffic.get("dense_head")},
         "cpu_baseline": cpu,

@@ -180,22 +180,26 @@ __global__ __launch_bounds__(kScatterThreads) void scatter_kernel(const int32_t 
 //
 // Two launches on the caller's stream.
 //
-// dense_slab_kernel: workgroup w owns a contiguous slab of rows and streams it
-// once.  Each wave takes U rows at a time; its 64 lanes read them with
-// VEC-byte loads (U loads in flight per lane), accumulate in fp32 and reduce
-// over the wave.  The slab writes its logits to the workspace and its
-// largest key.
+// Slab kernels (dense_stream_kernel for one or two queries over 16-byte
+// aligned rows, dense_slab_kernel otherwise): workgroup w owns a contiguous
+// slab of rows and streams it once with 16-byte (or narrower) non-temporal
+// loads, accumulates in fp32 and reduces over the wave.  The slab writes its
+// logits to the workspace and, per query, its kTopR largest keys.
 //
 // dense_merge_kernel: one workgroup per query.  Any T at or below the k-th
 // largest slab maximum is a lower bound of the k-th largest key overall (k
 // distinct elements are >= T), so every key of the answer is >= T, and only
-// the slabs whose maximum is >= T can hold one.  T is found by a radix
-// select over the maxima (8 bits per pass, from the first bit where they
-// differ, until the bucket of the k-th largest is taken whole), so exactly
-// k slabs qualify; the kernel gathers their keys >= T (typically little more
-// than k, with several row loads in flight per thread) and orders them by
-// rank.  The kernel boundary between the two launches is the only
-// cross-workgroup synchronisation: no atomics across workgroups, no fences.
+// the slabs whose maximum is >= T can hold one.  T is the k-th largest
+// maximum (a sorting network for k <= 64, else a radix select over the
+// maxima, 8 bits per pass from the first bit where they differ).  A
+// qualifying slab whose kTopR-th key is below T holds no key >= T outside
+// its list, so the answer normally comes from the lists alone, read in one
+// round trip; only slabs with kTopR or more keys >= T are read again from
+// the workspace.  The candidates (typically little more than k) are ordered
+// by rank.  The kernel boundary between the two launches is the only
+// cross-workgroup synchronisation: no atomics across workgroups, no fences
+// (a release fence per workgroup, needed for a last-workgroup merge inside
+// one launch, made the slab kernel several times slower on MI355X).
 
 // Tuning knobs (compile-time; defaults measured on MI355X).
 #ifndef VIE_DENSE_UNROLL
@@ -247,46 +251,94 @@ __device__ __forceinline__ float wave_sum_multi(float (&v)[N], int lane)
 template <int N> struct Log2 { static constexpr int value = 1 + Log2<N / 2>::value; };
 template <> struct Log2<1> { static constexpr int value = 0; };
 
-// The two largest of a set of distinct keys, (b1 > b2), 0 for "none".
-__device__ __forceinline__ void top2_insert(uint64_t key, uint64_t &b1, uint64_t &b2)
-{
-    // selects only: branches here make the compiler keep (b1, b2) in scratch
-    const uint64_t hi = key > b1 ? key : b1, lo = key > b1 ? b1 : key;
-    b2 = lo > b2 ? lo : b2;
-    b1 = hi;
-}
+// Per-slab candidate lists: the kTopR largest keys of a slab, in descending
+// order, 0 for "none" (no element has key 0: the id half of a key is never
+// zero).  Four keys per slab let the merge take the top k from the lists
+// alone unless some slab holds four or more keys above the threshold.
+constexpr int kTopR = 4;
 
-__device__ __forceinline__ void top2_merge(uint64_t o1, uint64_t o2, uint64_t &b1, uint64_t &b2)
-{
-    const uint64_t hi = o1 > b1 ? o1 : b1, lo = o1 > b1 ? b1 : o1;
-    const uint64_t r2 = o2 > b2 ? o2 : b2;
-    b1 = hi;
-    b2 = lo > r2 ? lo : r2;
-}
-
-// Top two over the lanes whose index differs in the bits of `span` (xor
-// steps from span down to 1); every such lane ends with the result.
-template <int SPAN>
-__device__ __forceinline__ void top2_reduce(uint64_t &b1, uint64_t &b2)
+// Inserts key into the descending list b (selects only: branches here make
+// the compiler keep the list in scratch).
+__device__ __forceinline__ void topr_insert(uint64_t key, uint64_t (&b)[kTopR])
 {
 #pragma unroll
-    for (int o = SPAN; o >= 1; o >>= 1) {
-        const uint64_t o1 = __shfl_xor(b1, o, kWave), o2 = __shfl_xor(b2, o, kWave);
-        top2_merge(o1, o2, b1, b2);
+    for (int i = 0; i < kTopR; ++i) {
+        const bool gt = key > b[i];
+        const uint64_t hi = gt ? key : b[i];
+        key = gt ? b[i] : key;
+        b[i] = hi;
+    }
+}
+
+// b := the kTopR largest of the descending lists b and o.  Taking the larger
+// of b[i] and o[kTopR - 1 - i] keeps the kTopR largest of the union as a
+// bitonic sequence, which two half-cleaner stages order.
+__device__ __forceinline__ void topr_merge(const uint64_t (&o)[kTopR], uint64_t (&b)[kTopR])
+{
+#pragma unroll
+    for (int i = 0; i < kTopR; ++i) b[i] = o[kTopR - 1 - i] > b[i] ? o[kTopR - 1 - i] : b[i];
+#pragma unroll
+    for (int st = kTopR / 2; st >= 1; st >>= 1)
+#pragma unroll
+        for (int i = 0; i < kTopR; ++i)
+            if ((i & st) == 0) {
+                const uint64_t x = b[i], y = b[i + st];
+                b[i] = x > y ? x : y;
+                b[i + st] = x > y ? y : x;
+            }
+}
+
+// The kTopR largest over the lanes whose index differs in the bits of
+// `span` (xor steps from span down to FROM); every such lane ends with them.
+template <int SPAN, int FROM = 1>
+__device__ __forceinline__ void topr_reduce(uint64_t (&b)[kTopR])
+{
+#pragma unroll
+    for (int o = SPAN; o >= FROM; o >>= 1) {
+        uint64_t t[kTopR];
+#pragma unroll
+        for (int i = 0; i < kTopR; ++i) t[i] = __shfl_xor(b[i], o, kWave);
+        topr_merge(t, b);
+    }
+}
+
+__device__ __forceinline__ void store_topr(uint64_t *dst, const uint64_t (&b)[kTopR])
+{
+    u32x4 *p = reinterpret_cast<u32x4 *>(dst);
+    p[0] = u32x4{(uint32_t)b[0], (uint32_t)(b[0] >> 32), (uint32_t)b[1], (uint32_t)(b[1] >> 32)};
+    p[1] = u32x4{(uint32_t)b[2], (uint32_t)(b[2] >> 32), (uint32_t)b[3], (uint32_t)(b[3] >> 32)};
+}
+
+// End of a vector-path slab: its logits (z, [nq][zpitch] in LDS) go to the
+// workspace, coalesced, and wave q finds the kTopR largest keys of query q.
+template <int NT>
+__device__ __forceinline__ void slab_epilogue(const float *z, int zpitch, int nq, int nrows, int64_t r0, int64_t V,
+                                              float *__restrict__ zout, uint64_t *__restrict__ tops)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    for (int q = 0; q < nq; ++q) {
+        const float *zq = z + q * zpitch;
+        float *oq = zout + (int64_t)q * V + r0;
+        for (int i = tid; i < nrows; i += NT) oq[i] = zq[i];
+    }
+    for (int q = wave; q < nq; q += NT / kWave) {
+        const float *zq = z + q * zpitch;
+        uint64_t b[kTopR] = {0ull, 0ull, 0ull, 0ull};
+        for (int i = lane; i < nrows; i += kWave) topr_insert(make_key(zq[i], (int32_t)(r0 + i)), b);
+        topr_reduce<kWave / 2>(b);
+        if (lane == 0) store_topr(tops + ((int64_t)q * gridDim.x + blockIdx.x) * kTopR, b);
     }
 }
 
 template <int VEC, bool BF16, int NB>
 __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 8 : 4))) void
 dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
-                  int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ maxes)
+                  int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ tops)
 {
     extern __shared__ __align__(16) char smem[];
-    __shared__ uint64_t s_top[NB][kDenseWaves][2];
     constexpr int U = NB >= 8 ? 2 : VIE_DENSE_ROWS;  // rows in flight per wave
     constexpr int NV = NB * U;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-    const int nwg = gridDim.x;
     const int hbytes = (row_bytes + 15) & ~15;
     char *hs = smem;                                                   // [NB][hbytes]
     float *z = reinterpret_cast<float *>(smem + (size_t)NB * hbytes);  // [NB][rows_per_wg]
@@ -331,31 +383,89 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
     }
     __syncthreads();
 
-    // the slab's logits (coalesced) and its two largest keys, per query
-    for (int q = 0; q < nq; ++q) {
-        const float *zq = z + q * rows_per_wg;
-        float *oq = zout + (int64_t)q * V + r0;
-        uint64_t b1 = 0ull, b2 = 0ull;
-        for (int i = tid; i < nrows; i += kDenseThreads) {
-            oq[i] = zq[i];
-            top2_insert(make_key(zq[i], (int32_t)(r0 + i)), b1, b2);
+    slab_epilogue<kDenseThreads>(z, rows_per_wg, nq, nrows, r0, V, zout, tops);
+}
+
+// One or two queries over 16-byte aligned rows.  A lane's chunks of the
+// queries stay in registers for the whole kernel (no LDS reads in the loop),
+// the first row loads are issued before the queries are read, and each wave
+// issues the loads of its next row group before it reduces the current one,
+// so the load stream does not drain between groups.  A row of CPL 16-byte
+// chunks per lane (the last ones predicated off where the row is shorter);
+// a group is U rows.  Sums are formed in the same order as in
+// dense_slab_kernel, so both give identical logits.
+template <int CPL> struct StreamRows { static constexpr int value = CPL >= 4 ? 1 : 4 / CPL; };
+
+template <bool BF16, int NB, int CPL>
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 && CPL <= 2 ? 8 : 4))) void
+dense_stream_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
+                    int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ tops)
+{
+    constexpr int U = StreamRows<CPL>::value;
+    constexpr int NV = NB * U;
+    extern __shared__ __align__(16) char smem[];
+    float *z = reinterpret_cast<float *>(smem);  // [NB][rows_per_wg]
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int nchunk = row_bytes / 16;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_wg;
+    const int nrows = (int)max<int64_t>(0, min<int64_t>(rows_per_wg, V - r0));
+    const int ngroups = (nrows + U - 1) / U;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    bool live[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) live[j] = lane + kWave * j < nchunk;
+
+    u32x4 a[U][CPL], b[U][CPL];
+    auto load_group = [&](int gi, u32x4(&buf)[U][CPL]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const u32x4 *w = reinterpret_cast<const u32x4 *>(W + (r0 + min(gi * U + u, nrows - 1)) * (int64_t)row_bytes);
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) buf[u][j] = live[j] ? __builtin_nontemporal_load(w + lane + kWave * j) : zero;
         }
-        top2_reduce<32>(b1, b2);
-        if (lane == 0) {
-            s_top[q][wave][0] = b1;
-            s_top[q][wave][1] = b2;
+    };
+    int g = wave;
+    if (g < ngroups) load_group(g, a);
+    u32x4 hv[NB][CPL];
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+            hv[q][j] = live[j] && q < nq
+                           ? reinterpret_cast<const u32x4 *>(hq + (int64_t)q * row_bytes)[lane + kWave * j]
+                           : zero;
+
+    auto reduce_group = [&](int gi, const u32x4(&buf)[U][CPL]) {
+        float acc[NV];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) acc[v] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+#pragma unroll
+            for (int q = 0; q < NB; ++q)
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[q * U + u] = dot_vec<16, BF16>(buf[u][j], hv[q][j], acc[q * U + u]);
+        const float total = wave_sum_multi<NV>(acc, lane);
+        constexpr int lg = 6 - Log2<NV>::value;
+        if ((lane & ((1 << lg) - 1)) == 0) {
+            const int v = lane >> lg, q = v / U, u = v % U;
+            if (gi * U + u < nrows) z[q * rows_per_wg + gi * U + u] = total;
         }
+    };
+    for (; g < ngroups; g += 2 * kDenseWaves) {
+        const int g1 = g + kDenseWaves, g2 = g1 + kDenseWaves;
+        if (g1 < ngroups) load_group(g1, b);
+        reduce_group(g, a);
+        if (g2 < ngroups) load_group(g2, a);
+        if (g1 < ngroups) reduce_group(g1, b);
     }
     __syncthreads();
-    if (tid < nq) {
-        uint64_t b1 = 0ull, b2 = 0ull;
-        for (int w = 0; w < kDenseWaves; ++w) top2_merge(s_top[tid][w][0], s_top[tid][w][1], b1, b2);
-        maxes[((int64_t)tid * nwg + blockIdx.x) * 2] = b1;
-        maxes[((int64_t)tid * nwg + blockIdx.x) * 2 + 1] = b2;
-    }
+    slab_epilogue<kDenseThreads>(z, rows_per_wg, nq, nrows, r0, V, zout, tops);
 }
 
 constexpr int kGatherBatch = 8;  // row loads in flight per thread while gathering
+constexpr int kMergeBuckets = 256;     // histogram of the slab maxima
+constexpr int kMergeBucketShift = 18;  // order-space width of a bucket (log2)
 constexpr int kMergeWaves = kMergeThreads / kWave;
 
 // Sorts one key per lane of a wave, largest first (bitonic network over xor
@@ -437,142 +547,183 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
     __shared__ uint32_t hist[256];
     __shared__ uint64_t gat[kMergeGather];
     __shared__ uint64_t lists[kMergeWaves][kWave];
-    __shared__ int cand[kMergeThreads], scan[kWave];
-    __shared__ uint64_t second[kMergeThreads];
-    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count, s_done;
+    __shared__ int cand[kMergeThreads], scan[kMergeThreads];
+    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count, s_omax, s_bucket;
     __shared__ unsigned long long s_prefix, s_and, s_or, s_T;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave, q = blockIdx.x;
     const float *zq = zbuf + (int64_t)q * V;
-    const uint64_t *tq = tops + (int64_t)q * nwg * 2;  // (largest, second largest) key per slab
 
-    uint64_t m = 0ull, m2 = 0ull;
+    // the slab's list of its kTopR largest keys, in one round trip
+    uint64_t key[kTopR] = {0ull, 0ull, 0ull, 0ull};
     if (tid < nwg) {
-        const u32x4 v = *reinterpret_cast<const u32x4 *>(tq + 2 * tid);
-        m = ((uint64_t)v.y << 32) | v.x;
-        m2 = ((uint64_t)v.w << 32) | v.z;
+        const u32x4 *p = reinterpret_cast<const u32x4 *>(tops + ((int64_t)q * nwg + tid) * kTopR);
+        const u32x4 v0 = p[0], v1 = p[1];
+        key[0] = ((uint64_t)v0.y << 32) | v0.x;
+        key[1] = ((uint64_t)v0.w << 32) | v0.z;
+        key[2] = ((uint64_t)v1.y << 32) | v1.x;
+        key[3] = ((uint64_t)v1.w << 32) | v1.z;
     }
-    second[tid] = m2;
+    const uint64_t m = key[0];  // the slab's maximum
     if (tid == 0) {
         s_nc = 0;
         s_n = 0;
         s_nscan = 0;
-        s_done = 0;
         s_and = ~0ull;
         s_or = 0ull;
+        s_T = 0ull;
+        s_omax = 0u;
+        s_bucket = kMergeBuckets;
     }
-    if (k <= kWave && nwg >= k) {
+    if (tid < kMergeBuckets) hist[tid] = 0u;
+    // 1. T, a lower bound of the k-th largest slab maximum.  First one pass:
+    //    a histogram of the maxima by their distance below the largest one
+    //    in the order space of the logits, 2^kMergeBucketShift per bucket
+    //    (1/32 of a binade for positive logits); T is the lower edge of the
+    //    bucket in which the count from the top reaches k.  The slabs above
+    //    T are then k or a few more.
+    const uint32_t mo = (uint32_t)(m >> 32);
+    {
+        uint32_t w = mo;
+#pragma unroll
+        for (int x = 32; x >= 1; x >>= 1) w = max(w, (uint32_t)__shfl_xor(w, x, kWave));
+        __syncthreads();
+        if (lane == 0) atomicMax(&s_omax, w);
+        __syncthreads();
+        const uint32_t top = s_omax;
+        const uint32_t dist = (top - mo) >> kMergeBucketShift;
+        if (tid < nwg && dist < (uint32_t)kMergeBuckets) atomicAdd(&hist[dist], 1u);
+        __syncthreads();
+        if (tid < kWave) {  // wave 0: the bucket where the count from the top reaches k
+            constexpr int per = kMergeBuckets / kWave;
+            uint32_t c[per], sum = 0;
+#pragma unroll
+            for (int j = 0; j < per; ++j) {
+                c[j] = hist[per * lane + j];
+                sum += c[j];
+            }
+            uint32_t incl = sum;
+#pragma unroll
+            for (int x = 1; x < kWave; x <<= 1) {
+                const uint32_t t = __shfl_up(incl, x, kWave);
+                if (lane >= x) incl += t;
+            }
+            uint32_t above = incl - sum;
+#pragma unroll
+            for (int j = 0; j < per; ++j) {
+                if (above < (uint32_t)k && (uint32_t)k <= above + c[j]) {
+                    const uint64_t span = (uint64_t)(per * lane + j + 1) << kMergeBucketShift;
+                    s_bucket = per * lane + j;
+                    s_T = (uint64_t)top + 1 > span ? ((uint64_t)top + 1 - span) << 32 : 0ull;
+                }
+                above += c[j];
+            }
+        }
+        __syncthreads();
+    }
+    if (s_bucket < (uint32_t)kMergeBuckets) {
+        // T from the histogram
+    } else if (k <= kWave && nwg >= k) {
         // 1. T = the k-th largest slab maximum, exactly: every wave sorts its
         //    64 maxima, then pairs of sorted lists merge (keeping the larger
         //    64) in four rounds until wave 0 holds the largest 64.
-        uint64_t key = wave_sort_desc(m, lane);
+        uint64_t srt = wave_sort_desc(m, lane);
 #pragma unroll
         for (int span = 1; span < kMergeWaves; span <<= 1) {
-            if ((wave & (2 * span - 1)) == span) lists[wave][lane] = key;
+            if ((wave & (2 * span - 1)) == span) lists[wave][lane] = srt;
             __syncthreads();
             if ((wave & (2 * span - 1)) == 0) {
                 const uint64_t other = lists[wave + span][kWave - 1 - lane];
-                key = wave_bitonic_merge_desc(other > key ? other : key, lane);
+                srt = wave_bitonic_merge_desc(other > srt ? other : srt, lane);
             }
         }
-        // 2. the k slabs whose maximum is >= T hold every key >= T; a slab's
-        //    maximum is its only such key unless its second largest is >= T
-        //    too, and only those slabs are read again
-        if (wave == 0) {
-            const uint64_t T = __shfl(key, k - 1, kWave);
-            const int slab = lane < k ? (int)(key_id(key) / rows_per_wg) : 0;
-            const bool rescan = lane < k && second[slab] >= T;
-            if (__ballot(rescan) == 0ull) {
-                // no slab holds a second key >= T: the answer is these k maxima, already in order
-                if (lane < k) {
-                    ids[(int64_t)q * k + lane] = key_id(key);
-                    logits[(int64_t)q * k + lane] = key_logit(key);
-                }
-                if (lane == 0) s_done = 1u;
-            } else if (lane < k) {
-                cand[lane] = slab;
-                if (rescan) scan[atomicAdd(&s_nscan, 1u)] = slab;
-                else gat[atomicAdd(&s_n, 1u)] = key;
-            }
-            if (lane == 0) {
-                s_T = T;
-                s_nc = (uint32_t)k;
-            }
+        const uint64_t t = __shfl(srt, k - 1, kWave);
+        if (tid == 0) s_T = t;
+    } else if (nwg >= k) {
+        // 1'. any k: T by radix select over the maxima, 8 bits per pass from
+        //     the first bit where they differ, until the bucket of the k-th
+        //     largest is taken whole (so exactly k slabs have maximum >= T)
+        __syncthreads();
+        uint64_t a = tid < nwg ? m : ~0ull, o = m;
+#pragma unroll
+        for (int x = 32; x >= 1; x >>= 1) {
+            a &= __shfl_xor(a, x, kWave);
+            o |= __shfl_xor(o, x, kWave);
+        }
+        if (lane == 0) {
+            atomicAnd(&s_and, (unsigned long long)a);
+            atomicOr(&s_or, (unsigned long long)o);
         }
         __syncthreads();
-        if (s_done) return;
-        gather_slabs(zq, V, scan, (int)s_nscan, rows_per_wg, s_T, gat, &s_n);
-    } else {
-        // 1'. any k, or fewer slabs than k: T by radix select over the
-        //     maxima, 8 bits per pass from the first bit where they differ,
-        //     until the bucket of the k-th largest is taken whole (T = 0 with
-        //     fewer slabs than k: every slab); every slab with maximum >= T
-        //     is read
-        __syncthreads();
-        uint64_t T = 0ull;
-        if (nwg >= k) {
-            uint64_t a = tid < nwg ? m : ~0ull, o = m;
+        const uint64_t diff = s_and ^ s_or;
+        uint64_t prefix = s_and;
+        if (diff != 0ull) {
+            // bits >= hi are known (in prefix); each pass decides bits [lo, hi)
+            int hi = 64 - __clzll((long long)diff);
+            prefix &= hi >= 64 ? 0ull : (~0ull << hi);
+            uint32_t want = (uint32_t)k;
+            for (;;) {
+                const int lo = hi > 8 ? hi - 8 : 0;
+                const uint64_t known = hi >= 64 ? 0ull : (~0ull << hi);
+                const uint64_t dmask = (1ull << (hi - lo)) - 1ull;
+                if (tid < 256) hist[tid] = 0u;
+                __syncthreads();
+                if (tid < nwg && (m & known) == prefix) atomicAdd(&hist[(m >> lo) & dmask], 1u);
+                __syncthreads();
+                if (tid < kWave) {  // wave 0: the bucket holding the want-th largest
+                    uint32_t c[4], sum = 0;
 #pragma unroll
-            for (int x = 32; x >= 1; x >>= 1) {
-                a &= __shfl_xor(a, x, kWave);
-                o |= __shfl_xor(o, x, kWave);
-            }
-            if (lane == 0) {
-                atomicAnd(&s_and, (unsigned long long)a);
-                atomicOr(&s_or, (unsigned long long)o);
-            }
-            __syncthreads();
-            const uint64_t diff = s_and ^ s_or;
-            uint64_t prefix = s_and;
-            if (diff != 0ull) {
-                // bits >= hi are known (in prefix); each pass decides bits [lo, hi)
-                int hi = 64 - __clzll((long long)diff);
-                prefix &= hi >= 64 ? 0ull : (~0ull << hi);
-                uint32_t want = (uint32_t)k;
-                for (;;) {
-                    const int lo = hi > 8 ? hi - 8 : 0;
-                    const uint64_t known = hi >= 64 ? 0ull : (~0ull << hi);
-                    const uint64_t dmask = (1ull << (hi - lo)) - 1ull;
-                    if (tid < 256) hist[tid] = 0u;
-                    __syncthreads();
-                    if (tid < nwg && (m & known) == prefix) atomicAdd(&hist[(m >> lo) & dmask], 1u);
-                    __syncthreads();
-                    if (tid < kWave) {  // wave 0: the bucket holding the want-th largest
-                        uint32_t c[4], sum = 0;
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            c[j] = hist[255 - 4 * lane - j];
-                            sum += c[j];
-                        }
-                        uint32_t incl = sum;
-#pragma unroll
-                        for (int x = 1; x < kWave; x <<= 1) {
-                            const uint32_t t = __shfl_up(incl, x, kWave);
-                            if (lane >= x) incl += t;
-                        }
-                        uint32_t above = incl - sum;
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            if (above < want && want <= above + c[j]) {
-                                s_prefix = prefix | ((uint64_t)(255 - 4 * lane - j) << lo);
-                                s_want = want - above;
-                                s_count = c[j];
-                            }
-                            above += c[j];
-                        }
+                    for (int j = 0; j < 4; ++j) {
+                        c[j] = hist[255 - 4 * lane - j];
+                        sum += c[j];
                     }
-                    __syncthreads();
-                    prefix = s_prefix;
-                    want = s_want;
-                    if (s_count == want || lo == 0) break;  // uniform: shared values after a barrier
-                    hi = lo;
+                    uint32_t incl = sum;
+#pragma unroll
+                    for (int x = 1; x < kWave; x <<= 1) {
+                        const uint32_t t = __shfl_up(incl, x, kWave);
+                        if (lane >= x) incl += t;
+                    }
+                    uint32_t above = incl - sum;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (above < want && want <= above + c[j]) {
+                            s_prefix = prefix | ((uint64_t)(255 - 4 * lane - j) << lo);
+                            s_want = want - above;
+                            s_count = c[j];
+                        }
+                        above += c[j];
+                    }
                 }
+                __syncthreads();
+                prefix = s_prefix;
+                want = s_want;
+                if (s_count == want || lo == 0) break;  // uniform: shared values after a barrier
+                hi = lo;
             }
-            T = prefix;
         }
-        if (tid < nwg && m >= T) cand[atomicAdd(&s_nc, 1u)] = tid;
-        if (tid == 0) s_T = T;
+        if (tid == 0) s_T = prefix;
+    }
+    // (fewer slabs than k: T = 0, every slab qualifies)
+    __syncthreads();
+    {
+        // 2. every key >= T lies in a slab whose maximum is >= T.  A slab
+        //    whose last listed key is below T has all its keys >= T in its
+        //    list; the others (four or more keys >= T) are read again.
+        const uint64_t T = s_T;
+        if (tid < nwg && m >= T) {
+            cand[atomicAdd(&s_nc, 1u)] = tid;
+            if (key[kTopR - 1] >= T) {
+                scan[atomicAdd(&s_nscan, 1u)] = tid;
+            } else {
+#pragma unroll
+                for (int i = 0; i < kTopR; ++i)
+                    if (key[i] >= T) {
+                        const uint32_t slot = atomicAdd(&s_n, 1u);
+                        if (slot < (uint32_t)kMergeGather) gat[slot] = key[i];
+                    }
+            }
+        }
         __syncthreads();
-        gather_slabs(zq, V, cand, (int)s_nc, rows_per_wg, T, gat, &s_n);
+        if (s_nscan) gather_slabs(zq, V, scan, (int)s_nscan, rows_per_wg, T, gat, &s_n);
     }
     __syncthreads();
     const uint64_t T = s_T;
@@ -711,10 +862,10 @@ template <int NQT, int KC>
 __global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t *__restrict__ W, int64_t V, int d,
                                                                    const uint16_t *__restrict__ hq, int nq,
                                                                    int rows_per_wg, float *__restrict__ zout,
-                                                                   uint64_t *__restrict__ maxes)
+                                                                   uint64_t *__restrict__ tops)
 {
     extern __shared__ __align__(16) char smem[];
-    __shared__ uint64_t s_top[16 * NQT][kMfmaWaves][2];
+    __shared__ uint64_t s_top[16 * NQT][kMfmaWaves][kTopR];
     constexpr int kPitch = mfma_pitch(KC);
     constexpr int kSteps = KC / 32;                     // MFMA steps per stage
     constexpr int kLanesPerRow = KC / 8;                // 16-byte pieces per staged row
@@ -748,9 +899,11 @@ __global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t
         hoff[j] = row * kPitch + hcol[j] * 2;
     }
 
-    uint64_t best[NQT], best2[NQT];
+    uint64_t best[NQT][kTopR];
 #pragma unroll
-    for (int n = 0; n < NQT; ++n) best[n] = best2[n] = 0ull;
+    for (int n = 0; n < NQT; ++n)
+#pragma unroll
+        for (int i = 0; i < kTopR; ++i) best[n][i] = 0ull;
 
     // every wave runs the same number of iterations (the workgroup barriers
     // need it); rows past the slab are clamped and discarded
@@ -825,30 +978,30 @@ __global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t
                         if (lr + i < nrows) {
                             const float z = acc[m][n][i];
                             zout[(int64_t)q * V + r0 + lr + i] = z;
-                            top2_insert(make_key(z, (int32_t)(r0 + lr + i)), best[n], best2[n]);
+                            topr_insert(make_key(z, (int32_t)(r0 + lr + i)), best[n]);
                         }
                 }
             }
     }
-    // per query: the two largest over the four lane groups, then over the waves
+    // per query: the kTopR largest over the four lane groups, then over the waves
 #pragma unroll
     for (int n = 0; n < NQT; ++n) {
-        uint64_t b1 = best[n], b2 = best2[n];
-        for (int o = 16; o <= 32; o <<= 1) {
-            const uint64_t o1 = __shfl_xor(b1, o, kWave), o2 = __shfl_xor(b2, o, kWave);
-            top2_merge(o1, o2, b1, b2);
-        }
-        if (g == 0) {
-            s_top[n * 16 + r][wave][0] = b1;
-            s_top[n * 16 + r][wave][1] = b2;
-        }
+        topr_reduce<32, 16>(best[n]);
+        if (g == 0)
+#pragma unroll
+            for (int i = 0; i < kTopR; ++i) s_top[n * 16 + r][wave][i] = best[n][i];
     }
     __syncthreads();
     if (tid < nq) {
-        uint64_t b1 = 0ull, b2 = 0ull;
-        for (int w = 0; w < kMfmaWaves; ++w) top2_merge(s_top[tid][w][0], s_top[tid][w][1], b1, b2);
-        maxes[((int64_t)tid * gridDim.x + blockIdx.x) * 2] = b1;
-        maxes[((int64_t)tid * gridDim.x + blockIdx.x) * 2 + 1] = b2;
+        uint64_t b[kTopR], o[kTopR];
+#pragma unroll
+        for (int i = 0; i < kTopR; ++i) b[i] = s_top[tid][0][i];
+        for (int w = 1; w < kMfmaWaves; ++w) {
+#pragma unroll
+            for (int i = 0; i < kTopR; ++i) o[i] = s_top[tid][w][i];
+            topr_merge(o, b);
+        }
+        store_topr(tops + ((int64_t)tid * gridDim.x + blockIdx.x) * kTopR, b);
     }
 }
 
@@ -1780,9 +1933,54 @@ bool dense_plan(int64_t V, int row_bytes, DensePlan &p)
     return true;
 }
 
+// Chunks of 16 bytes per lane per row for the streaming kernel (0: not served).
+int stream_cpl(int row_bytes, int nb)
+{
+    const int c = (row_bytes / 16 + kWave - 1) / kWave;
+    const int cpl = c <= 1 ? 1 : c <= 2 ? 2 : c <= 4 ? 4 : c <= 8 ? 8 : 0;
+    return nb == 2 && cpl > 4 ? 0 : cpl;
+}
+
+template <bool BF16, int NB, int CPL>
+hipError_t stream_launch(const void *W, int64_t V, int row_bytes, const char *h, int nq, int k, const DensePlan &p,
+                         float *zbuf, uint64_t *tops, int32_t *ids, float *logits, hipStream_t s)
+{
+    const size_t lds = (size_t)NB * p.rpw * 4;
+    auto kern = dense_stream_kernel<BF16, NB, CPL>;
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    kern<<<p.nwg, kDenseThreads, lds, s>>>(static_cast<const char *>(W), V, row_bytes, h, nq, p.rpw, zbuf, tops);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, tops, V, p.rpw, p.nwg, k, ids, logits);
+    return hipGetLastError();
+}
+
+template <bool BF16>
+hipError_t stream_launch_cpl(int cpl, int nb, const void *W, int64_t V, int row_bytes, const char *h, int nq, int k,
+                             const DensePlan &p, float *zbuf, uint64_t *tops, int32_t *ids, float *logits,
+                             hipStream_t s)
+{
+    if (nb == 1) {
+        switch (cpl) {
+        case 1: return stream_launch<BF16, 1, 1>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+        case 2: return stream_launch<BF16, 1, 2>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+        case 4: return stream_launch<BF16, 1, 4>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+        default: return stream_launch<BF16, 1, 8>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+        }
+    }
+    switch (cpl) {
+    case 1: return stream_launch<BF16, 2, 1>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+    case 2: return stream_launch<BF16, 2, 2>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+    default: return stream_launch<BF16, 2, 4>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+    }
+}
+
 template <int VEC, bool BF16, int NB>
 hipError_t dense_launch(const void *W, int64_t V, int row_bytes, const char *h, int nq, int k, const DensePlan &p,
-                        float *zbuf, uint64_t *maxes, int32_t *ids, float *logits, hipStream_t s)
+                        float *zbuf, uint64_t *tops, int32_t *ids, float *logits, hipStream_t s)
 {
     const size_t lds = dense_lds(NB, row_bytes, p.rpw);
     auto kern = dense_slab_kernel<VEC, BF16, NB>;
@@ -1790,23 +1988,23 @@ hipError_t dense_launch(const void *W, int64_t V, int row_bytes, const char *h, 
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    kern<<<p.nwg, kDenseThreads, lds, s>>>(static_cast<const char *>(W), V, row_bytes, h, nq, p.rpw, zbuf, maxes);
+    kern<<<p.nwg, kDenseThreads, lds, s>>>(static_cast<const char *>(W), V, row_bytes, h, nq, p.rpw, zbuf, tops);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, maxes, V, p.rpw, p.nwg, k, ids, logits);
+    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, tops, V, p.rpw, p.nwg, k, ids, logits);
     return hipGetLastError();
 }
 
 template <int VEC, bool BF16>
 hipError_t dense_launch_nb(int nb, const void *W, int64_t V, int row_bytes, const char *h, int nq, int k,
-                           const DensePlan &p, float *zbuf, uint64_t *maxes, int32_t *ids, float *logits,
+                           const DensePlan &p, float *zbuf, uint64_t *tops, int32_t *ids, float *logits,
                            hipStream_t s)
 {
     switch (nb) {
-    case 1: return dense_launch<VEC, BF16, 1>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
-    case 2: return dense_launch<VEC, BF16, 2>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
-    case 4: return dense_launch<VEC, BF16, 4>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
-    default: return dense_launch<VEC, BF16, 8>(W, V, row_bytes, h, nq, k, p, zbuf, maxes, ids, logits, s);
+    case 1: return dense_launch<VEC, BF16, 1>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+    case 2: return dense_launch<VEC, BF16, 2>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+    case 4: return dense_launch<VEC, BF16, 4>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+    default: return dense_launch<VEC, BF16, 8>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
     }
 }
 
@@ -1837,7 +2035,7 @@ int dense_pass(int B) { return B >= kMfmaMinB ? kMfmaMaxNB : kDenseMaxNB; }
 
 template <int NQT, int KC>
 hipError_t mfma_launch(const void *W, int64_t V, int d, const char *h, int nq, int k, const DensePlan &p,
-                       float *zbuf, uint64_t *maxes, int32_t *ids, float *logits, hipStream_t s)
+                       float *zbuf, uint64_t *tops, int32_t *ids, float *logits, hipStream_t s)
 {
     auto kern = dense_mfma_kernel<NQT, KC>;
     constexpr size_t lds = mfma_lds(NQT, KC);
@@ -1846,18 +2044,19 @@ hipError_t mfma_launch(const void *W, int64_t V, int d, const char *h, int nq, i
         if (e != hipSuccess) return e;
     }
     kern<<<p.nwg, kMfmaThreads, lds, s>>>(static_cast<const uint16_t *>(W), V, d,
-                                           reinterpret_cast<const uint16_t *>(h), nq, p.rpw, zbuf, maxes);
+                                           reinterpret_cast<const uint16_t *>(h), nq, p.rpw, zbuf, tops);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, maxes, V, p.rpw, p.nwg, k, ids, logits);
+    dense_merge_kernel<<<nq, kMergeThreads, 0, s>>>(zbuf, tops, V, p.rpw, p.nwg, k, ids, logits);
     return hipGetLastError();
 }
 
 }  // namespace
 
-// Workspace: the logits [nb][V] fp32 (256-byte padded), then the two
-// largest keys of every slab [nb][slabs][2] u64, nb = the queries of one pass (at most 8 on the vector
-// path, 64 on the matrix-core path, never more than B).
+// Workspace: the logits [nb][V] fp32 (256-byte padded), then the kTopR
+// largest keys of every slab [nb][slabs][kTopR] u64, nb = the queries of one
+// pass (at most 8 on the vector path, 64 on the matrix-core path, never more
+// than B).
 size_t dense_workspace_bytes(int64_t V, int d, int B, int k)
 {
     (void)d;
@@ -1865,7 +2064,7 @@ size_t dense_workspace_bytes(int64_t V, int d, int B, int k)
     const int pass = dense_pass(B);
     const int nb = B < pass ? B : pass;
     const int slabs = std::max(dense_grid(V), mfma_plan(V).nwg);
-    return (((size_t)nb * V * 4 + 255) & ~(size_t)255) + (size_t)nb * slabs * 16;
+    return (((size_t)nb * V * 4 + 255) & ~(size_t)255) + (size_t)nb * slabs * 8 * kTopR;
 }
 
 vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const void *h, int B, int k, int32_t *ids,
@@ -1879,7 +2078,7 @@ vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const v
     const int pass = dense_pass(B);
     const int nbw = B < pass ? B : pass;
     float *zbuf = static_cast<float *>(ws);
-    uint64_t *maxes = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) +
+    uint64_t *tops = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) +
                                                    (((size_t)nbw * V * 4 + 255) & ~(size_t)255));
     const char *hb = static_cast<const char *>(h);
     if (use_mfma(dtype, d, B, W, h)) {
@@ -1889,9 +2088,9 @@ vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const v
             const char *hp = hb + (int64_t)q0 * row_bytes;
             int32_t *ip = ids + (int64_t)q0 * k;
             float *lp = logits + (int64_t)q0 * k;
-            hipError_t e = nq <= 16   ? mfma_launch<1, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, maxes, ip, lp, s)
-                           : nq <= 32 ? mfma_launch<2, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, maxes, ip, lp, s)
-                                      : mfma_launch<4, VIE_MFMA_KC4>(W, V, d, hp, nq, k, mp, zbuf, maxes, ip, lp, s);
+            hipError_t e = nq <= 16   ? mfma_launch<1, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s)
+                           : nq <= 32 ? mfma_launch<2, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s)
+                                      : mfma_launch<4, VIE_MFMA_KC4>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s);
             if (e != hipSuccess) return launched(e, "dense top-k (matrix cores) launch");
         }
         return VIE_OK;
@@ -1905,17 +2104,21 @@ vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const v
         int32_t *ip = ids + (int64_t)q0 * k;
         float *lp = logits + (int64_t)q0 * k;
         hipError_t e;
-        if (vec == 16)
-            e = bf ? dense_launch_nb<16, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s)
-                   : dense_launch_nb<16, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
+        const int cpl = stream_cpl(row_bytes, nb);
+        if (vec == 16 && nb <= 2 && cpl && (uintptr_t)hp % 16 == 0)
+            e = bf ? stream_launch_cpl<true>(cpl, nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s)
+                   : stream_launch_cpl<false>(cpl, nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s);
+        else if (vec == 16)
+            e = bf ? dense_launch_nb<16, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s)
+                   : dense_launch_nb<16, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s);
         else if (vec == 8)
-            e = bf ? dense_launch_nb<8, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s)
-                   : dense_launch_nb<8, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
+            e = bf ? dense_launch_nb<8, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s)
+                   : dense_launch_nb<8, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s);
         else if (vec == 4)
-            e = bf ? dense_launch_nb<4, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s)
-                   : dense_launch_nb<4, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
+            e = bf ? dense_launch_nb<4, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s)
+                   : dense_launch_nb<4, false>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s);
         else
-            e = dense_launch_nb<2, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, maxes, ip, lp, s);
+            e = dense_launch_nb<2, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s);
         if (e != hipSuccess) return launched(e, "dense top-k launch");
     }
     return VIE_OK;

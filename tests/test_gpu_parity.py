@@ -71,6 +71,14 @@ DENSE_CASES = [
     (777, 37, synth.BF16, 17, 30),     # odd row: batched on the vector path
     (4000, 96, synth.F32, 24, 40),     # fp32 batch: vector path, passes of 8
     (1000, 64, synth.BF16, 16, 50),    # fewer slabs than k on the matrix-core path
+    # one or two queries over 16-byte aligned rows: the streaming slab kernel
+    (30011, 640, synth.BF16, 1, 50),   # 80 chunks: the second chunk on 16 lanes only
+    (12000, 1536, synth.BF16, 1, 64),  # 3 of 4 chunks per lane
+    (9001, 3072, synth.BF16, 1, 50),   # 6 of 8 chunks per lane
+    (7001, 2048, synth.BF16, 2, 50),   # two queries, 4 chunks per lane
+    (5003, 3072, synth.BF16, 2, 10),   # two queries, rows too long for it: the slab kernel
+    (8000, 1000, synth.F32, 1, 30),    # fp32, 250 chunks
+    (4000, 256, synth.F32, 2, 40),     # fp32, two queries, one chunk per lane
 ]
 
 
@@ -115,6 +123,32 @@ def test_dense_clustered_top_keys(vie, B):
     parity.check_logits(W, synth.BF16, H, ids, lg, "clustered")
     parity.check_id_sets(W, synth.BF16, H, ids, oid, osc[:, -1], what="clustered")
     assert all(np.isin(ids[b], np.arange(1000 * b, 1000 * b + 120)).sum() >= 40 for b in range(B))
+
+
+@pytest.mark.parametrize("B,dtype", [(1, synth.BF16), (2, synth.BF16), (1, synth.F32), (4, synth.BF16),
+                                     (16, synth.BF16)])
+def test_dense_slab_lists_boundary(vie, B, dtype):
+    # each slab passes its four largest keys to the merge; here single slabs
+    # hold exactly 3, 4 and 5 of the top k (rows 2560 apart start a slab both
+    # for 20-row slabs of the vector path and 128-row slabs of the matrix
+    # cores), so the merge takes a list whole, must read a slab whose fourth
+    # key clears the threshold, and must find a fifth key outside the list
+    V, d, k = 20000, 128, 20
+    W = synth.make_w(V, d, dtype, 91)
+    H, _ = synth.make_queries(W, dtype, B, 92)
+    Wf = synth.stored_values_f32(W, dtype).copy()
+    hf = synth.stored_values_f32(H, dtype)
+    planted = np.concatenate([np.arange(0, 3), np.arange(2560, 2564), np.arange(5120, 5125)])
+    Wf[planted] = hf[0] * (4.0 + 0.1 * np.arange(len(planted)))[:, None] / (hf[0] @ hf[0]) * 10.0
+    W = Wf if dtype == synth.F32 else synth.f32_to_bf16_bits(Wf)
+    head = vie.DenseHead(dev_tensor(vie, W, dtype), max_batch=B, max_k=k)
+    ids, lg = head(dev_tensor(vie, H, dtype), k)
+    torch.cuda.synchronize()
+    ids, lg = ids.cpu().numpy(), lg.cpu().numpy()
+    oid, olg, osc = O.topk(W, dtype, H, k)
+    assert set(planted.tolist()) <= set(oid[0].tolist())
+    parity.check_logits(W, dtype, H, ids, lg, "slab lists")
+    parity.check_id_sets(W, dtype, H, ids, oid, osc[:, -1], what="slab lists")
 
 
 @pytest.mark.parametrize("V,k", [(30000, 64), (200000, 100)])

@@ -102,6 +102,42 @@ typedef struct {
 vie_status vie_index_build(const void *W_host, vie_dtype dtype, int64_t V, int32_t d,
                            const vie_build_params *params, vie_index **out);
 
+/* Parameters of the GPU batch construction (vie_index_build_gpu). */
+typedef struct {
+    int32_t K;          /* candidates per node: the K rows nearest by inner
+                           product; 1 <= K <= min(V - 1, 128) */
+    int32_t M0;         /* list cap; 2 <= M0 <= 256 */
+    int64_t chunk_rows; /* rows of W_out per Gram block: the library holds
+                           chunk_rows x V fp32 scores in device scratch; 0
+                           selects about 2 GiB */
+} vie_gpu_build_params;
+
+/* Builds a single-layer graph over the V rows of W_dev (device memory,
+ * [V][d] of dtype, 16-byte aligned rows) on the current HIP device, as a
+ * batch: (1) the K rows nearest to each row i by inner product (j != i, fp32
+ * accumulation), ordered by (score desc, id asc); (2) the forward list of i:
+ * the neighbour-selection heuristic of Malkov & Yashunin (Algorithm 4) over
+ * those candidates with cap M0 -- in candidate order e is kept iff
+ * <w_e, w_i> > <w_e, w_r> for every r kept before it; at most M0 candidates
+ * are kept whole; (3) reverse edges: i joins the list of every j in its
+ * forward list, after j's forward list, in (score desc, id asc) order, up to
+ * M0 entries.  The entry point is the row of largest squared norm (ties: the
+ * smaller id).  Section 3 builds the index offline from the rows of W_out
+ * with inner product as the similarity; construction on the GPU is the
+ * future work of Section 5, and this batch form (one layer, maxlevel 0) is
+ * the library's own.  The graph searches with vie_query like any index: the
+ * greedy upper layers are empty.  On return the graph is complete, on the
+ * device (as after vie_index_to_device with W_dev, which must stay allocated)
+ * and on the host (save, export); the index reports M = max(2, M0 / 2)
+ * (capped at M0), ef_construction = K, seed 0.  The call allocates device
+ * scratch (chunk_rows x V x 4 bytes of scores plus about V (8K + 16 M0)
+ * bytes) and releases it before returning; it enqueues on hip_stream and
+ * waits for it.
+ * Errors: VIE_EINVAL (NULL, sizes, params), VIE_EUNSUPPORTED (rows not
+ * 16-byte aligned), VIE_ENOMEM, VIE_EHIP (a HIP or rocBLAS call failed). */
+vie_status vie_index_build_gpu(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d,
+                               const vie_gpu_build_params *params, void *hip_stream, vie_index **out);
+
 /* Writes the index file (format below).  Errors: VIE_EINVAL, VIE_EIO. */
 vie_status vie_index_save(const vie_index *index, const char *path);
 

@@ -128,6 +128,32 @@ vie_status vie_index_build(const void *W_host, vie_dtype dtype, int64_t V, int32
     return VIE_OK;
 }
 
+vie_status vie_index_build_gpu(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d,
+                               const vie_gpu_build_params *p, void *hip_stream, vie_index **out)
+{
+    g_last_error.clear();
+    if (!W_dev || !p || !out) return fail(VIE_EINVAL, "NULL argument");
+    *out = nullptr;
+    if (vie_status s = check_dims(V, d, dtype)) return s;
+    if (V < 2) return fail(VIE_EINVAL, "V = %lld: the batch graph needs two rows", (long long)V);
+    if (p->K < 1 || p->K > kMaxGpuBuildK || p->K > V - 1)
+        return fail(VIE_EINVAL, "K = %d out of range [1, min(V - 1, %d)]", p->K, kMaxGpuBuildK);
+    if (p->M0 < 2 || p->M0 > kMaxM0) return fail(VIE_EINVAL, "M0 = %d out of range [2, %d]", p->M0, kMaxM0);
+    if (p->chunk_rows < 0) return fail(VIE_EINVAL, "chunk_rows = %lld < 0", (long long)p->chunk_rows);
+    const int row_bytes = d * elem_bytes(dtype);
+    if (row_bytes % 16 || (uintptr_t)W_dev % 16)
+        return fail(VIE_EUNSUPPORTED, "GPU build needs 16-byte aligned rows (d = %d of dtype %d)", d, (int)dtype);
+    vie_index *ix = new (std::nothrow) vie_index;
+    if (!ix) return fail(VIE_ENOMEM, "cannot allocate the index");
+    if (vie_status s = build_knn_graph_gpu(W_dev, dtype, V, d, p->K, p->M0, p->chunk_rows,
+                                           static_cast<hipStream_t>(hip_stream), ix->g, ix->dev)) {
+        delete ix;
+        return s;
+    }
+    *out = ix;
+    return VIE_OK;
+}
+
 vie_status vie_index_save(const vie_index *ix, const char *path)
 {
     g_last_error.clear();

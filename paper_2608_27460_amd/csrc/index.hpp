@@ -18,6 +18,7 @@ constexpr int kMaxM0 = 256;       // cap on M0 (layer 0)
 constexpr int kMaxK = 1024;       // largest k of any query
 constexpr int kMaxEf = 8192;      // largest beam of the HNSW kernel (LDS permitting)
 constexpr int kMaxD = 8192;       // largest row width
+constexpr int kMaxGpuBuildK = 128;  // candidates per node of the GPU batch build
 
 inline int elem_bytes(int dtype) { return dtype == VIE_F32 ? 4 : 2; }
 
@@ -54,6 +55,9 @@ void set_error(const char *fmt, ...) __attribute__((format(printf, 1, 2)));
 vie_status fail(vie_status s, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 
 uint64_t w_fingerprint(const void *W, int dtype, int64_t V, int d);
+// The same fingerprint from the rows it samples (rows 0, s, 2s, ... below V,
+// then row V - 1, with s = max(1, V / 1024)), packed in that order.
+uint64_t w_fingerprint_rows(const void *rows, int dtype, int64_t V, int d, int64_t n_rows);
 int node_level(uint64_t seed, int64_t i, int M);
 
 vie_status build_graph(const void *W, int dtype, int64_t V, int d, const vie_build_params &p, Graph &g);
@@ -97,6 +101,13 @@ size_t hnsw_lds_limit();
 size_t dense_workspace_bytes(int64_t V, int d, int B, int k);
 vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const void *h, int B, int k,
                              int32_t *ids, float *logits, void *ws, hipStream_t s);
+
+// Batch construction of a single-layer graph on the GPU (knn_build.hip):
+// exact K nearest rows by inner product, the Algorithm 4 heuristic with cap
+// M0, reverse edges in the free slots, entry = the largest squared norm.
+// Fills the host graph and its device copy (dg.W = W_dev).
+vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, int K, int M0, int64_t chunk_rows,
+                               hipStream_t s, Graph &g, DeviceGraph &dg);
 
 vie_status launch_scatter(const int32_t *ids, const float *logits, int B, int k, int64_t V, float *out,
                           hipStream_t s);

@@ -61,6 +61,19 @@ uint64_t w_fingerprint(const void *W, int dtype, int64_t V, int d)
     return fnv1a(h, base + (size_t)(V - 1) * row, row);
 }
 
+uint64_t w_fingerprint_rows(const void *rows, int dtype, int64_t V, int d, int64_t n_rows)
+{
+    uint64_t h = kFnvOffset;
+    int32_t d32 = d;
+    uint32_t dt = (uint32_t)dtype;
+    h = fnv1a(h, &V, 8);
+    h = fnv1a(h, &d32, 4);
+    h = fnv1a(h, &dt, 4);
+    const size_t row = (size_t)d * elem_bytes(dtype);
+    for (int64_t t = 0; t < n_rows; ++t) h = fnv1a(h, static_cast<const char *>(rows) + (size_t)t * row, row);
+    return h;
+}
+
 vie_status validate_graph(const Graph &g)
 {
     if (g.V < 1 || g.V >= (int64_t(1) << 31)) return fail(VIE_EFORMAT, "V = %lld out of range", (long long)g.V);

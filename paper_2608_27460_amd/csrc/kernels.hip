@@ -9,45 +9,21 @@
 //   hnsw_kernel         HNSW k-NN search (Sections 2-3; Malkov & Yashunin
 //                       Algorithms 2 and 5), one workgroup per query.
 //
-// Ordering: a candidate is the 64-bit key (ord(logit) << 32) | ~id, where
-// ord() maps fp32 to an unsigned integer of the same order.  A larger key is
-// a better candidate: larger logit first, smaller id first on equal logits.
-// That is the (dist, id) order of the search with dist = -logit.
+// Ordering: candidates are the 64-bit keys of keys.hpp (larger logit first,
+// smaller id first on equal logits).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdint>
 
 #include "index.hpp"
+#include "keys.hpp"
 
 namespace vie {
 
 namespace {
 
 constexpr int kWave = 64;
-
-// ---------------------------------------------------------------------------
-// keys
-// ---------------------------------------------------------------------------
-
-__device__ __forceinline__ uint32_t f2ord(float f)
-{
-    const uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);  // -0 -> +0
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float ord2f(uint32_t o)
-{
-    return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
-}
-
-__device__ __forceinline__ uint64_t make_key(float logit, int32_t id)
-{
-    return ((uint64_t)f2ord(logit) << 32) | (uint64_t)(~(uint32_t)id);
-}
-
-__device__ __forceinline__ int32_t key_id(uint64_t k) { return (int32_t)(~(uint32_t)k); }
-__device__ __forceinline__ float key_logit(uint64_t k) { return ord2f((uint32_t)(k >> 32)); }
 
 // ---------------------------------------------------------------------------
 // dot products of stored rows with a query held in LDS

@@ -1,0 +1,596 @@
+// Batch construction of a single-layer graph over the rows of W_out on the
+// GPU.  Section 3 builds the index offline and prioritises its quality;
+// Section 5 names GPU construction as future work.  The graph is the batch
+// form also written out by the CPU oracle:
+//
+//   1. cand(i): the K rows nearest to row i by inner product (j != i), in the
+//      (score desc, id asc) order of the search;
+//   2. fwd(i): the neighbour-selection heuristic of Malkov & Yashunin
+//      (Algorithm 4) over cand(i) with cap M0: in candidate order, e is kept
+//      iff <w_e, w_i> > <w_e, w_r> for every r kept before it (a list of at
+//      most M0 candidates is kept whole);
+//   3. rev(j): every i with j in fwd(i);
+//   4. the list of j: fwd(j), then the nodes of rev(j) not in fwd(j) in
+//      (score desc, id asc) order, cut at M0 entries;
+//   5. entry point: the row of largest squared norm (ties: smaller id).
+//
+// Step 1 is a dense contraction: the Gram block S = W[rows] W^T of a chunk of
+// rows comes from a library GEMM (rocBLAS, fp32 accumulation), and one
+// workgroup per row selects its exact top K from S.  Steps 2-5 are this
+// file's kernels.  Scores are fp32 throughout; ties of equal scores are
+// broken by id exactly as the oracle breaks them.
+#include <hip/hip_runtime.h>
+#include <rocblas/rocblas.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "index.hpp"
+#include "keys.hpp"
+
+namespace vie {
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kTopkThreads = 256;
+constexpr int kDigitBits = 12;               // radix digit of the selection
+constexpr int kDigitBuckets = 1 << kDigitBits;
+constexpr int kGatherCap = 2048;             // keys a selection sorts in LDS
+constexpr int kSelectThreads = 256;
+constexpr int kSelectRows = 128;             // candidate rows of one Gram block (K <= 128)
+constexpr int kChunkBytes = 256;             // bytes of a row per staged chunk
+constexpr int kChunkPitch = kChunkBytes + 16;
+constexpr int kGramPitch = kSelectRows + 1;  // floats per Gram row in LDS
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+struct TopkShared {
+    uint32_t hist[kDigitBuckets];
+    uint64_t gat[kGatherCap];
+    uint32_t wsum[kTopkThreads / kWave];
+    uint32_t n, bucket, above, count;
+};
+
+// Exclusive prefix sum over the block of one value per thread.
+template <int NT>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *wsum)
+{
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    uint32_t incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t t = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += t;
+    }
+    if (lane == kWave - 1) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int w = 0; w < wave; ++w) base += wsum[w];
+    __syncthreads();
+    return base + incl - v;
+}
+
+// Sorts n <= kGatherCap keys in LDS, largest first (bitonic network over the
+// next power of two; the padding is 0, the smallest key).
+template <int NT>
+__device__ void block_sort_desc(uint64_t *a, int n)
+{
+    int p = 1;
+    while (p < n) p <<= 1;
+    for (int i = n + threadIdx.x; i < p; i += NT) a[i] = 0ull;
+    __syncthreads();
+    for (int size = 2; size <= p; size <<= 1)
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = threadIdx.x; i < p / 2; i += NT) {
+                const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+                const bool desc = (lo & size) == 0;
+                const uint64_t x = a[lo], y = a[hi];
+                if (desc ? x < y : x > y) {
+                    a[lo] = y;
+                    a[hi] = x;
+                }
+            }
+            __syncthreads();
+        }
+}
+
+// The K largest of the keys key_at(0 .. n-1) (0 = no key), sorted, into
+// sh.gat[0 .. K).  Exact: a radix select over the 64-bit keys, kDigitBits
+// per round from the top, narrows the bucket of the K-th largest until every
+// key at or above that bucket fits in LDS; those are gathered and sorted.
+// Keys are distinct, so at most 6 rounds are needed.  Returns the number of
+// keys found (< K only when fewer than K keys exist).
+template <int NT, typename KeyAt>
+__device__ int block_topk(int64_t n, int K, KeyAt key_at, TopkShared &sh)
+{
+    const int tid = threadIdx.x;
+    uint64_t prefix = 0ull;
+    int known = 0;
+    uint32_t want = (uint32_t)K;
+    uint64_t T = 0ull;
+    for (;;) {
+        const int width = 64 - known < kDigitBits ? 64 - known : kDigitBits;
+        const int shift = 64 - known - width;
+        const uint32_t nb = 1u << width;
+        for (int b = tid; b < kDigitBuckets; b += NT) sh.hist[b] = 0u;
+        if (tid == 0) {
+            sh.bucket = 0u;
+            sh.above = 0u;
+            sh.count = 0u;
+        }
+        __syncthreads();
+        for (int64_t i = tid; i < n; i += NT) {
+            const uint64_t key = key_at(i);
+            if (key != 0ull && (known == 0 || (key >> (64 - known)) == (prefix >> (64 - known))))
+                atomicAdd(&sh.hist[(uint32_t)(key >> shift) & (nb - 1)], 1u);
+        }
+        __syncthreads();
+        // buckets from the top: thread t holds buckets nb-1-16t .. nb-16-16t
+        constexpr int per = kDigitBuckets / NT;
+        uint32_t c[per], sum = 0;
+#pragma unroll
+        for (int j = 0; j < per; ++j) {
+            const int b = (int)nb - 1 - (per * tid + j);
+            c[j] = b >= 0 ? sh.hist[b] : 0u;
+            sum += c[j];
+        }
+        uint32_t above = block_exclusive_scan<NT>(sum, sh.wsum);
+        bool found = false;
+#pragma unroll
+        for (int j = 0; j < per; ++j) {
+            if (!found && above < want && want <= above + c[j]) {
+                sh.bucket = (uint32_t)((int)nb - 1 - (per * tid + j));
+                sh.above = above;
+                sh.count = c[j];
+                found = true;
+            }
+            above += c[j];
+        }
+        __syncthreads();
+        if (sh.count == 0u) {
+            // fewer than want keys match the prefix: take every key >= prefix
+            T = prefix == 0ull ? 1ull : prefix;
+            break;
+        }
+        const uint64_t lo = prefix | ((uint64_t)sh.bucket << shift);
+        const uint32_t total = ((uint32_t)K - want) + sh.above + sh.count;
+        if (total <= (uint32_t)kGatherCap || shift == 0) {
+            T = lo == 0ull ? 1ull : lo;
+            break;
+        }
+        prefix = lo;
+        known += width;
+        want -= sh.above;
+        __syncthreads();
+    }
+    if (tid == 0) sh.n = 0u;
+    __syncthreads();
+    for (int64_t i = tid; i < n; i += NT) {
+        const uint64_t key = key_at(i);
+        if (key >= T) {
+            const uint32_t slot = atomicAdd(&sh.n, 1u);
+            if (slot < (uint32_t)kGatherCap) sh.gat[slot] = key;
+        }
+    }
+    __syncthreads();
+    const int m = (int)min(sh.n, (uint32_t)kGatherCap);
+    block_sort_desc<NT>(sh.gat, m);
+    return m < K ? m : K;
+}
+
+// Step 1, per row of a chunk: the K nearest other rows from the chunk's
+// scores S [rows][ld] (row r of the chunk is row r0 + r of W_out).
+__global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__restrict__ S, int64_t ld, int64_t r0,
+                                                                int64_t V, int K, int32_t *__restrict__ cand,
+                                                                float *__restrict__ cand_score)
+{
+    __shared__ TopkShared sh;
+    const int64_t i = r0 + blockIdx.x;
+    const float *row = S + (int64_t)blockIdx.x * ld;
+    auto key_at = [&](int64_t j) -> uint64_t { return j == i ? 0ull : make_key(row[j], (int32_t)j); };
+    const int m = block_topk<kTopkThreads>(V, K, key_at, sh);
+    for (int t = threadIdx.x; t < K; t += kTopkThreads) {
+        const uint64_t key = t < m ? sh.gat[t] : 0ull;
+        cand[i * K + t] = t < m ? key_id(key) : -1;
+        cand_score[i * K + t] = t < m ? key_logit(key) : 0.0f;
+    }
+}
+
+// Two bf16 products per 32-bit word (the words are passed as plain integers:
+// bit-casting a vector lane in place compiled to the first lane here).
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float acc)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), acc,
+                                           false);
+}
+
+__device__ __forceinline__ float dot16(u32x4 a, u32x4 b, float acc, bool bf16)
+{
+    const uint32_t a0 = a.x, a1 = a.y, a2 = a.z, a3 = a.w;
+    const uint32_t b0 = b.x, b1 = b.y, b2 = b.z, b3 = b.w;
+    if (bf16) {
+        acc = dot2_bf16(a0, b0, acc);
+        acc = dot2_bf16(a1, b1, acc);
+        acc = dot2_bf16(a2, b2, acc);
+        return dot2_bf16(a3, b3, acc);
+    }
+    acc = fmaf(__uint_as_float(a0), __uint_as_float(b0), acc);
+    acc = fmaf(__uint_as_float(a1), __uint_as_float(b1), acc);
+    acc = fmaf(__uint_as_float(a2), __uint_as_float(b2), acc);
+    return fmaf(__uint_as_float(a3), __uint_as_float(b3), acc);
+}
+
+constexpr size_t kSelectBig = (size_t)kSelectRows * kChunkPitch > (size_t)kSelectRows * kGramPitch * 4
+                                   ? (size_t)kSelectRows * kChunkPitch
+                                   : (size_t)kSelectRows * kGramPitch * 4;
+constexpr size_t kSelectLds = kSelectBig + (size_t)kSelectRows * 8 + 256 * 4;
+
+// Step 2, one workgroup per node: the Gram matrix of its candidates (rows
+// staged through LDS in chunks of kChunkBytes, each thread an 8 x 8 block of
+// pairs, fp32 accumulation), then the heuristic scan in candidate order by
+// one wave.  A node with at most M0 candidates keeps them all.
+template <bool BF16>
+__global__ __launch_bounds__(kSelectThreads) void knn_select_kernel(const char *__restrict__ W, int row_bytes,
+                                                                    int K, int M0, const int32_t *__restrict__ cand,
+                                                                    const float *__restrict__ cand_score,
+                                                                    int32_t *__restrict__ fwd,
+                                                                    float *__restrict__ fwd_score,
+                                                                    int32_t *__restrict__ nfwd)
+{
+    extern __shared__ __align__(16) char smem[];
+    char *tile = smem;                                            // [128][kChunkPitch] staged rows
+    float *G = reinterpret_cast<float *>(smem);                   // [128][kGramPitch] after the tile
+    int32_t *cid = reinterpret_cast<int32_t *>(smem + kSelectBig);  // [128]
+    float *cs = reinterpret_cast<float *>(cid + kSelectRows);     // [128]
+    int32_t *kept = reinterpret_cast<int32_t *>(cs + kSelectRows);  // [<= 256]
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int64_t i = blockIdx.x;
+    int nc = 0;
+    for (int t = tid; t < kSelectRows; t += kSelectThreads) {
+        const int32_t c = t < K ? cand[i * K + t] : -1;
+        cid[t] = c;
+        cs[t] = t < K ? cand_score[i * K + t] : 0.0f;
+    }
+    __syncthreads();
+    for (int t = 0; t < K; ++t) nc += cid[t] >= 0;  // uniform
+    if (nc <= M0) {
+        for (int t = tid; t < M0; t += kSelectThreads) {
+            fwd[i * M0 + t] = t < nc ? cid[t] : -1;
+            fwd_score[i * M0 + t] = t < nc ? cs[t] : 0.0f;
+        }
+        if (tid == 0) nfwd[i] = nc;
+        return;
+    }
+    // Gram block: thread (ta, tb) owns pairs (ta + 16 x, tb + 16 y); rows 16
+    // apart keep the 16-byte reads of a wave on distinct LDS banks
+    const int ta = tid / 16, tb = tid % 16;
+    float acc[8][8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+#pragma unroll
+        for (int y = 0; y < 8; ++y) acc[x][y] = 0.0f;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    for (int c0 = 0; c0 < row_bytes; c0 += kChunkBytes) {
+        __syncthreads();
+        // stage 128 rows x 256 bytes: 16 pieces of 16 bytes per row
+        for (int p = tid; p < kSelectRows * (kChunkBytes / 16); p += kSelectThreads) {
+            const int r = p / (kChunkBytes / 16), piece = p % (kChunkBytes / 16);
+            const int off = c0 + 16 * piece;
+            const int32_t c = cid[r];
+            u32x4 v = zero;
+            if (c >= 0 && off < row_bytes)
+                v = *reinterpret_cast<const u32x4 *>(W + (int64_t)c * row_bytes + off);
+            *reinterpret_cast<u32x4 *>(tile + r * kChunkPitch + 16 * piece) = v;
+        }
+        __syncthreads();
+#pragma unroll 2
+        for (int piece = 0; piece < kChunkBytes / 16; ++piece) {
+            u32x4 a[8], b[8];
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                a[x] = *reinterpret_cast<const u32x4 *>(tile + (ta + 16 * x) * kChunkPitch + 16 * piece);
+#pragma unroll
+            for (int y = 0; y < 8; ++y)
+                b[y] = *reinterpret_cast<const u32x4 *>(tile + (tb + 16 * y) * kChunkPitch + 16 * piece);
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+#pragma unroll
+                for (int y = 0; y < 8; ++y) acc[x][y] = dot16(a[x], b[y], acc[x][y], BF16);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+#pragma unroll
+        for (int y = 0; y < 8; ++y) G[(ta + 16 * x) * kGramPitch + tb + 16 * y] = acc[x][y];
+    __syncthreads();
+    if (tid < kWave) {
+        // heuristic scan: e is kept iff s_e > <w_e, w_r> for every kept r
+        int nk = 0;
+        for (int e = 0; e < nc && nk < M0; ++e) {
+            const float se = cs[e];
+            bool bad = false;
+            for (int r = lane; r < nk; r += kWave) bad |= G[e * kGramPitch + kept[r]] >= se;
+            if (!__any(bad)) {
+                if (lane == 0) kept[nk] = e;
+                ++nk;
+                __builtin_amdgcn_wave_barrier();
+            }
+        }
+        for (int t = lane; t < M0; t += kWave) {
+            fwd[i * M0 + t] = t < nk ? cid[kept[t]] : -1;
+            fwd_score[i * M0 + t] = t < nk ? cs[kept[t]] : 0.0f;
+        }
+        if (lane == 0) nfwd[i] = nk;
+    }
+}
+
+__device__ __forceinline__ bool in_list(const int32_t *lst, int n, int32_t x)
+{
+    bool f = false;
+    for (int t = 0; t < n; ++t) f |= lst[t] == x;
+    return f;
+}
+
+// Step 3: reverse edges not already forward edges of their target.  Pass 0
+// counts them per target, pass 1 (after the scan) writes their keys.
+__global__ void knn_reverse_kernel(int64_t V, int M0, const int32_t *__restrict__ fwd,
+                                   const float *__restrict__ fwd_score, const int32_t *__restrict__ nfwd,
+                                   uint32_t *__restrict__ count, const int64_t *__restrict__ roff,
+                                   uint64_t *__restrict__ rev, int pass)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= V * M0) return;
+    const int64_t i = e / M0;
+    const int t = (int)(e - i * M0);
+    if (t >= nfwd[i]) return;
+    const int32_t j = fwd[e];
+    if (in_list(fwd + (int64_t)j * M0, nfwd[j], (int32_t)i)) return;
+    const uint32_t slot = atomicAdd(&count[j], 1u);
+    if (pass == 1) rev[roff[j] + slot] = make_key(fwd_score[e], (int32_t)i);
+}
+
+// Exclusive prefix sum of count[0 .. V) into roff[0 .. V] (one workgroup).
+__global__ __launch_bounds__(1024) void knn_scan_kernel(const uint32_t *__restrict__ count, int64_t V,
+                                                        int64_t *__restrict__ roff)
+{
+    __shared__ uint32_t wsum[16];
+    __shared__ int64_t s_base;
+    if (threadIdx.x == 0) s_base = 0;
+    __syncthreads();
+    for (int64_t b0 = 0; b0 < V; b0 += 1024) {
+        const int64_t j = b0 + threadIdx.x;
+        const uint32_t v = j < V ? count[j] : 0u;
+        const uint32_t ex = block_exclusive_scan<1024>(v, wsum);
+        const int64_t base = s_base;
+        if (j < V) roff[j] = base + ex;
+        __syncthreads();
+        if (threadIdx.x == 1023) s_base = base + ex + v;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) roff[V] = s_base;
+}
+
+// Step 4, one workgroup per node: the forward list, then the best reverse
+// edges in the free slots.
+__global__ __launch_bounds__(kTopkThreads) void knn_lists_kernel(int M0, const int32_t *__restrict__ fwd,
+                                                                 const int32_t *__restrict__ nfwd,
+                                                                 const int64_t *__restrict__ roff,
+                                                                 const uint64_t *__restrict__ rev,
+                                                                 int32_t *__restrict__ adj0)
+{
+    __shared__ TopkShared sh;
+    const int64_t j = blockIdx.x;
+    const int nf = nfwd[j];
+    const int free_slots = M0 - nf;
+    const int64_t off = roff[j], nr = roff[j + 1] - off;
+    int m = 0;
+    if (free_slots > 0 && nr > 0) {
+        auto key_at = [&](int64_t t) -> uint64_t { return rev[off + t]; };
+        m = block_topk<kTopkThreads>(nr, free_slots, key_at, sh);
+    }
+    for (int t = threadIdx.x; t < M0; t += kTopkThreads)
+        adj0[j * M0 + t] = t < nf ? fwd[j * M0 + t] : t < nf + m ? key_id(sh.gat[t - nf]) : -1;
+}
+
+// Step 5: the key (squared norm, id) of every row, the largest kept.
+template <bool BF16>
+__global__ void knn_entry_kernel(const char *__restrict__ W, int64_t V, int row_bytes,
+                                 unsigned long long *__restrict__ best)
+{
+    const int64_t i = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (i >= V) return;
+    const char *w = W + i * row_bytes;
+    float acc = 0.0f;
+    for (int c = 16 * lane; c < row_bytes; c += 16 * kWave) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(w + c);
+        acc = dot16(v, v, acc, BF16);
+    }
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, kWave);
+    if (lane == 0) atomicMax(best, (unsigned long long)make_key(acc, (int32_t)i));
+}
+
+struct Buffers {
+    float *S = nullptr;
+    int32_t *cand = nullptr, *fwd = nullptr, *nfwd = nullptr, *adj0 = nullptr, *upper_off = nullptr,
+            *upper = nullptr;
+    float *cand_score = nullptr, *fwd_score = nullptr;
+    uint32_t *count = nullptr;
+    int64_t *roff = nullptr;
+    uint64_t *rev = nullptr;
+    unsigned long long *best = nullptr;
+    void release()
+    {
+        void *p[] = {S, cand, fwd, nfwd, cand_score, fwd_score, count, roff, rev, best};
+        for (void *q : p)
+            if (q) (void)hipFree(q);
+        S = nullptr;
+        cand = fwd = nfwd = nullptr;
+        cand_score = fwd_score = nullptr;
+        count = nullptr;
+        roff = nullptr;
+        rev = nullptr;
+        best = nullptr;
+    }
+    void release_graph()
+    {
+        void *p[] = {adj0, upper_off, upper};
+        for (void *q : p)
+            if (q) (void)hipFree(q);
+        adj0 = upper_off = upper = nullptr;
+    }
+};
+
+template <typename T>
+bool dalloc(T *&p, size_t bytes)
+{
+    void *q = nullptr;
+    if (hipMalloc(&q, bytes < 16 ? 16 : bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    p = static_cast<T *>(q);
+    return true;
+}
+
+vie_status blas_fail(rocblas_status st, const char *what)
+{
+    return fail(VIE_EHIP, "%s failed: %s", what, rocblas_status_to_string(st));
+}
+
+}  // namespace
+
+vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, int K, int M0, int64_t chunk_rows,
+                               hipStream_t s, Graph &g, DeviceGraph &dg)
+{
+    const int row_bytes = d * elem_bytes(dtype);
+    const int64_t ld = (V + 3) & ~(int64_t)3;  // 16-byte aligned rows of scores
+    int64_t R = chunk_rows > 0 ? chunk_rows : ((int64_t)2 << 30) / (ld * 4);
+    R = std::max<int64_t>(1, std::min<int64_t>(R, V));
+    if (R * ld > ((int64_t)1 << 31)) return fail(VIE_EUNSUPPORTED, "GPU build: a score chunk of %lld rows is too large", (long long)R);
+    int dev = 0;
+    hipError_t he = hipGetDevice(&dev);
+    if (he != hipSuccess) return fail(VIE_EHIP, "hipGetDevice: %s", hipGetErrorString(he));
+    const size_t lds = kSelectLds;
+    auto sel = dtype == VIE_BF16 ? knn_select_kernel<true> : knn_select_kernel<false>;
+    he = hipFuncSetAttribute((const void *)sel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (he != hipSuccess) return fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he));
+
+    Buffers b;
+    const int64_t edges = V * M0;
+    if (!dalloc(b.S, (size_t)R * ld * 4) || !dalloc(b.cand, (size_t)V * K * 4) ||
+        !dalloc(b.cand_score, (size_t)V * K * 4) || !dalloc(b.fwd, (size_t)edges * 4) ||
+        !dalloc(b.fwd_score, (size_t)edges * 4) || !dalloc(b.nfwd, (size_t)V * 4) ||
+        !dalloc(b.count, (size_t)V * 4) || !dalloc(b.roff, (size_t)(V + 1) * 8) ||
+        !dalloc(b.rev, (size_t)edges * 8) || !dalloc(b.best, 8) || !dalloc(b.adj0, (size_t)edges * 4) ||
+        !dalloc(b.upper_off, (size_t)V * 4) || !dalloc(b.upper, 4)) {
+        b.release();
+        b.release_graph();
+        return fail(VIE_ENOMEM, "GPU build: device allocation failed (V = %lld, chunk of %lld rows)", (long long)V,
+                    (long long)R);
+    }
+    auto bail = [&](vie_status st) {
+        (void)hipStreamSynchronize(s);
+        b.release();
+        b.release_graph();
+        return st;
+    };
+
+    rocblas_handle h = nullptr;
+    rocblas_status bs = rocblas_create_handle(&h);
+    if (bs != rocblas_status_success) return bail(blas_fail(bs, "rocblas_create_handle"));
+    bs = rocblas_set_stream(h, s);
+    const float one = 1.0f, zero = 0.0f;
+    for (int64_t r0 = 0; r0 < V && bs == rocblas_status_success; r0 += R) {
+        const int64_t rows = std::min(R, V - r0);
+        // column-major view: W^T is d x V (ld d); scores (V x rows, ld) = W[all] . W[chunk]^T
+        const char *Wc = static_cast<const char *>(W_dev) + r0 * row_bytes;
+        if (dtype == VIE_F32)
+            bs = rocblas_sgemm(h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)V,
+                               (rocblas_int)rows, d, &one, static_cast<const float *>(W_dev), d,
+                               reinterpret_cast<const float *>(Wc), d, &zero, b.S, (rocblas_int)ld);
+        else
+            bs = rocblas_gemm_ex(h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)V,
+                                 (rocblas_int)rows, d, &one, W_dev, rocblas_datatype_bf16_r, d, Wc,
+                                 rocblas_datatype_bf16_r, d, &zero, b.S, rocblas_datatype_f32_r, (rocblas_int)ld, b.S,
+                                 rocblas_datatype_f32_r, (rocblas_int)ld, rocblas_datatype_f32_r,
+                                 rocblas_gemm_algo_standard, 0, 0);
+        if (bs != rocblas_status_success) break;
+        knn_topk_kernel<<<(unsigned)rows, kTopkThreads, 0, s>>>(b.S, ld, r0, V, K, b.cand, b.cand_score);
+        he = hipGetLastError();
+        if (he != hipSuccess) break;
+    }
+    (void)rocblas_destroy_handle(h);
+    if (bs != rocblas_status_success) return bail(blas_fail(bs, "GPU build: Gram GEMM"));
+    if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: top-k launch: %s", hipGetErrorString(he)));
+
+    sel<<<(unsigned)V, kSelectThreads, lds, s>>>(static_cast<const char *>(W_dev), row_bytes, K, M0, b.cand,
+                                                 b.cand_score, b.fwd, b.fwd_score, b.nfwd);
+    he = hipMemsetAsync(b.count, 0, (size_t)V * 4, s);
+    const unsigned eg = (unsigned)((edges + 255) / 256);
+    if (he == hipSuccess) {
+        knn_reverse_kernel<<<eg, 256, 0, s>>>(V, M0, b.fwd, b.fwd_score, b.nfwd, b.count, b.roff, b.rev, 0);
+        knn_scan_kernel<<<1, 1024, 0, s>>>(b.count, V, b.roff);
+        he = hipMemsetAsync(b.count, 0, (size_t)V * 4, s);
+    }
+    if (he == hipSuccess) {
+        knn_reverse_kernel<<<eg, 256, 0, s>>>(V, M0, b.fwd, b.fwd_score, b.nfwd, b.count, b.roff, b.rev, 1);
+        knn_lists_kernel<<<(unsigned)V, kTopkThreads, 0, s>>>(M0, b.fwd, b.nfwd, b.roff, b.rev, b.adj0);
+        he = hipMemsetAsync(b.best, 0, 8, s);
+    }
+    if (he == hipSuccess) {
+        const unsigned eb = (unsigned)((V + 3) / 4);
+        if (dtype == VIE_BF16) knn_entry_kernel<true><<<eb, 256, 0, s>>>(static_cast<const char *>(W_dev), V, row_bytes, b.best);
+        else knn_entry_kernel<false><<<eb, 256, 0, s>>>(static_cast<const char *>(W_dev), V, row_bytes, b.best);
+        he = hipMemsetAsync(b.upper_off, 0xFF, (size_t)V * 4, s);  // every node on layer 0 only: -1
+    }
+    if (he == hipSuccess) he = hipGetLastError();
+    if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
+
+    // host form of the graph (the index file and vie_index_export read it)
+    g = Graph();
+    g.V = V;
+    g.d = d;
+    g.dtype = dtype;
+    g.M0 = M0;
+    g.M = std::min(M0, std::max(2, M0 / 2));
+    g.efC = K;
+    g.seed = 0;
+    g.maxlevel = 0;
+    g.levels.assign((size_t)V, 0);
+    g.adj0.resize((size_t)edges);
+    g.upper_off.assign((size_t)V, -1);
+    unsigned long long best = 0;
+    he = hipMemcpyAsync(g.adj0.data(), b.adj0, (size_t)edges * 4, hipMemcpyDeviceToHost, s);
+    if (he == hipSuccess) he = hipMemcpyAsync(&best, b.best, 8, hipMemcpyDeviceToHost, s);
+    // the rows the W_out fingerprint samples
+    const int64_t step = V / 1024 > 1 ? V / 1024 : 1;
+    std::vector<int64_t> rows;
+    for (int64_t r = 0; r < V; r += step) rows.push_back(r);
+    rows.push_back(V - 1);
+    std::vector<char> sample(rows.size() * (size_t)row_bytes);
+    for (size_t t = 0; t < rows.size() && he == hipSuccess; ++t)
+        he = hipMemcpyAsync(sample.data() + t * row_bytes, static_cast<const char *>(W_dev) + rows[t] * row_bytes,
+                            row_bytes, hipMemcpyDeviceToHost, s);
+    if (he == hipSuccess) he = hipStreamSynchronize(s);
+    if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
+    g.entry = (int32_t)(~(uint32_t)best);
+    g.fingerprint = w_fingerprint_rows(sample.data(), dtype, V, d, (int64_t)rows.size());
+    b.release();
+
+    dg = DeviceGraph();
+    dg.device = dev;
+    dg.W = W_dev;
+    dg.adj0 = b.adj0;
+    dg.upper_off = b.upper_off;
+    dg.upper = b.upper;
+    return VIE_OK;
+}
+
+}  // namespace vie

@@ -34,6 +34,10 @@ class BuildParams(C.Structure):
                 ("seed", C.c_uint64), ("select", C.c_int32)]
 
 
+class GpuBuildParams(C.Structure):
+    _fields_ = [("K", C.c_int32), ("M0", C.c_int32), ("chunk_rows", C.c_int64)]
+
+
 class IndexDesc(C.Structure):
     _fields_ = [("V", C.c_int64), ("d", C.c_int32), ("dtype", C.c_int32), ("M", C.c_int32), ("M0", C.c_int32),
                 ("ef_construction", C.c_int32), ("maxlevel", C.c_int32), ("entry", C.c_int32),
@@ -49,6 +53,7 @@ def _load() -> C.CDLL:
     st = C.c_int
     sig = {
         "vie_index_build": (st, [vp, i32, i64, i32, C.POINTER(BuildParams), C.POINTER(vp)]),
+        "vie_index_build_gpu": (st, [vp, i32, i64, i32, C.POINTER(GpuBuildParams), vp, C.POINTER(vp)]),
         "vie_index_save": (st, [vp, C.c_char_p]),
         "vie_index_load": (st, [C.c_char_p, vp, C.POINTER(vp)]),
         "vie_index_to_device": (st, [vp, vp, vp]),
@@ -138,6 +143,23 @@ class Index:
         _check(lib.vie_index_build(W.ctypes.data_as(C.c_void_p), dtype, W.shape[0], W.shape[1], C.byref(p),
                                    C.byref(h)))
         return cls(h)
+
+    @classmethod
+    def build_gpu(cls, W_dev, K: int, M0: int, chunk_rows: int = 0) -> "Index":
+        """Single-layer batch graph over the rows of the device matrix W_dev
+        (vie_index_build_gpu); the index comes back on W_dev's device."""
+        torch = _torch()
+        dt = _dtype_of_tensor(W_dev)
+        V, d = W_dev.shape
+        p = GpuBuildParams(K, M0, chunk_rows)
+        h = C.c_void_p()
+        with torch.cuda.device(W_dev.device):
+            _check(lib.vie_index_build_gpu(_dev_ptr(W_dev, "W_dev"), dt, V, d, C.byref(p), _stream(W_dev),
+                                           C.byref(h)))
+        ix = cls(h)
+        ix._W_dev = W_dev
+        ix._q8 = None
+        return ix
 
     @classmethod
     def load(cls, path: str, W: np.ndarray | None = None) -> "Index":

@@ -1,0 +1,164 @@
+"""GPU batch graph construction (vie_index_build_gpu) against the oracle's
+batch construction on the same rows.
+
+With small-integer rows every fp32 inner product is exact, so the GPU graph
+must equal the oracle's bit for bit (lists, entry point, index file); such
+rows also produce many equal scores, which exercises every tie rule and the
+multi-round selection.  On random rows fp32 and fp64 scores differ in the
+last bits, so a list may differ only where a decision was a near tie.
+"""
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2608_27460_amd import synth
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def vie():
+    assert torch.cuda.is_available(), "the gpu tests need an MI355X"
+    from paper_2608_27460_amd import vie as v
+    return v
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def integer_rows(V, d, dtype, seed, lo=-3, hi=3, hubs=()):
+    rng = np.random.default_rng(seed)
+    Wf = rng.integers(lo, hi + 1, size=(V, d)).astype(np.float32)
+    for rows, factor in hubs:
+        Wf[rows] *= factor
+    return Wf if dtype == synth.F32 else synth.f32_to_bf16_bits(Wf)
+
+
+def build_both(vie, W, dtype, K, M0, chunk_rows=0):
+    Wd = vie.host_to_torch(W, dtype).cuda()
+    ix = vie.Index.build_gpu(Wd, K, M0, chunk_rows)
+    torch.cuda.synchronize()
+    g = O.knn_graph(W, dtype, K, M0)
+    return ix, g, Wd
+
+
+@pytest.mark.parametrize("V,d,dtype,K,M0,chunk", [
+    (600, 16, synth.F32, 24, 12, 0),
+    (3000, 64, synth.BF16, 64, 32, 0),
+    (2000, 32, synth.BF16, 128, 64, 0),     # the largest K
+    (1500, 48, synth.F32, 40, 64, 0),       # K <= M0: candidates kept whole
+    (2500, 32, synth.BF16, 48, 24, 700),    # four Gram chunks, the last one ragged
+    (129, 8, synth.BF16, 128, 16, 0),       # K = V - 1
+])
+def test_integer_rows_give_the_oracle_graph(vie, tmp_path, V, d, dtype, K, M0, chunk):
+    say("gpu build (integer rows)", V, d, dtype, K, M0, chunk)
+    W = integer_rows(V, d, dtype, V + d)
+    ix, g, _ = build_both(vie, W, dtype, K, M0, chunk)
+    ex = ix.export()
+    info = ix.info()
+    assert info["maxlevel"] == 0 and info["entry"] == g.entry and info["on_device"] == 1
+    bad = np.nonzero(np.any(ex["adj0"] != g.adj0, axis=1))[0]
+    assert len(bad) == 0, "lists differ at %d nodes, first %s: gpu %s oracle %s" % (
+        len(bad), bad[:5], ex["adj0"][bad[0]].tolist(), g.adj0[bad[0]].tolist())
+    # the index files of both implementations are byte-identical
+    pg, po = str(tmp_path / "gpu.vie"), str(tmp_path / "oracle.vie")
+    ix.save(pg)
+    O.save_graph(g, po, W)
+    assert open(pg, "rb").read() == open(po, "rb").read()
+
+
+def test_integer_hub_rows_with_large_reverse_lists(vie):
+    # five rows of ten times the norm are near to nearly every row, so each
+    # collects thousands of reverse edges (more than one selection round holds)
+    V, d, K, M0 = 6000, 32, 32, 16
+    W = integer_rows(V, d, synth.BF16, 5, hubs=[(np.arange(5) * 1000 + 7, 10.0)])
+    ix, g, _ = build_both(vie, W, synth.BF16, K, M0)
+    ex = ix.export()
+    assert ix.info()["entry"] == g.entry
+    assert np.array_equal(ex["adj0"], g.adj0)
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
+def test_random_rows_match_the_oracle_up_to_near_ties(vie, dtype):
+    V, d, K, M0 = 4000, 128, 64, 32
+    W = synth.make_w(V, d, dtype, 17)
+    ix, g, Wd = build_both(vie, W, dtype, K, M0)
+    ex = ix.export()
+    assert O.check_graph(O.Graph(V, d, dtype, max(2, M0 // 2), M0, K, 0, 0, ix.info()["entry"],
+                                 np.zeros(V, np.uint8), ex["adj0"], -np.ones(V, np.int32),
+                                 np.zeros((0, max(2, M0 // 2)), np.int32))) == ""
+    same = np.all(ex["adj0"] == g.adj0, axis=1)
+    say("identical lists: %d of %d" % (same.sum(), V))
+    assert same.mean() >= 0.98
+    # every node keeps its exact nearest other row first (the heuristic keeps
+    # the first candidate) unless that choice is a near tie in fp64
+    Wf = synth.stored_values_f32(W, dtype).astype(np.float64)
+    Gm = Wf @ Wf.T
+    np.fill_diagonal(Gm, -np.inf)
+    best = np.argmax(Gm, axis=1)
+    first = ex["adj0"][:, 0]
+    for i in np.nonzero(first != best)[0]:
+        a, b = Gm[i, best[i]], Gm[i, first[i]]
+        assert abs(a - b) <= 1e-5 * abs(a), (i, a, b)
+    # a search on the GPU graph walks the same path as the oracle's search on it
+    H, _ = synth.make_queries(W, dtype, 32, 18)
+    h = vie.host_to_torch(H, dtype).cuda()
+    ids, lg, st = ix.query(h, 10, 48, stats=True)
+    torch.cuda.synchronize()
+    gg = O.Graph(V, d, dtype, max(2, M0 // 2), M0, K, 0, 0, ix.info()["entry"], np.zeros(V, np.uint8),
+                 ex["adj0"], -np.ones(V, np.int32), np.zeros((0, max(2, M0 // 2)), np.int32))
+    oid, olg, ost, _ = O.hnsw_search(W, dtype, gg, H, 10, 48, validate=False)
+    same_walk = np.all(st.cpu().numpy().astype(np.uint32) == ost, axis=1)
+    assert same_walk.sum() >= 31
+    for q in np.nonzero(same_walk)[0]:
+        assert set(ids.cpu().numpy()[q].tolist()) == set(oid[q].tolist())
+
+
+def test_rejects_bad_parameters(vie):
+    W = torch.zeros((100, 16), dtype=torch.bfloat16, device="cuda")
+    for K, M0 in [(0, 8), (100, 8), (129, 8), (8, 1), (8, 257)]:
+        with pytest.raises(vie.VieError):
+            vie.Index.build_gpu(W, K, M0)
+    with pytest.raises(vie.VieError):
+        vie.Index.build_gpu(torch.zeros((100, 12), dtype=torch.bfloat16, device="cuda"), 8, 8)  # 24-byte rows
+
+
+def test_qwen_shaped_head_sampled(vie):
+    # the full 151936 x 1024 bf16 head: invariants, the entry point, and the
+    # first list entry of sampled nodes against brute force
+    wl = synth.WORKLOADS["qwen3-0.6b"]
+    W = wl.make_w()
+    Wd = vie.host_to_torch(W, wl.dtype).cuda()
+    say("gpu build, qwen shape")
+    t0 = time.perf_counter()
+    ix = vie.Index.build_gpu(Wd, 64, 64)
+    torch.cuda.synchronize()
+    say("built in %.3f s" % (time.perf_counter() - t0))
+    ex = ix.export()
+    info = ix.info()
+    V, M0 = wl.V, 64
+    gg = O.Graph(V, wl.d, wl.dtype, 32, M0, 64, 0, 0, info["entry"], np.zeros(V, np.uint8), ex["adj0"],
+                 -np.ones(V, np.int32), np.zeros((0, 32), np.int32))
+    assert O.check_graph(gg) == ""
+    Wf = synth.stored_values_f32(W, wl.dtype)
+    norms = np.einsum("ij,ij->i", Wf.astype(np.float64), Wf.astype(np.float64))
+    top = np.argmax(norms)
+    assert info["entry"] == top or abs(norms[info["entry"]] - norms[top]) <= 1e-5 * norms[top]
+    rng = np.random.default_rng(0)
+    sample = rng.choice(V, 16, replace=False)
+    eid, _, esc = O.topk(W, wl.dtype, W[sample], 2)
+    for n, i in enumerate(sample):
+        nearest = eid[n, 1] if eid[n, 0] == i else eid[n, 0]
+        got = ex["adj0"][i, 0]
+        if got != nearest:
+            s = O.pair_scores(W, wl.dtype, W[i:i + 1], np.zeros(2, np.int32), np.array([nearest, got], np.int32))
+            assert abs(s[0] - s[1]) <= 1e-4 * abs(s[0]), (i, nearest, got, s)

@@ -15,6 +15,11 @@ the exact dense head) and the per-kernel roofline figures are reported next
 to it.  The CPU baseline is the plain-C oracle's HNSW search on the same
 graph (one thread, a bounded sample of the same queries).
 
+The batch-graph leg builds a single-layer graph over W_out on the GPU
+(vie_index_build_gpu: exact 128 nearest rows by inner product, the
+neighbour-selection heuristic, reverse edges) and searches it at B = 1 with
+the same protocol, next to the HNSW graph built on the host CPUs.
+
 The other workloads (--workload tiny | llama3.2-1b | gemma3-270m |
 llama3.2-3b) run the same protocol at their own shapes, ef and k; the Gemma
 shape adds a k sweep (20, 50, 100) and the Llama-3.2-3B shape a sweep of
@@ -84,6 +89,10 @@ def main() -> int:
                     help="forced-inclusion tokens of the forced leg (ids 0..n-1 stand in for special tokens)")
     ap.add_argument("--widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[2, 4, 8],
                     help="expansion widths of the vie_query_ex sweep (comma separated)")
+    ap.add_argument("--batch-graph-k", type=int, default=128,
+                    help="candidates per node of the GPU-built batch graph leg (0: skip the leg)")
+    ap.add_argument("--batch-graph-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024],
+                    help="extra beam widths searched on the batch graph (first --sweep-queries queries)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="finish with a device copy of this many MiB (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -116,6 +125,7 @@ def main() -> int:
     gpath = os.path.join(args.cache, "%s-M%d-efC%d-seed%d.vie" % (wl.name, wl.M, wl.efC, wl.seed_levels))
     t0 = time.time()
     ix = None
+    cpu_build_s = None
     if os.path.exists(gpath):
         try:
             ix = vie.Index.load(gpath, W)
@@ -126,7 +136,8 @@ def main() -> int:
         nt = min(16, os.cpu_count() or 1)
         ix = vie.Index.build(W, wl.dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=nt)
         ix.save(gpath)
-        log("[bench] graph built with %d threads in %.1fs" % (nt, time.time() - t0))
+        cpu_build_s = time.time() - t0
+        log("[bench] graph built with %d threads in %.1fs" % (nt, cpu_build_s))
     info = ix.info()
 
     Wd = vie.host_to_torch(W, wl.dtype).to(dev)
@@ -274,6 +285,44 @@ def main() -> int:
         ix.attach_int8(None, None)
         del qrows, qscale
 
+    # ---- batch graph built on the GPU (vie_index_build_gpu), searched at B = 1 ----
+    batch = None
+    if args.batch_graph_k:
+        Kb = min(args.batch_graph_k, wl.V - 1)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        bix = vie.Index.build_gpu(Wd, Kb, wl.M0)  # first call: includes the GEMM library's set-up
+        first_s = time.perf_counter() - t0
+        del bix
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        bix = vie.Index.build_gpu(Wd, Kb, wl.M0)
+        build_s = time.perf_counter() - t0
+        bsweep = {}
+        for e in sorted(set(wl.ef) | {ef} | set(args.batch_graph_ef)):
+            nq = Q if e <= max(max(wl.ef), ef) else min(Q, args.sweep_queries)
+            bi = torch.empty((nq, k), dtype=torch.int32, device=dev)
+            bl = torch.empty((nq, k), dtype=torch.float32, device=dev)
+            bs = torch.empty((nq, 2), dtype=torch.int32, device=dev)
+            b_us = per_call_us(lambda c: bix.query_into(hv[c], k, e, bi[c:c + 1], bl[c:c + 1], bs[c:c + 1]), nq)
+            bst = bs.cpu().numpy().astype(np.int64)
+            bsweep[str(e)] = {"us_per_query": round(b_us, 2), "queries": nq,
+                              "recall_at_k": round(recall(bi.cpu().numpy(), exact_ids[:nq]), 4),
+                              "recall_at_2": round(recall(bi.cpu().numpy(), exact_ids[:nq], 2), 4),
+                              "mean_n_dist": float(bst[:, 0].mean()), "mean_n_expand": float(bst[:, 1].mean())}
+        bix.query_into(Hd, k, ef, ids, lg, st)
+        torch.cuda.synchronize()
+        a.record(stream)
+        bix.query_into(Hd, k, ef, ids, lg, st)
+        b.record(stream)
+        torch.cuda.synchronize()
+        batch = {"K": Kb, "M0": wl.M0, "build_s": round(build_s, 4), "first_build_s": round(first_s, 4),
+                 "cpu_hnsw_build_s": None if cpu_build_s is None else round(cpu_build_s, 2),
+                 "entry": bix.info()["entry"], "ef_sweep": bsweep,
+                 "batched_queries_per_s": round(Q / (a.elapsed_time(b) * 1e-3), 1),
+                 "batched_recall_at_k": round(recall(ids.cpu().numpy(), exact_ids), 4)}
+        del bix
+
     # ---- forced-inclusion tokens (stand-in: the first 64 ids; B = 1) -------
     forced = None
     if args.forced:
@@ -380,7 +429,7 @@ def main() -> int:
                  "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
                  "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
                  "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None,
-                 "int8_sweep": q_sweep or None, "forced": forced},
+                 "int8_sweep": q_sweep or None, "forced": forced, "batch_graph": batch},
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,

@@ -1,13 +1,20 @@
 // gfx950 (CDNA4) kernels of the vector-index output head.
 //
-//   scatter_kernel      Section 3: full-vocabulary logits, -inf except the
-//                       retrieved ids.
-//   dense_slab_kernel,  exact head z = W_out h fused with top-k (Section 3;
-//   dense_mfma_kernel,  the dense baseline of Section 4.1): slab logits on
-//   dense_merge_kernel  the vector ALUs (one to a few queries) or the matrix
-//                       cores (batches), then the top k from slab summaries.
-//   hnsw_kernel         HNSW k-NN search (Sections 2-3; Malkov & Yashunin
-//                       Algorithms 2 and 5), one workgroup per query.
+//   scatter_kernel       Section 3: full-vocabulary logits, -inf except the
+//                        retrieved ids.
+//   dense_stream_kernel, exact head z = W_out h fused with top-k (Section 3;
+//   dense_slab_kernel,   the dense baseline of Section 4.1): slab logits on
+//   dense_mfma_kernel,   the vector ALUs (one to a few queries) or the
+//   dense_merge_kernel   matrix cores (batches), then the top k from the
+//                        slabs' candidate lists.
+//   hnsw_kernel          HNSW k-NN search (Sections 2-3; Malkov & Yashunin
+//                        Algorithms 2 and 5), one workgroup per query.
+//   hnsw_multi_kernel    the same search expanding several beam entries per
+//                        layer-0 step, optionally on int8 rows (Section 5's
+//                        open problems: sequential traversal, quantization).
+//   quantize_kernel      per-row scaled int8 copy of W_out.
+//   forced_kernel        search result joined with explicitly scored ids
+//                        (Section 3's forced-inclusion tokens).
 //
 // Ordering: candidates are the 64-bit keys of keys.hpp (larger logit first,
 // smaller id first on equal logits).

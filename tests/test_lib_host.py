@@ -177,6 +177,25 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_scatter(fake, fake, 1, 0, 100, fake, None) == vie.EINVAL
     assert L.vie_scatter(fake, fake, 1, 5, 0, fake, None) == vie.EINVAL
     assert L.vie_scatter(None, fake, 1, 5, 100, fake, None) == vie.EINVAL
+    out = C.c_void_p()
+    gp = lambda K, M0, chunk=0: C.byref(vie.GpuBuildParams(K, M0, chunk))  # noqa: E731
+    for args, want in [((None, 1, 1000, 64, gp(32, 16)), vie.EINVAL),
+                       ((fake, 1, 1000, 64, None), vie.EINVAL),
+                       ((fake, 1, 1, 64, gp(32, 16)), vie.EINVAL),         # V = 1
+                       ((fake, 1, 1000, 0, gp(32, 16)), vie.EINVAL),       # d
+                       ((fake, 5, 1000, 64, gp(32, 16)), vie.EINVAL),      # dtype
+                       ((fake, 1, 1000, 64, gp(0, 16)), vie.EINVAL),       # K = 0
+                       ((fake, 1, 1000, 64, gp(129, 16)), vie.EINVAL),     # K > 128
+                       ((fake, 1, 100, 64, gp(100, 16)), vie.EINVAL),      # K > V - 1
+                       ((fake, 1, 1000, 64, gp(32, 1)), vie.EINVAL),       # M0 < 2
+                       ((fake, 1, 1000, 64, gp(32, 257)), vie.EINVAL),     # M0 > 256
+                       ((fake, 1, 1000, 64, gp(32, 16, -1)), vie.EINVAL),  # chunk_rows < 0
+                       ((fake, 1, 1000, 12, gp(32, 16)), vie.EUNSUPPORTED),            # 24-byte rows
+                       ((C.c_void_p(4096 + 8), 1, 1000, 64, gp(32, 16)), vie.EUNSUPPORTED)]:  # misaligned
+        assert L.vie_index_build_gpu(*args, None, C.byref(out)) == want, args
+        assert not out.value
+    assert L.vie_last_error() == b"GPU build needs 16-byte aligned rows (d = 64 of dtype 1)"
+    assert L.vie_scatter(None, fake, 1, 5, 100, fake, None) == vie.EINVAL
     assert L.vie_last_error() == b"NULL argument"
 
 

@@ -183,17 +183,103 @@ __device__ int block_topk(int64_t n, int K, KeyAt key_at, TopkShared &sh)
 }
 
 // Step 1, per row of a chunk: the K nearest other rows from the chunk's
-// scores S [rows][ld] (row r of the chunk is row r0 + r of W_out).
+// scores S [rows][ld] (row r of the chunk is row r0 + r of W_out; rows start
+// 16-byte aligned).  A sample of the row (every kSampleEvery-th block of
+// kTopkThreads scores) gives a threshold T0 with about twice the sample's
+// share of K keys above it; one vectorized pass then gathers every key >= T0.
+// If at least K and at most kGatherCap keys were gathered, every key of the
+// answer is among them (K keys are >= T0, so the K-th largest is too) and a
+// sort finishes; otherwise the exact radix select runs.  The sample only
+// decides the speed, never the result.
+constexpr int kSampleEvery = 8;
+
 __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__restrict__ S, int64_t ld, int64_t r0,
                                                                 int64_t V, int K, int32_t *__restrict__ cand,
                                                                 float *__restrict__ cand_score)
 {
     __shared__ TopkShared sh;
+    const int tid = threadIdx.x;
     const int64_t i = r0 + blockIdx.x;
     const float *row = S + (int64_t)blockIdx.x * ld;
     auto key_at = [&](int64_t j) -> uint64_t { return j == i ? 0ull : make_key(row[j], (int32_t)j); };
-    const int m = block_topk<kTopkThreads>(V, K, key_at, sh);
-    for (int t = threadIdx.x; t < K; t += kTopkThreads) {
+
+    // sample: blocks 0, kSampleEvery, 2 kSampleEvery, ... of kTopkThreads scores
+    for (int bkt = tid; bkt < kDigitBuckets; bkt += kTopkThreads) sh.hist[bkt] = 0u;
+    if (tid == 0) {
+        sh.n = 0u;
+        sh.bucket = 0u;
+        sh.count = 0u;
+    }
+    __syncthreads();
+    uint32_t ns = 0;
+    for (int64_t j0 = 0; j0 < V; j0 += (int64_t)kSampleEvery * kTopkThreads) {
+        const int64_t j = j0 + tid;
+        ns += (uint32_t)min<int64_t>(kTopkThreads, V - j0);
+        if (j < V) {
+            const uint64_t key = key_at(j);
+            if (key) atomicAdd(&sh.hist[(uint32_t)(key >> (64 - kDigitBits))], 1u);
+        }
+    }
+    const uint32_t want = (uint32_t)((2 * (int64_t)K * ns + V - 1) / V) + 4;
+    __syncthreads();
+    {
+        constexpr int per = kDigitBuckets / kTopkThreads;
+        uint32_t c[per], sum = 0;
+#pragma unroll
+        for (int j = 0; j < per; ++j) {
+            c[j] = sh.hist[kDigitBuckets - 1 - (per * tid + j)];
+            sum += c[j];
+        }
+        uint32_t above = block_exclusive_scan<kTopkThreads>(sum, sh.wsum);
+#pragma unroll
+        for (int j = 0; j < per; ++j) {
+            if (above < want && want <= above + c[j]) {
+                sh.bucket = (uint32_t)(kDigitBuckets - 1 - (per * tid + j));
+                sh.count = 1u;
+            }
+            above += c[j];
+        }
+    }
+    __syncthreads();
+    // (fewer sampled keys than want: T0 = 1, every key)
+    const uint64_t T0 = sh.count ? ((uint64_t)sh.bucket << (64 - kDigitBits)) | 1ull : 1ull;
+    // gather every key >= T0, four scores per load, four loads in flight
+    const int64_t n4 = (V + 3) / 4;
+    const float4 *row4 = reinterpret_cast<const float4 *>(row);
+    for (int64_t b0 = 0; b0 < n4; b0 += 4 * kTopkThreads) {
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t q = b0 + u * kTopkThreads + tid;
+            v[u] = q < n4 ? row4[q] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t j = 4 * (b0 + u * kTopkThreads + tid);
+            const float x[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (j + e < V && j + e != i) {
+                    const uint64_t key = make_key(x[e], (int32_t)(j + e));
+                    if (key >= T0) {
+                        const uint32_t slot = atomicAdd(&sh.n, 1u);
+                        if (slot < (uint32_t)kGatherCap) sh.gat[slot] = key;
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    const uint32_t ng = sh.n;
+    int m;
+    if (ng >= (uint32_t)K && ng <= (uint32_t)kGatherCap) {
+        block_sort_desc<kTopkThreads>(sh.gat, (int)ng);
+        m = K;
+    } else {
+        __syncthreads();
+        m = block_topk<kTopkThreads>(V, K, key_at, sh);
+    }
+    for (int t = tid; t < K; t += kTopkThreads) {
         const uint64_t key = t < m ? sh.gat[t] : 0ull;
         cand[i * K + t] = t < m ? key_id(key) : -1;
         cand_score[i * K + t] = t < m ? key_logit(key) : 0.0f;

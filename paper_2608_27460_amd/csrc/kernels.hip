@@ -1050,9 +1050,11 @@ __global__ __launch_bounds__(kQuantWaves *kWave) void quantize_kernel(const void
 //
 // Latency hiding that keeps those semantics: the next step expands either
 // the entry that is now second best among the unexpanded ones, or the best
-// node this step inserts.  Both layer-0 lists are fetched during this step's
+// node this step inserts, and which one is known as soon as the rows are
+// scored.  Both layer-0 lists are fetched into registers during this step's
 // row loads (the second with spare threads, each new node's by the group
-// that scores its row), so the next step finds its list in LDS.  The beam is
+// that scores its row), and the threads holding the winner's list claim its
+// neighbours for the next step while the others merge the beam.  The beam is
 // double buffered (merge from one buffer into the other).
 
 struct HnswShared {
@@ -1060,6 +1062,9 @@ struct HnswShared {
     uint32_t nnew, nkeep;
     uint32_t first, second, nbeam;
     int32_t pfa_id, pfb_id;  // nodes whose layer-0 lists sit in pfa[] / pfb[]
+    // hnsw_kernel's layer-0 loop: per step parity
+    unsigned long long bestp[2];
+    uint32_t nnewp[2], nkeepp[2], firstp[2];
 };
 
 __device__ __forceinline__ void clear_bits(uint32_t *vis, int words)
@@ -1189,10 +1194,6 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     p += (size_t)maxdeg * 8;
     int32_t *cid = reinterpret_cast<int32_t *>(p);
     p += (size_t)maxdeg * 4;
-    int32_t *pfa = reinterpret_cast<int32_t *>(p);
-    p += (size_t)M0 * 4;
-    int32_t *pfb = reinterpret_cast<int32_t *>(p);
-    p += (size_t)M0 * 4;
     uint8_t *flag = reinterpret_cast<uint8_t *>(p);
     p += (size_t)ef;
     uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
@@ -1201,11 +1202,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 
     const char *h = hq + (int64_t)q * row_bytes;
     for (int i = tid; i < hbytes; i += NT) hs[i] = i < row_bytes ? h[i] : 0;
-    if (tid == 0) {
-        sh.best = 0;
-        sh.pfa_id = -1;
-        sh.pfb_id = -1;
-    }
+    if (tid == 0) sh.best = 0;
     __syncthreads();
 
     const int gl = tid % G;
@@ -1216,47 +1213,57 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
                                                    vis, sh, n_dist, n_expand);
 
     // layer 0: beam of ef keys, sorted descending, with expanded flags,
-    // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...).  Three
-    // workgroup barriers per expansion: after the claim, after the row
-    // scores, after the merge.  Every shared counter is reset by thread 0 in
-    // a phase where no other thread reads or updates it.
+    // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...).  Two
+    // workgroup barriers per expansion.  Step t: (score) the rows of the
+    // nodes claimed for step t are scored while the list of the second-best
+    // unexpanded entry is fetched into registers; (merge) the kept keys are
+    // merged into the other buffer while the node expanded at step t + 1 --
+    // the better of the best kept key and that second entry, both known at
+    // this point -- has its list claimed by the threads that hold it in
+    // registers.  Counters used across the two phases are double buffered by
+    // the parity of t and reset by thread 0 only in a phase where no other
+    // thread reads or updates them.
     clear_bits(vis, vwords);
     __syncthreads();
     if (tid == 0) {
         vis[key_id(cur) >> 5] |= 1u << (key_id(cur) & 31);
         beam[0] = cur;
-        flag[0] = 0;
+        flag[0] = 1;  // expanded at step 0
         sh.nbeam = 1;
-        sh.first = 0;
-        sh.nnew = 0;
-        sh.second = 0xFFFFFFFFu;
+        sh.firstp[0] = 0;
+        sh.firstp[1] = 0xFFFFFFFFu;
+        sh.nnewp[0] = sh.nnewp[1] = 0;
+        sh.nkeepp[0] = sh.nkeepp[1] = 0;
+        sh.bestp[0] = sh.bestp[1] = 0ull;
     }
     __syncthreads();
-    for (;;) {
-        const uint32_t first = sh.first, nbeam = sh.nbeam;
-        if (first >= nbeam) break;
-        const int32_t c = key_id(beam[first]);
-        const int32_t *lst = sh.pfa_id == c ? pfa : (sh.pfb_id == c ? pfb : nullptr);
-        if (tid == 0) {
-            flag[first] = 1;  // read again only after the next barrier
-            sh.nkeep = 0;     // last read before the previous merge
-            sh.best = 0;
-        }
-        ++n_expand;
-        // claim the unseen neighbours; find the next unexpanded entry after first
+    {
+        // claim the layer-0 entry point's neighbours for step 0
+        const int32_t c = key_id(cur);
         for (int t = tid; t < M0; t += NT) {
-            const int32_t e = lst ? lst[t] : adj0[(int64_t)c * M0 + t];
-            if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
+            const int32_t e = adj0[(int64_t)c * M0 + t];
+            if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnewp[0], 1u)] = e;
         }
-        for (int i0 = (int)first + 1 + (tid & ~(kWave - 1)); i0 < (int)nbeam; i0 += NT) {
+    }
+    __syncthreads();
+    for (int step = 0;; ++step) {
+        const int par = step & 1;
+        // ---- score ----
+        const uint32_t first = sh.firstp[par], nbeam = sh.nbeam;
+        const int nn = (int)sh.nnewp[par];
+        ++n_expand;
+        n_dist += nn;
+        if (tid == 0) sh.firstp[par ^ 1] = 0xFFFFFFFFu;  // last read in the previous step's score phase
+        // the second-best unexpanded entry: every wave scans the flags itself
+        uint32_t second = 0xFFFFFFFFu;
+        for (int i0 = (int)first + 1; i0 < (int)nbeam; i0 += kWave) {
             const int i = i0 + lane;
             const uint64_t ball = __ballot(i < (int)nbeam && !flag[i]);
-            if (ball && lane == 0) atomicMin(&sh.second, (uint32_t)(i0 + __ffsll((long long)ball) - 1));
+            if (ball) {
+                second = (uint32_t)(i0 + __ffsll((long long)ball) - 1);
+                break;
+            }
         }
-        __syncthreads();
-        const int nn = (int)sh.nnew;
-        n_dist += nn;
-        const uint32_t second = sh.second;
         const int32_t ida = second < nbeam ? key_id(beam[second]) : -1;
         // spare threads fetch the second entry's list while the rows load
         int32_t pfv = -1;
@@ -1277,31 +1284,44 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             }
             const float s = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
             const uint64_t key = make_key(s, e);
-            if (gl == 0 && key > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = key;
+            if (gl == 0 && key > worst) ckey[atomicAdd(&sh.nkeepp[par], 1u)] = key;
             if (key > gbest) {
                 gbest = key;
 #pragma unroll
                 for (int u = 0; u < kPfbPerLane; ++u) glist[u] = l[u];
             }
         }
-        if (gl == 0 && gbest > worst) atomicMax(&sh.best, (unsigned long long)gbest);
-        if (tid == 0) sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
+        if (gl == 0 && gbest > worst) atomicMax(&sh.bestp[par], (unsigned long long)gbest);
         __syncthreads();
-        if (ida >= 0 && pft >= 0) pfa[pft] = pfv;
-        const uint64_t bestnew = sh.best;
-        if (pfb_on && bestnew != 0ull && gbest == bestnew) {
+        // ---- merge, and the claim of the next step ----
+        const uint64_t bestnew = sh.bestp[par];
+        const int nk = (int)sh.nkeepp[par];
+        const uint64_t second_key = ida >= 0 ? beam[second] : 0ull;
+        const uint64_t next = bestnew > second_key ? bestnew : second_key;  // expanded at step + 1
+        if (next != 0ull) {
+            if (next == second_key) {
+                if (pft >= 0 && pfv >= 0 && claim(vis, pfv)) cid[atomicAdd(&sh.nnewp[par ^ 1], 1u)] = pfv;
+            } else if (pfb_on) {
+                if (gbest == bestnew) {
 #pragma unroll
-            for (int u = 0; u < kPfbPerLane; ++u) {
-                const int t = gl + u * G;
-                if (t < M0) pfb[t] = glist[u];
+                    for (int u = 0; u < kPfbPerLane; ++u) {
+                        const int t = gl + u * G;
+                        if (t < M0 && glist[u] >= 0 && claim(vis, glist[u]))
+                            cid[atomicAdd(&sh.nnewp[par ^ 1], 1u)] = glist[u];
+                    }
+                }
+            } else {
+                const int32_t c = key_id(next);
+                for (int t = tid; t < M0; t += NT) {
+                    const int32_t e = adj0[(int64_t)c * M0 + t];
+                    if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnewp[par ^ 1], 1u)] = e;
+                }
             }
         }
-        const int nk = (int)sh.nkeep;
         // merge the beam (nbeam, sorted) and the kept keys (nk, unordered,
         // distinct) into beam2, keeping the best ef: a kept key lands at
         // (kept keys above it) + (beam keys above it), a beam key at its
-        // index + (kept keys above it).  The new first unexpanded entry is
-        // the best kept key or the old second.
+        // index + (kept keys above it).  The next expanded entry is marked.
         const int total = min((int)nbeam + nk, ef);
         for (int j = tid; j < nk; j += NT) {
             const uint64_t key = ckey[j];
@@ -1315,8 +1335,8 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             const int pos = lo + above;
             if (pos < total) {
                 beam2[pos] = key;
-                flag2[pos] = 0;
-                if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
+                flag2[pos] = key == next;
+                if (key == next) sh.firstp[par ^ 1] = (uint32_t)pos;
             }
         }
         for (int i = tid; i < (int)nbeam; i += NT) {
@@ -1326,16 +1346,15 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             const int pos = i + above;
             if (pos < total) {
                 beam2[pos] = key;
-                flag2[pos] = flag[i];
-                if (i == (int)second) atomicMin(&sh.first, (uint32_t)pos);
+                flag2[pos] = flag[i] | (key == next);
+                if (key == next) sh.firstp[par ^ 1] = (uint32_t)pos;
             }
         }
         if (tid == 0) {
             sh.nbeam = (uint32_t)total;
-            sh.pfa_id = ida;
-            sh.pfb_id = pfb_on && bestnew != 0ull ? key_id(bestnew) : -1;
-            sh.nnew = 0;  // read after the claim barrier only
-            sh.second = 0xFFFFFFFFu;
+            sh.nnewp[par] = 0;     // read at the top of this step only
+            sh.nkeepp[par ^ 1] = 0;  // last used in the previous step
+            sh.bestp[par ^ 1] = 0ull;
         }
         __syncthreads();
         uint64_t *tb = beam;
@@ -1344,6 +1363,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         uint8_t *tf = flag;
         flag = flag2;
         flag2 = tf;
+        if (next == 0ull) break;
     }
 
     const int nb = (int)sh.nbeam;
@@ -2112,7 +2132,7 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t maxdeg = (size_t)(M0 > M ? M0 : M);
-    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + maxdeg * (8 + 4) + (size_t)M0 * 8 + (size_t)ef_eff * 2;
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + maxdeg * (8 + 4) + (size_t)ef_eff * 2;
     n = (n + 15) & ~(size_t)15;
     return n + (size_t)((V + 31) / 32) * 4;
 }

@@ -795,8 +795,8 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
 // which scatters a wave's accesses over 16 rows; streamed that way W_out
 // reaches barely half of the HBM bandwidth.  So each wave stages its rows
 // through its own slice of LDS: a stage is read with non-temporal loads that
-// cover whole contiguous row segments (the next stage is loaded while the
-// current one is multiplied), written to LDS and read back in operand
+// cover whole contiguous row segments (the next one or two stages are loaded
+// while the current one is multiplied), written to LDS and read back in operand
 // layout.  The reduction index is free to permute, so lane (r, g) =
 // (lane % 16, lane / 16) takes columns 32 t + 8 g .. + 7 of step t for its
 // row r and the same columns of its query.  The queries' columns of a stage
@@ -811,11 +811,25 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
 #ifndef VIE_MFMA_MAX_WGS
 #define VIE_MFMA_MAX_WGS 1024
 #endif
+// Stage width (columns) and W stages loaded ahead, per pass size (up to
+// 16, 32 or 64 queries); defaults measured on MI355X.
+#ifndef VIE_MFMA_KC1
+#define VIE_MFMA_KC1 256
+#endif
+#ifndef VIE_MFMA_LA1
+#define VIE_MFMA_LA1 1
+#endif
+#ifndef VIE_MFMA_KC2
+#define VIE_MFMA_KC2 128
+#endif
+#ifndef VIE_MFMA_LA2
+#define VIE_MFMA_LA2 2
+#endif
 #ifndef VIE_MFMA_KC4
 #define VIE_MFMA_KC4 128
 #endif
-#ifndef VIE_MFMA_KC12
-#define VIE_MFMA_KC12 256
+#ifndef VIE_MFMA_LA4
+#define VIE_MFMA_LA4 1
 #endif
 
 constexpr int kMfmaWaves = 4;
@@ -841,8 +855,8 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c)
                                                    c, 0, 0, 0);
 }
 
-template <int NQT, int KC>
-__global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t *__restrict__ W, int64_t V, int d,
+template <int NQT, int KC, int LA>
+__global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(2))) void dense_mfma_kernel(const uint16_t *__restrict__ W, int64_t V, int d,
                                                                    const uint16_t *__restrict__ hq, int nq,
                                                                    int rows_per_wg, float *__restrict__ zout,
                                                                    uint64_t *__restrict__ tops)
@@ -896,10 +910,19 @@ __global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t
 #pragma unroll
         for (int j = 0; j < kLoads; ++j)
             wrow[j] = W + (r0 + min(rb + kRowsPerLoad * j + srow, nrows - 1)) * (int64_t)d;
-        u32x4 pre[kLoads];
+        // W stages run LA ahead: stage st's loads sit in buffer st % LA
+        // (the loop is unrolled over the buffers, so no in-flight load is
+        // ever copied); the query stage runs one ahead
+        u32x4 pre[LA][kLoads];
 #pragma unroll
-        for (int j = 0; j < kLoads; ++j)
-            pre[j] = scol + 8 <= d ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + scol)) : zero;
+        for (int b = 0; b < LA; ++b)
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j) {
+                const int c = b * KC + scol;
+                pre[b][j] = b < nstage && c + 8 <= d
+                                ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + c))
+                                : zero;
+            }
         u32x4 hpre[kHLoads];
 #pragma unroll
         for (int j = 0; j < kHLoads; ++j)
@@ -910,43 +933,51 @@ __global__ __launch_bounds__(kMfmaThreads) void dense_mfma_kernel(const uint16_t
 #pragma unroll
             for (int n = 0; n < NQT; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-        for (int st = 0; st < nstage; ++st) {
-            const int c0 = st * KC;
-            __syncthreads();  // every wave is done with the previous query stage
-            // this stage into LDS, then the next stage's loads
+        for (int st0 = 0; st0 < nstage; st0 += LA) {
 #pragma unroll
-            for (int j = 0; j < kLoads; ++j)
-                *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) = pre[j];
-#pragma unroll
-            for (int j = 0; j < kHLoads; ++j) *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = hpre[j];
-            if (st + 1 < nstage) {
-                const int c = c0 + KC + scol;
+            for (int b = 0; b < LA; ++b) {
+                const int st = st0 + b;
+                if (st >= nstage) break;  // uniform across the workgroup
+                const int c0 = st * KC;
+                __syncthreads();  // every wave is done with the previous query stage
+                // this stage into LDS, then the loads of stage st + LA (W) and st + 1 (queries)
 #pragma unroll
                 for (int j = 0; j < kLoads; ++j)
-                    pre[j] = c + 8 <= d ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + c))
+                    *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) = pre[b][j];
+#pragma unroll
+                for (int j = 0; j < kHLoads; ++j) *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = hpre[j];
+                if (st + LA < nstage) {
+                    const int c = c0 + LA * KC + scol;
+#pragma unroll
+                    for (int j = 0; j < kLoads; ++j)
+                        pre[b][j] = c + 8 <= d
+                                        ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + c))
                                         : zero;
-#pragma unroll
-                for (int j = 0; j < kHLoads; ++j) {
-                    const int ch = c0 + KC + hcol[j];
-                    hpre[j] = ch + 8 <= d ? *reinterpret_cast<const u32x4 *>(hrowp[j] + ch) : zero;
                 }
-            }
-            __syncthreads();  // the query stage is complete
+                if (st + 1 < nstage) {
 #pragma unroll
-            for (int t = 0; t < kSteps; ++t) {
-                u32x4 a[2];
-#pragma unroll
-                for (int m = 0; m < 2; ++m)
-                    a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
-#pragma unroll
-                for (int n = 0; n < NQT; ++n) {
-                    const u32x4 bv =
-                        *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
-#pragma unroll
-                    for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
+                    for (int j = 0; j < kHLoads; ++j) {
+                        const int ch = c0 + KC + hcol[j];
+                        hpre[j] = ch + 8 <= d ? *reinterpret_cast<const u32x4 *>(hrowp[j] + ch) : zero;
+                    }
                 }
+                __syncthreads();  // the query stage is complete
+#pragma unroll
+                for (int t = 0; t < kSteps; ++t) {
+                    u32x4 a[2];
+#pragma unroll
+                    for (int m = 0; m < 2; ++m)
+                        a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                    for (int n = 0; n < NQT; ++n) {
+                        const u32x4 bv =
+                            *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
             }
-            __builtin_amdgcn_wave_barrier();
         }
         // lane (r, g) holds rows 4 g + i of each 16-row tile for query 16 n + r
 #pragma unroll
@@ -2036,11 +2067,11 @@ bool use_mfma(int dtype, int d, int B, const void *W, const void *h)
 // Queries per pass of either path.
 int dense_pass(int B) { return B >= kMfmaMinB ? kMfmaMaxNB : kDenseMaxNB; }
 
-template <int NQT, int KC>
+template <int NQT, int KC, int LA>
 hipError_t mfma_launch(const void *W, int64_t V, int d, const char *h, int nq, int k, const DensePlan &p,
                        float *zbuf, uint64_t *tops, int32_t *ids, float *logits, hipStream_t s)
 {
-    auto kern = dense_mfma_kernel<NQT, KC>;
+    auto kern = dense_mfma_kernel<NQT, KC, LA>;
     constexpr size_t lds = mfma_lds(NQT, KC);
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -2091,9 +2122,10 @@ vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const v
             const char *hp = hb + (int64_t)q0 * row_bytes;
             int32_t *ip = ids + (int64_t)q0 * k;
             float *lp = logits + (int64_t)q0 * k;
-            hipError_t e = nq <= 16   ? mfma_launch<1, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s)
-                           : nq <= 32 ? mfma_launch<2, VIE_MFMA_KC12>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s)
-                                      : mfma_launch<4, VIE_MFMA_KC4>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s);
+            hipError_t e =
+                nq <= 16   ? mfma_launch<1, VIE_MFMA_KC1, VIE_MFMA_LA1>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s)
+                : nq <= 32 ? mfma_launch<2, VIE_MFMA_KC2, VIE_MFMA_LA2>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s)
+                           : mfma_launch<4, VIE_MFMA_KC4, VIE_MFMA_LA4>(W, V, d, hp, nq, k, mp, zbuf, tops, ip, lp, s);
             if (e != hipSuccess) return launched(e, "dense top-k (matrix cores) launch");
         }
         return VIE_OK;

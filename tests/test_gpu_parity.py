@@ -65,6 +65,8 @@ DENSE_CASES = [
     # batched bf16 on the matrix cores
     (20011, 256, synth.BF16, 16, 50),  # one 16-query tile, ragged slab tail
     (9000, 1000, synth.BF16, 33, 64),  # three query tiles padded to four, column tail
+    (9000, 1000, synth.BF16, 20, 64),  # two query tiles, stages loaded two ahead
+    (5000, 1400, synth.BF16, 24, 30),  # an odd number of 128-column stages, column tail
     (2500, 40, synth.BF16, 20, 5),     # a row shorter than one 128-column step
     (3000, 64, synth.BF16, 130, 10),   # passes of 64, 64 and 2 queries
     (262147, 64, synth.BF16, 16, 20),  # several row blocks per slab

@@ -1370,7 +1370,8 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
                 if (key == next) sh.firstp[par ^ 1] = (uint32_t)pos;
             }
         }
-        for (int i = tid; i < (int)nbeam; i += NT) {
+        // the beam keys on the other half of the workgroup, in parallel with the kept keys
+        for (int i = (tid + NT / 2) % NT; i < (int)nbeam; i += NT) {
             const uint64_t key = beam[i];
             int above = 0;
             for (int t = 0; t < nk; ++t) above += ckey[t] > key;

@@ -1782,7 +1782,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
             }
         }
-        for (int i = tid; i < (int)nbeam; i += NT) {
+        for (int i = (tid + NT / 2) % NT; i < (int)nbeam; i += NT) {  // the other half of the workgroup
             const uint64_t key = beam[i];
             const int pos = i + kept_above(key);
             if (pos < total) {

@@ -1144,6 +1144,44 @@ __device__ __forceinline__ float row_dot(const char *__restrict__ W, int64_t row
     return acc;
 }
 
+// row_dot in two halves, so that other work can run while the row loads:
+// row_issue loads up to RowCpl chunks per lane, row_finish dots them (and any
+// chunks beyond) with h and reduces over the group.
+template <int VEC, bool BF16, int G>
+__device__ __forceinline__ void row_issue(const char *__restrict__ W, int64_t row, int row_bytes, int gl,
+                                          typename Vec<VEC>::T (&buf)[RowCpl<BF16>::value])
+{
+    typedef typename Vec<VEC>::T T;
+    const T *w = reinterpret_cast<const T *>(W + row * (int64_t)row_bytes);
+    const int nchunk = row_bytes / VEC;
+#pragma unroll
+    for (int i = 0; i < RowCpl<BF16>::value; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) buf[i] = w[c];
+    }
+}
+
+template <int VEC, bool BF16, int G>
+__device__ __forceinline__ float row_finish(const char *__restrict__ W, int64_t row, int row_bytes, const char *hs,
+                                            int gl, const typename Vec<VEC>::T (&buf)[RowCpl<BF16>::value])
+{
+    typedef typename Vec<VEC>::T T;
+    const T *w = reinterpret_cast<const T *>(W + row * (int64_t)row_bytes);
+    const T *h = reinterpret_cast<const T *>(hs);
+    const int nchunk = row_bytes / VEC;
+    constexpr int CPL = RowCpl<BF16>::value;
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        if (c < nchunk) acc = dot_vec<VEC, BF16>(buf[i], h[c], acc);
+    }
+    for (int c = gl + CPL * G; c < nchunk; c += G) acc = dot_vec<VEC, BF16>(w[c], h[c], acc);
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, G);
+    return acc;
+}
+
 // Scores the entry point, then SEARCH-LAYER with a result set of one
 // (greedy) through layers maxlevel..1; returns the key of the layer-0 entry
 // point.  cid holds at least M ids; counts go to n_dist / n_expand.
@@ -1285,6 +1323,22 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         ++n_expand;
         n_dist += nn;
         if (tid == 0) sh.firstp[par ^ 1] = 0xFFFFFFFFu;  // last read in the previous step's score phase
+        // the first row of this group (and its list) starts loading before
+        // the scan below, which then runs under the load latency
+        typedef typename Vec<VEC>::T TV;
+        TV rbuf[RowCpl<BF16>::value];
+        int32_t l0[kPfbPerLane] = {-1, -1, -1, -1};
+        const int32_t e0 = grp < nn ? cid[grp] : -1;
+        if (e0 >= 0) {
+            if (pfb_on) {
+#pragma unroll
+                for (int u = 0; u < kPfbPerLane; ++u) {
+                    const int t = gl + u * G;
+                    l0[u] = t < M0 ? adj0[(int64_t)e0 * M0 + t] : -1;
+                }
+            }
+            row_issue<VEC, BF16, G>(W, e0, row_bytes, gl, rbuf);
+        }
         // the second-best unexpanded entry: every wave scans the flags itself
         uint32_t second = 0xFFFFFFFFu;
         for (int i0 = (int)first + 1; i0 < (int)nbeam; i0 += kWave) {
@@ -1303,7 +1357,15 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
         uint64_t gbest = 0ull;  // best key this group scored, and its node's list
         int32_t glist[kPfbPerLane];
-        for (int j = grp; j < nn; j += kGroups) {
+        if (e0 >= 0) {
+            const float s = row_finish<VEC, BF16, G>(W, e0, row_bytes, hs, gl, rbuf);
+            const uint64_t key = make_key(s, e0);
+            if (gl == 0 && key > worst) ckey[atomicAdd(&sh.nkeepp[par], 1u)] = key;
+            gbest = key;
+#pragma unroll
+            for (int u = 0; u < kPfbPerLane; ++u) glist[u] = l0[u];
+        }
+        for (int j = grp + kGroups; j < nn; j += kGroups) {
             const int32_t e = cid[j];
             int32_t l[kPfbPerLane];
             if (pfb_on) {

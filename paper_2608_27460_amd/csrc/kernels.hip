@@ -377,15 +377,19 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
 // chunks per lane (the last ones predicated off where the row is shorter);
 // a group is U rows.  Sums are formed in the same order as in
 // dense_slab_kernel, so both give identical logits.
-template <int CPL> struct StreamRows { static constexpr int value = CPL >= 4 ? 1 : 4 / CPL; };
+#ifndef VIE_STREAM_ROWS2
+#define VIE_STREAM_ROWS2 4  // rows per group when a row is two chunks per lane (a power of two)
+#endif
+template <int CPL> struct StreamRows { static constexpr int value = CPL >= 4 ? 1 : CPL == 2 ? VIE_STREAM_ROWS2 : 4 / CPL; };
 
 template <bool BF16, int NB, int CPL>
-__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 && CPL <= 2 ? 8 : 4))) void
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 && CPL * StreamRows<CPL>::value <= 4 ? 8 : 4))) void
 dense_stream_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
                     int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ tops)
 {
     constexpr int U = StreamRows<CPL>::value;
     constexpr int NV = NB * U;
+    static_assert((NV & (NV - 1)) == 0 && NV <= kWave, "the wave reduction sums a power of two of values");
     extern __shared__ __align__(16) char smem[];
     float *z = reinterpret_cast<float *>(smem);  // [NB][rows_per_wg]
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -841,7 +845,10 @@ constexpr int kMfmaRowsPerWave = 32;              // two 16-row tiles
 constexpr int kMfmaRowsPerIter = kMfmaWaves * kMfmaRowsPerWave;
 static_assert(kMfmaMaxWgs <= kMergeThreads, "the merge gives every slab maximum a thread");
 
-constexpr int mfma_pitch(int KC) { return KC * 2 + 16; }  // LDS bytes per staged row (padded)
+#ifndef VIE_MFMA_PAD
+#define VIE_MFMA_PAD 16
+#endif
+constexpr int mfma_pitch(int KC) { return KC * 2 + VIE_MFMA_PAD; }  // LDS bytes per staged row (padded)
 constexpr size_t mfma_lds(int NQT, int KC)
 {
     return (size_t)(kMfmaWaves * kMfmaRowsPerWave + 16 * NQT) * mfma_pitch(KC);

@@ -46,7 +46,16 @@ constexpr int kChunkPitch = kChunkBytes + 16;
 constexpr int kGramPitch = kSelectRows + 1;  // floats per Gram row in LDS
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+// 16 x 16 tile += A (16 rows x 32 columns) B^T, bf16 operands, fp32 accumulation
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+}
 
 struct TopkShared {
     uint32_t hist[kDigitBuckets];
@@ -351,14 +360,26 @@ __global__ __launch_bounds__(kSelectThreads) void knn_select_kernel(const char *
         if (tid == 0) nfwd[i] = nc;
         return;
     }
-    // Gram block: thread (ta, tb) owns pairs (ta + 16 x, tb + 16 y); rows 16
-    // apart keep the 16-byte reads of a wave on distinct LDS banks
+    // Gram block.  bf16 rows: on the matrix cores, wave w owns the 64 x 64
+    // block (rows 64 (w / 2), columns 64 (w % 2)) as 4 x 4 tiles of
+    // v_mfma_f32_16x16x32_bf16, lane (r, g) supplying columns 8 g .. 8 g + 7
+    // of each 32-column step for row r of a tile.  fp32 rows: on the vector
+    // ALUs, thread (ta, tb) owns pairs (ta + 16 x, tb + 16 y) (rows 16 apart
+    // keep the 16-byte reads of a wave on distinct LDS banks).
     const int ta = tid / 16, tb = tid % 16;
-    float acc[8][8];
+    const int wv = tid / kWave, mr = lane & 15, mg = lane >> 4;
+    const int rb = 64 * (wv >> 1), cb = 64 * (wv & 1);
+    constexpr int NX = BF16 ? 1 : 8;
+    float acc[NX][NX];
+    f32x4 macc[4][4];
 #pragma unroll
-    for (int x = 0; x < 8; ++x)
+    for (int x = 0; x < NX; ++x)
 #pragma unroll
-        for (int y = 0; y < 8; ++y) acc[x][y] = 0.0f;
+        for (int y = 0; y < NX; ++y) acc[x][y] = 0.0f;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n) macc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     const u32x4 zero = {0u, 0u, 0u, 0u};
     for (int c0 = 0; c0 < row_bytes; c0 += kChunkBytes) {
         __syncthreads();
@@ -373,26 +394,53 @@ __global__ __launch_bounds__(kSelectThreads) void knn_select_kernel(const char *
             *reinterpret_cast<u32x4 *>(tile + r * kChunkPitch + 16 * piece) = v;
         }
         __syncthreads();
+        if constexpr (BF16) {
+#pragma unroll
+            for (int t = 0; t < kChunkBytes / 64; ++t) {  // 32 bf16 columns per step
+                u32x4 a[4], b[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    a[m] = *reinterpret_cast<const u32x4 *>(tile + (rb + 16 * m + mr) * kChunkPitch + 64 * t + 16 * mg);
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    b[n] = *reinterpret_cast<const u32x4 *>(tile + (cb + 16 * n + mr) * kChunkPitch + 64 * t + 16 * mg);
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) macc[m][n] = mfma_bf16(a[m], b[n], macc[m][n]);
+            }
+        } else {
 #pragma unroll 2
-        for (int piece = 0; piece < kChunkBytes / 16; ++piece) {
-            u32x4 a[8], b[8];
+            for (int piece = 0; piece < kChunkBytes / 16; ++piece) {
+                u32x4 a[NX], b[NX];
 #pragma unroll
-            for (int x = 0; x < 8; ++x)
-                a[x] = *reinterpret_cast<const u32x4 *>(tile + (ta + 16 * x) * kChunkPitch + 16 * piece);
+                for (int x = 0; x < NX; ++x)
+                    a[x] = *reinterpret_cast<const u32x4 *>(tile + (ta + 16 * x) * kChunkPitch + 16 * piece);
 #pragma unroll
-            for (int y = 0; y < 8; ++y)
-                b[y] = *reinterpret_cast<const u32x4 *>(tile + (tb + 16 * y) * kChunkPitch + 16 * piece);
+                for (int y = 0; y < NX; ++y)
+                    b[y] = *reinterpret_cast<const u32x4 *>(tile + (tb + 16 * y) * kChunkPitch + 16 * piece);
 #pragma unroll
-            for (int x = 0; x < 8; ++x)
+                for (int x = 0; x < NX; ++x)
 #pragma unroll
-                for (int y = 0; y < 8; ++y) acc[x][y] = dot16(a[x], b[y], acc[x][y], BF16);
+                    for (int y = 0; y < NX; ++y) acc[x][y] = dot16(a[x], b[y], acc[x][y], false);
+            }
         }
     }
     __syncthreads();
+    if constexpr (BF16) {
+        // lane (r, g) holds rows 4 g + i of tile m against row r of tile n
 #pragma unroll
-    for (int x = 0; x < 8; ++x)
+        for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int y = 0; y < 8; ++y) G[(ta + 16 * x) * kGramPitch + tb + 16 * y] = acc[x][y];
+            for (int n = 0; n < 4; ++n)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) G[(rb + 16 * m + 4 * mg + e) * kGramPitch + cb + 16 * n + mr] = macc[m][n][e];
+    } else {
+#pragma unroll
+        for (int x = 0; x < NX; ++x)
+#pragma unroll
+            for (int y = 0; y < NX; ++y) G[(ta + 16 * x) * kGramPitch + tb + 16 * y] = acc[x][y];
+    }
     __syncthreads();
     if (tid < kWave) {
         // heuristic scan: e is kept iff s_e > <w_e, w_r> for every kept r

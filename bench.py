@@ -20,6 +20,12 @@ The batch-graph leg builds a single-layer graph over W_out on the GPU
 neighbour-selection heuristic, reverse edges) and searches it at B = 1 with
 the same protocol, next to the HNSW graph built on the host CPUs.
 
+The recall-target leg finds, for each traversal (sequential beam, 8
+expansions per step, 8 per step on int8 rows with the exact re-rank; on the
+HNSW graph and on the batch graph), the smallest beam width in 128 .. 4096
+whose recall@k reaches 0.95 on the first 128 queries, and its per-call time
+next to the dense head's.
+
 The other workloads (--workload tiny | llama3.2-1b | gemma3-270m |
 llama3.2-3b) run the same protocol at their own shapes, ef and k; the Gemma
 shape adds a k sweep (20, 50, 100) and the Llama-3.2-3B shape a sweep of
@@ -93,6 +99,10 @@ def main() -> int:
                     help="candidates per node of the GPU-built batch graph leg (0: skip the leg)")
     ap.add_argument("--batch-graph-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024],
                     help="extra beam widths searched on the batch graph (first --sweep-queries queries)")
+    ap.add_argument("--target-recall", type=float, default=0.95,
+                    help="recall@k that the beam-width search of each traversal aims for (0 skips it)")
+    ap.add_argument("--target-ef", type=lambda x: [int(v) for v in x.split(",") if v],
+                    default=[128, 256, 512, 1024, 2048, 4096], help="beam widths tried, in order, for the target")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="finish with a device copy of this many MiB (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -210,6 +220,23 @@ def main() -> int:
         kk = kk or a.shape[1]
         return float(np.mean([len(set(x[:kk].tolist()) & set(y[:kk].tolist())) / kk for x, y in zip(a, b)]))
 
+    def reach(index, width, int8, nq):
+        # the smallest beam of --target-ef whose recall@k on the first nq
+        # queries reaches --target-recall; per-call kernel time as per_call_us
+        ri = torch.empty((nq, k), dtype=torch.int32, device=dev)
+        rl = torch.empty((nq, k), dtype=torch.float32, device=dev)
+        tried = {}
+        for e in sorted(v for v in args.target_ef if v >= k):
+            us = per_call_us(lambda c: index.query_into(hv[c], k, e, ri[c:c + 1], rl[c:c + 1], None, width, int8), nq)
+            r = recall(ri.cpu().numpy(), exact_ids[:nq])
+            tried[str(e)] = [round(us, 2), round(r, 4)]
+            if r >= args.target_recall:
+                return {"ef": e, "us_per_query": round(us, 2), "recall_at_k": round(r, 4), "tried": tried}
+        return {"ef": None, "us_per_query": None, "recall_at_k": None, "tried": tried}
+
+    target = {}
+    tq = min(Q, args.sweep_queries)
+
     # ---- ef sweep (same protocol; one warm-up and one timed pass each) ----
     # Beams wider than the workload's own ef values run on the first
     # --sweep-queries queries only.
@@ -255,6 +282,11 @@ def main() -> int:
                             "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
                             "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean())}
 
+    if args.target_recall > 0:
+        log("[bench] beam widths reaching recall@k %.2f" % args.target_recall)
+        target["hnsw"] = reach(ix, 1, False, tq)
+        target["hnsw_width_8"] = reach(ix, 8, False, tq)
+
     # ---- int8 rows for layer 0, exact re-rank (B = 1, first 256 queries) ----
     q_sweep = {}
     if args.int8_widths and wl.d % 16 == 0:
@@ -282,8 +314,11 @@ def main() -> int:
         torch.cuda.synchronize()
         q_sweep["batched_width_%d" % wb] = {"queries_per_s": round(Q / (a.elapsed_time(b) * 1e-3), 1),
                                              "recall_at_k": round(recall(ids.cpu().numpy(), exact_ids), 4)}
+        if args.target_recall > 0:
+            target["hnsw_int8_width_8"] = reach(ix, 8, True, tq)
         ix.attach_int8(None, None)
-        del qrows, qscale
+        if not args.batch_graph_k:
+            del qrows, qscale
 
     # ---- batch graph built on the GPU (vie_index_build_gpu), searched at B = 1 ----
     batch = None
@@ -316,6 +351,13 @@ def main() -> int:
         bix.query_into(Hd, k, ef, ids, lg, st)
         b.record(stream)
         torch.cuda.synchronize()
+        if args.target_recall > 0:
+            target["batch_graph"] = reach(bix, 1, False, tq)
+            target["batch_graph_width_8"] = reach(bix, 8, False, tq)
+            if args.int8_widths and wl.d % 16 == 0:
+                bix.attach_int8(qrows, qscale)
+                target["batch_graph_int8_width_8"] = reach(bix, 8, True, tq)
+                bix.attach_int8(None, None)
         batch = {"K": Kb, "M0": wl.M0, "build_s": round(build_s, 4), "first_build_s": round(first_s, 4),
                  "cpu_hnsw_build_s": None if cpu_build_s is None else round(cpu_build_s, 2),
                  "entry": bix.info()["entry"], "ef_sweep": bsweep,
@@ -429,7 +471,9 @@ def main() -> int:
                  "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
                  "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
                  "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None,
-                 "int8_sweep": q_sweep or None, "forced": forced, "batch_graph": batch},
+                 "int8_sweep": q_sweep or None, "forced": forced, "batch_graph": batch,
+                 "recall_target": ({"recall_at_k": args.target_recall, "queries": tq,
+                                    "dense_us_per_query": round(d_us, 2), **target} if target else None)},
         "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
                   "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
         "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,

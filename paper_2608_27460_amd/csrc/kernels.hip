@@ -78,6 +78,34 @@ __device__ __forceinline__ float dot_vec(typename Vec<VEC>::T w, typename Vec<VE
     return acc;
 }
 
+// One DPP move within each row of 16 lanes (CTRL: a quad_perm, row mirror
+// or half-row mirror pattern; every source lane lies in the same row).
+template <int CTRL> __device__ __forceinline__ float dpp_move(float v)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+template <int CTRL> __device__ __forceinline__ int dpp_move(int v)
+{
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, true);
+}
+
+// Sum over the G lanes of an aligned group (G = 16, 32 or 64), the same
+// bits in every lane of the group: within a row of 16 lanes by DPP (lane ^ 1
+// and lane ^ 2 by quad permutes, then the half-row and row mirrors, each
+// pairing a lane with one of the other half), across rows by xor shuffles.
+// Each step adds two values in either order, so every lane rounds alike.
+template <int G, typename T> __device__ __forceinline__ T group_sum(T v)
+{
+    static_assert(G == 16 || G == 32 || G == 64, "groups of 16, 32 or 64 lanes");
+    v += dpp_move<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+    v += dpp_move<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+    v += dpp_move<0x141>(v);  // row_half_mirror
+    v += dpp_move<0x140>(v);  // row_mirror
+    if constexpr (G >= 32) v += __shfl_xor(v, 16, kWave);
+    if constexpr (G >= 64) v += __shfl_xor(v, 32, kWave);
+    return v;
+}
+
 // Partial dot of row `row` (row_bytes bytes at W) by the G lanes of a group:
 // lane `gl` covers chunks gl, gl + G, ... of VEC bytes.  Reduced over the
 // group with xor shuffles; every lane of the group returns the full sum.
@@ -1122,38 +1150,9 @@ __device__ __forceinline__ bool claim(uint32_t *vis, int32_t id)
 template <bool BF16> struct RowCpl { static constexpr int value = BF16 ? 8 : 4; };
 
 // <row, h> by the G lanes of a group (lane gl of the group covers chunks gl,
-// gl + G, ...): up to RowCpl chunks per lane are loaded before any is used.
-// Every lane of the group returns the sum.
-template <int VEC, bool BF16, int G>
-__device__ __forceinline__ float row_dot(const char *__restrict__ W, int64_t row, int row_bytes, const char *hs,
-                                         int gl)
-{
-    typedef typename Vec<VEC>::T T;
-    const T *w = reinterpret_cast<const T *>(W + row * (int64_t)row_bytes);
-    const T *h = reinterpret_cast<const T *>(hs);
-    const int nchunk = row_bytes / VEC;
-    constexpr int CPL = RowCpl<BF16>::value;
-    T buf[CPL];
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        const int c = gl + i * G;
-        if (c < nchunk) buf[i] = w[c];
-    }
-    float acc = 0.0f;
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        const int c = gl + i * G;
-        if (c < nchunk) acc = dot_vec<VEC, BF16>(buf[i], h[c], acc);
-    }
-    for (int c = gl + CPL * G; c < nchunk; c += G) acc = dot_vec<VEC, BF16>(w[c], h[c], acc);
-#pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, G);
-    return acc;
-}
-
-// row_dot in two halves, so that other work can run while the row loads:
-// row_issue loads up to RowCpl chunks per lane, row_finish dots them (and any
-// chunks beyond) with h and reduces over the group.
+// gl + G, ...): up to RowCpl chunks per lane are loaded before any is used,
+// chunks past the row's end read as zeros.  Every lane of the group returns
+// the sum.
 template <int VEC, bool BF16, int G>
 __device__ __forceinline__ void row_issue(const char *__restrict__ W, int64_t row, int row_bytes, int gl,
                                           typename Vec<VEC>::T (&buf)[RowCpl<BF16>::value])
@@ -1164,10 +1163,14 @@ __device__ __forceinline__ void row_issue(const char *__restrict__ W, int64_t ro
 #pragma unroll
     for (int i = 0; i < RowCpl<BF16>::value; ++i) {
         const int c = gl + i * G;
-        if (c < nchunk) buf[i] = w[c];
+        buf[i] = c < nchunk ? w[c] : T{};
     }
 }
 
+// The second half of row_dot: the query's chunks are read from LDS in
+// batches of four before any of them is used (their index clamped to the
+// row, so no branch; a clamped chunk meets a zero row chunk), dotted with the row chunks
+// in buf (and any chunks beyond RowCpl per lane), then summed over the group.
 template <int VEC, bool BF16, int G>
 __device__ __forceinline__ float row_finish(const char *__restrict__ W, int64_t row, int row_bytes, const char *hs,
                                             int gl, const typename Vec<VEC>::T (&buf)[RowCpl<BF16>::value])
@@ -1177,16 +1180,27 @@ __device__ __forceinline__ float row_finish(const char *__restrict__ W, int64_t 
     const T *h = reinterpret_cast<const T *>(hs);
     const int nchunk = row_bytes / VEC;
     constexpr int CPL = RowCpl<BF16>::value;
+    constexpr int HB = CPL < 2 ? CPL : 2;  // query chunks per batch of reads (register budget)
     float acc = 0.0f;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        const int c = gl + i * G;
-        if (c < nchunk) acc = dot_vec<VEC, BF16>(buf[i], h[c], acc);
+    for (int i0 = 0; i0 < CPL; i0 += HB) {
+        T hv[HB];
+#pragma unroll
+        for (int i = 0; i < HB; ++i) hv[i] = h[min(gl + (i0 + i) * G, nchunk - 1)];
+#pragma unroll
+        for (int i = 0; i < HB; ++i) acc = dot_vec<VEC, BF16>(buf[i0 + i], hv[i], acc);
     }
     for (int c = gl + CPL * G; c < nchunk; c += G) acc = dot_vec<VEC, BF16>(w[c], h[c], acc);
-#pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, G);
-    return acc;
+    return group_sum<G>(acc);
+}
+
+template <int VEC, bool BF16, int G>
+__device__ __forceinline__ float row_dot(const char *__restrict__ W, int64_t row, int row_bytes, const char *hs,
+                                         int gl)
+{
+    typename Vec<VEC>::T buf[RowCpl<BF16>::value];
+    row_issue<VEC, BF16, G>(W, row, row_bytes, gl, buf);
+    return row_finish<VEC, BF16, G>(W, row, row_bytes, hs, gl, buf);
 }
 
 // Scores the entry point, then SEARCH-LAYER with a result set of one
@@ -1336,15 +1350,19 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         TV rbuf[RowCpl<BF16>::value];
         int32_t l0[kPfbPerLane] = {-1, -1, -1, -1};
         const int32_t e0 = grp < nn ? cid[grp] : -1;
+        // (an opaque copy of the lane index: the per-lane addresses are then
+        // formed here, not held in registers across the whole loop)
+        int glv = gl;
+        __asm__ volatile("" : "+v"(glv));
         if (e0 >= 0) {
             if (pfb_on) {
 #pragma unroll
                 for (int u = 0; u < kPfbPerLane; ++u) {
-                    const int t = gl + u * G;
+                    const int t = glv + u * G;
                     l0[u] = t < M0 ? adj0[(int64_t)e0 * M0 + t] : -1;
                 }
             }
-            row_issue<VEC, BF16, G>(W, e0, row_bytes, gl, rbuf);
+            row_issue<VEC, BF16, G>(W, e0, row_bytes, glv, rbuf);
         }
         // the second-best unexpanded entry: every wave scans the flags itself
         uint32_t second = 0xFFFFFFFFu;

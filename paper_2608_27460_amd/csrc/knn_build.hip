@@ -325,9 +325,10 @@ constexpr size_t kSelectBig = (size_t)kSelectRows * kChunkPitch > (size_t)kSelec
 constexpr size_t kSelectLds = kSelectBig + (size_t)kSelectRows * 8 + 256 * 4;
 
 // Step 2, one workgroup per node: the Gram matrix of its candidates (rows
-// staged through LDS in chunks of kChunkBytes, each thread an 8 x 8 block of
-// pairs, fp32 accumulation), then the heuristic scan in candidate order by
-// one wave.  A node with at most M0 candidates keeps them all.
+// staged through LDS in chunks of kChunkBytes, fp32 accumulation; matrix
+// cores for bf16 rows, vector ALUs for fp32 rows), then the heuristic scan
+// in candidate order by one wave.  A node with at most M0 candidates keeps
+// them all.
 template <bool BF16>
 __global__ __launch_bounds__(kSelectThreads) void knn_select_kernel(const char *__restrict__ W, int row_bytes,
                                                                     int K, int M0, const int32_t *__restrict__ cand,

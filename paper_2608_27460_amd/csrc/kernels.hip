@@ -1519,7 +1519,9 @@ constexpr int kMaxWidth = 8;        // widest expansion step
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
 
 // <row a, h> and <row b, h> (b < 0: only a) with both rows' chunks loaded
-// before either is used.
+// before either is used (chunks past the row's end read as zeros), the
+// query's chunks read from LDS two at a time before use (index clamped to
+// the row), and both sums taken over the group as in group_sum.
 template <int VEC, bool BF16, int G>
 __device__ __forceinline__ void row_dot2(const char *__restrict__ W, int64_t ra, int64_t rb, int row_bytes,
                                          const char *hs, int gl, float &sa, float &sb)
@@ -1534,35 +1536,40 @@ __device__ __forceinline__ void row_dot2(const char *__restrict__ W, int64_t ra,
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
         const int c = gl + i * G;
-        if (c < nchunk) {
-            ba[i] = wa[c];
-            if (rb >= 0) bb[i] = wb[c];
-        }
+        ba[i] = c < nchunk ? wa[c] : T{};
+        bb[i] = c < nchunk && rb >= 0 ? wb[c] : T{};
     }
+    constexpr int HB = 1;
     float xa = 0.0f, xb = 0.0f;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        const int c = gl + i * G;
-        if (c < nchunk) {
-            xa = dot_vec<VEC, BF16>(ba[i], h[c], xa);
-            if (rb >= 0) xb = dot_vec<VEC, BF16>(bb[i], h[c], xb);
+    for (int i0 = 0; i0 < CPL; i0 += HB) {
+        T hv[HB];
+#pragma unroll
+        for (int i = 0; i < HB; ++i) hv[i] = h[min(gl + (i0 + i) * G, nchunk - 1)];
+#pragma unroll
+        for (int i = 0; i < HB; ++i) {
+            xa = dot_vec<VEC, BF16>(ba[i0 + i], hv[i], xa);
+            xb = dot_vec<VEC, BF16>(bb[i0 + i], hv[i], xb);
         }
     }
     for (int c = gl + CPL * G; c < nchunk; c += G) {
         xa = dot_vec<VEC, BF16>(wa[c], h[c], xa);
         if (rb >= 0) xb = dot_vec<VEC, BF16>(wb[c], h[c], xb);
     }
-#pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1) {
-        xa += __shfl_xor(xa, m, G);
-        xb += __shfl_xor(xb, m, G);
-    }
-    sa = xa;
-    sb = xb;
+    sa = group_sum<G>(xa);
+    sb = group_sum<G>(xb);
+}
+
+__device__ __forceinline__ int sdot16(u32x4 w, u32x4 h, int acc)
+{
+    acc = __builtin_amdgcn_sdot4((int)w.x, (int)h.x, acc, false);
+    acc = __builtin_amdgcn_sdot4((int)w.y, (int)h.y, acc, false);
+    acc = __builtin_amdgcn_sdot4((int)w.z, (int)h.z, acc, false);
+    return __builtin_amdgcn_sdot4((int)w.w, (int)h.w, acc, false);
 }
 
 // Integer <q_a, hq> and <q_b, hq> over int8 rows of d bytes (d % 16 == 0;
-// b < 0: only a), both rows' chunks loaded before either is used.
+// b < 0: only a), loaded and summed as in row_dot2.
 template <int G>
 __device__ __forceinline__ void row_dot2_q8(const int8_t *__restrict__ Q, int64_t ra, int64_t rb, int d,
                                             const int8_t *hq, int gl, int &ia, int &ib)
@@ -1572,54 +1579,32 @@ __device__ __forceinline__ void row_dot2_q8(const int8_t *__restrict__ Q, int64_
     const u32x4 *h = reinterpret_cast<const u32x4 *>(hq);
     const int nchunk = d / 16;
     constexpr int CPL = 4;  // int8 rows are at most half a stored row: G lanes cover them in 4 chunks
+    const u32x4 zero = {0u, 0u, 0u, 0u};
     u32x4 ba[CPL], bb[CPL];
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
         const int c = gl + i * G;
-        if (c < nchunk) {
-            ba[i] = qa[c];
-            if (rb >= 0) bb[i] = qb[c];
-        }
+        ba[i] = c < nchunk ? qa[c] : zero;
+        bb[i] = c < nchunk && rb >= 0 ? qb[c] : zero;
     }
     int xa = 0, xb = 0;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        const int c = gl + i * G;
-        if (c < nchunk) {
-            const u32x4 hv = h[c];
-            xa = __builtin_amdgcn_sdot4((int)ba[i].x, (int)hv.x, xa, false);
-            xa = __builtin_amdgcn_sdot4((int)ba[i].y, (int)hv.y, xa, false);
-            xa = __builtin_amdgcn_sdot4((int)ba[i].z, (int)hv.z, xa, false);
-            xa = __builtin_amdgcn_sdot4((int)ba[i].w, (int)hv.w, xa, false);
-            if (rb >= 0) {
-                xb = __builtin_amdgcn_sdot4((int)bb[i].x, (int)hv.x, xb, false);
-                xb = __builtin_amdgcn_sdot4((int)bb[i].y, (int)hv.y, xb, false);
-                xb = __builtin_amdgcn_sdot4((int)bb[i].z, (int)hv.z, xb, false);
-                xb = __builtin_amdgcn_sdot4((int)bb[i].w, (int)hv.w, xb, false);
-            }
+    for (int i0 = 0; i0 < CPL; i0 += 2) {
+        u32x4 hv[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) hv[i] = h[min(gl + (i0 + i) * G, nchunk - 1)];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            xa = sdot16(ba[i0 + i], hv[i], xa);
+            xb = sdot16(bb[i0 + i], hv[i], xb);
         }
     }
     for (int c = gl + CPL * G; c < nchunk; c += G) {
-        const u32x4 hv = h[c], wa = qa[c];
-        xa = __builtin_amdgcn_sdot4((int)wa.x, (int)hv.x, xa, false);
-        xa = __builtin_amdgcn_sdot4((int)wa.y, (int)hv.y, xa, false);
-        xa = __builtin_amdgcn_sdot4((int)wa.z, (int)hv.z, xa, false);
-        xa = __builtin_amdgcn_sdot4((int)wa.w, (int)hv.w, xa, false);
-        if (rb >= 0) {
-            const u32x4 wb = qb[c];
-            xb = __builtin_amdgcn_sdot4((int)wb.x, (int)hv.x, xb, false);
-            xb = __builtin_amdgcn_sdot4((int)wb.y, (int)hv.y, xb, false);
-            xb = __builtin_amdgcn_sdot4((int)wb.z, (int)hv.z, xb, false);
-            xb = __builtin_amdgcn_sdot4((int)wb.w, (int)hv.w, xb, false);
-        }
+        xa = sdot16(qa[c], h[c], xa);
+        if (rb >= 0) xb = sdot16(qb[c], h[c], xb);
     }
-#pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1) {
-        xa += __shfl_xor(xa, m, G);
-        xb += __shfl_xor(xb, m, G);
-    }
-    ia = xa;
-    ib = xb;
+    ia = group_sum<G>(xa);
+    ib = group_sum<G>(xb);
 }
 
 // Layer-0 score from int8 rows: fp32(integer dot) * row scale * query scale,

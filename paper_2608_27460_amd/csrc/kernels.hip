@@ -1133,6 +1133,15 @@ struct HnswShared {
     uint32_t nnewp[2], nkeepp[2], firstp[2];
 };
 
+// p rounded up to 16 bytes past base (base 16-byte aligned), by pointer
+// arithmetic only: a pointer into LDS keeps its address space, so the
+// compiler emits LDS instructions for it (a round trip through an integer
+// would make every access a generic one, which also waits on global loads).
+template <typename T> __device__ __forceinline__ T *align16_past(char *base, char *p)
+{
+    return reinterpret_cast<T *>(base + (((p - base) + 15) & ~(ptrdiff_t)15));
+}
+
 __device__ __forceinline__ void clear_bits(uint32_t *vis, int words)
 {
     for (int i = threadIdx.x; i < words; i += blockDim.x) vis[i] = 0u;
@@ -1288,7 +1297,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     p += (size_t)ef;
     uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
     p += (size_t)ef;
-    uint32_t *vis = reinterpret_cast<uint32_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);
+    uint32_t *vis = align16_past<uint32_t>(smem, p);
 
     const char *h = hq + (int64_t)q * row_bytes;
     for (int i = tid; i < hbytes; i += NT) hs[i] = i < row_bytes ? h[i] : 0;
@@ -1654,9 +1663,9 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)ef;
     uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
     p += (size_t)ef;
-    int8_t *hq8 = reinterpret_cast<int8_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);  // Q8: the int8 query
+    int8_t *hq8 = align16_past<int8_t>(smem, p);  // Q8: the int8 query
     p = reinterpret_cast<char *>(hq8) + d8;
-    uint32_t *vis = reinterpret_cast<uint32_t *>(((uintptr_t)p + 15) & ~(uintptr_t)15);
+    uint32_t *vis = align16_past<uint32_t>(smem, p);
 
     const char *h = hq + (int64_t)q * row_bytes;
     for (int i = tid; i < hbytes; i += NT) hs[i] = i < row_bytes ? h[i] : 0;
@@ -1737,7 +1746,11 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
 #pragma unroll
             for (int u = 0; u < kMaxWidth; ++u)
                 if (u < width && lc_id[u] == c) src = u;
-            const int32_t e = src >= 0 ? lcache[src * M0 + slot] : adj0[(int64_t)c * M0 + slot];
+            // two guarded loads, not one through a selected pointer (that
+            // would be a generic load, which waits on both memory counters)
+            const int32_t ec = src >= 0 ? lcache[max(src, 0) * M0 + slot] : -1;
+            const int32_t eg = src < 0 ? adj0[(int64_t)c * M0 + slot] : -1;
+            const int32_t e = src >= 0 ? ec : eg;
             if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
         }
         __syncthreads();

@@ -411,7 +411,7 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
 template <int CPL> struct StreamRows { static constexpr int value = CPL >= 4 ? 1 : CPL == 2 ? VIE_STREAM_ROWS2 : 4 / CPL; };
 
 template <bool BF16, int NB, int CPL>
-__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 && CPL * StreamRows<CPL>::value <= 4 ? 8 : 4))) void
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 && CPL <= 2 && CPL * StreamRows<CPL>::value <= 4 ? 8 : 4))) void
 dense_stream_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
                     int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ tops)
 {

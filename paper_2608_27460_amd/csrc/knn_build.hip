@@ -532,23 +532,40 @@ __global__ __launch_bounds__(kTopkThreads) void knn_lists_kernel(int M0, const i
         adj0[j * M0 + t] = t < nf ? fwd[j * M0 + t] : t < nf + m ? key_id(sh.gat[t - nf]) : -1;
 }
 
-// Step 5: the key (squared norm, id) of every row, the largest kept.
+// Step 5: the key (squared norm, id) of every row, the largest kept.  Each
+// wave takes rows grid-stride and keeps its best key; the workgroup's best
+// goes to *best with one atomic (one per row would serialise on the word).
+constexpr int kEntryThreads = 256;
+constexpr int kEntryBlocks = 2048;
+
 template <bool BF16>
-__global__ void knn_entry_kernel(const char *__restrict__ W, int64_t V, int row_bytes,
-                                 unsigned long long *__restrict__ best)
+__global__ __launch_bounds__(kEntryThreads) void knn_entry_kernel(const char *__restrict__ W, int64_t V,
+                                                                  int row_bytes, unsigned long long *__restrict__ best)
 {
-    const int64_t i = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    const int lane = threadIdx.x & (kWave - 1);
-    if (i >= V) return;
-    const char *w = W + i * row_bytes;
-    float acc = 0.0f;
-    for (int c = 16 * lane; c < row_bytes; c += 16 * kWave) {
-        const u32x4 v = *reinterpret_cast<const u32x4 *>(w + c);
-        acc = dot16(v, v, acc, BF16);
-    }
+    __shared__ unsigned long long wbest[kEntryThreads / kWave];
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    const int64_t nwaves = (int64_t)gridDim.x * (kEntryThreads / kWave);
+    unsigned long long mine = 0ull;
+    for (int64_t i = (int64_t)blockIdx.x * (kEntryThreads / kWave) + wv; i < V; i += nwaves) {
+        const char *w = W + i * row_bytes;
+        float acc = 0.0f;
+        for (int c = 16 * lane; c < row_bytes; c += 16 * kWave) {
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(w + c);
+            acc = dot16(v, v, acc, BF16);
+        }
 #pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, kWave);
-    if (lane == 0) atomicMax(best, (unsigned long long)make_key(acc, (int32_t)i));
+        for (int o = kWave / 2; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, kWave);
+        const unsigned long long key = make_key(acc, (int32_t)i);
+        mine = key > mine ? key : mine;
+    }
+    if (lane == 0) wbest[wv] = mine;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long m = wbest[0];
+#pragma unroll
+        for (int x = 1; x < kEntryThreads / kWave; ++x) m = wbest[x] > m ? wbest[x] : m;
+        if (m) atomicMax(best, m);
+    }
 }
 
 struct Buffers {
@@ -680,9 +697,11 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
         he = hipMemsetAsync(b.best, 0, 8, s);
     }
     if (he == hipSuccess) {
-        const unsigned eb = (unsigned)((V + 3) / 4);
-        if (dtype == VIE_BF16) knn_entry_kernel<true><<<eb, 256, 0, s>>>(static_cast<const char *>(W_dev), V, row_bytes, b.best);
-        else knn_entry_kernel<false><<<eb, 256, 0, s>>>(static_cast<const char *>(W_dev), V, row_bytes, b.best);
+        const unsigned eb = (unsigned)std::min<int64_t>((V + 3) / 4, kEntryBlocks);
+        if (dtype == VIE_BF16)
+            knn_entry_kernel<true><<<eb, kEntryThreads, 0, s>>>(static_cast<const char *>(W_dev), V, row_bytes, b.best);
+        else
+            knn_entry_kernel<false><<<eb, kEntryThreads, 0, s>>>(static_cast<const char *>(W_dev), V, row_bytes, b.best);
         he = hipMemsetAsync(b.upper_off, 0xFF, (size_t)V * 4, s);  // every node on layer 0 only: -1
     }
     if (he == hipSuccess) he = hipGetLastError();

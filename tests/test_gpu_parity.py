@@ -76,6 +76,7 @@ DENSE_CASES = [
     # one or two queries over 16-byte aligned rows: the streaming slab kernel
     (30011, 640, synth.BF16, 1, 50),   # 80 chunks: the second chunk on 16 lanes only
     (12000, 1536, synth.BF16, 1, 64),  # 3 of 4 chunks per lane
+    (6007, 2048, synth.BF16, 1, 50),   # 4 of 4 chunks per lane (the Llama-3.2-1B row width)
     (9001, 3072, synth.BF16, 1, 50),   # 6 of 8 chunks per lane
     (7001, 2048, synth.BF16, 2, 50),   # two queries, 4 chunks per lane
     (5003, 3072, synth.BF16, 2, 10),   # two queries, rows too long for it: the slab kernel

@@ -1154,6 +1154,14 @@ __device__ __forceinline__ bool claim(uint32_t *vis, int32_t id)
     return (atomicOr(&vis[id >> 5], bit) & bit) == 0u;
 }
 
+// 64-bit value of lane l (l uniform across the wave).
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // Row chunks per lane held in registers (fp32 rows: 4, which avoids the
 // register spills 8 causes there).
 template <bool BF16> struct RowCpl { static constexpr int value = BF16 ? 8 : 4; };
@@ -1525,6 +1533,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 // rows' loads in flight.
 
 constexpr int kMaxWidth = 8;        // widest expansion step
+constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
 
 // <row a, h> and <row b, h> (b < 0: only a) with both rows' chunks loaded
@@ -1659,10 +1668,14 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)nid * 4;
     int32_t *lcache = reinterpret_cast<int32_t *>(p);
     p += (size_t)cap * 4;
+    // flag arrays 8-byte aligned and padded to 8 bytes: the picks scan reads
+    // them eight flags per lane
+    const int efp = (ef + 7) & ~7;
+    p = smem + (((p - smem) + 7) & ~(ptrdiff_t)7);
     uint8_t *flag = reinterpret_cast<uint8_t *>(p);
-    p += (size_t)ef;
+    p += (size_t)efp;
     uint8_t *flag2 = reinterpret_cast<uint8_t *>(p);
-    p += (size_t)ef;
+    p += (size_t)efp;
     int8_t *hq8 = align16_past<int8_t>(smem, p);  // Q8: the int8 query
     p = reinterpret_cast<char *>(hq8) + d8;
     uint32_t *vis = align16_past<uint32_t>(smem, p);
@@ -1720,16 +1733,53 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
 #pragma unroll
         for (int t = 0; t < kMaxWidth; ++t) pick[t] = -1;
         int np = 0, after = -1;
-        for (int i0 = (int)first; i0 < (int)nbeam && after < 0; i0 += kWave) {
-            uint64_t ball = __ballot(i0 + lane < (int)nbeam && !flag[i0 + lane]);
+        if ((int)nbeam - (int)first <= kPickNarrowSpan) {
+            // a short span: one flag per lane, 64 entries per round
+            for (int i0 = (int)first; i0 < (int)nbeam && after < 0; i0 += kWave) {
+                uint64_t ball = __ballot(i0 + lane < (int)nbeam && !flag[i0 + lane]);
 #pragma unroll
-            for (int t = 0; t < kMaxWidth; ++t)
-                if (t < width && pick[t] < 0 && ball) {
-                    pick[t] = i0 + __ffsll((long long)ball) - 1;
-                    ball &= ball - 1;
-                    ++np;
+                for (int t = 0; t < kMaxWidth; ++t)
+                    if (t < width && pick[t] < 0 && ball) {
+                        pick[t] = i0 + __ffsll((long long)ball) - 1;
+                        ball &= ball - 1;
+                        ++np;
+                    }
+                if (np == width && ball && after < 0) after = i0 + __ffsll((long long)ball) - 1;
+            }
+        } else {
+            // eight flags per lane (512 entries per round): bit 8 b of a lane's
+            // mask is set when entry 8 lane + b is unexpanded and in [first, nbeam);
+            // the lanes with such entries are then taken in order by ballot, and
+            // their entries by scalar bit scans, so every wave finds the same picks
+            for (int b0 = (int)first & ~7; b0 < (int)nbeam && after < 0; b0 += 8 * kWave) {
+                const int i = b0 + 8 * lane;
+                uint64_t m = 0ull;
+                if (i < (int)nbeam) {
+                    m = ~*reinterpret_cast<const uint64_t *>(flag + i) & 0x0101010101010101ull;
+                    const int lo = (int)first - i, hi = (int)nbeam - i;
+                    if (lo >= 8) m = 0ull;
+                    else if (lo > 0) m &= ~0ull << (8 * lo);
+                    if (hi < 8) m &= (1ull << (8 * hi)) - 1ull;
                 }
-            if (np == width && ball && after < 0) after = i0 + __ffsll((long long)ball) - 1;
+                uint64_t lanes = __ballot(m != 0ull);
+                while (lanes != 0ull && after < 0) {
+                    const int L = __ffsll((long long)lanes) - 1;
+                    uint64_t ml = readlane64(m, L);
+                    while (ml != 0ull && after < 0) {
+                        const int idx = b0 + 8 * L + (__ffsll((long long)ml) - 1) / 8;
+                        if (np < width) {
+#pragma unroll
+                            for (int t = 0; t < kMaxWidth; ++t)
+                                if (t == np) pick[t] = idx;
+                            ++np;
+                        } else {
+                            after = idx;
+                        }
+                        ml &= ml - 1ull;
+                    }
+                    lanes &= lanes - 1ull;
+                }
+            }
         }
         if (np == 0) break;
         if (tid == 0) sh.nkeep = 0;  // last read before the previous merge
@@ -2260,7 +2310,8 @@ size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t cap = (size_t)width * M0, nid = cap > (size_t)M ? cap : (size_t)M;
-    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + cap * 8 + nid * 4 + cap * 4 + (size_t)ef_eff * 2;
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + cap * 8 + nid * 4 + cap * 4;
+    n = ((n + 7) & ~(size_t)7) + 2 * (((size_t)ef_eff + 7) & ~(size_t)7);  // 8-aligned flag arrays
     n = (n + 15) & ~(size_t)15;
     if (q8) n += (size_t)((d + 15) & ~15);
     return n + (size_t)((V + 31) / 32) * 4;

@@ -225,7 +225,9 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
     exact, _, _ = O.topk(W, synth.BF16, H, 50)
     with tempfile.TemporaryDirectory() as tmp:
         ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
-        for k, ef in [(10, 10), (50, 64), (50, 200)]:
+        # ef = 600: more than 256 entries past the first unexpanded one, so the
+        # picks are found eight flags per lane until the span shortens
+        for k, ef in [(10, 10), (50, 64), (50, 200), (50, 600)]:
             h = dev_tensor(vie, H, synth.BF16)
             ids, lg, st = ix.query(h, k, ef, stats=True, width=width)
             torch.cuda.synchronize()
@@ -297,7 +299,7 @@ def test_int8_rows_bitwise(vie, V, d, dtype):
     assert np.array_equal(sc.cpu().numpy().view(np.uint32), osc.view(np.uint32))
 
 
-@pytest.mark.parametrize("width", [1, 4])
+@pytest.mark.parametrize("width", [1, 4, 8])
 def test_int8_search_matches_oracle(vie, width):
     """Layer 0 on int8 scores (integer dot, fp32 scale products) walks exactly
     the oracle's path; the re-ranked result matches within the tolerances."""
@@ -311,7 +313,7 @@ def test_int8_search_matches_oracle(vie, width):
         ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
         q, sc = vie.quantize_rows(ix._W_dev, synth.BF16)
         ix.attach_int8(q, sc)
-        for k, ef in [(10, 40), (50, 100)]:
+        for k, ef in [(10, 40), (50, 100), (50, 512)]:
             ids, lg, st = ix.query(dev_tensor(vie, H, synth.BF16), k, ef, stats=True, width=width, int8=True)
             torch.cuda.synchronize()
             ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)

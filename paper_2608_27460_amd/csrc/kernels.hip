@@ -89,6 +89,40 @@ template <int CTRL> __device__ __forceinline__ int dpp_move(int v)
     return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, true);
 }
 
+// The value held by lane (lane ^ s), s = 1, 2, 4, 8, 16 or 32, without an
+// LDS round trip: DPP within rows of 16 lanes (quad permutes for 1 and 2,
+// row shifts up and down for 4, a row rotation by 8 for 8) and the permlane
+// swaps across rows (16, 32).  Every lane of the wave must be active.  s is
+// a compile-time constant wherever these are called (unrolled loops), so the
+// switch folds away.
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v, int s)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    switch (s) {
+    case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true);   // quad_perm [1, 0, 3, 2]
+    case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true);   // quad_perm [2, 3, 0, 1]
+    case 4: {
+        const uint32_t up = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x104, 0xF, 0xF, true);  // row_shl:4
+        const uint32_t dn = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
+        return (lane & 4) ? dn : up;
+    }
+    case 8: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, true);  // row_ror:8
+    case 16: {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    }
+    case 32: {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return (lane & 32) ? r[0] : r[1];
+    }
+    default: return (uint32_t)__shfl_xor((int)v, s, kWave);
+    }
+}
+__device__ __forceinline__ uint64_t xor_lane(uint64_t v, int s)
+{
+    return ((uint64_t)xor_lane((uint32_t)(v >> 32), s) << 32) | xor_lane((uint32_t)v, s);
+}
+
 // Sum over the G lanes of an aligned group (G = 16, 32 or 64), the same
 // bits in every lane of the group: within a row of 16 lanes by DPP (lane ^ 1
 // and lane ^ 2 by quad permutes, then the half-row and row mirrors, each
@@ -491,7 +525,7 @@ __device__ __forceinline__ uint64_t wave_sort_desc(uint64_t key, int lane)
     for (int size = 2; size <= kWave; size <<= 1)
 #pragma unroll
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            const uint64_t other = __shfl_xor(key, stride, kWave);
+            const uint64_t other = xor_lane(key, stride);
             const bool keep_max = ((lane & stride) == 0) == ((lane & size) == 0);
             key = keep_max ? (other > key ? other : key) : (other < key ? other : key);
         }
@@ -503,7 +537,7 @@ __device__ __forceinline__ uint64_t wave_bitonic_merge_desc(uint64_t key, int la
 {
 #pragma unroll
     for (int stride = kWave / 2; stride > 0; stride >>= 1) {
-        const uint64_t other = __shfl_xor(key, stride, kWave);
+        const uint64_t other = xor_lane(key, stride);
         key = (lane & stride) == 0 ? (other > key ? other : key) : (other < key ? other : key);
     }
     return key;
@@ -599,8 +633,14 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
     const uint32_t mo = (uint32_t)(m >> 32);
     {
         uint32_t w = mo;
-#pragma unroll
-        for (int x = 32; x >= 1; x >>= 1) w = max(w, (uint32_t)__shfl_xor(w, x, kWave));
+        // (strides written out: a loop here is left rolled, and xor_lane's
+        // stride switch would then run as branches)
+        w = max(w, xor_lane(w, 32));
+        w = max(w, xor_lane(w, 16));
+        w = max(w, xor_lane(w, 8));
+        w = max(w, xor_lane(w, 4));
+        w = max(w, xor_lane(w, 2));
+        w = max(w, xor_lane(w, 1));
         __syncthreads();
         if (lane == 0) atomicMax(&s_omax, w);
         __syncthreads();

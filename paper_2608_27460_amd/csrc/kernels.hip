@@ -123,6 +123,21 @@ __device__ __forceinline__ uint64_t xor_lane(uint64_t v, int s)
     return ((uint64_t)xor_lane((uint32_t)(v >> 32), s) << 32) | xor_lane((uint32_t)v, s);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave by DPP: shifts right by
+// 1, 2, 4 and 8 within each row of 16 lanes (lanes shifted in read zero),
+// then lane 15 of each row added into rows 1 and 3 and lane 31 into rows 2
+// and 3.  Every lane of the wave must be active.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
+{
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, true);   // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, true);   // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, true);   // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, true);   // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return x;
+}
+
 // Sum over the G lanes of an aligned group (G = 16, 32 or 64), the same
 // bits in every lane of the group: within a row of 16 lanes by DPP (lane ^ 1
 // and lane ^ 2 by quad permutes, then the half-row and row mirrors, each
@@ -158,28 +173,6 @@ __device__ __forceinline__ float group_row_dot(const char *__restrict__ W, int64
 #pragma unroll
     for (int m = G / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, G);
     return acc;
-}
-
-// ---------------------------------------------------------------------------
-// block-wide helpers
-// ---------------------------------------------------------------------------
-
-// Inclusive prefix sum of v over the block (NT threads, NT / 64 waves).
-template <int NT>
-__device__ __forceinline__ uint32_t block_inclusive_scan(uint32_t v, uint32_t *s_wave)
-{
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t t = __shfl_up(v, o, kWave);
-        if (lane >= o) v += t;
-    }
-    if (lane == kWave - 1) s_wave[wave] = v;
-    __syncthreads();
-    uint32_t base = 0;
-    for (int w = 0; w < wave; ++w) base += s_wave[w];
-    __syncthreads();
-    return v + base;
 }
 
 // ---------------------------------------------------------------------------
@@ -656,12 +649,7 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
                 c[j] = hist[per * lane + j];
                 sum += c[j];
             }
-            uint32_t incl = sum;
-#pragma unroll
-            for (int x = 1; x < kWave; x <<= 1) {
-                const uint32_t t = __shfl_up(incl, x, kWave);
-                if (lane >= x) incl += t;
-            }
+            const uint32_t incl = wave_incl_scan(sum);
             uint32_t above = incl - sum;
 #pragma unroll
             for (int j = 0; j < per; ++j) {
@@ -731,12 +719,7 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
                         c[j] = hist[255 - 4 * lane - j];
                         sum += c[j];
                     }
-                    uint32_t incl = sum;
-#pragma unroll
-                    for (int x = 1; x < kWave; x <<= 1) {
-                        const uint32_t t = __shfl_up(incl, x, kWave);
-                        if (lane >= x) incl += t;
-                    }
+                    const uint32_t incl = wave_incl_scan(sum);
                     uint32_t above = incl - sum;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {

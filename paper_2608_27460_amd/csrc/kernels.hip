@@ -590,7 +590,8 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
     __shared__ uint64_t gat[kMergeGather];
     __shared__ uint64_t lists[kMergeWaves][kWave];
     __shared__ int cand[kMergeThreads], scan[kMergeThreads];
-    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count, s_omax, s_bucket;
+    __shared__ uint32_t s_nc, s_n, s_nscan, s_want, s_count, s_bucket;
+    __shared__ uint32_t s_wmax[kMergeWaves];
     __shared__ unsigned long long s_prefix, s_and, s_or, s_T;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave, q = blockIdx.x;
     const float *zq = zbuf + (int64_t)q * V;
@@ -613,7 +614,6 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
         s_and = ~0ull;
         s_or = 0ull;
         s_T = 0ull;
-        s_omax = 0u;
         s_bucket = kMergeBuckets;
     }
     if (tid < kMergeBuckets) hist[tid] = 0u;
@@ -634,10 +634,11 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
         w = max(w, xor_lane(w, 4));
         w = max(w, xor_lane(w, 2));
         w = max(w, xor_lane(w, 1));
-        __syncthreads();
-        if (lane == 0) atomicMax(&s_omax, w);
-        __syncthreads();
-        const uint32_t top = s_omax;
+        if (lane == 0) s_wmax[wave] = w;
+        __syncthreads();  // also publishes the zeroed histogram and counters
+        uint32_t top = s_wmax[0];
+#pragma unroll
+        for (int x = 1; x < kMergeWaves; ++x) top = max(top, s_wmax[x]);
         const uint32_t dist = (top - mo) >> kMergeBucketShift;
         if (tid < nwg && dist < (uint32_t)kMergeBuckets) atomicAdd(&hist[dist], 1u);
         __syncthreads();

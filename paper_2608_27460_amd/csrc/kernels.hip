@@ -335,7 +335,7 @@ __device__ __forceinline__ void topr_reduce(uint64_t (&b)[kTopR])
     for (int o = SPAN; o >= FROM; o >>= 1) {
         uint64_t t[kTopR];
 #pragma unroll
-        for (int i = 0; i < kTopR; ++i) t[i] = __shfl_xor(b[i], o, kWave);
+        for (int i = 0; i < kTopR; ++i) t[i] = xor_lane(b[i], o);
         topr_merge(t, b);
     }
 }

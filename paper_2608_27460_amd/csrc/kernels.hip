@@ -277,12 +277,12 @@ __device__ __forceinline__ float wave_sum_multi(float (&v)[N], int lane)
         for (int i = 0; i < n / 2; ++i) {
             const float give = upper ? v[i] : v[i + n / 2];
             const float keep = upper ? v[i + n / 2] : v[i];
-            v[i] = keep + __shfl_xor(give, o, kWave);
+            v[i] = keep + __uint_as_float(xor_lane(__float_as_uint(give), o));
         }
     }
     float a = v[0];
 #pragma unroll
-    for (int o = 32 / N; o >= 1; o >>= 1) a += __shfl_xor(a, o, kWave);
+    for (int o = 32 / N; o >= 1; o >>= 1) a += __uint_as_float(xor_lane(__float_as_uint(a), o));
     return a;
 }
 

@@ -138,10 +138,17 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
     return x;
 }
 
+// xor_lane for 32-bit values of any type (float, int).
+template <typename T> __device__ __forceinline__ T xor_lane_as(T v, int s)
+{
+    return __builtin_bit_cast(T, xor_lane(__builtin_bit_cast(uint32_t, v), s));
+}
+
 // Sum over the G lanes of an aligned group (G = 16, 32 or 64), the same
 // bits in every lane of the group: within a row of 16 lanes by DPP (lane ^ 1
 // and lane ^ 2 by quad permutes, then the half-row and row mirrors, each
-// pairing a lane with one of the other half), across rows by xor shuffles.
+// pairing a lane with one of the other half), across rows by permlane swaps
+// (the partner lanes of a 32- or 64-lane group lie inside the group).
 // Each step adds two values in either order, so every lane rounds alike.
 template <int G, typename T> __device__ __forceinline__ T group_sum(T v)
 {
@@ -150,8 +157,8 @@ template <int G, typename T> __device__ __forceinline__ T group_sum(T v)
     v += dpp_move<0x4E>(v);   // quad_perm [2, 3, 0, 1]
     v += dpp_move<0x141>(v);  // row_half_mirror
     v += dpp_move<0x140>(v);  // row_mirror
-    if constexpr (G >= 32) v += __shfl_xor(v, 16, kWave);
-    if constexpr (G >= 64) v += __shfl_xor(v, 32, kWave);
+    if constexpr (G >= 32) v += xor_lane_as(v, 16);
+    if constexpr (G >= 64) v += xor_lane_as(v, 32);
     return v;
 }
 

@@ -104,6 +104,30 @@ def test_dense_topk_matches_oracle(vie, V, d, dtype, B, k):
         assert np.array_equal(ids2.cpu().numpy(), ids) and np.array_equal(lg2.cpu().numpy(), lg)
 
 
+@pytest.mark.parametrize("B,k", [(1, 50), (1, 100), (16, 50), (16, 100)])
+def test_dense_far_maximum_takes_the_exact_fallbacks(vie, B, k):
+    # one planted row per query scores about 2^20 times the usual maximum, so
+    # the merge's histogram window (eight binades below the largest slab
+    # maximum) holds fewer than k slab maxima: k <= 64 takes the sorting
+    # network over the maxima, larger k the radix select
+    V, d = 20000, 128
+    W = synth.make_w(V, d, synth.BF16, 141)
+    H, _ = synth.make_queries(W, synth.BF16, B, 142)
+    Wf = synth.bf16_bits_to_f32(W).copy()
+    hf = synth.bf16_bits_to_f32(H)
+    for b in range(B):
+        Wf[7 + 100 * b] = hf[b] / (hf[b] @ hf[b]) * 2.0 ** 20
+    W = synth.f32_to_bf16_bits(Wf)
+    head = vie.DenseHead(dev_tensor(vie, W, synth.BF16), max_batch=B, max_k=k)
+    ids, lg = head(dev_tensor(vie, H, synth.BF16), k)
+    torch.cuda.synchronize()
+    ids, lg = ids.cpu().numpy(), lg.cpu().numpy()
+    oid, olg, osc = O.topk(W, synth.BF16, H, k)
+    parity.check_logits(W, synth.BF16, H, ids, lg, "far maximum")
+    parity.check_id_sets(W, synth.BF16, H, ids, oid, osc[:, -1], what="far maximum")
+    assert all(ids[b, 0] == 7 + 100 * b for b in range(B))
+
+
 @pytest.mark.parametrize("B", [1, 4])
 def test_dense_clustered_top_keys(vie, B):
     # the best rows sit next to each other, so several slabs hold many of

@@ -382,18 +382,36 @@ __global__ __launch_bounds__(kSelectThreads) void knn_select_kernel(const char *
 #pragma unroll
         for (int n = 0; n < 4; ++n) macc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     const u32x4 zero = {0u, 0u, 0u, 0u};
-    for (int c0 = 0; c0 < row_bytes; c0 += kChunkBytes) {
-        __syncthreads();
-        // stage 128 rows x 256 bytes: 16 pieces of 16 bytes per row
-        for (int p = tid; p < kSelectRows * (kChunkBytes / 16); p += kSelectThreads) {
-            const int r = p / (kChunkBytes / 16), piece = p % (kChunkBytes / 16);
-            const int off = c0 + 16 * piece;
+    // stage 128 rows x 256 bytes per chunk (16 pieces of 16 bytes per row,
+    // kPieces per thread); for bf16 rows the next chunk's pieces load into
+    // registers while the current one is multiplied
+    constexpr int kPieces = kSelectRows * (kChunkBytes / 16) / kSelectThreads;
+    static_assert(kPieces * kSelectThreads == kSelectRows * (kChunkBytes / 16), "staging shape");
+    u32x4 pre[kPieces];
+    auto load_chunk = [&](int c0) {
+#pragma unroll
+        for (int j = 0; j < kPieces; ++j) {
+            const int p = tid + j * kSelectThreads;
+            const int r = p / (kChunkBytes / 16), off = c0 + 16 * (p % (kChunkBytes / 16));
             const int32_t c = cid[r];
-            u32x4 v = zero;
-            if (c >= 0 && off < row_bytes)
-                v = *reinterpret_cast<const u32x4 *>(W + (int64_t)c * row_bytes + off);
-            *reinterpret_cast<u32x4 *>(tile + r * kChunkPitch + 16 * piece) = v;
+            pre[j] = c >= 0 && off < row_bytes ? *reinterpret_cast<const u32x4 *>(W + (int64_t)c * row_bytes + off)
+                                               : zero;
         }
+    };
+    // (bf16 rows only: fp32 rows hold an 8 x 8 block of sums per thread, and
+    // the extra registers would halve their occupancy)
+    if constexpr (BF16) load_chunk(0);
+    for (int c0 = 0; c0 < row_bytes; c0 += kChunkBytes) {
+        __syncthreads();  // every wave is done with the previous chunk
+        if constexpr (!BF16) load_chunk(c0);
+#pragma unroll
+        for (int j = 0; j < kPieces; ++j) {
+            const int p = tid + j * kSelectThreads;
+            *reinterpret_cast<u32x4 *>(tile + (p / (kChunkBytes / 16)) * kChunkPitch + 16 * (p % (kChunkBytes / 16))) =
+                pre[j];
+        }
+        if constexpr (BF16)
+            if (c0 + kChunkBytes < row_bytes) load_chunk(c0 + kChunkBytes);
         __syncthreads();
         if constexpr (BF16) {
 #pragma unroll

@@ -220,13 +220,20 @@ __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__r
         sh.count = 0u;
     }
     __syncthreads();
+    // (kSampleBatch sampled blocks per round: their loads are all in flight
+    // before the first histogram update)
+    constexpr int kSampleBatch = 8;
     uint32_t ns = 0;
-    for (int64_t j0 = 0; j0 < V; j0 += (int64_t)kSampleEvery * kTopkThreads) {
-        const int64_t j = j0 + tid;
-        ns += (uint32_t)min<int64_t>(kTopkThreads, V - j0);
-        if (j < V) {
-            const uint64_t key = key_at(j);
-            if (key) atomicAdd(&sh.hist[(uint32_t)(key >> (64 - kDigitBits))], 1u);
+    for (int64_t j0 = 0; j0 < V; j0 += (int64_t)kSampleBatch * kSampleEvery * kTopkThreads) {
+        float x[kSampleBatch];  // loads first (index clamped, no branch), keys after
+#pragma unroll
+        for (int u = 0; u < kSampleBatch; ++u)
+            x[u] = row[min<int64_t>(j0 + (int64_t)u * kSampleEvery * kTopkThreads + tid, V - 1)];
+#pragma unroll
+        for (int u = 0; u < kSampleBatch; ++u) {
+            const int64_t jb = j0 + (int64_t)u * kSampleEvery * kTopkThreads, j = jb + tid;
+            if (jb < V) ns += (uint32_t)min<int64_t>(kTopkThreads, V - jb);
+            if (j < V && j != i) atomicAdd(&sh.hist[(uint32_t)(make_key(x[u], (int32_t)j) >> (64 - kDigitBits))], 1u);
         }
     }
     const uint32_t want = (uint32_t)((2 * (int64_t)K * ns + V - 1) / V) + 4;
@@ -252,18 +259,19 @@ __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__r
     __syncthreads();
     // (fewer sampled keys than want: T0 = 1, every key)
     const uint64_t T0 = sh.count ? ((uint64_t)sh.bucket << (64 - kDigitBits)) | 1ull : 1ull;
-    // gather every key >= T0, four scores per load, four loads in flight
+    // gather every key >= T0, four scores per load, kGatherLoads loads in flight
+    constexpr int kGatherLoads = 8;
     const int64_t n4 = (V + 3) / 4;
     const float4 *row4 = reinterpret_cast<const float4 *>(row);
-    for (int64_t b0 = 0; b0 < n4; b0 += 4 * kTopkThreads) {
-        float4 v[4];
+    for (int64_t b0 = 0; b0 < n4; b0 += kGatherLoads * kTopkThreads) {
+        float4 v[kGatherLoads];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kGatherLoads; ++u) {
             const int64_t q = b0 + u * kTopkThreads + tid;
             v[u] = q < n4 ? row4[q] : float4{0.0f, 0.0f, 0.0f, 0.0f};
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kGatherLoads; ++u) {
             const int64_t j = 4 * (b0 + u * kTopkThreads + tid);
             const float x[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
 #pragma unroll

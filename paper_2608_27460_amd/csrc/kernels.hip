@@ -1319,7 +1319,11 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     const int hbytes = (row_bytes + 15) & ~15;
     const int vwords = (int)((V + 31) / 32);
     const int maxdeg = M0 > M ? M0 : M;
-    const bool pfb_on = M0 <= kPfbPerLane * G;
+    // list entries prefetched per lane: enough for M0 = 64 at every group
+    // width (16-lane groups: 4, 32: 2, 64: 1), which spares registers in the
+    // wider groups; longer lists take the unprefetched claim
+    constexpr int PF = G >= 64 ? 1 : G >= 32 ? 2 : kPfbPerLane;
+    const bool pfb_on = M0 <= PF * G;
     // LDS carve-up (sizes mirror hnsw_lds_bytes)
     char *p = smem;
     char *hs = p;
@@ -1396,7 +1400,9 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         // the scan below, which then runs under the load latency
         typedef typename Vec<VEC>::T TV;
         TV rbuf[RowCpl<BF16>::value];
-        int32_t l0[kPfbPerLane] = {-1, -1, -1, -1};
+        int32_t l0[PF];
+#pragma unroll
+        for (int u = 0; u < PF; ++u) l0[u] = -1;
         const int32_t e0 = grp < nn ? cid[grp] : -1;
         // (an opaque copy of the lane index: the per-lane addresses are then
         // formed here, not held in registers across the whole loop)
@@ -1405,7 +1411,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         if (e0 >= 0) {
             if (pfb_on) {
 #pragma unroll
-                for (int u = 0; u < kPfbPerLane; ++u) {
+                for (int u = 0; u < PF; ++u) {
                     const int t = glv + u * G;
                     l0[u] = t < M0 ? adj0[(int64_t)e0 * M0 + t] : -1;
                 }
@@ -1429,21 +1435,21 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
         if (ida >= 0 && pft >= 0) pfv = adj0[(int64_t)ida * M0 + pft];
         const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
         uint64_t gbest = 0ull;  // best key this group scored, and its node's list
-        int32_t glist[kPfbPerLane];
+        int32_t glist[PF];
         if (e0 >= 0) {
             const float s = row_finish<VEC, BF16, G>(W, e0, row_bytes, hs, gl, rbuf);
             const uint64_t key = make_key(s, e0);
             if (gl == 0 && key > worst) ckey[atomicAdd(&sh.nkeepp[par], 1u)] = key;
             gbest = key;
 #pragma unroll
-            for (int u = 0; u < kPfbPerLane; ++u) glist[u] = l0[u];
+            for (int u = 0; u < PF; ++u) glist[u] = l0[u];
         }
         for (int j = grp + kGroups; j < nn; j += kGroups) {
             const int32_t e = cid[j];
-            int32_t l[kPfbPerLane];
+            int32_t l[PF];
             if (pfb_on) {
 #pragma unroll
-                for (int u = 0; u < kPfbPerLane; ++u) {
+                for (int u = 0; u < PF; ++u) {
                     const int t = gl + u * G;
                     l[u] = t < M0 ? adj0[(int64_t)e * M0 + t] : -1;
                 }
@@ -1454,7 +1460,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             if (key > gbest) {
                 gbest = key;
 #pragma unroll
-                for (int u = 0; u < kPfbPerLane; ++u) glist[u] = l[u];
+                for (int u = 0; u < PF; ++u) glist[u] = l[u];
             }
         }
         if (gl == 0 && gbest > worst) atomicMax(&sh.bestp[par], (unsigned long long)gbest);
@@ -1470,7 +1476,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             } else if (pfb_on) {
                 if (gbest == bestnew) {
 #pragma unroll
-                    for (int u = 0; u < kPfbPerLane; ++u) {
+                    for (int u = 0; u < PF; ++u) {
                         const int t = gl + u * G;
                         if (t < M0 && glist[u] >= 0 && claim(vis, glist[u]))
                             cid[atomicAdd(&sh.nnewp[par ^ 1], 1u)] = glist[u];

@@ -1688,7 +1688,10 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int vwords = (int)((V + 31) / 32);
     const int cap = width * M0;  // most nodes claimed in one step
     const int nid = cap > M ? cap : M;
-    const bool cache_on = M0 <= kPfbPerLane * G;
+    // list entries a group keeps per lane (as in hnsw_kernel: enough for
+    // M0 = 64 at every group width)
+    constexpr int PF = G >= 64 ? 1 : G >= 32 ? 2 : kPfbPerLane;
+    const bool cache_on = M0 <= PF * G;
     const int d = row_bytes / (BF16 ? 2 : 4);
     const int d8 = Q8 ? (d + 15) & ~15 : 0;
     // LDS carve-up (sizes mirror hnsw_multi_lds_bytes)
@@ -1847,17 +1850,17 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         // score the new rows, two per group at a time; keep the keys that
         // can enter the beam, and the lists of a group's first rows
         uint64_t rk[kMultiHeld];
-        int32_t rl[kMultiHeld][kPfbPerLane];
+        int32_t rl[kMultiHeld][PF];
 #pragma unroll
         for (int r = 0; r < kMultiHeld; ++r) rk[r] = 0ull;
         int r = 0;
         for (int j = grp; j < nn; j += 2 * kGroups, r += 2) {
             const int32_t ea = cid[j];
             const int32_t eb = j + kGroups < nn ? cid[j + kGroups] : -1;
-            int32_t la[kPfbPerLane], lb[kPfbPerLane];
+            int32_t la[PF], lb[PF];
             if (cache_on && r < kMultiHeld) {
 #pragma unroll
-                for (int u = 0; u < kPfbPerLane; ++u) {
+                for (int u = 0; u < PF; ++u) {
                     const int t = gl + u * G;
                     la[u] = t < M0 ? adj0[(int64_t)ea * M0 + t] : -1;
                     lb[u] = t < M0 && eb >= 0 ? adj0[(int64_t)eb * M0 + t] : -1;
@@ -1882,7 +1885,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                     rk[x] = ka > worst ? ka : 0ull;
                     rk[x + 1] = kb > worst ? kb : 0ull;
 #pragma unroll
-                    for (int u = 0; u < kPfbPerLane; ++u) {
+                    for (int u = 0; u < PF; ++u) {
                         rl[x][u] = la[u];
                         rl[x + 1][u] = lb[u];
                     }
@@ -1927,7 +1930,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                     const int above = kept_above(rk[x]);
                     if (above < width) {
 #pragma unroll
-                        for (int u = 0; u < kPfbPerLane; ++u) {
+                        for (int u = 0; u < PF; ++u) {
                             const int t = gl + u * G;
                             if (t < M0) lcache[above * M0 + t] = rl[x][u];
                         }

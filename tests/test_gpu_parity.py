@@ -465,3 +465,60 @@ def test_hnsw_row_shapes_of_each_workload(vie, name):
     ix.to_device(dev_tensor(vie, W, wl.dtype))
     for k in wl.k:
         _compare_hnsw(vie, ix, W, wl.dtype, g, H, k, max(wl.ef), "%s k=%d" % (name, k))
+
+
+@pytest.mark.parametrize("d,dtype", [(2048, synth.BF16), (3072, synth.BF16), (1500, synth.BF16), (384, synth.F32),
+                                     (1000, synth.F32)])
+def test_multi_and_int8_at_wide_rows(vie, d, dtype):
+    """Several expansions per step and int8 layer-0 scores on rows wide
+    enough for the 32- and 64-lane groups (bf16 rows of 2048 and 3072 values,
+    a ragged 1500; fp32 rows of 384 and 1000), against the oracle's
+    multi-expansion and int8 searches on the same graph; int8 rows whose
+    width is not a multiple of 16 are refused."""
+    say("multi/int8 wide rows", d, dtype)
+    V = 6000
+    W = synth.make_w(V, d, dtype, 700 + d)
+    H, _ = synth.make_queries(W, dtype, 16, 701 + d)
+    ix = vie.Index.build(W, dtype, 16, 40, seed=702 + d, n_threads=16)
+    e, info = ix.export(), ix.info()
+    g = O.Graph(V, d, dtype, info["M"], info["M0"], 40, 702 + d, info["maxlevel"], info["entry"],
+                e["levels"], e["adj0"], e["upper_off"], e["upper"])
+    ix.to_device(dev_tensor(vie, W, dtype))
+    k, ef = 50, 128
+    # one expansion per step (hnsw_kernel at the same widths; 3000-byte rows
+    # load 8 bytes per lane chunk)
+    _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "hnsw d=%d" % d)
+    h = dev_tensor(vie, H, dtype)
+    for width in (2, 4, 8):
+        ids, lg, st = ix.query(h, k, ef, stats=True, width=width)
+        torch.cuda.synchronize()
+        ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+        oid, olg, ost = O.hnsw_search_multi(W, dtype, g, H, k, ef, width, validate=False)
+        same = np.all(st == ost, axis=1)
+        what = "multi d=%d width=%d" % (d, width)
+        parity.check_logits(W, dtype, H, ids, lg, what)
+        osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
+        parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
+        assert int((~same).sum()) <= max(1, len(H) // 20), what
+        say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))
+    oq, osc = O.quantize_rows(W, dtype)
+    q, sc = vie.quantize_rows(ix._W_dev, dtype)
+    assert np.array_equal(q.cpu().numpy(), oq)
+    if d % 16 != 0:
+        # int8 layer-0 scores load 16-byte chunks of a row: refused on the host
+        with pytest.raises(vie.VieError, match="divisible by 16"):
+            ix.attach_int8(q, sc)
+        return
+    ix.attach_int8(q, sc)
+    for width in (1, 8):
+        ids, lg, st = ix.query(h, k, ef, stats=True, width=width, int8=True)
+        torch.cuda.synchronize()
+        ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+        oid, olg, ost = O.hnsw_search_q(W, dtype, g, oq, osc, H, k, ef, width, validate=False)
+        what = "int8 d=%d width=%d" % (d, width)
+        same = np.all(st == ost, axis=1)
+        assert int((~same).sum()) == 0, "%s: %d traversal divergences" % (what, int((~same).sum()))
+        parity.check_logits(W, dtype, H, ids, lg, what)
+        osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
+        parity.check_id_sets(W, dtype, H, ids, oid, osk, what=what)
+        say("  %s mean n_dist=%.0f" % (what, st[:, 0].mean()))

@@ -522,3 +522,30 @@ def test_multi_and_int8_at_wide_rows(vie, d, dtype):
         osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
         parity.check_id_sets(W, dtype, H, ids, oid, osk, what=what)
         say("  %s mean n_dist=%.0f" % (what, st[:, 0].mean()))
+
+
+@pytest.mark.parametrize("V,d,dtype", [(3001, 37, synth.BF16), (2500, 38, synth.BF16), (2000, 5, synth.F32),
+                                       (2500, 36, synth.BF16)])
+def test_hnsw_narrow_loads_match_oracle(vie, V, d, dtype):
+    """Rows whose size is not a multiple of 16 bytes (74 bytes: 2-byte
+    chunks; 76 and 20 bytes: 4-byte chunks; 72 bytes: 8-byte chunks), one
+    and four expansions per step, against the oracle on its own graph."""
+    say("hnsw narrow loads", V, d, dtype)
+    W = synth.make_w(V, d, dtype, 300 + d)
+    H, _ = synth.make_queries(W, dtype, 24, 301 + d)
+    g = O.hnsw_build(W, dtype, 8, 40, 302 + d)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, dtype, tmp)
+        for k, ef in [(10, 50), (50, 128)]:
+            _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "hnsw d=%d k=%d ef=%d" % (d, k, ef))
+            ids, lg, st = ix.query(dev_tensor(vie, H, dtype), k, ef, stats=True, width=4)
+            torch.cuda.synchronize()
+            ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+            oid, olg, ost = O.hnsw_search_multi(W, dtype, g, H, k, ef, 4, validate=False)
+            same = np.all(st == ost, axis=1)
+            what = "multi d=%d k=%d ef=%d" % (d, k, ef)
+            parity.check_logits(W, dtype, H, ids, lg, what)
+            osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
+            parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
+            assert int((~same).sum()) <= max(1, len(H) // 20), what
+            say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))

@@ -58,6 +58,8 @@ def build_both(vie, W, dtype, K, M0, chunk_rows=0):
     (1500, 48, synth.F32, 40, 64, 0),       # K <= M0: candidates kept whole
     (2500, 32, synth.BF16, 48, 24, 700),    # four Gram chunks, the last one ragged
     (129, 8, synth.BF16, 128, 16, 0),       # K = V - 1
+    (1200, 3072, synth.BF16, 64, 32, 0),    # the Llama-3.2-3B row width: 24 staged chunks per row
+    (1800, 1000, synth.F32, 48, 24, 500),   # 4000-byte fp32 rows (last chunk partial), ragged Gram chunks
 ])
 def test_integer_rows_give_the_oracle_graph(vie, tmp_path, V, d, dtype, K, M0, chunk):
     say("gpu build (integer rows)", V, d, dtype, K, M0, chunk)

@@ -549,3 +549,45 @@ def test_hnsw_narrow_loads_match_oracle(vie, V, d, dtype):
             parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
             assert int((~same).sum()) <= max(1, len(H) // 20), what
             say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))
+
+
+@pytest.mark.parametrize("V,d,dtype", [(3000, 2048, synth.BF16), (3000, 3072, synth.BF16), (3001, 37, synth.BF16),
+                                       (2000, 1000, synth.F32)])
+def test_forced_tokens_at_other_row_widths(vie, V, d, dtype):
+    """Forced-inclusion ids scored by 32- and 64-lane groups (bf16 rows of
+    2048 and 3072 values, fp32 rows of 1000) and with 2-byte lane chunks
+    (bf16 rows of 37 values), after one and four expansions per step."""
+    say("forced widths", V, d, dtype)
+    k, ef = 20, 40
+    W = synth.make_w(V, d, dtype, 950 + d)
+    H, _ = synth.make_queries(W, dtype, 16, 951 + d)
+    ix = vie.Index.build(W, dtype, 8, 40, seed=952 + d, n_threads=16)
+    e, info = ix.export(), ix.info()
+    g = O.Graph(V, d, dtype, info["M"], info["M0"], 40, 952 + d, info["maxlevel"], info["entry"],
+                e["levels"], e["adj0"], e["upper_off"], e["upper"])
+    ix.to_device(dev_tensor(vie, W, dtype))
+    for width in (1, 4):
+        if width == 1:
+            oid, olg, ost, _ = O.hnsw_search(W, dtype, g, H, k, ef, validate=False)
+        else:
+            oid, olg, ost = O.hnsw_search_multi(W, dtype, g, H, k, ef, width, validate=False)
+        rng = np.random.default_rng(d + width)
+        forced = np.unique(np.concatenate([oid[0, :10], rng.choice(V, 50, replace=False)])).astype(np.int32)
+        n = forced.size
+        fid, flg = O.forced_merge(W, dtype, H, oid, forced)
+        ids = torch.empty((len(H), k + n), dtype=torch.int32, device="cuda")
+        lg = torch.empty((len(H), k + n), dtype=torch.float32, device="cuda")
+        st = torch.empty((len(H), 2), dtype=torch.int32, device="cuda")
+        ix.query_forced_into(dev_tensor(vie, H, dtype), k, ef, torch.from_numpy(forced).cuda(), ids, lg, st, width)
+        torch.cuda.synchronize()
+        ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+        what = "forced d=%d width=%d" % (d, width)
+        same = np.all(st == ost, axis=1)
+        assert int((~same).sum()) <= 1, what
+        parity.check_logits(W, dtype, H, ids, lg, what)
+        osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
+        parity.check_id_sets(W, dtype, H, ids, fid, osk, queries=np.nonzero(same)[0], what=what)
+        for q in np.nonzero(same)[0]:
+            assert set(forced.tolist()) <= set(ids[q].tolist()), what
+            assert (ids[q] >= 0).sum() == (fid[q] >= 0).sum(), what
+        say("  %s n=%d divergent=%d" % (what, n, int((~same).sum())))

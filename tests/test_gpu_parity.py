@@ -468,11 +468,11 @@ def test_hnsw_row_shapes_of_each_workload(vie, name):
 
 
 @pytest.mark.parametrize("d,dtype", [(2048, synth.BF16), (3072, synth.BF16), (1500, synth.BF16), (384, synth.F32),
-                                     (1000, synth.F32)])
+                                     (1000, synth.F32), (1008, synth.F32)])
 def test_multi_and_int8_at_wide_rows(vie, d, dtype):
     """Several expansions per step and int8 layer-0 scores on rows wide
     enough for the 32- and 64-lane groups (bf16 rows of 2048 and 3072 values,
-    a ragged 1500; fp32 rows of 384 and 1000), against the oracle's
+    a ragged 1500; fp32 rows of 384, 1000 and 1008), against the oracle's
     multi-expansion and int8 searches on the same graph; int8 rows whose
     width is not a multiple of 16 are refused."""
     say("multi/int8 wide rows", d, dtype)

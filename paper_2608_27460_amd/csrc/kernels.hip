@@ -51,28 +51,39 @@ template <> struct Vec<2> { typedef uint16_t T; };
 __device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
 
-__device__ __forceinline__ float dot_word(uint32_t w, uint32_t h, float acc, bool bf16)
+// Accumulator of a dot product.  A product of two bf16 values is exact in
+// fp32 and the sums are fp32; a product of two fp32 values is exact in fp64
+// and the sums are fp64, rounded to fp32 once at the end, so fp32 rows give
+// the exact score to within the fp32 rounding of the result.
+template <bool BF16> struct AccOf { typedef float T; };
+template <> struct AccOf<false> { typedef double T; };
+
+__device__ __forceinline__ float dot_word(uint32_t w, uint32_t h, float acc)
 {
-    if (bf16)
-        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, h),
-                                               acc, false);
-    return fmaf(__uint_as_float(w), __uint_as_float(h), acc);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, h), acc,
+                                           false);
+}
+__device__ __forceinline__ double dot_word(uint32_t w, uint32_t h, double acc)
+{
+    return fma((double)__uint_as_float(w), (double)__uint_as_float(h), acc);
 }
 
 template <int VEC, bool BF16>
-__device__ __forceinline__ float dot_vec(typename Vec<VEC>::T w, typename Vec<VEC>::T h, float acc)
+__device__ __forceinline__ typename AccOf<BF16>::T dot_vec(typename Vec<VEC>::T w, typename Vec<VEC>::T h,
+                                                           typename AccOf<BF16>::T acc)
 {
     if constexpr (VEC == 16) {
-        acc = dot_word(w.x, h.x, acc, BF16);
-        acc = dot_word(w.y, h.y, acc, BF16);
-        acc = dot_word(w.z, h.z, acc, BF16);
-        acc = dot_word(w.w, h.w, acc, BF16);
+        acc = dot_word(w.x, h.x, acc);
+        acc = dot_word(w.y, h.y, acc);
+        acc = dot_word(w.z, h.z, acc);
+        acc = dot_word(w.w, h.w, acc);
     } else if constexpr (VEC == 8) {
-        acc = dot_word(w.x, h.x, acc, BF16);
-        acc = dot_word(w.y, h.y, acc, BF16);
+        acc = dot_word(w.x, h.x, acc);
+        acc = dot_word(w.y, h.y, acc);
     } else if constexpr (VEC == 4) {
-        acc = dot_word(w, h, acc, BF16);
-    } else {  // one bf16
+        acc = dot_word(w, h, acc);
+    } else {  // one bf16 (rows of an odd number of bf16 values)
+        static_assert(BF16, "2-byte chunks hold bf16 values");
         acc = fmaf(__uint_as_float((uint32_t)w << 16), __uint_as_float((uint32_t)h << 16), acc);
     }
     return acc;
@@ -87,6 +98,13 @@ template <int CTRL> __device__ __forceinline__ float dpp_move(float v)
 template <int CTRL> __device__ __forceinline__ int dpp_move(int v)
 {
     return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL> __device__ __forceinline__ double dpp_move(double v)
+{
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)u, CTRL, 0xF, 0xF, true);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, true);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
 // The value held by lane (lane ^ s), s = 1, 2, 4, 8, 16 or 32, without an
@@ -138,10 +156,13 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
     return x;
 }
 
-// xor_lane for 32-bit values of any type (float, int).
+// xor_lane for 32- and 64-bit values of any type (float, int, double).
 template <typename T> __device__ __forceinline__ T xor_lane_as(T v, int s)
 {
-    return __builtin_bit_cast(T, xor_lane(__builtin_bit_cast(uint32_t, v), s));
+    if constexpr (sizeof(T) == 8)
+        return __builtin_bit_cast(T, xor_lane(__builtin_bit_cast(uint64_t, v), s));
+    else
+        return __builtin_bit_cast(T, xor_lane(__builtin_bit_cast(uint32_t, v), s));
 }
 
 // Sum over the G lanes of an aligned group (G = 16, 32 or 64), the same
@@ -160,26 +181,6 @@ template <int G, typename T> __device__ __forceinline__ T group_sum(T v)
     if constexpr (G >= 32) v += xor_lane_as(v, 16);
     if constexpr (G >= 64) v += xor_lane_as(v, 32);
     return v;
-}
-
-// Partial dot of row `row` (row_bytes bytes at W) by the G lanes of a group:
-// lane `gl` covers chunks gl, gl + G, ... of VEC bytes.  Reduced over the
-// group with xor shuffles; every lane of the group returns the full sum.
-template <int VEC, bool BF16, int G, bool STREAM = false>
-__device__ __forceinline__ float group_row_dot(const char *__restrict__ W, int64_t row, int row_bytes,
-                                               const char *hs, int gl)
-{
-    typedef typename Vec<VEC>::T T;
-    const T *w = reinterpret_cast<const T *>(W + row * (int64_t)row_bytes);
-    const T *h = reinterpret_cast<const T *>(hs);
-    const int nchunk = row_bytes / VEC;
-    float acc = 0.0f;
-#pragma unroll 4
-    for (int c = gl; c < nchunk; c += G)
-        acc = dot_vec<VEC, BF16>(STREAM ? __builtin_nontemporal_load(w + c) : w[c], h[c], acc);
-#pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, G);
-    return acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -274,22 +275,22 @@ static_assert(kDenseMaxWgs <= kMergeThreads, "the merge gives every slab maximum
 // steps halve the set each lane carries (lanes trade the half they give
 // away), the rest are plain xor steps; afterwards lane l holds the total of
 // value index l >> (6 - log2 N).
-template <int N>
-__device__ __forceinline__ float wave_sum_multi(float (&v)[N], int lane)
+template <int N, typename T>
+__device__ __forceinline__ T wave_sum_multi(T (&v)[N], int lane)
 {
 #pragma unroll
     for (int n = N, o = 32; n > 1; n >>= 1, o >>= 1) {
         const bool upper = lane & o;
 #pragma unroll
         for (int i = 0; i < n / 2; ++i) {
-            const float give = upper ? v[i] : v[i + n / 2];
-            const float keep = upper ? v[i + n / 2] : v[i];
-            v[i] = keep + __uint_as_float(xor_lane(__float_as_uint(give), o));
+            const T give = upper ? v[i] : v[i + n / 2];
+            const T keep = upper ? v[i + n / 2] : v[i];
+            v[i] = keep + xor_lane_as(give, o);
         }
     }
-    float a = v[0];
+    T a = v[0];
 #pragma unroll
-    for (int o = 32 / N; o >= 1; o >>= 1) a += __uint_as_float(xor_lane(__float_as_uint(a), o));
+    for (int o = 32 / N; o >= 1; o >>= 1) a += xor_lane_as(a, o);
     return a;
 }
 
@@ -404,9 +405,9 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
 #pragma unroll
         for (int u = 0; u < U; ++u)
             wr[u] = reinterpret_cast<const TV *>(W + (r0 + min(rb + u, nrows - 1)) * (int64_t)row_bytes);
-        float acc[NV];
+        typename AccOf<BF16>::T acc[NV];
 #pragma unroll
-        for (int v = 0; v < NV; ++v) acc[v] = 0.0f;
+        for (int v = 0; v < NV; ++v) acc[v] = 0;
 #pragma unroll VIE_DENSE_UNROLL
         for (int c = lane; c < nchunk; c += kWave) {
             TV wv[U];
@@ -419,7 +420,7 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
                 for (int u = 0; u < U; ++u) acc[q * U + u] = dot_vec<VEC, BF16>(wv[u], hv, acc[q * U + u]);
             }
         }
-        const float total = wave_sum_multi<NV>(acc, lane);
+        const float total = (float)wave_sum_multi<NV>(acc, lane);
         constexpr int lg = 6 - Log2<NV>::value;
         if ((lane & ((1 << lg) - 1)) == 0) {
             const int v = lane >> lg, q = v / U, u = v % U;
@@ -485,16 +486,16 @@ dense_stream_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const 
                            : zero;
 
     auto reduce_group = [&](int gi, const u32x4(&buf)[U][CPL]) {
-        float acc[NV];
+        typename AccOf<BF16>::T acc[NV];
 #pragma unroll
-        for (int v = 0; v < NV; ++v) acc[v] = 0.0f;
+        for (int v = 0; v < NV; ++v) acc[v] = 0;
 #pragma unroll
         for (int j = 0; j < CPL; ++j)
 #pragma unroll
             for (int q = 0; q < NB; ++q)
 #pragma unroll
                 for (int u = 0; u < U; ++u) acc[q * U + u] = dot_vec<16, BF16>(buf[u][j], hv[q][j], acc[q * U + u]);
-        const float total = wave_sum_multi<NV>(acc, lane);
+        const float total = (float)wave_sum_multi<NV>(acc, lane);
         constexpr int lg = 6 - Log2<NV>::value;
         if ((lane & ((1 << lg) - 1)) == 0) {
             const int v = lane >> lg, q = v / U, u = v % U;
@@ -806,7 +807,9 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
     __shared__ unsigned long long s_cnt;
     uint64_t lo = T, hi = ~0ull;  // invariant: count(>= lo) >= k, count(>= hi + 1) < k
     while (lo < hi) {
-        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        // lo < mid <= hi, so every round shrinks [lo, hi]; written so that
+        // nothing wraps when the interval is the whole key space (T = 0)
+        const uint64_t mid = hi - (hi - lo) / 2;
         if (tid == 0) s_cnt = 0;
         __syncthreads();
         unsigned long long c = 0;
@@ -1229,7 +1232,7 @@ __device__ __forceinline__ float row_finish(const char *__restrict__ W, int64_t 
     const int nchunk = row_bytes / VEC;
     constexpr int CPL = RowCpl<BF16>::value;
     constexpr int HB = CPL < 2 ? CPL : 2;  // query chunks per batch of reads (register budget)
-    float acc = 0.0f;
+    typename AccOf<BF16>::T acc = 0;
 #pragma unroll
     for (int i0 = 0; i0 < CPL; i0 += HB) {
         T hv[HB];
@@ -1239,7 +1242,7 @@ __device__ __forceinline__ float row_finish(const char *__restrict__ W, int64_t 
         for (int i = 0; i < HB; ++i) acc = dot_vec<VEC, BF16>(buf[i0 + i], hv[i], acc);
     }
     for (int c = gl + CPL * G; c < nchunk; c += G) acc = dot_vec<VEC, BF16>(w[c], h[c], acc);
-    return group_sum<G>(acc);
+    return (float)group_sum<G>(acc);
 }
 
 template <int VEC, bool BF16, int G>
@@ -1595,7 +1598,7 @@ __device__ __forceinline__ void row_dot2(const char *__restrict__ W, int64_t ra,
         bb[i] = c < nchunk && rb >= 0 ? wb[c] : T{};
     }
     constexpr int HB = 1;
-    float xa = 0.0f, xb = 0.0f;
+    typename AccOf<BF16>::T xa = 0, xb = 0;
 #pragma unroll
     for (int i0 = 0; i0 < CPL; i0 += HB) {
         T hv[HB];
@@ -1611,8 +1614,8 @@ __device__ __forceinline__ void row_dot2(const char *__restrict__ W, int64_t ra,
         xa = dot_vec<VEC, BF16>(wa[c], h[c], xa);
         if (rb >= 0) xb = dot_vec<VEC, BF16>(wb[c], h[c], xb);
     }
-    sa = group_sum<G>(xa);
-    sb = group_sum<G>(xb);
+    sa = (float)group_sum<G>(xa);
+    sb = (float)group_sum<G>(xb);
 }
 
 __device__ __forceinline__ int sdot16(u32x4 w, u32x4 h, int acc)

@@ -82,6 +82,11 @@ DENSE_CASES = [
     (5003, 3072, synth.BF16, 2, 10),   # two queries, rows too long for it: the slab kernel
     (8000, 1000, synth.F32, 1, 30),    # fp32, 250 chunks
     (4000, 256, synth.F32, 2, 40),     # fp32, two queries, one chunk per lane
+    # fewer slabs than k over more rows than the merge holds in LDS: every
+    # row is a candidate and the merge bisects the whole key space
+    (5000, 64, synth.BF16, 4, 50),     # matrix cores: 40 slabs of 128 rows
+    (5000, 64, synth.F32, 1, 1024),    # vector path: 1000 slabs of 5 rows
+    (151936, 64, synth.BF16, 1, 1024), # vector path: 1020 slabs of 149 rows
 ]
 
 
@@ -201,20 +206,41 @@ def _load_on_gpu(vie, g, W, dtype, tmp):
     return ix
 
 
-def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, max_diverge=0.05):
+def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None):
+    """One launch of the search variant (width expansions per layer-0 step;
+    int8 = the oracle's (rows, scales) when layer 0 walks int8 rows) against
+    the oracle's search of the same variant on the same graph: every query
+    must walk the oracle's path (equal distance and expansion counts), its
+    id set must equal the oracle's up to near ties at the k-th score, and its
+    logits must agree with the exact scores."""
     h = dev_tensor(vie, H, dtype)
-    ids, lg, st = ix.query(h, k, ef, stats=True)
+    ids, lg, st = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None)
     torch.cuda.synchronize()
     ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
-    oid, olg, ost, _ = O.hnsw_search(W, dtype, g, H, k, ef, validate=False)
+    if int8 is not None:
+        oid, olg, ost = parity.oracle_rows(O.hnsw_search_q, H, W, dtype, g, int8[0], int8[1], None, k, ef, width,
+                                           validate=False)
+    elif width > 1:
+        oid, olg, ost = parity.oracle_rows(O.hnsw_search_multi, H, W, dtype, g, None, k, ef, width, validate=False)
+    else:
+        oid, olg, ost, _ = parity.oracle_rows(O.hnsw_search, H, W, dtype, g, None, k, ef, validate=False)
     same = np.all(st == ost, axis=1)
     ndiv = int((~same).sum())
+    assert ndiv == 0, "%s: %d traversal divergences (queries %s)" % (what, ndiv, np.nonzero(~same)[0][:8].tolist())
     parity.check_logits(W, dtype, H, ids, lg, what)
     valid = oid[:, -1] >= 0
     osk = np.where(valid, parity.exact_scores(W, dtype, H, np.where(oid >= 0, oid, 0))[:, -1], 0)
-    parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same & valid)[0], what=what)
-    assert ndiv <= max(1, int(max_diverge * len(H))), "%s: %d traversal divergences" % (what, ndiv)
+    parity.check_id_sets(W, dtype, H, ids, oid, osk, what=what)
     return ids, st, ndiv
+
+
+def _library_graph(ix, W, dtype, efC, seed):
+    """The oracle's view (a Graph) of a graph built by the library."""
+    e, info = ix.export(), ix.info()
+    g = O.Graph(W.shape[0], W.shape[1], dtype, info["M"], info["M0"], efC, seed, info["maxlevel"], info["entry"],
+                e["levels"], e["adj0"], e["upper_off"], e["upper"])
+    assert O.check_graph(g) == ""
+    return g
 
 
 @pytest.mark.parametrize("V,d,dtype,M,efC", [(3000, 64, synth.F32, 8, 60), (5000, 128, synth.BF16, 12, 80),
@@ -262,7 +288,7 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
             parity.check_logits(W, synth.BF16, H, ids, lg, what)
             osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
             parity.check_id_sets(W, synth.BF16, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
-            assert int((~same).sum()) <= max(1, len(H) // 20), what
+            assert int((~same).sum()) == 0, what
             say("  %s recall@k=%.3f mean n_dist=%.0f n_expand=%.1f" %
                 (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
 
@@ -301,7 +327,7 @@ def test_forced_tokens_match_oracle(vie, case):
         torch.cuda.synchronize()
     ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
     same = np.all(st == ost, axis=1)
-    assert int((~same).sum()) <= 1, case
+    assert int((~same).sum()) == 0, case
     parity.check_logits(W, synth.BF16, H, ids, lg, "forced " + case)
     osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
     parity.check_id_sets(W, synth.BF16, H, ids, fid, osk, queries=np.nonzero(same)[0], what="forced " + case)
@@ -499,7 +525,7 @@ def test_multi_and_int8_at_wide_rows(vie, d, dtype):
         parity.check_logits(W, dtype, H, ids, lg, what)
         osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
         parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
-        assert int((~same).sum()) <= max(1, len(H) // 20), what
+        assert int((~same).sum()) == 0, what
         say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))
     oq, osc = O.quantize_rows(W, dtype)
     q, sc = vie.quantize_rows(ix._W_dev, dtype)
@@ -547,7 +573,7 @@ def test_hnsw_narrow_loads_match_oracle(vie, V, d, dtype):
             parity.check_logits(W, dtype, H, ids, lg, what)
             osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
             parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
-            assert int((~same).sum()) <= max(1, len(H) // 20), what
+            assert int((~same).sum()) == 0, what
             say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))
 
 
@@ -583,7 +609,7 @@ def test_forced_tokens_at_other_row_widths(vie, V, d, dtype):
         ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
         what = "forced d=%d width=%d" % (d, width)
         same = np.all(st == ost, axis=1)
-        assert int((~same).sum()) <= 1, what
+        assert int((~same).sum()) == 0, what
         parity.check_logits(W, dtype, H, ids, lg, what)
         osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
         parity.check_id_sets(W, dtype, H, ids, fid, osk, queries=np.nonzero(same)[0], what=what)
@@ -591,3 +617,84 @@ def test_forced_tokens_at_other_row_widths(vie, V, d, dtype):
             assert set(forced.tolist()) <= set(ids[q].tolist()), what
             assert (ids[q] >= 0).sum() == (fid[q] >= 0).sum(), what
         say("  %s n=%d divergent=%d" % (what, n, int((~same).sum())))
+
+
+# ------------------------------------- configurations of the workloads
+
+def _variants(vie, ix, W, dtype, g, H, k, ef, what, widths=(1, 8), int8=True):
+    """The sequential search, the multi-expansion search and, for rows of a
+    multiple of 16 values, the int8 walk, each against the oracle."""
+    for width in widths:
+        ids, st, _ = _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "%s width=%d" % (what, width), width=width)
+        say("  %s width=%d mean n_dist=%.0f n_expand=%.1f" % (what, width, st[:, 0].mean(), st[:, 1].mean()))
+    if int8 and W.shape[1] % 16 == 0:
+        oq, osc = O.quantize_rows(W, dtype)
+        q, sc = vie.quantize_rows(ix._W_dev, dtype)
+        ix.attach_int8(q, sc)
+        for width in widths:
+            _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "%s int8 width=%d" % (what, width), width=width,
+                          int8=(oq, osc))
+        ix.attach_int8(None, None)
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
+def test_hnsw_batches_of_256_and_more(vie, dtype):
+    """300 queries in one launch take the 256-thread workgroups of every
+    search variant; each query still walks the oracle's path."""
+    say("hnsw B=300", dtype)
+    V, d, B = 8000, 256, 300
+    W = synth.make_w(V, d, dtype, 1500)
+    H, _ = synth.make_queries(W, dtype, B, 1501)
+    ix = vie.Index.build(W, dtype, 16, 60, seed=1502, n_threads=16)
+    g = _library_graph(ix, W, dtype, 60, 1502)
+    ix.to_device(dev_tensor(vie, W, dtype))
+    _variants(vie, ix, W, dtype, g, H, 50, 128, "B=300")
+
+
+@pytest.mark.parametrize("d", [640, 1024, 2048, 3072])
+def test_hnsw_degree_64_at_model_row_widths(vie, d):
+    """M = 32 (layer-0 lists of M0 = 64, the degree of every model-shaped
+    workload) at the row widths of the Gemma-, Qwen-, Llama-1B- and
+    Llama-3B-shaped heads: the lists fill the per-lane prefetch exactly."""
+    say("hnsw M0=64", d)
+    V = 6000
+    W = synth.make_w(V, d, synth.BF16, 1600 + d)
+    H, _ = synth.make_queries(W, synth.BF16, 32, 1601 + d)
+    ix = vie.Index.build(W, synth.BF16, 32, 100, seed=1602 + d, n_threads=16)
+    g = _library_graph(ix, W, synth.BF16, 100, 1602 + d)
+    assert g.M0 == 64 and (g.adj0 >= 0).sum(axis=1).max() == 64
+    ix.to_device(dev_tensor(vie, W, synth.BF16))
+    for k, ef in [(50, 128), (50, 512)]:
+        _variants(vie, ix, W, synth.BF16, g, H, k, ef, "M0=64 d=%d ef=%d" % (d, ef))
+
+
+@pytest.mark.parametrize("d", [256, 2048])
+def test_hnsw_lists_longer_than_the_prefetch(vie, d):
+    """Layer-0 lists of up to 128 ids (M0 = 128, more than a lane group
+    prefetches: 64 ids for 16- and 32-lane groups) are claimed from HBM."""
+    say("hnsw M0=128", d)
+    V = 5000
+    W = synth.make_w(V, d, synth.BF16, 1700 + d)
+    H, _ = synth.make_queries(W, synth.BF16, 24, 1701 + d)
+    ix = vie.Index.build(W, synth.BF16, 32, 160, seed=1702 + d, n_threads=16, M0=128)
+    g = _library_graph(ix, W, synth.BF16, 160, 1702 + d)
+    assert g.M0 == 128 and (g.adj0 >= 0).sum(axis=1).max() > 64
+    ix.to_device(dev_tensor(vie, W, synth.BF16))
+    _variants(vie, ix, W, synth.BF16, g, H, 50, 200, "M0=128 d=%d" % d, widths=(1, 4))
+
+
+def test_hnsw_full_size_gemma_graph(vie):
+    """The Gemma-3-270M-shaped head at full size (262144 rows of 640 bf16
+    values with 10% hub rows: the largest visited bitmap, 32 KiB), its graph
+    built by the library at M = 32, ef_construction = 200: 32 queries at
+    ef = 128 and ef = 2048, sequential and 8 expansions per step, bf16 and
+    int8 rows, each against the oracle's search of the exported graph."""
+    wl = synth.WORKLOADS["gemma3-270m"]
+    W = wl.make_w()
+    H, _ = wl.make_queries(W, Q=32)
+    ix = vie.Index.build(W, wl.dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=16)
+    g = _library_graph(ix, W, wl.dtype, wl.efC, wl.seed_levels)
+    say("gemma full: maxlevel %d entry %d" % (g.maxlevel, g.entry))
+    ix.to_device(dev_tensor(vie, W, wl.dtype))
+    for ef in (128, 2048):
+        _variants(vie, ix, W, wl.dtype, g, H, 50, ef, "gemma full ef=%d" % ef)

@@ -418,16 +418,13 @@ typedef struct {
     int dtype, d;
 } obuilt;
 
-/* Builds the graph over the V rows of W.  select_mode: 0 = heuristic (MY18
- * Algorithm 4), 1 = simple (m nearest).  Returns an opaque handle or NULL. */
-void *oracle_hnsw_build(const void *W, int dtype, int64_t V, int d, int M, int M0, int efC,
-                        uint64_t seed, int select_mode)
+/* Builds the graph over the V rows of W with the given node levels.
+ * select_mode: 0 = heuristic (MY18 Algorithm 4), 1 = simple (m nearest).
+ * Returns an opaque handle or NULL. */
+static void *build_with_levels(const void *W, int dtype, int64_t V, int d, int M, int M0, int efC,
+                               uint64_t seed, const uint8_t *lv, int select_mode)
 {
-    if (V < 1 || d < 1 || M < 2 || M0 < M || efC < 1) return NULL;
-    uint8_t *lv = malloc((size_t)V);
-    oracle_levels(V, M, seed, lv);
     ograph *g = ograph_alloc(V, M, M0, lv);
-    free(lv);
     obuilt *ob = calloc(1, sizeof *ob);
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0,
                    malloc(sizeof(cand) * (size_t)V), malloc(sizeof(cand) * (size_t)(efC + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
@@ -511,6 +508,30 @@ done:
     free(xa);
     free(xe);
     return ob;
+}
+
+/* The graph of MY18 Algorithm 1 with levels drawn as stated above. */
+void *oracle_hnsw_build(const void *W, int dtype, int64_t V, int d, int M, int M0, int efC,
+                        uint64_t seed, int select_mode)
+{
+    if (V < 1 || d < 1 || M < 2 || M0 < M || efC < 1) return NULL;
+    uint8_t *lv = malloc((size_t)V);
+    if (!lv) return NULL;
+    oracle_levels(V, M, seed, lv);
+    void *h = build_with_levels(W, dtype, V, d, M, M0, efC, seed, lv, select_mode);
+    free(lv);
+    return h;
+}
+
+/* The same insertion with caller-chosen levels (levels[i] <= 16), so that a
+ * small hand-traced build can make the cases of Algorithm 1 happen. */
+void *oracle_hnsw_build_levels(const void *W, int dtype, int64_t V, int d, int M, int M0, int efC,
+                               const uint8_t *levels, int select_mode)
+{
+    if (V < 1 || d < 1 || M < 2 || M0 < M || efC < 1 || !levels) return NULL;
+    for (int64_t i = 0; i < V; ++i)
+        if (levels[i] > OR_MAX_LEVEL) return NULL;
+    return build_with_levels(W, dtype, V, d, M, M0, efC, 0, levels, select_mode);
 }
 
 void oracle_graph_free(void *h)

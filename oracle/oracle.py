@@ -37,6 +37,8 @@ def lib() -> C.CDLL:
         L.oracle_levels.argtypes = [i64, i32, u64, vp]
         L.oracle_hnsw_build.argtypes = [vp, i32, i64, i32, i32, i32, i32, u64, i32]
         L.oracle_hnsw_build.restype = vp
+        L.oracle_hnsw_build_levels.argtypes = [vp, i32, i64, i32, i32, i32, i32, vp, i32]
+        L.oracle_hnsw_build_levels.restype = vp
         L.oracle_graph_free.argtypes = [vp]
         L.oracle_graph_info.argtypes = [vp, vp]
         L.oracle_graph_export.argtypes = [vp, vp, vp, vp, vp]
@@ -184,12 +186,21 @@ def levels(V: int, M: int, seed: int) -> np.ndarray:
 
 
 def hnsw_build(W: np.ndarray, dtype: int, M: int, efC: int, seed: int, M0: int | None = None,
-               select: str = "heuristic") -> Graph:
-    """HNSW over the rows of W, inner product similarity (MY18 Alg. 1 + 4)."""
+               select: str = "heuristic", levels: np.ndarray | None = None) -> Graph:
+    """HNSW over the rows of W, inner product similarity (MY18 Alg. 1 + 4).
+    levels (uint8 [V]) replaces the seeded level draw when given."""
     W = _check_w(W, dtype)
     V, d = W.shape
     M0 = 2 * M if M0 is None else M0
-    h = lib().oracle_hnsw_build(_p(W), dtype, V, d, M, M0, efC, seed, 0 if select == "heuristic" else 1)
+    mode = 0 if select == "heuristic" else 1
+    if levels is None:
+        h = lib().oracle_hnsw_build(_p(W), dtype, V, d, M, M0, efC, seed, mode)
+    else:
+        lv = np.ascontiguousarray(levels, np.uint8)
+        if lv.shape != (V,):
+            raise ValueError("levels must hold one value per row")
+        h = lib().oracle_hnsw_build_levels(_p(W), dtype, V, d, M, M0, efC, _p(lv), mode)
+        seed = 0
     if not h:
         raise ValueError("oracle_hnsw_build failed")
     try:

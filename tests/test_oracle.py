@@ -177,6 +177,57 @@ def test_build_is_deterministic():
     assert (a.entry, a.maxlevel) == (b.entry, b.maxlevel)
 
 
+def _build_trace_case():
+    """tests/golden/build_trace.txt: rows, levels, parameters and the graph
+    worked out by hand (MY18 Alg. 1 + 4 as the paper's index)."""
+    lines = [l.split() for l in open(os.path.join(GOLDEN, "build_trace.txt")) if l.strip() and l[0] != "#"]
+    f = {l[0]: l[1:] for l in lines}
+    W = np.array([[float(x) for x in r.split(",")] for r in f["rows"]], np.float32)
+    levels = np.array([int(x) for x in f["levels"]], np.uint8)
+    prm = dict(x.split("=") for x in f["params"])
+    lists = {}
+    for layer in ("layer0", "layer1"):
+        for item in f[layer]:
+            node, ids = item.split(":")
+            lists[(int(layer[-1]), int(node))] = [int(x) for x in ids.split(",")]
+    return W, levels, int(prm["M"]), int(prm["M0"]), int(prm["efC"]), int(f["entry"][0]), \
+        int(f["maxlevel"][0]), lists
+
+
+def test_build_golden_hand_trace():
+    """Every list (in stored order), the entry point and the top level of a
+    build traced by hand: layer-0 lists overflow and are cut by the Alg. 4
+    heuristic (to fewer than the cap), the whole layer-1 result of node 5 is
+    its layer-0 entry set (its nearest alone would give it the list [1, 4]),
+    node 1 raises the entry point and nodes 3 and 5, at the same level, do
+    not move it."""
+    W, levels, M, M0, efC, entry, maxlevel, lists = _build_trace_case()
+    g = O.hnsw_build(W, synth.F32, M, efC, 0, M0=M0, levels=levels)
+    assert O.check_graph(g) == ""
+    assert (g.entry, g.maxlevel) == (entry, maxlevel)
+    assert np.array_equal(g.levels, levels)
+    for u in range(g.V):
+        row = g.adj0[u]
+        assert row[row >= 0].tolist() == lists[(0, u)], (u, row)
+        if levels[u] >= 1:
+            up = g.upper[g.upper_off[u]]
+            assert up[up >= 0].tolist() == lists[(1, u)], (u, up)
+        else:
+            assert g.upper_off[u] == -1 and (1, u) not in lists
+    # the heuristic is what cut the lists: the simple rule keeps the 3 nearest
+    s = O.hnsw_build(W, synth.F32, M, efC, 0, M0=M0, levels=levels, select="simple")
+    assert [s.adj0[u][s.adj0[u] >= 0].tolist() for u in (1, 2, 3)] == [[4, 2, 5], [4, 1, 0], [0, 6, 5]]
+
+
+def test_build_levels_argument_matches_the_seeded_draw():
+    W = synth.make_w(500, 12, synth.F32, 77)
+    a = O.hnsw_build(W, synth.F32, 6, 30, 11)
+    b = O.hnsw_build(W, synth.F32, 6, 30, 0, levels=O.levels(500, 6, 11))
+    for f in ("levels", "adj0", "upper_off", "upper"):
+        assert np.array_equal(getattr(a, f), getattr(b, f))
+    assert (a.entry, a.maxlevel) == (b.entry, b.maxlevel)
+
+
 def test_graph_size_matches_memory_formula():
     # Section 3: the index adds 8M bytes per node with 32-bit ids, i.e. 2M layer-0 ids.
     _, g = _build(M=8)

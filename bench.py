@@ -1,44 +1,43 @@
 #!/usr/bin/env python3
 """Benchmark of the vector-index output head on one MI355X.
 
-Workload: the Qwen3-0.6B-shaped head (|V| = 151936, d = 1024, bf16 rows,
-fp32 accumulation), M = 32, ef_construction = 200, k = 50, 1024 seeded
-synthetic queries, each served at batch size 1.
+Workload (default): the Llama-3.2-3B-shaped head, |V| = 128256 rows of
+d = 3072 bf16 values (fp32 accumulation), k = 50, 1024 seeded synthetic
+queries served one per call (B = 1), HNSW graph with M = 32 (M0 = 64),
+ef_construction = 200, built by the library on the host CPUs.
 
-A step is one pass of the head over the 1024 queries, one call per query on
-one stream: HNSW search (greedy upper layers + layer-0 beam, ef = 128) and
-scatter of the 50 retrieved logits into a -inf-filled 151936-wide row.  The
-exact dense head (GEMV + fused top-k, then the same scatter) runs as the
-baseline leg in the same run, with the same protocol.  `value` is the HNSW
-head's queries per second; the dense leg, the ef sweep, recall@50 (against
-the exact dense head) and the per-kernel roofline figures are reported next
-to it.  The CPU baseline is the plain-C oracle's HNSW search on the same
-graph (one thread, a bounded sample of the same queries).
+The beam width is the one the method needs: for each traversal (the
+sequential search; 8 expansions per step; 8 per step on int8 rows with the
+exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
+0.95 on the first 128 queries (recall against the exact dense head, itself
+parity-tested against the oracle).  The fastest of them at its ef is the
+headline traversal.
 
-The batch-graph leg builds a single-layer graph over W_out on the GPU
-(vie_index_build_gpu: exact 128 nearest rows by inner product, the
-neighbour-selection heuristic, reverse edges) and searches it at B = 1 with
-the same protocol, next to the HNSW graph built on the host CPUs.
+A step is 128 queries, each a call of the head at B = 1 on one stream: the
+search and the scatter of its 50 logits into a -inf-filled 128256-wide row;
+successive steps take successive blocks of the 1024 queries.  `value` is the
+headline traversal's queries per second over the timed steps.  Beside it, in
+the same run and with the same protocol: the sequential traversal at its own
+ef, the exact dense head (GEMV + fused top-k + scatter; calls alternate
+between two copies of W_out so that no call finds the matrix in the 256 MB
+Infinity Cache), per-call percentiles (p10/p50/p90), an fp32-row leg of the
+same shape (the paper's precision), queries per call B = 1/4/16/64, the
+batch graph built on the GPU, forced-inclusion tokens, the per-launch kernel
+times and algorithmic bytes behind the roofline figures, and the oracle on
+the host cores: its queries/s, and its ids, counts and expansion order
+compared with the GPU's for every query it ran.
 
-The recall-target leg finds, for each traversal (sequential beam, 8
-expansions per step, 8 per step on int8 rows with the exact re-rank; on the
-HNSW graph and on the batch graph), the smallest beam width in 128 .. 4096
-whose recall@k reaches 0.95 on the first 128 queries, and its per-call time
-next to the dense head's.
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--quick]
 
-The other workloads (--workload tiny | llama3.2-1b | gemma3-270m |
-llama3.2-3b) run the same protocol at their own shapes, ef and k; the Gemma
-shape adds a k sweep (20, 50, 100) and the Llama-3.2-3B shape a sweep of
-queries per call (1, 4, 16, 64: HNSW with one workgroup per query against
-the dense head, which switches to the matrix cores from 3 queries on).
-
-    python bench.py [--steps K] [--warmup W] [--workload NAME]
+Other workloads: --workload tiny | qwen3-0.6b | llama3.2-1b | gemma3-270m.
 """
 from __future__ import annotations
 
 import argparse
+import concurrent.futures as cf
 import json
 import os
+import platform
 import sys
 import time
 
@@ -48,13 +47,25 @@ METRIC = "us/query and queries/s of top-k output head at B=1 (HNSW vs dense), %H
 HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SRC = os.path.join(ROOT, "paper_2608_27460_amd", "csrc", "kernels.hip")
+NODE_MASK = (1 << 26) - 1
+
+TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0)
+    "sequential": (1, False),
+    "width8": (8, False),
+    "int8_width8": (8, True),
+}
+KERNEL_OF = {
+    "sequential": "hnsw_kernel",
+    "width8": "hnsw_multi_kernel (bf16 rows, 8 per step)",
+    "int8_width8": "hnsw_multi_kernel (int8 rows, 8 per step, exact re-rank)",
+}
 
 
 def measured_traffic(workload):
     """HBM bytes per launch from the committed counter summary of this workload
     (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading of a
-    plain device copy of known size).  None when no summary exists or when the
-    kernel source has changed since the counters were taken."""
+    plain device copy of known size).  Empty when no summary exists or when
+    the kernel source has changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.txt" % workload)
     if not os.path.exists(path):
@@ -74,35 +85,66 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def pct(a):
+    a = np.asarray(a, np.float64)
+    return {"p10": round(float(np.percentile(a, 10)), 2), "p50": round(float(np.percentile(a, 50)), 2),
+            "p90": round(float(np.percentile(a, 90)), 2), "mean": round(float(a.mean()), 2)}
+
+
+def layer_counts(trace, graph, M):
+    """(upper-layer expansions, layer-0 expansions, distance evaluations above
+    layer 0) of one query, replayed from its expansion record on the graph:
+    on each upper layer the search visits its entry point and every
+    neighbour of the nodes it expands; the first entry point is scored once."""
+    t = trace[trace >= 0]
+    node, lay = t & NODE_MASK, t >> 27
+    up_exp = int((lay >= 1).sum())
+    n_up = 1
+    for L in sorted(set(lay[lay >= 1].tolist()), reverse=True):
+        nodes = node[lay == L]
+        vis = {int(nodes[0])}
+        for u in nodes:
+            lst = graph["upper"][graph["upper_off"][u] + L - 1]
+            vis.update(int(x) for x in lst if x >= 0)
+        n_up += len(vis) - 1
+    return up_exp, int((lay == 0).sum()), n_up
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="qwen3-0.6b")
-    ap.add_argument("--ef", type=int, default=0, help="beam width (default: the workload's middle ef)")
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="llama3.2-3b")
     ap.add_argument("--k", type=int, default=0, help="results per query (default: the workload's middle k)")
-    ap.add_argument("--queries", type=int, default=0, help="queries per step (default: the workload's)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
+    ap.add_argument("--step-queries", type=int, default=128, help="queries per timed step")
+    ap.add_argument("--target-recall", type=float, default=0.95)
+    ap.add_argument("--calib-queries", type=int, default=128, help="queries that choose each traversal's ef")
+    ap.add_argument("--ef-ladder", type=lambda x: [int(v) for v in x.split(",") if v],
+                    default=[128, 256, 512, 1024, 2048, 4096])
+    ap.add_argument("--traversal", default="", help="force the headline traversal (default: the fastest)")
+    ap.add_argument("--ef", type=int, default=0, help="force the headline beam width (skips the calibration)")
+    ap.add_argument("--quick", action="store_true",
+                    help="headline and dense legs only (no fp32, batch, graph, forced or CPU legs): for profilers")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="wall-clock budget of the oracle leg")
+    ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: min(16, nproc))")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cache", default=os.environ.get("VIE_CACHE", "/tmp/vie_cache"))
-    ap.add_argument("--sweep-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024, 2048, 4096],
-                    help="extra beam widths of the ef sweep (comma separated)")
-    ap.add_argument("--sweep-queries", type=int, default=128, help="queries per extra sweep point")
-    ap.add_argument("--int8-widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[1, 4, 8],
-                    help="expansion widths of the int8-row sweep (comma separated; empty: skip)")
+    ap.add_argument("--no-fp32", action="store_true")
     ap.add_argument("--forced", type=int, default=64,
                     help="forced-inclusion tokens of the forced leg (ids 0..n-1 stand in for special tokens)")
-    ap.add_argument("--widths", type=lambda x: [int(v) for v in x.split(",") if v], default=[2, 4, 8],
-                    help="expansion widths of the vie_query_ex sweep (comma separated)")
     ap.add_argument("--batch-graph-k", type=int, default=128,
                     help="candidates per node of the GPU-built batch graph leg (0: skip the leg)")
-    ap.add_argument("--batch-graph-ef", type=lambda x: [int(v) for v in x.split(",") if v], default=[512, 1024],
-                    help="extra beam widths searched on the batch graph (first --sweep-queries queries)")
-    ap.add_argument("--target-recall", type=float, default=0.95,
-                    help="recall@k that the beam-width search of each traversal aims for (0 skips it)")
-    ap.add_argument("--target-ef", type=lambda x: [int(v) for v in x.split(",") if v],
-                    default=[128, 256, 512, 1024, 2048, 4096], help="beam widths tried, in order, for the target")
+    ap.add_argument("--cache", default=os.environ.get("VIE_CACHE", "/tmp/vie_cache"))
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="finish with a device copy of this many MiB (a known-size reference for HBM counters)")
     args = ap.parse_args()
@@ -120,333 +162,344 @@ def main() -> int:
         print("bench.py needs an MI355X", file=sys.stderr)
         return 2
     wl = synth.WORKLOADS[args.workload]
-    Q = args.queries or wl.Q
+    Q = wl.Q
     k = args.k or wl.k[len(wl.k) // 2]
-    ef = args.ef or wl.ef[len(wl.ef) // 2]
     s = wl.elem_bytes
+    SQ = min(args.step_queries, Q)
+    nthreads = min(16, os.cpu_count() or 1)
     dev = torch.device("cuda:0")
 
     t0 = time.time()
     W = wl.make_w()
-    H, _ = wl.make_queries(W, Q=Q)
+    H, _ = wl.make_queries(W)
     log("[bench] inputs %s: %.1fs" % (wl.name, time.time() - t0))
 
-    os.makedirs(args.cache, exist_ok=True)
-    gpath = os.path.join(args.cache, "%s-M%d-efC%d-seed%d.vie" % (wl.name, wl.M, wl.efC, wl.seed_levels))
-    t0 = time.time()
-    ix = None
-    cpu_build_s = None
-    if os.path.exists(gpath):
-        try:
-            ix = vie.Index.load(gpath, W)
-            log("[bench] graph loaded from %s" % gpath)
-        except vie.VieError as e:
-            log("[bench] cached graph rejected (%s); rebuilding" % e)
-    if ix is None:
-        nt = min(16, os.cpu_count() or 1)
-        ix = vie.Index.build(W, wl.dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=nt)
-        ix.save(gpath)
-        cpu_build_s = time.time() - t0
-        log("[bench] graph built with %d threads in %.1fs" % (nt, cpu_build_s))
+    def graph_for(Wh, dtype, tag):
+        os.makedirs(args.cache, exist_ok=True)
+        path = os.path.join(args.cache, "%s-%s-M%d-efC%d-seed%d.vie" % (wl.name, tag, wl.M, wl.efC, wl.seed_levels))
+        t = time.time()
+        if os.path.exists(path):
+            try:
+                ix_ = vie.Index.load(path, Wh)
+                log("[bench] graph loaded from %s" % path)
+                return ix_, None
+            except vie.VieError as e:
+                log("[bench] cached graph rejected (%s); rebuilding" % e)
+        ix_ = vie.Index.build(Wh, dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=nthreads)
+        ix_.save(path)
+        log("[bench] %s graph built with %d threads in %.1fs" % (tag, nthreads, time.time() - t))
+        return ix_, time.time() - t
+
+    ix, cpu_build_s = graph_for(W, wl.dtype, synth.DTYPE_NAMES[wl.dtype])
     info = ix.info()
+    graph = ix.export()
 
     Wd = vie.host_to_torch(W, wl.dtype).to(dev)
     Hd = vie.host_to_torch(H, wl.dtype).to(dev)
     ix.to_device(Wd)
-    head = vie.DenseHead(Wd, max_batch=1, max_k=k)
-    ids = torch.empty((Q, k), dtype=torch.int32, device=dev)
-    lg = torch.empty((Q, k), dtype=torch.float32, device=dev)
-    st = torch.empty((Q, 2), dtype=torch.int32, device=dev)
-    dids = torch.empty((Q, k), dtype=torch.int32, device=dev)
-    dlg = torch.empty((Q, k), dtype=torch.float32, device=dev)
-    row = torch.empty((1, wl.V), dtype=torch.float32, device=dev)  # the step's full-vocab logits
-    hv = [Hd[q:q + 1] for q in range(Q)]
-    iv, lv, sv = [ids[q:q + 1] for q in range(Q)], [lg[q:q + 1] for q in range(Q)], [st[q:q + 1] for q in range(Q)]
-    div, dlv = [dids[q:q + 1] for q in range(Q)], [dlg[q:q + 1] for q in range(Q)]
     stream = torch.cuda.current_stream(dev)
+    row = torch.empty((1, wl.V), dtype=torch.float32, device=dev)  # a call's full-vocabulary logits
+    hv = [Hd[q:q + 1] for q in range(Q)]
+    qrows = qscale = None
+    if wl.d % 16 == 0:
+        qrows, qscale = vie.quantize_rows(Wd, wl.dtype)
+        ix.attach_int8(qrows, qscale)
+    travs = [t for t in TRAVERSALS if not TRAVERSALS[t][1] or qrows is not None]
 
-    def hnsw_step(ef_=ef):
-        for q in range(Q):
-            ix.query_into(hv[q], k, ef_, iv[q], lv[q], sv[q])
-            vie.scatter_into(iv[q], lv[q], wl.V, row)
+    def out_bufs(n, kk=k):
+        return (torch.empty((n, kk), dtype=torch.int32, device=dev), torch.empty((n, kk), dtype=torch.float32,
+                                                                                device=dev),
+                torch.empty((n, 2), dtype=torch.int32, device=dev))
 
-    def dense_step():
-        for q in range(Q):
-            vie.dense_topk_into(Wd, hv[q], k, div[q], dlv[q], head.workspace)
-            vie.scatter_into(div[q], dlv[q], wl.V, row)
+    def events(n):
+        return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
 
-    def timed(step, K, W_):
-        # K steps between two events on the launch stream (nothing else recorded inside)
-        for _ in range(W_):
-            step()
-        torch.cuda.synchronize()
-        outer = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-        t = time.perf_counter()
-        outer[0].record(stream)
-        for i in range(K):
-            step()
-        outer[1].record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t
-        return outer[0].elapsed_time(outer[1]), wall
-
-    def per_call_us(fn, n_calls):
-        # mean event-timed duration of n_calls back-to-back calls (after one warm-up call)
+    def back_to_back(fn, n):
+        """Mean event-timed duration (us) of n back-to-back calls after one warm-up call."""
         fn(0)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = events(2)
         e0.record(stream)
-        for c in range(n_calls):
+        for c in range(n):
             fn(c)
         e1.record(stream)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / n_calls
+        return e0.elapsed_time(e1) * 1e3 / n
 
-    # ---- HNSW head (the method) ----------------------------------------
-    log("[bench] HNSW head: %d steps x %d queries, ef=%d" % (args.steps, Q, ef))
-    h_ms, h_wall = timed(hnsw_step, args.steps, args.warmup)
-    stats = st.cpu().numpy().astype(np.int64)
-    hnsw_ids = ids.cpu().numpy()
-    # ---- dense head (the baseline) -------------------------------------
-    log("[bench] dense head: %d steps x %d queries" % (args.steps, Q))
-    d_ms, d_wall = timed(dense_step, args.steps, args.warmup)
-    exact_ids = dids.cpu().numpy()
-    # ---- per-launch kernel time: Q back-to-back calls between two events ----
-    # (the roofline figures; the kernels alone, no scatter and no events in between)
-    h_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, iv[c], lv[c], sv[c]), Q)
-    d_us = per_call_us(lambda c: vie.dense_topk_into(Wd, hv[c], k, div[c], dlv[c], head.workspace), Q)
+    def per_call(fn, n):
+        """Event-timed duration (us) of each of n calls (an event between calls)."""
+        fn(0)
+        torch.cuda.synchronize()
+        ev = events(n + 1)
+        ev[0].record(stream)
+        for c in range(n):
+            fn(c)
+            ev[c + 1].record(stream)
+        torch.cuda.synchronize()
+        return [ev[c].elapsed_time(ev[c + 1]) * 1e3 for c in range(n)]
+
+    def timed_steps(step, K, Wu):
+        """K steps between two events on the launch stream (nothing recorded inside)."""
+        for i in range(Wu):
+            step(i)
+        torch.cuda.synchronize()
+        e0, e1 = events(2)
+        t = time.perf_counter()
+        e0.record(stream)
+        for i in range(K):
+            step(Wu + i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1), time.perf_counter() - t
 
     def recall(a, b, kk=None):
         kk = kk or a.shape[1]
         return float(np.mean([len(set(x[:kk].tolist()) & set(y[:kk].tolist())) / kk for x, y in zip(a, b)]))
 
-    def reach(index, width, int8, nq):
-        # the smallest beam of --target-ef whose recall@k on the first nq
-        # queries reaches --target-recall; per-call kernel time as per_call_us
-        ri = torch.empty((nq, k), dtype=torch.int32, device=dev)
-        rl = torch.empty((nq, k), dtype=torch.float32, device=dev)
+    # ---- exact top-k of every query (the dense head; parity-tested) --------
+    dense = vie.DenseHead(Wd, max_batch=64, max_k=max(k, max(wl.k)))
+    ex_ids = torch.empty((Q, k), dtype=torch.int32, device=dev)
+    ex_lg = torch.empty((Q, k), dtype=torch.float32, device=dev)
+    for q0 in range(0, Q, 64):
+        vie.dense_topk_into(Wd, Hd[q0:q0 + 64], k, ex_ids[q0:q0 + 64], ex_lg[q0:q0 + 64], dense.workspace)
+    exact_ids = ex_ids.cpu().numpy()
+
+    def search_into(index, trav, ef, q, ids_, lg_, st_=None, trace=None):
+        width, int8 = TRAVERSALS[trav]
+        index.query_into(hv[q], k, ef, ids_, lg_, st_, width, int8, trace)
+
+    # ---- each traversal's beam width for the recall target ----------------
+    nc = min(Q, args.calib_queries)
+    ci, cl, cs = out_bufs(nc)
+    calib = {}
+    chosen = {}
+    for trav in travs:
+        if args.ef:
+            chosen[trav] = args.ef
+            continue
         tried = {}
-        for e in sorted(v for v in args.target_ef if v >= k):
-            us = per_call_us(lambda c: index.query_into(hv[c], k, e, ri[c:c + 1], rl[c:c + 1], None, width, int8), nq)
-            r = recall(ri.cpu().numpy(), exact_ids[:nq])
-            tried[str(e)] = [round(us, 2), round(r, 4)]
+        for ef in args.ef_ladder:
+            if ef < k:
+                continue
+            us = back_to_back(lambda c: search_into(ix, trav, ef, c, ci[c:c + 1], cl[c:c + 1]), nc)
+            r = recall(ci.cpu().numpy(), exact_ids[:nc])
+            tried[str(ef)] = {"us_per_query": round(us, 2), "recall_at_k": round(r, 4)}
             if r >= args.target_recall:
-                return {"ef": e, "us_per_query": round(us, 2), "recall_at_k": round(r, 4), "tried": tried}
-        return {"ef": None, "us_per_query": None, "recall_at_k": None, "tried": tried}
+                chosen[trav] = ef
+                break
+        calib[trav] = {"ef": chosen.get(trav), "tried": tried}
+        log("[bench] %s: ef %s reaches recall@%d %.2f" % (trav, chosen.get(trav), k, args.target_recall))
+    reachable = [t for t in travs if chosen.get(t)]
+    if not reachable:
+        log("[bench] no traversal reaches the recall target; the headline falls back to the widest beam")
+        chosen = {t: max(args.ef_ladder) for t in travs}
+        reachable = travs
+    if args.traversal:
+        head_trav = args.traversal
+    elif args.ef:
+        head_trav = "int8_width8" if "int8_width8" in travs else "width8"
+    else:
+        head_trav = min(reachable, key=lambda t: calib[t]["tried"][str(chosen[t])]["us_per_query"])
+    ef = chosen[head_trav]
 
-    target = {}
-    tq = min(Q, args.sweep_queries)
+    # ---- headline: K steps of SQ queries at B = 1 --------------------------
+    hi, hl, hs = out_bufs(Q)
+    iv = [hi[q:q + 1] for q in range(Q)]
+    lv = [hl[q:q + 1] for q in range(Q)]
+    sv = [hs[q:q + 1] for q in range(Q)]
 
-    # ---- ef sweep (same protocol; one warm-up and one timed pass each) ----
-    # Beams wider than the workload's own ef values run on the first
-    # --sweep-queries queries only.
-    sweep = {}
-    for e in sorted(set(wl.ef) | {ef} | set(args.sweep_ef)):
-        nq = Q if e <= max(max(wl.ef), ef) else min(Q, args.sweep_queries)
+    def head_step(i, trav=head_trav, ef_=None):
+        ef_ = ef_ or chosen[trav]
+        q0 = (i * SQ) % Q
+        for q in range(q0, min(Q, q0 + SQ)):
+            search_into(ix, trav, ef_, q, iv[q], lv[q], sv[q])
+            vie.scatter_into(iv[q], lv[q], wl.V, row)
 
-        def step_e(e=e, nq=nq):
-            for q in range(nq):
-                ix.query_into(hv[q], k, e, iv[q], lv[q], sv[q])
-                vie.scatter_into(iv[q], lv[q], wl.V, row)
+    log("[bench] headline %s at ef=%d: %d steps x %d queries" % (head_trav, ef, args.steps, SQ))
+    h_ms, h_wall = timed_steps(head_step, args.steps, args.warmup)
+    # every query once (untimed) for recall, counts and expansion records
+    cap = max(ef, k) + 1024
+    trace = torch.full((Q, cap), -1, dtype=torch.int32, device=dev)
+    for q0 in range(0, Q, 256):
+        width, int8 = TRAVERSALS[head_trav]
+        ix.query_into(Hd[q0:q0 + 256], k, ef, hi[q0:q0 + 256], hl[q0:q0 + 256], hs[q0:q0 + 256], width, int8,
+                      trace[q0:q0 + 256])
+    head_ids, head_lg = hi.cpu().numpy(), hl.cpu().numpy()
+    head_st = hs.cpu().numpy().astype(np.int64)
+    head_tr = trace.cpu().numpy()
+    head_calls = per_call(lambda c: (search_into(ix, head_trav, ef, c, iv[c], lv[c]),
+                                     vie.scatter_into(iv[c], lv[c], wl.V, row)), min(Q, 256))
+    head_kernel_us = back_to_back(lambda c: search_into(ix, head_trav, ef, c, iv[c], lv[c]), SQ)
 
-        ms_e, _ = timed(step_e, 1, 1)
-        sweep[str(e)] = {"us_per_query": round(ms_e * 1e3 / nq, 2), "queries": nq,
-                         "recall_at_k": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq]), 4),
-                         "recall_at_2": round(recall(ids.cpu().numpy()[:nq], exact_ids[:nq], 2), 4),
-                         "mean_n_dist": float(st.cpu().numpy()[:nq, 0].mean())}
-    # ---- all queries in one launch (one workgroup each) -------------------
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ix.query_into(Hd, k, ef, ids, lg, st)
-    a.record(stream)
-    ix.query_into(Hd, k, ef, ids, lg, st)
-    b.record(stream)
-    torch.cuda.synchronize()
-    batched_s = a.elapsed_time(b) * 1e-3
-    batched_qps = Q / batched_s
-    bst = st.cpu().numpy().astype(np.float64)
-    batched_bytes = float((bst[:, 0] * wl.d * s + bst[:, 1] * wl.M0 * 4 + wl.d * s + k * 8).sum())
-    batched_gbs = batched_bytes / batched_s / 1e9
+    # ---- the sequential traversal at its own ef (the paper's search) -------
+    seq = None
+    if head_trav != "sequential" and not args.quick and chosen.get("sequential"):
+        ef_s = chosen["sequential"]
+        nseq = min(Q, 64)
+        calls = per_call(lambda c: (search_into(ix, "sequential", ef_s, c, iv[c], lv[c], sv[c]),
+                                    vie.scatter_into(iv[c], lv[c], wl.V, row)), nseq)
+        seq = {"ef": ef_s, "queries": nseq, "us_per_query": pct(calls),
+               "recall_at_k": round(recall(hi.cpu().numpy()[:nseq], exact_ids[:nseq]), 4),
+               "kernel": KERNEL_OF["sequential"]}
 
-    # ---- expansion-width sweep (vie_query_ex; B = 1, first 256 queries) ---
-    w_sweep = {}
-    for wd in args.widths:
-        nq = min(Q, 256)
-        wi = torch.empty((nq, k), dtype=torch.int32, device=dev)
-        wlg = torch.empty((nq, k), dtype=torch.float32, device=dev)
-        ws = torch.empty((nq, 2), dtype=torch.int32, device=dev)
-        w_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, wi[c:c + 1], wlg[c:c + 1], ws[c:c + 1], wd), nq)
-        wst = ws.cpu().numpy().astype(np.int64)
-        w_sweep[str(wd)] = {"us_per_query": round(w_us, 2), "queries": nq,
-                            "recall_at_k": round(recall(wi.cpu().numpy(), exact_ids[:nq]), 4),
-                            "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
-                            "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean())}
+    # ---- dense head: calls alternate between two copies of W_out -----------
+    Wd2 = Wd.clone()
+    Ws = [Wd, Wd2]
+    di, dl, _ = out_bufs(Q)
+    div_, dlv_ = [di[q:q + 1] for q in range(Q)], [dl[q:q + 1] for q in range(Q)]
+    dhead = vie.DenseHead(Wd, max_batch=1, max_k=k)
 
-    if args.target_recall > 0:
-        log("[bench] beam widths reaching recall@k %.2f" % args.target_recall)
-        target["hnsw"] = reach(ix, 1, False, tq)
-        target["hnsw_width_8"] = reach(ix, 8, False, tq)
+    def dense_call(q, scatter=True):
+        vie.dense_topk_into(Ws[q & 1], hv[q], k, div_[q], dlv_[q], dhead.workspace)
+        if scatter:
+            vie.scatter_into(div_[q], dlv_[q], wl.V, row)
 
-    # ---- int8 rows for layer 0, exact re-rank (B = 1, first 256 queries) ----
-    q_sweep = {}
-    if args.int8_widths and wl.d % 16 == 0:
-        qrows, qscale = vie.quantize_rows(Wd, wl.dtype)
-        ix.attach_int8(qrows, qscale)
-        for wd in args.int8_widths:
-            nq = min(Q, 256)
-            wi = torch.empty((nq, k), dtype=torch.int32, device=dev)
-            wlg = torch.empty((nq, k), dtype=torch.float32, device=dev)
-            ws = torch.empty((nq, 2), dtype=torch.int32, device=dev)
-            w_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, wi[c:c + 1], wlg[c:c + 1], ws[c:c + 1], wd,
-                                                       True), nq)
-            wst = ws.cpu().numpy().astype(np.int64)
-            q_sweep[str(wd)] = {"us_per_query": round(w_us, 2), "queries": nq,
-                                "recall_at_k": round(recall(wi.cpu().numpy(), exact_ids[:nq]), 4),
-                                "recall_at_2": round(recall(wi.cpu().numpy(), exact_ids[:nq], 2), 4),
-                                "mean_n_dist": float(wst[:, 0].mean()), "mean_n_expand": float(wst[:, 1].mean()),
-                                "row_bytes_per_query": float(wst[:, 0].mean() * wl.d)}
-        wb = max(args.int8_widths)
-        torch.cuda.synchronize()
-        ix.query_into(Hd, k, ef, ids, lg, st, wb, True)
-        a.record(stream)
-        ix.query_into(Hd, k, ef, ids, lg, st, wb, True)
-        b.record(stream)
-        torch.cuda.synchronize()
-        q_sweep["batched_width_%d" % wb] = {"queries_per_s": round(Q / (a.elapsed_time(b) * 1e-3), 1),
-                                             "recall_at_k": round(recall(ids.cpu().numpy(), exact_ids), 4)}
-        if args.target_recall > 0:
-            target["hnsw_int8_width_8"] = reach(ix, 8, True, tq)
-        ix.attach_int8(None, None)
-        if not args.batch_graph_k:
-            del qrows, qscale
+    def dense_step(i):
+        q0 = (i * SQ) % Q
+        for q in range(q0, min(Q, q0 + SQ)):
+            dense_call(q)
 
-    # ---- batch graph built on the GPU (vie_index_build_gpu), searched at B = 1 ----
-    batch = None
-    if args.batch_graph_k:
-        Kb = min(args.batch_graph_k, wl.V - 1)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        bix = vie.Index.build_gpu(Wd, Kb, wl.M0)  # first call: includes the GEMM library's set-up
-        first_s = time.perf_counter() - t0
-        del bix
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        bix = vie.Index.build_gpu(Wd, Kb, wl.M0)
-        build_s = time.perf_counter() - t0
-        bsweep = {}
-        for e in sorted(set(wl.ef) | {ef} | set(args.batch_graph_ef)):
-            nq = Q if e <= max(max(wl.ef), ef) else min(Q, args.sweep_queries)
-            bi = torch.empty((nq, k), dtype=torch.int32, device=dev)
-            bl = torch.empty((nq, k), dtype=torch.float32, device=dev)
-            bs = torch.empty((nq, 2), dtype=torch.int32, device=dev)
-            b_us = per_call_us(lambda c: bix.query_into(hv[c], k, e, bi[c:c + 1], bl[c:c + 1], bs[c:c + 1]), nq)
-            bst = bs.cpu().numpy().astype(np.int64)
-            bsweep[str(e)] = {"us_per_query": round(b_us, 2), "queries": nq,
-                              "recall_at_k": round(recall(bi.cpu().numpy(), exact_ids[:nq]), 4),
-                              "recall_at_2": round(recall(bi.cpu().numpy(), exact_ids[:nq], 2), 4),
-                              "mean_n_dist": float(bst[:, 0].mean()), "mean_n_expand": float(bst[:, 1].mean())}
-        bix.query_into(Hd, k, ef, ids, lg, st)
-        torch.cuda.synchronize()
-        a.record(stream)
-        bix.query_into(Hd, k, ef, ids, lg, st)
-        b.record(stream)
-        torch.cuda.synchronize()
-        if args.target_recall > 0:
-            target["batch_graph"] = reach(bix, 1, False, tq)
-            target["batch_graph_width_8"] = reach(bix, 8, False, tq)
-            if args.int8_widths and wl.d % 16 == 0:
-                bix.attach_int8(qrows, qscale)
-                target["batch_graph_int8_width_8"] = reach(bix, 8, True, tq)
-                bix.attach_int8(None, None)
-        batch = {"K": Kb, "M0": wl.M0, "build_s": round(build_s, 4), "first_build_s": round(first_s, 4),
-                 "cpu_hnsw_build_s": None if cpu_build_s is None else round(cpu_build_s, 2),
-                 "entry": bix.info()["entry"], "ef_sweep": bsweep,
-                 "batched_queries_per_s": round(Q / (a.elapsed_time(b) * 1e-3), 1),
-                 "batched_recall_at_k": round(recall(ids.cpu().numpy(), exact_ids), 4)}
-        del bix
+    log("[bench] dense head: %d steps x %d queries" % (args.steps, SQ))
+    d_ms, d_wall = timed_steps(dense_step, args.steps, args.warmup)
+    dense_calls = per_call(lambda c: dense_call(c), min(Q, 256))
+    d_kernel_us = back_to_back(lambda c: dense_call(c, scatter=False), SQ)
+    assert np.array_equal(di.cpu().numpy()[:SQ], exact_ids[:SQ])  # both copies give the exact top k
+    del Wd2, Ws
 
-    # ---- forced-inclusion tokens (stand-in: the first 64 ids; B = 1) -------
-    forced = None
-    if args.forced:
-        nq = min(Q, 256)
-        fids = torch.arange(args.forced, dtype=torch.int32, device=dev)
-        fi = torch.empty((nq, k + args.forced), dtype=torch.int32, device=dev)
-        fl = torch.empty((nq, k + args.forced), dtype=torch.float32, device=dev)
-        f_us = per_call_us(lambda c: ix.query_forced_into(hv[c], k, ef, fids, fi[c:c + 1], fl[c:c + 1]), nq)
-        p_us = per_call_us(lambda c: ix.query_into(hv[c], k, ef, iv[c], lv[c]), nq)
-        forced = {"n": args.forced, "ids": "0..%d" % (args.forced - 1), "queries": nq,
-                  "us_per_query": round(f_us, 2), "search_only_us_per_query": round(p_us, 2)}
-
-    # ---- k sweep (workloads quoted at several k; B = 1, first 256 queries) --
-    k_sweep = {}
-    if len(wl.k) > 1:
-        nq = min(Q, 256)
-        for kk in wl.k:
-            ik = torch.empty((nq, kk), dtype=torch.int32, device=dev)
-            lk = torch.empty((nq, kk), dtype=torch.float32, device=dev)
-            dk = torch.empty((nq, kk), dtype=torch.int32, device=dev)
-            dlk = torch.empty((nq, kk), dtype=torch.float32, device=dev)
-            hk = vie.DenseHead(Wd, max_batch=1, max_k=kk)
-            h_us_k = per_call_us(lambda c: ix.query_into(hv[c], kk, ef, ik[c:c + 1], lk[c:c + 1]), nq)
-            d_us_k = per_call_us(lambda c: vie.dense_topk_into(Wd, hv[c], kk, dk[c:c + 1], dlk[c:c + 1],
-                                                               hk.workspace), nq)
-            k_sweep[str(kk)] = {"hnsw_us_per_query": round(h_us_k, 2), "dense_us_per_query": round(d_us_k, 2),
-                                "recall_at_k": round(recall(ik.cpu().numpy(), dk.cpu().numpy()), 4),
-                                "queries": nq}
-            del hk
-
-    # ---- batch sweep (queries per call; HNSW: one workgroup per query) ----
-    b_sweep = {}
-    if len(wl.B) > 1:
-        bdense = vie.DenseHead(Wd, max_batch=max(wl.B), max_k=k)
-        for Bc in wl.B:
-            ncall = Q // Bc
-            bi = torch.empty((ncall * Bc, k), dtype=torch.int32, device=dev)
-            bl = torch.empty((ncall * Bc, k), dtype=torch.float32, device=dev)
-            di = torch.empty((ncall * Bc, k), dtype=torch.int32, device=dev)
-            dl = torch.empty((ncall * Bc, k), dtype=torch.float32, device=dev)
-            hs = [Hd[c * Bc:(c + 1) * Bc] for c in range(ncall)]
-            h_call = per_call_us(lambda c: ix.query_into(hs[c], k, ef, bi[c * Bc:(c + 1) * Bc],
-                                                         bl[c * Bc:(c + 1) * Bc]), ncall)
-            d_call = per_call_us(lambda c: vie.dense_topk_into(Wd, hs[c], k, di[c * Bc:(c + 1) * Bc],
-                                                               dl[c * Bc:(c + 1) * Bc], bdense.workspace), ncall)
-            b_sweep[str(Bc)] = {"hnsw_us_per_call": round(h_call, 2), "dense_us_per_call": round(d_call, 2),
-                                "hnsw_queries_per_s": round(Bc * 1e6 / h_call, 1),
-                                "dense_queries_per_s": round(Bc * 1e6 / d_call, 1),
-                                "dense_hbm_frac": round(wl.V * wl.d * s / (d_call * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-                                "recall_at_k": round(recall(bi.cpu().numpy(), di.cpu().numpy()), 4),
-                                "calls": ncall}
-        del bdense
-
-    # ---- roofline figures ----------------------------------------------------
-    n_dist, n_exp = stats[:, 0].astype(np.float64), stats[:, 1].astype(np.float64)
-    hnsw_bytes = n_dist * wl.d * s + n_exp * wl.M0 * 4 + wl.d * s + k * 8  # per launch (one query)
-    hnsw_gbs = float(hnsw_bytes.mean()) / (h_us * 1e-6) / 1e9
+    # ---- roofline figures --------------------------------------------------
+    M, M0 = info["M"], info["M0"]
+    nd, ne = head_st[:, 0].astype(np.float64), head_st[:, 1].astype(np.float64)
+    lc = np.array([layer_counts(head_tr[q], graph, M) for q in range(Q)], np.float64)
+    up_exp, l0_exp, nd_up = lc[:, 0], lc[:, 1], lc[:, 2]
+    assert np.array_equal(up_exp + l0_exp, ne), "expansion records disagree with the counters"
+    lists = up_exp * M * 4 + l0_exp * M0 * 4
+    width, int8 = TRAVERSALS[head_trav]
+    if int8:
+        nd_l0 = nd - nd_up
+        head_bytes = nd_up * wl.d * s + nd_l0 * (wl.d + 4) + np.minimum(max(ef, k), nd_l0) * wl.d * s + lists
+    else:
+        head_bytes = nd * wl.d * s + lists
+    head_bytes = head_bytes + wl.d * s + k * 8
+    head_gbs = float(head_bytes[:SQ].mean()) / (head_kernel_us * 1e-6) / 1e9
     dense_bytes = wl.V * wl.d * s + wl.d * s + k * 8
-    dense_gbs = dense_bytes / (d_us * 1e-6) / 1e9
-
+    dense_gbs = dense_bytes / (d_kernel_us * 1e-6) / 1e9
     traffic = measured_traffic(args.workload)
-    h_qps = Q * args.steps / (h_ms * 1e-3)
-    d_qps = Q * args.steps / (d_ms * 1e-3)
+    h_qps = SQ * args.steps / (h_ms * 1e-3)
+    d_qps = SQ * args.steps / (d_ms * 1e-3)
 
-    # ---- CPU baseline: the oracle on the host cores ----------------------
+    legs = {}
+    if not args.quick:
+        # ---- fp32 rows of the same shape (the paper's precision) ----------
+        if not args.no_fp32 and wl.dtype == synth.BF16:
+            W32 = synth.make_w(wl.V, wl.d, synth.F32, wl.seed_w, wl.hub_frac, seed_hub=wl.seed_hub)
+            H32, _ = synth.make_queries(W32, synth.F32, Q, wl.seed_q)
+            ix32, b32 = graph_for(W32, synth.F32, "f32")
+            W32d = vie.host_to_torch(W32, synth.F32).to(dev)
+            H32d = vie.host_to_torch(H32, synth.F32).to(dev)
+            ix32.to_device(W32d)
+            n32 = min(Q, 64)
+            e_i, e_l, _ = out_bufs(n32)
+            h32 = vie.DenseHead(W32d, max_batch=1, max_k=k)
+            dcalls = per_call(lambda c: vie.dense_topk_into(W32d, H32d[c:c + 1], k, e_i[c:c + 1], e_l[c:c + 1],
+                                                            h32.workspace), n32)
+            ex32 = e_i.cpu().numpy()
+            f_trav = head_trav
+            if TRAVERSALS[f_trav][1]:
+                q32, s32 = vie.quantize_rows(W32d, synth.F32)
+                ix32.attach_int8(q32, s32)
+            f_i, f_l, _ = out_bufs(n32)
+            fw, f8 = TRAVERSALS[f_trav]
+            hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None, fw,
+                                                        f8), n32)
+            legs["fp32_rows"] = {
+                "W_bytes": wl.V * wl.d * 4, "queries": n32, "dense_us_per_query": pct(dcalls),
+                "dense_hbm_frac": round(wl.V * wl.d * 4 / (np.median(dcalls) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                "hnsw": {"traversal": f_trav, "ef": ef, "us_per_query": pct(hcalls),
+                         "recall_at_k": round(recall(f_i.cpu().numpy(), ex32), 4)},
+                "graph_build_s": None if b32 is None else round(b32, 1)}
+            del ix32, W32d, H32d, h32
+            torch.cuda.empty_cache()
+
+        # ---- queries per call (HNSW: one workgroup per query) --------------
+        if len(wl.B) > 1:
+            bs = {}
+            for Bc in wl.B:
+                ncall = min(Q // Bc, 64)
+                bi, bl, _ = out_bufs(ncall * Bc)
+                hb = [Hd[c * Bc:(c + 1) * Bc] for c in range(ncall)]
+                w8, i8 = TRAVERSALS[head_trav]
+                h_call = back_to_back(lambda c: ix.query_into(hb[c], k, ef, bi[c * Bc:(c + 1) * Bc],
+                                                              bl[c * Bc:(c + 1) * Bc], None, w8, i8), ncall)
+                d_call = back_to_back(lambda c: vie.dense_topk_into(Wd, hb[c], k, bi[c * Bc:(c + 1) * Bc],
+                                                                    bl[c * Bc:(c + 1) * Bc], dense.workspace), ncall)
+                bs[str(Bc)] = {"hnsw_us_per_call": round(h_call, 2), "dense_us_per_call": round(d_call, 2),
+                               "hnsw_queries_per_s": round(Bc * 1e6 / h_call, 1),
+                               "dense_queries_per_s": round(Bc * 1e6 / d_call, 1),
+                               "dense_hbm_frac": round(wl.V * wl.d * s / (d_call * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                               "calls": ncall}
+            legs["queries_per_call"] = {"traversal": head_trav, "ef": ef, "B": bs}
+
+        # ---- all queries in one launch --------------------------------------
+        torch.cuda.synchronize()
+        a, b = events(2)
+        w8, i8 = TRAVERSALS[head_trav]
+        ix.query_into(Hd, k, ef, hi, hl, hs, w8, i8)
+        a.record(stream)
+        ix.query_into(Hd, k, ef, hi, hl, hs, w8, i8)
+        b.record(stream)
+        torch.cuda.synchronize()
+        one_launch_s = a.elapsed_time(b) * 1e-3
+        legs["one_launch"] = {"queries": Q, "queries_per_s": round(Q / one_launch_s, 1),
+                              "hbm_frac": round(float(head_bytes.sum()) / one_launch_s / 1e9 / HBM_PEAK_GBS, 4)}
+
+        # ---- batch graph built on the GPU, searched at B = 1 ----------------
+        if args.batch_graph_k:
+            Kb = min(args.batch_graph_k, wl.V - 1)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            bix = vie.Index.build_gpu(Wd, Kb, wl.M0)
+            torch.cuda.synchronize()
+            first_s = time.perf_counter() - t0
+            del bix
+            t0 = time.perf_counter()
+            bix = vie.Index.build_gpu(Wd, Kb, wl.M0)
+            torch.cuda.synchronize()
+            build_s = time.perf_counter() - t0
+            if qrows is not None:
+                bix.attach_int8(qrows, qscale)
+            bi, bl, _ = out_bufs(nc)
+            tried, bef = {}, None
+            for e in args.ef_ladder:
+                if e < k:
+                    continue
+                us = back_to_back(lambda c: search_into(bix, head_trav, e, c, bi[c:c + 1], bl[c:c + 1]), nc)
+                r = recall(bi.cpu().numpy(), exact_ids[:nc])
+                tried[str(e)] = {"us_per_query": round(us, 2), "recall_at_k": round(r, 4)}
+                if r >= args.target_recall:
+                    bef = e
+                    break
+            legs["batch_graph"] = {"K": Kb, "M0": wl.M0, "build_s": round(build_s, 4),
+                                   "first_build_s": round(first_s, 4), "traversal": head_trav, "ef": bef,
+                                   "tried": tried}
+            del bix
+
+        # ---- forced-inclusion tokens (stand-in: the first ids) --------------
+        if args.forced:
+            nf = min(Q, 128)
+            fids = torch.arange(args.forced, dtype=torch.int32, device=dev)
+            fi = torch.empty((nf, k + args.forced), dtype=torch.int32, device=dev)
+            fl = torch.empty((nf, k + args.forced), dtype=torch.float32, device=dev)
+            w8, i8 = TRAVERSALS[head_trav]
+            f_us = back_to_back(lambda c: ix.query_forced_into(hv[c], k, ef, fids, fi[c:c + 1], fl[c:c + 1], None, w8,
+                                                               i8), nf)
+            legs["forced"] = {"n": args.forced, "ids": "0..%d" % (args.forced - 1), "queries": nf,
+                              "us_per_query": round(f_us, 2), "search_only_us_per_query": round(head_kernel_us, 2)}
+
+    # ---- the oracle on the host cores: throughput and parity ---------------
     cpu = None
-    if not args.no_cpu_baseline:
-        from oracle import oracle as O
-        g, _ = O.load_graph(gpath)
-        O.check_graph(g)
-        done, t = 0, time.perf_counter()
-        while time.perf_counter() - t < args.cpu_seconds and done < Q:
-            O.hnsw_search(W, wl.dtype, g, H[done:done + 8], k, ef, validate=False)
-            done += min(8, Q - done)
-        cpu_s = time.perf_counter() - t
-        t = time.perf_counter()
-        O.topk(W, wl.dtype, H[:1], k)
-        bf_s = time.perf_counter() - t
-        cpu = {"value": round(done / cpu_s, 2), "unit": "queries/s", "cores": 1, "kind": "oracle",
-               "sample": "HNSW search (ef=%d, k=%d) of the first %d of the %d queries on the same graph, one "
-                         "thread; exact brute-force top-k of 1 query: %.2f s" % (ef, k, done, Q, bf_s),
-               "brute_force_queries_per_s": round(1.0 / bf_s, 3)}
+    if not args.no_cpu_baseline and not args.quick:
+        cpu = oracle_leg(args, wl, W, H, ix, graph, info, head_trav, ef, k, head_ids, head_lg, head_st, head_tr,
+                         cap, nthreads)
 
     out = {
         "metric": METRIC,
@@ -461,30 +514,29 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == synth.BF16 else "f32",
         "data": "synthetic, seeded: rows N(0, I/d) x LogNormal(0, 0.25) norms, h = sum of 3 rows + N(0, 0.1/d)",
-        "config": {"workload": wl.name, "V": wl.V, "d": wl.d, "B": 1, "k": k, "ef": ef, "M": wl.M, "M0": wl.M0,
-                   "ef_construction": wl.efC, "queries_per_step": Q, "accumulate": "fp32",
-                   "graph": {"maxlevel": info["maxlevel"], "entry": info["entry"]}},
-        "hnsw": {"us_per_query": round(h_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(h_qps, 1),
-                 "kernel_us": round(h_us, 2), "recall_at_k": round(recall(hnsw_ids, exact_ids), 4),
-                 "recall_at_2": round(recall(hnsw_ids, exact_ids, 2), 4),
-                 "mean_n_dist": float(n_dist.mean()), "mean_n_expand": float(n_exp.mean()),
-                 "row_bytes_per_query": float((n_dist * wl.d * s).mean()),
-                 "batched_queries_per_s": round(batched_qps, 1), "wall_s": round(h_wall, 3), "ef_sweep": sweep,
-                 "width_sweep": w_sweep or None, "k_sweep": k_sweep or None, "batch_sweep": b_sweep or None,
-                 "int8_sweep": q_sweep or None, "forced": forced, "batch_graph": batch,
-                 "recall_target": ({"recall_at_k": args.target_recall, "queries": tq,
-                                    "dense_us_per_query": round(d_us, 2), **target} if target else None)},
-        "dense": {"us_per_query": round(d_ms * 1e3 / (Q * args.steps), 2), "queries_per_s": round(d_qps, 1),
-                  "kernel_us": round(d_us, 2), "wall_s": round(d_wall, 3)},
-        "roofline": {"kernel": "hnsw_kernel", "bound": "hbm", "achieved": round(hnsw_gbs, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(hnsw_gbs / HBM_PEAK_GBS, 5),
-                     "traffic": traffic.get("hnsw_kernel")},
-        "roofline_batched": {"kernel": "hnsw_kernel, all %d queries in one launch" % Q, "bound": "hbm",
-                             "achieved": round(batched_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                             "frac": round(batched_gbs / HBM_PEAK_GBS, 4), "traffic": None},
-        "roofline_dense": {"kernel": "dense_stream_kernel+dense_merge_kernel", "bound": "hbm", "achieved": round(dense_gbs, 1),
-                           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dense_gbs / HBM_PEAK_GBS, 4),
-                           "traffic": traffic.get("dense_head")},
+        "config": {"workload": wl.name, "V": wl.V, "d": wl.d, "B": 1, "k": k, "traversal": head_trav, "ef": ef,
+                   "M": M, "M0": M0, "ef_construction": wl.efC, "queries": Q, "queries_per_step": SQ,
+                   "recall_target": args.target_recall, "accumulate": "fp32",
+                   "graph": {"maxlevel": info["maxlevel"], "entry": info["entry"],
+                             "build_s_16_threads": None if cpu_build_s is None else round(cpu_build_s, 1)}},
+        "hnsw": {"traversal": head_trav, "ef": ef, "kernel": KERNEL_OF[head_trav],
+                 "us_per_query": round(h_ms * 1e3 / (SQ * args.steps), 2), "queries_per_s": round(h_qps, 1),
+                 "per_call_us": pct(head_calls), "kernel_us": round(head_kernel_us, 2),
+                 "recall_at_k": round(recall(head_ids, exact_ids), 4),
+                 "recall_at_2": round(recall(head_ids, exact_ids, 2), 4),
+                 "mean_n_dist": float(nd.mean()), "mean_n_expand": float(ne.mean()),
+                 "mean_upper_n_dist": float(nd_up.mean()), "bytes_per_query": float(head_bytes.mean()),
+                 "wall_s": round(h_wall, 3), "sequential": seq, "ef_for_recall_target": calib},
+        "dense": {"us_per_query": round(d_ms * 1e3 / (SQ * args.steps), 2), "queries_per_s": round(d_qps, 1),
+                  "per_call_us": pct(dense_calls), "kernel_us": round(d_kernel_us, 2), "W_copies": 2,
+                  "wall_s": round(d_wall, 3)},
+        "legs": legs,
+        "roofline": {"kernel": KERNEL_OF[head_trav], "bound": "hbm", "achieved": round(head_gbs, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(head_gbs / HBM_PEAK_GBS, 5),
+                     "traffic": traffic.get(head_trav)},
+        "roofline_dense": {"kernel": "dense_stream_kernel+dense_merge_kernel", "bound": "hbm",
+                           "achieved": round(dense_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(dense_gbs / HBM_PEAK_GBS, 4), "traffic": traffic.get("dense_head")},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -495,6 +547,73 @@ def main() -> int:
         dst.copy_(src)
         torch.cuda.synchronize()
     return 0
+
+
+def oracle_leg(args, wl, W, H, ix, graph, info, trav, ef, k, gids, glg, gst, gtr, cap, nthreads):
+    """The plain-C oracle (test infrastructure) on the host cores: the same
+    traversal on the same graph for as many of the same queries as fit in the
+    budget, with T threads over chunks of queries (ctypes releases the GIL),
+    plus a few queries on one thread; its ids, counts and expansion records
+    are compared with the GPU's for every query it ran."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from oracle import oracle as O
+    import parity
+
+    g = O.Graph(wl.V, wl.d, wl.dtype, info["M"], info["M0"], wl.efC, wl.seed_levels, info["maxlevel"],
+                info["entry"], graph["levels"], graph["adj0"], graph["upper_off"], graph["upper"])
+    width, int8 = TRAVERSALS[trav]
+    oq = osc = None
+    if int8:
+        oq, osc = O.quantize_rows(W, wl.dtype)
+
+    def run(a, b):
+        if int8:
+            return O.hnsw_search_q(W, wl.dtype, g, oq, osc, H[a:b], k, ef, width, validate=False, trace_cap=cap)
+        if width > 1:
+            return O.hnsw_search_multi(W, wl.dtype, g, H[a:b], k, ef, width, validate=False, trace_cap=cap)
+        r = O.hnsw_search(W, wl.dtype, g, H[a:b], k, ef, validate=False, trace_cap=cap)
+        return r[0], r[1], r[2], r[4]
+
+    T = args.cpu_threads or nthreads
+    t1 = time.perf_counter()
+    one = [run(q, q + 1) for q in range(2)]
+    single_us = (time.perf_counter() - t1) * 1e6 / 2
+    results = {}
+    t = time.perf_counter()
+    nxt = 2
+    with cf.ThreadPoolExecutor(T) as ex:
+        while time.perf_counter() - t < args.cpu_seconds and nxt < len(H):
+            chunk = list(range(nxt, min(len(H), nxt + T)))
+            for q, r in zip(chunk, ex.map(lambda q: run(q, q + 1), chunk)):
+                results[q] = r
+            nxt = chunk[-1] + 1
+    wall = time.perf_counter() - t
+    for q in range(2):
+        results[q] = one[q]
+    done = sorted(results)
+    same = near = 0
+    worst_gap, unexplained = 0.0, []
+    ex_sc = {}
+    for q in done:
+        oid, olg, ost, otr = (x[0] for x in results[q])
+        if np.array_equal(gst[q], ost.astype(np.int64)) and np.array_equal(gtr[q], otr):
+            same += 1
+            continue
+        try:
+            r = parity.first_divergence(W, wl.dtype, g, H[q], gtr[q], otr, max(ef, k), int8=int8)
+            near += 1
+            worst_gap = max(worst_gap, r[4] if r else 0.0)
+        except AssertionError as e:
+            unexplained.append((q, str(e)[:160]))
+    ids_equal = sum(int(set(gids[q].tolist()) == set(results[q][0][0].tolist())) for q in done)
+    return {"value": round((len(done) - 2) / wall, 2), "unit": "queries/s", "cores": T, "kind": "oracle",
+            "sample": "%s search (ef=%d, k=%d) of %d of the %d queries on the same graph: %d on %d threads in "
+                      "%.1f s, 2 on one thread" % (trav, ef, k, len(done), len(H), len(done) - 2, T, wall),
+            "single_thread_us_per_query": round(single_us, 1), "cpu_model": cpu_model(),
+            "nproc": os.cpu_count(),
+            "parity": {"queries": len(done), "same_expansions_and_counts": same, "near_tie_divergences": near,
+                       "worst_near_tie_gap": worst_gap, "unexplained": unexplained[:4],
+                       "same_id_sets": ids_equal}}
 
 
 if __name__ == "__main__":

@@ -192,6 +192,18 @@ typedef struct {
     int32_t int8_rows;    /* 1: layer-0 scores from the int8 rows attached with
                              vie_index_attach_int8, final beam re-ranked on
                              the stored rows; 0: stored rows throughout */
+    int32_t *trace_dev;   /* NULL, or a device buffer int32[B][trace_cap]
+                             (caller owned) that receives each query's
+                             expansions in order: entry t is
+                             (layer << 27) | (s << 26) | node for
+                             t < min(expanded nodes, trace_cap), s = 1 for
+                             the first node of a step (every node of a
+                             one-expansion step); the nodes one layer-0 step
+                             expands together appear best first; entries
+                             past the last expansion are not written.
+                             Needs V < 2^26.  A diagnostic: it lets a
+                             caller replay and compare a traversal. */
+    int32_t trace_cap;    /* entries per query of trace_dev (>= 1 when set) */
 } vie_search_params;
 
 /* vie_query with a layer-0 step that expands the expand_width best

@@ -309,7 +309,21 @@ typedef struct {
     const float *qscale;
     const int8_t *qh;
     float sh;
+    /* optional record of the expansions of one query, in order: entry t is
+     * (layer << 27) | (s << 26) | node for t < trace_cap, s = 1 for the first
+     * node a step expands */
+    int32_t *trace;
+    int trace_cap;
 } searcher;
+
+/* Counts an expansion of node id on layer lc and records it (first: the
+ * first node of its step). */
+static void note_expand(searcher *s, int lc, int32_t id, int first)
+{
+    if (s->trace && s->n_expand < (uint64_t)s->trace_cap)
+        s->trace[s->n_expand] = (int32_t)(((uint32_t)lc << 27) | ((uint32_t)(first != 0) << 26) | (uint32_t)id);
+    s->n_expand++;
+}
 
 static double qdist(searcher *s, const double *q, int32_t id)
 {
@@ -360,7 +374,7 @@ static int search_layer(searcher *s, const ograph *g, const double *q, const can
         for (int i = 1; i < nR; ++i)
             if (nearer(s->R[fi], s->R[i])) fi = i;
         if (nearer(s->R[fi], c)) break; /* all elements of W are evaluated */
-        s->n_expand++;
+        note_expand(s, lc, c.id, 1);
         int32_t *lst = olist(g, c.id, lc);
         for (int j = 0; j < lst[0]; ++j) {
             int32_t e = lst[1 + j];
@@ -427,7 +441,7 @@ static void *build_with_levels(const void *W, int dtype, int64_t V, int d, int M
     ograph *g = ograph_alloc(V, M, M0, lv);
     obuilt *ob = calloc(1, sizeof *ob);
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0,
-                   malloc(sizeof(cand) * (size_t)V), malloc(sizeof(cand) * (size_t)(efC + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
+                   malloc(sizeof(cand) * (size_t)V), malloc(sizeof(cand) * (size_t)(efC + 2)), 0, 0, NULL, NULL, NULL, 0.0f, NULL, 0 };
     int capmax = efC + M0 + M + 4; /* search result, or a selection plus an over-full list */
     cand *Wc = malloc(sizeof(cand) * (size_t)capmax);
     cand *ep = malloc(sizeof(cand) * (size_t)capmax);
@@ -675,19 +689,21 @@ int oracle_graph_check(int64_t V, int M, int M0, int maxlevel, int32_t entry, co
 int oracle_hnsw_search(const void *W, int dtype, int64_t V, int d, int M, int M0, int maxlevel,
                        int32_t entry, const uint8_t *levels, const int32_t *adj0, const int32_t *upper_off,
                        const int32_t *upper, const void *h, int B, int k, int ef, int32_t *ids,
-                       float *logits, uint32_t *stats, int32_t *l0_entry)
+                       float *logits, uint32_t *stats, int32_t *l0_entry, int32_t *trace, int trace_cap)
 {
     if (V < 1 || d < 1 || B < 1 || k < 1 || k > V || ef < 1 || entry < 0 || entry >= V) return -1;
     ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
     int efe = ef > k ? ef : k; /* ef < k is read as ef = k */
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
-                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, NULL, NULL, NULL, 0.0f, NULL, 0 };
     cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
     double *q = malloc(sizeof(double) * (size_t)d);
     int rc = 0;
     if (!g || !s.seen || !s.C || !s.R || !out || !q) { rc = -1; goto done; }
     for (int b = 0; b < B; ++b) {
         s.n_dist = s.n_expand = 0;
+        s.trace = trace ? trace + (int64_t)b * trace_cap : NULL;
+        s.trace_cap = trace_cap;
         widen(h, dtype, d, b, q);
         cand ep = { qdist(&s, q, entry), entry };
         for (int lc = maxlevel; lc >= 1; --lc) {
@@ -770,7 +786,7 @@ static int beam_multi(searcher *s, const ograph *g, const double *q, cand ep, in
         int n = nR;
         for (int t = 0; t < np; ++t) {
             R[pick[t]].expanded = 1;
-            s->n_expand++;
+            note_expand(s, 0, R[pick[t]].c.id, t == 0);
             const int32_t *lst = olist(g, R[pick[t]].c.id, 0);
             for (int j = 0; j < lst[0]; ++j) {
                 const int32_t e = lst[1 + j];
@@ -797,20 +813,22 @@ static int beam_multi(searcher *s, const ograph *g, const double *q, cand ep, in
 int oracle_hnsw_search_multi(const void *W, int dtype, int64_t V, int d, int M, int M0, int maxlevel,
                              int32_t entry, const uint8_t *levels, const int32_t *adj0, const int32_t *upper_off,
                              const int32_t *upper, const void *h, int B, int k, int ef, int expand_width,
-                             int32_t *ids, float *logits, uint32_t *stats)
+                             int32_t *ids, float *logits, uint32_t *stats, int32_t *trace, int trace_cap)
 {
     if (V < 1 || d < 1 || B < 1 || k < 1 || k > V || ef < 1 || entry < 0 || entry >= V || expand_width < 1)
         return -1;
     ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
     int efe = ef > k ? ef : k;
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
-                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, NULL, NULL, NULL, 0.0f };
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, NULL, NULL, NULL, 0.0f, NULL, 0 };
     cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
     double *q = malloc(sizeof(double) * (size_t)d);
     int rc = 0;
     if (!g || !s.seen || !s.C || !s.R || !out || !q) { rc = -1; goto done; }
     for (int b = 0; b < B; ++b) {
         s.n_dist = s.n_expand = 0;
+        s.trace = trace ? trace + (int64_t)b * trace_cap : NULL;
+        s.trace_cap = trace_cap;
         widen(h, dtype, d, b, q);
         cand ep = { qdist(&s, q, entry), entry };
         for (int lc = maxlevel; lc >= 1; --lc) {
@@ -989,14 +1007,15 @@ void oracle_quantize_rows(const void *W, int dtype, int64_t V, int d, int8_t *q,
 int oracle_hnsw_search_q(const void *W, int dtype, int64_t V, int d, int M, int M0, int maxlevel, int32_t entry,
                          const uint8_t *levels, const int32_t *adj0, const int32_t *upper_off, const int32_t *upper,
                          const int8_t *qw, const float *qscale, const void *h, int B, int k, int ef,
-                         int expand_width, int32_t *ids, float *logits, uint32_t *stats)
+                         int expand_width, int32_t *ids, float *logits, uint32_t *stats, int32_t *trace,
+                         int trace_cap)
 {
     if (V < 1 || d < 1 || B < 1 || k < 1 || k > V || ef < 1 || entry < 0 || entry >= V || expand_width < 1)
         return -1;
     ograph *g = from_flat(V, M, M0, maxlevel, entry, levels, adj0, upper_off, upper);
     int efe = ef > k ? ef : k;
     searcher s = { W, dtype, d, V, calloc((size_t)V, sizeof(uint32_t)), 0, malloc(sizeof(cand) * (size_t)V),
-                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, qw, qscale, NULL, 0.0f };
+                   malloc(sizeof(cand) * (size_t)(efe + 2)), 0, 0, qw, qscale, NULL, 0.0f, NULL, 0 };
     cand *out = malloc(sizeof(cand) * (size_t)(efe + 2));
     scored *ex = malloc(sizeof(scored) * (size_t)(efe + 2));
     double *q = malloc(sizeof(double) * (size_t)d);
@@ -1006,6 +1025,8 @@ int oracle_hnsw_search_q(const void *W, int dtype, int64_t V, int d, int M, int 
     s.qh = qh;
     for (int b = 0; b < B; ++b) {
         s.n_dist = s.n_expand = 0;
+        s.trace = trace ? trace + (int64_t)b * trace_cap : NULL;
+        s.trace_cap = trace_cap;
         widen(h, dtype, d, b, q);
         s.sh = quantize_vec(h, dtype, d, b, qh);
         cand ep = { qdist(&s, q, entry), entry };

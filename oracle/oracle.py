@@ -45,10 +45,10 @@ def lib() -> C.CDLL:
         L.oracle_graph_check.argtypes = [i64, i32, i32, i32, i32, vp, vp, vp, vp, i64, C.c_char_p, i32]
         L.oracle_graph_check.restype = i32
         L.oracle_hnsw_search.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
-                                         i32, i32, i32, vp, vp, vp, vp]
+                                         i32, i32, i32, vp, vp, vp, vp, vp, i32]
         L.oracle_hnsw_search.restype = i32
         L.oracle_hnsw_search_multi.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp,
-                                               i32, i32, i32, i32, vp, vp, vp]
+                                               i32, i32, i32, i32, vp, vp, vp, vp, i32]
         L.oracle_hnsw_search_multi.restype = i32
         L.oracle_forced_merge.argtypes = [vp, i32, i64, i32, vp, i32, i32, vp, i32, vp, vp, vp]
         L.oracle_forced_merge.restype = i32
@@ -56,7 +56,7 @@ def lib() -> C.CDLL:
         L.oracle_knn_graph.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp, vp]
         L.oracle_knn_graph.restype = i32
         L.oracle_hnsw_search_q.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
-                                           i32, i32, i32, i32, vp, vp, vp]
+                                           i32, i32, i32, i32, vp, vp, vp, vp, i32]
         L.oracle_hnsw_search_q.restype = i32
         L.oracle_w_fingerprint.argtypes = [vp, i32, i64, i32]
         L.oracle_w_fingerprint.restype = u64
@@ -228,10 +228,17 @@ def check_graph(g: Graph) -> str:
     return "" if rc == 0 else (msg.value.decode() or "invalid")
 
 
+def _trace_buf(B: int, cap: int):
+    return (np.full((B, cap), -1, np.int32), cap) if cap > 0 else (None, 0)
+
+
 def hnsw_search(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int, ef: int,
-                validate: bool = True):
+                validate: bool = True, trace_cap: int = 0):
     """K-NN-SEARCH (MY18 Alg. 5 over Alg. 2): ids [B,k], logits [B,k],
-    stats [B,2] = (n_dist, n_expand), layer-0 start node [B]."""
+    stats [B,2] = (n_dist, n_expand), layer-0 start node [B]; with trace_cap
+    > 0 also the expansions of each query in order, [B, trace_cap] int32 of
+    (layer << 27) | (s << 26) | node (s = 1: first node of its step), -1
+    past the last."""
     W = _check_w(W, dtype)
     h = _check_h(h, dtype, W.shape[1])
     if validate:
@@ -243,20 +250,23 @@ def hnsw_search(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int, ef: 
     lg = np.empty((B, k), np.float32)
     st = np.empty((B, 2), np.uint32)
     l0 = np.empty(B, np.int32)
+    tr, cap = _trace_buf(B, trace_cap)
     up = np.ascontiguousarray(g.upper, np.int32)
     rc = lib().oracle_hnsw_search(_p(W), dtype, W.shape[0], W.shape[1], g.M, g.M0, g.maxlevel, g.entry,
                                   _p(np.ascontiguousarray(g.levels)), _p(np.ascontiguousarray(g.adj0)),
                                   _p(np.ascontiguousarray(g.upper_off)), _p(up) if up.size else None,
-                                  _p(h), B, k, ef, _p(ids), _p(lg), _p(st), _p(l0))
+                                  _p(h), B, k, ef, _p(ids), _p(lg), _p(st), _p(l0),
+                                  _p(tr) if cap else None, cap)
     if rc != 0:
         raise ValueError("oracle_hnsw_search: bad arguments")
-    return ids, lg, st, l0
+    return (ids, lg, st, l0, tr) if cap else (ids, lg, st, l0)
 
 
 def hnsw_search_multi(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int, ef: int,
-                      expand_width: int, validate: bool = True):
+                      expand_width: int, validate: bool = True, trace_cap: int = 0):
     """K-NN-SEARCH whose layer-0 step expands the expand_width best
-    unexpanded beam entries at once: ids [B,k], logits [B,k], stats [B,2]."""
+    unexpanded beam entries at once: ids [B,k], logits [B,k], stats [B,2]
+    (and the expansions, as hnsw_search, with trace_cap > 0)."""
     W = _check_w(W, dtype)
     h = _check_h(h, dtype, W.shape[1])
     if validate:
@@ -267,14 +277,16 @@ def hnsw_search_multi(W: np.ndarray, dtype: int, g: Graph, h: np.ndarray, k: int
     ids = np.empty((B, k), np.int32)
     lg = np.empty((B, k), np.float32)
     st = np.empty((B, 2), np.uint32)
+    tr, cap = _trace_buf(B, trace_cap)
     up = np.ascontiguousarray(g.upper, np.int32)
     rc = lib().oracle_hnsw_search_multi(_p(W), dtype, W.shape[0], W.shape[1], g.M, g.M0, g.maxlevel, g.entry,
                                         _p(np.ascontiguousarray(g.levels)), _p(np.ascontiguousarray(g.adj0)),
                                         _p(np.ascontiguousarray(g.upper_off)), _p(up) if up.size else None,
-                                        _p(h), B, k, ef, expand_width, _p(ids), _p(lg), _p(st))
+                                        _p(h), B, k, ef, expand_width, _p(ids), _p(lg), _p(st),
+                                        _p(tr) if cap else None, cap)
     if rc != 0:
         raise ValueError("oracle_hnsw_search_multi: bad arguments")
-    return ids, lg, st
+    return (ids, lg, st, tr) if cap else (ids, lg, st)
 
 
 def forced_merge(W: np.ndarray, dtype: int, h: np.ndarray, ids_in: np.ndarray, forced: np.ndarray):
@@ -306,7 +318,7 @@ def quantize_rows(W: np.ndarray, dtype: int):
 
 
 def hnsw_search_q(W: np.ndarray, dtype: int, g: Graph, qw: np.ndarray, qscale: np.ndarray, h: np.ndarray, k: int,
-                  ef: int, expand_width: int = 1, validate: bool = True):
+                  ef: int, expand_width: int = 1, validate: bool = True, trace_cap: int = 0):
     """K-NN-SEARCH with int8 layer-0 distances and an exact re-rank of the
     final beam: ids [B,k], logits [B,k], stats [B,2]."""
     W = _check_w(W, dtype)
@@ -321,14 +333,16 @@ def hnsw_search_q(W: np.ndarray, dtype: int, g: Graph, qw: np.ndarray, qscale: n
     ids = np.empty((B, k), np.int32)
     lg = np.empty((B, k), np.float32)
     st = np.empty((B, 2), np.uint32)
+    tr, cap = _trace_buf(B, trace_cap)
     up = np.ascontiguousarray(g.upper, np.int32)
     rc = lib().oracle_hnsw_search_q(_p(W), dtype, W.shape[0], W.shape[1], g.M, g.M0, g.maxlevel, g.entry,
                                     _p(np.ascontiguousarray(g.levels)), _p(np.ascontiguousarray(g.adj0)),
                                     _p(np.ascontiguousarray(g.upper_off)), _p(up) if up.size else None, _p(qw),
-                                    _p(qscale), _p(h), B, k, ef, expand_width, _p(ids), _p(lg), _p(st))
+                                    _p(qscale), _p(h), B, k, ef, expand_width, _p(ids), _p(lg), _p(st),
+                                    _p(tr) if cap else None, cap)
     if rc != 0:
         raise ValueError("oracle_hnsw_search_q: bad arguments")
-    return ids, lg, st
+    return (ids, lg, st, tr) if cap else (ids, lg, st)
 
 
 def knn_graph(W: np.ndarray, dtype: int, K: int, M0: int, seed: int = 0, with_forward: bool = False):

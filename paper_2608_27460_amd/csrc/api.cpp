@@ -255,9 +255,9 @@ void vie_index_free(vie_index *ix)
 }
 
 namespace {
-vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
-                      bool int8_rows, const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev,
-                      float *logits_dev, uint32_t *stats_dev, void *hip_stream);
+vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                      const vie_search_params *params, const int32_t *forced_dev, int32_t n_forced,
+                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream);
 
 vie_status check_params(const vie_search_params *params)
 {
@@ -266,6 +266,8 @@ vie_status check_params(const vie_search_params *params)
         return fail(VIE_EINVAL, "expand_width = %d outside 1..8", params->expand_width);
     if (params->int8_rows != 0 && params->int8_rows != 1)
         return fail(VIE_EINVAL, "int8_rows = %d is neither 0 nor 1", params->int8_rows);
+    if (params->trace_dev && params->trace_cap < 1)
+        return fail(VIE_EINVAL, "trace_cap = %d < 1 with a trace buffer", params->trace_cap);
     return VIE_OK;
 }
 }  // namespace
@@ -297,7 +299,7 @@ vie_status vie_query(const vie_index *ix, const void *h_dev, int32_t B, int32_t 
                      float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     g_last_error.clear();
-    return query_impl(ix, h_dev, B, k, ef, 1, false, nullptr, 0, ids_dev, logits_dev, stats_dev, hip_stream);
+    return query_impl(ix, h_dev, B, k, ef, nullptr, nullptr, 0, ids_dev, logits_dev, stats_dev, hip_stream);
 }
 
 vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
@@ -307,8 +309,7 @@ vie_status vie_query_ex(const vie_index *ix, const void *h_dev, int32_t B, int32
     g_last_error.clear();
     if (!params) return fail(VIE_EINVAL, "NULL argument");
     if (vie_status r = check_params(params)) return r;
-    return query_impl(ix, h_dev, B, k, ef, params->expand_width, params->int8_rows != 0, nullptr, 0, ids_dev,
-                      logits_dev, stats_dev, hip_stream);
+    return query_impl(ix, h_dev, B, k, ef, params, nullptr, 0, ids_dev, logits_dev, stats_dev, hip_stream);
 }
 
 vie_status vie_query_forced(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
@@ -317,22 +318,25 @@ vie_status vie_query_forced(const vie_index *ix, const void *h_dev, int32_t B, i
 {
     g_last_error.clear();
     if (vie_status r = check_params(params)) return r;
-    const int width = params ? params->expand_width : 1;
-    const bool int8_rows = params && params->int8_rows != 0;
     if (n_forced < 0 || n_forced > kMaxForced)
         return fail(VIE_EINVAL, "n_forced = %d outside 0..%d", n_forced, kMaxForced);
     if (n_forced > 0 && !forced_dev) return fail(VIE_EINVAL, "NULL argument");
-    return query_impl(ix, h_dev, B, k, ef, width, int8_rows, forced_dev, n_forced, ids_dev, logits_dev, stats_dev,
-                      hip_stream);
+    return query_impl(ix, h_dev, B, k, ef, params, forced_dev, n_forced, ids_dev, logits_dev, stats_dev, hip_stream);
 }
 
 namespace {
-vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef, int32_t width,
-                      bool int8_rows, const int32_t *forced_dev, int32_t n_forced, int32_t *ids_dev,
-                      float *logits_dev, uint32_t *stats_dev, void *hip_stream)
+// params NULL: one expansion per step on the stored rows, no trace.
+vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t k, int32_t ef,
+                      const vie_search_params *params, const int32_t *forced_dev, int32_t n_forced,
+                      int32_t *ids_dev, float *logits_dev, uint32_t *stats_dev, void *hip_stream)
 {
     if (!ix || !h_dev || !ids_dev || !logits_dev) return fail(VIE_EINVAL, "NULL argument");
     const Graph &g = ix->g;
+    const int width = params ? params->expand_width : 1;
+    const bool int8_rows = params && params->int8_rows != 0;
+    int32_t *trace = params ? params->trace_dev : nullptr;
+    if (trace && g.V >= (int64_t(1) << 26))
+        return fail(VIE_EUNSUPPORTED, "an expansion trace needs V < 2^26 (V = %lld)", (long long)g.V);
     if (vie_status s = check_k(k, g.V, B)) return s;
     if (ef < 1) return fail(VIE_EINVAL, "ef = %d < 1", ef);
     const int ef_eff = ef > k ? ef : k;
@@ -364,6 +368,8 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
     a.stats = stats_dev;
     a.width = width;
     a.ldo = k + n_forced;
+    a.trace = trace;
+    a.trace_cap = trace ? params->trace_cap : 0;
     if (int8_rows) {
         if (!ix->dev.q8) return fail(VIE_ESTATE, "no int8 rows attached (call vie_index_attach_int8)");
         a.q8 = ix->dev.q8;

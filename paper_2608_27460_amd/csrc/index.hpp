@@ -88,6 +88,8 @@ struct HnswLaunch {
     int32_t *ids;
     float *logits;
     uint32_t *stats;
+    int32_t *trace = nullptr;  // [B][trace_cap] expansion record (nullptr: none)
+    int trace_cap = 0;
 };
 // Launchers return VIE_OK, VIE_EUNSUPPORTED for a shape they cannot serve, or
 // VIE_EHIP for a failed launch; the detail goes to set_error().

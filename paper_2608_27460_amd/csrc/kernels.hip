@@ -1257,11 +1257,20 @@ __device__ __forceinline__ float row_dot(const char *__restrict__ W, int64_t row
 // Scores the entry point, then SEARCH-LAYER with a result set of one
 // (greedy) through layers maxlevel..1; returns the key of the layer-0 entry
 // point.  cid holds at least M ids; counts go to n_dist / n_expand.
+// Records expansion number n (node id on layer lc; first: the first node
+// its step expands) in the query's trace row.
+__device__ __forceinline__ void note_expand(int32_t *trace, int cap, uint32_t n, int lc, int32_t id, bool first)
+{
+    if (trace && n < (uint32_t)cap)
+        trace[n] = (int32_t)(((uint32_t)lc << 27) | ((uint32_t)first << 26) | (uint32_t)id);
+}
+
 template <int NT, int VEC, bool BF16, int G>
 __device__ uint64_t descend_upper(const char *__restrict__ W, int64_t V, int row_bytes,
                                   const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M,
                                   int maxlevel, int32_t entry, const char *hs, int32_t *cid, uint32_t *vis,
-                                  HnswShared &sh, uint32_t &n_dist, uint32_t &n_expand)
+                                  HnswShared &sh, uint32_t &n_dist, uint32_t &n_expand, int32_t *trace,
+                                  int trace_cap)
 {
     constexpr int kGroups = NT / G;
     const int tid = threadIdx.x, gl = tid % G, grp = tid / G;
@@ -1279,7 +1288,10 @@ __device__ uint64_t descend_upper(const char *__restrict__ W, int64_t V, int row
         if (tid == 0) vis[key_id(cur) >> 5] |= 1u << (key_id(cur) & 31);
         for (;;) {
             const int32_t c = key_id(cur);
-            if (tid == 0) sh.nnew = 0;
+            if (tid == 0) {
+                sh.nnew = 0;
+                note_expand(trace, trace_cap, n_expand, lc, c, true);
+            }
             __syncthreads();
             ++n_expand;
             const int32_t *lst = upper + ((int64_t)upper_off[c] + lc - 1) * M;
@@ -1312,13 +1324,14 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
     const char *__restrict__ hq, int k, int ef, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
-    uint32_t *__restrict__ stats)
+    uint32_t *__restrict__ stats, int32_t *__restrict__ trace_all, int trace_cap)
 {
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
     constexpr int kGroups = NT / G;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int q = blockIdx.x;
+    int32_t *trace = trace_all ? trace_all + (int64_t)q * trace_cap : nullptr;
     const int hbytes = (row_bytes + 15) & ~15;
     const int vwords = (int)((V + 31) / 32);
     const int maxdeg = M0 > M ? M0 : M;
@@ -1355,7 +1368,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     uint32_t n_dist = 0, n_expand = 0;
 
     uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
-                                                   vis, sh, n_dist, n_expand);
+                                                   vis, sh, n_dist, n_expand, trace, trace_cap);
 
     // layer 0: beam of ef keys, sorted descending, with expanded flags,
     // double buffered (beam/flag -> beam2/flag2 -> beam/flag ...).  Two
@@ -1372,6 +1385,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
     __syncthreads();
     if (tid == 0) {
         vis[key_id(cur) >> 5] |= 1u << (key_id(cur) & 31);
+        note_expand(trace, trace_cap, n_expand, 0, key_id(cur), true);
         beam[0] = cur;
         flag[0] = 1;  // expanded at step 0
         sh.nbeam = 1;
@@ -1527,6 +1541,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
             }
         }
         if (tid == 0) {
+            if (next != 0ull) note_expand(trace, trace_cap, n_expand, 0, key_id(next), true);  // step + 1
             sh.nbeam = (uint32_t)total;
             sh.nnewp[par] = 0;     // read at the top of this step only
             sh.nkeepp[par ^ 1] = 0;  // last used in the previous step
@@ -1678,7 +1693,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
     const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
-    uint32_t *__restrict__ stats, const int8_t *__restrict__ q8, const float *__restrict__ q8scale)
+    uint32_t *__restrict__ stats, const int8_t *__restrict__ q8, const float *__restrict__ q8scale,
+    int32_t *__restrict__ trace_all, int trace_cap)
 {
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
@@ -1743,8 +1759,9 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int gl = tid % G;
     const int grp = tid / G;
     uint32_t n_dist = 0, n_expand = 0;
+    int32_t *trace = trace_all ? trace_all + (int64_t)q * trace_cap : nullptr;
     uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
-                                                   vis, sh, n_dist, n_expand);
+                                                   vis, sh, n_dist, n_expand, trace, trace_cap);
 
     if constexpr (Q8) {  // the layer-0 entry point scored again on its int8 row
         if (grp == 0) {
@@ -1825,7 +1842,14 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             }
         }
         if (np == 0) break;
-        if (tid == 0) sh.nkeep = 0;  // last read before the previous merge
+        if (tid == 0) {
+            sh.nkeep = 0;  // last read before the previous merge
+            if (trace) {
+#pragma unroll
+                for (int t = 0; t < kMaxWidth; ++t)
+                    if (t < np) note_expand(trace, trace_cap, n_expand + t, 0, key_id(beam[pick[t]]), t == 0);
+            }
+        }
         n_expand += np;
         // claim the unseen neighbours of the picks (node t / M0, slot t % M0)
         for (int t = tid; t < np * M0; t += NT) {
@@ -2382,7 +2406,8 @@ hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
         }
         kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
                                    a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h),
-                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.ldo, a.stats, a.q8, a.q8scale);
+                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.ldo, a.stats, a.q8, a.q8scale,
+                                   a.trace, a.trace_cap);
         return hipGetLastError();
     }
     auto kern = hnsw_kernel<NT, VEC, BF16, G>;
@@ -2392,7 +2417,7 @@ hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
     }
     kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
                                a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h), a.k,
-                               a.ef_eff, a.ids, a.logits, a.ldo, a.stats);
+                               a.ef_eff, a.ids, a.logits, a.ldo, a.stats, a.trace, a.trace_cap);
     return hipGetLastError();
 }
 

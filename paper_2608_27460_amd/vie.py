@@ -26,7 +26,8 @@ class VieError(RuntimeError):
 
 
 class SearchParams(C.Structure):
-    _fields_ = [("expand_width", C.c_int32), ("int8_rows", C.c_int32)]
+    _fields_ = [("expand_width", C.c_int32), ("int8_rows", C.c_int32), ("trace_dev", C.c_void_p),
+                ("trace_cap", C.c_int32)]
 
 
 class BuildParams(C.Structure):
@@ -202,18 +203,21 @@ class Index:
         _check(lib.vie_index_attach_int8(self._h, _dev_ptr(q, "q"), _dev_ptr(scale, "scale")))
         self._q8 = (q, scale)
 
-    def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1, int8: bool = False) -> None:
+    def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1, int8: bool = False,
+                   trace=None) -> None:
         """HNSW top-k of h [B, d] into preallocated ids int32 [B, k], logits fp32 [B, k]
         (and stats uint32-as-int32 [B, 2]) on the current stream; width > 1
         expands that many beam entries per layer-0 step, int8 walks layer 0 on
-        the attached int8 rows (vie_query_ex)."""
+        the attached int8 rows, trace (int32 [B, cap]) receives each query's
+        expansions as (layer << 27) | node (vie_query_ex)."""
         B = h.shape[0]
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        if width == 1 and not int8:
+        if width == 1 and not int8 and trace is None:
             _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"),
                                  _dev_ptr(logits, "logits"), sp, _stream(h)))
         else:
-            prm = SearchParams(width, int(int8))
+            prm = SearchParams(width, int(int8), None if trace is None else _dev_ptr(trace, "trace"),
+                               0 if trace is None else trace.shape[1])
             _check(lib.vie_query_ex(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
@@ -224,12 +228,15 @@ class Index:
         B = h.shape[0]
         n = int(forced.numel())
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        prm = SearchParams(width, int(int8))
+        prm = SearchParams(width, int(int8), None, 0)
         fp = _dev_ptr(forced, "forced") if n else None
         _check(lib.vie_query_forced(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), fp, n, _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
-    def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1, int8: bool = False):
+    def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1, int8: bool = False,
+              trace_cap: int = 0):
+        """(ids, logits), plus stats if asked, plus the expansion trace
+        [B, trace_cap] (-1 past the last expansion) if trace_cap > 0."""
         torch = _torch()
         if h.dim() == 1:
             h = h.unsqueeze(0)
@@ -237,8 +244,10 @@ class Index:
         ids = torch.empty((B, k), dtype=torch.int32, device=h.device)
         lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
         st = torch.empty((B, 2), dtype=torch.int32, device=h.device) if stats else None
-        self.query_into(h, k, ef, ids, lg, st, width, int8)
-        return (ids, lg, st) if stats else (ids, lg)
+        tr = torch.full((B, trace_cap), -1, dtype=torch.int32, device=h.device) if trace_cap > 0 else None
+        self.query_into(h, k, ef, ids, lg, st, width, int8, tr)
+        out = (ids, lg) + ((st,) if stats else ())
+        return out + (tr,) if tr is not None else out
 
     def close(self) -> None:
         if self._h:

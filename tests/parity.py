@@ -9,9 +9,10 @@ Tolerances (stated for the head in its specification):
   the query's largest returned logit) only keeps the bound finite for logits
   at zero;
 * order: logits non-increasing, ids distinct;
-* HNSW traversal: equal (n_dist, n_expand) means the GPU walked the same path;
-  queries whose counts differ are counted as traversal divergences (they can
-  only start at a near tie of an fp32 against a float64 comparison).
+* HNSW traversal: the GPU walked the oracle's path when its expansion record
+  (the nodes it expanded, in order) and its counts equal the oracle's; a
+  query that parts from the path must do so at a near tie (first_divergence
+  below), and is counted instead of compared by ids.
 """
 from __future__ import annotations
 
@@ -96,3 +97,93 @@ def oracle_rows(fn, H, *args, threads=None, **kw):
     if not isinstance(outs[0], tuple):
         return np.concatenate(outs)
     return tuple(np.concatenate([o[i] for o in outs]) for i in range(len(outs[0])))
+
+
+# ------------------------------------------------ traversal divergences
+
+NODE_MASK = (1 << 26) - 1
+
+
+def _decode(trace):
+    t = np.asarray(trace)
+    t = t[t >= 0]
+    return t & NODE_MASK, (t >> 26) & 1, t >> 27
+
+
+def first_divergence(W, dtype, g, h, tg, to, ef_eff, rel=REL_CUT, int8=False):
+    """Explains where a traversal left the oracle's.  tg / to: the GPU's and
+    the oracle's expansion records of one query ((layer << 27) | (first of
+    step << 26) | node, -1 padded); h: the query [d].
+
+    Up to the first differing entry both walked the same nodes, so on the
+    layer L of that step both hold the same visited set S (the layer's entry
+    and every neighbour of a node expanded there) and the same expanded set
+    E.  Each side's beam is the best ef of S in its own arithmetic (ef = 1
+    above layer 0), and a step expands the best unexpanded entries of it.
+    With the oracle's fp64 order, x its ef-th best score in S and y the next:
+    if the GPU took a where the oracle took b, then either both lie in the
+    oracle's beam and their order flipped (|s_a - s_b| small), or b left the
+    GPU's beam (s_b - y small), or a entered it (x - s_a small); a side that
+    stopped or ended its step earlier counts as taking nothing.  Returns
+    (index, L, a, b, gap) with the smallest relative gap of those that apply
+    (None if the records are equal), or raises AssertionError when none of
+    them is within rel (not a near tie)."""
+    ng, fg, lg_ = _decode(tg)
+    no, fo, lo_ = _decode(to)
+    n = min(len(ng), len(no))
+    i = 0
+    while i < n and ng[i] == no[i] and fg[i] == fo[i] and lg_[i] == lo_[i]:
+        i += 1
+    if i == len(ng) and i == len(no):
+        return None
+    # the step in which they part: both start one at i, or i lies inside a
+    # step both began before
+    g_new = i >= len(ng) or fg[i] == 1
+    o_new = i >= len(no) or fo[i] == 1
+    if g_new and o_new:
+        s0 = i
+        layers = [x[i] for x, m in ((lg_, len(ng)), (lo_, len(no))) if i < m]
+        L = max(layers)
+    else:
+        s0 = max(j for j in range(i) if fg[j] == 1)
+        L = int(lg_[s0])
+    pre_nodes, pre_layers = ng[:s0], lg_[:s0]
+    on_L = [int(x) for x, l in zip(pre_nodes, pre_layers) if l == L]
+    assert on_L, "records part at the first expansion of layer %d (its entry point)" % L
+    assert not (int8 and L == 0), "int8 layer-0 scores are computed alike on both sides"
+    if L == 0:
+        lists = {u: [int(x) for x in g.adj0[u] if x >= 0] for u in on_L}
+    else:
+        lists = {u: [int(x) for x in g.upper[g.upper_off[u] + L - 1] if x >= 0] for u in on_L}
+    S = {on_L[0]}
+    for u in on_L:
+        S.update(lists[u])
+    S = np.array(sorted(S), np.int32)
+    E = set(on_L)
+    sc = O.pair_scores(W, dtype, np.atleast_2d(h), np.zeros(len(S), np.int32), S)
+    order = np.lexsort((S, -sc))
+    S, sc = S[order], sc[order]
+    ef = 1 if L >= 1 else ef_eff
+    in_beam = {int(u) for u in S[:ef]}
+    score = {int(u): float(v) for u, v in zip(S, sc)}
+    x = float(sc[ef - 1]) if len(S) >= ef else None
+    y = float(sc[ef]) if len(S) > ef else None
+
+    def taken(nodes, flags, layers, m):
+        if i >= m or layers[i] != L or (i > s0 and flags[i] == 1):
+            return None  # stopped this layer, or ended this step
+        return int(nodes[i])
+
+    a, b = taken(ng, fg, lg_, len(ng)), taken(no, fo, lo_, len(no))
+    assert a is None or a not in E, "GPU expanded node %d twice" % a
+    gaps = []
+    if a is not None and b is not None and a in in_beam and b in in_beam:
+        gaps.append(abs(score[a] - score[b]) / max(abs(score[a]), abs(score[b])))
+    if b is not None and b in in_beam and y is not None:
+        gaps.append((score[b] - y) / max(abs(y), abs(score[b])))
+    if a is not None and a not in in_beam and x is not None:
+        gaps.append((x - score[a]) / max(abs(x), abs(score[a])))
+    gap = min(gaps) if gaps else float("inf")
+    assert gap <= rel, "expansion %d on layer %d: GPU took %s, oracle %s; the nearest tie is %.3g relative" % (
+        i, L, a, b, gap)
+    return i, L, a, b, gap

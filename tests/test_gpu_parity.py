@@ -209,29 +209,51 @@ def _load_on_gpu(vie, g, W, dtype, tmp):
 def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None):
     """One launch of the search variant (width expansions per layer-0 step;
     int8 = the oracle's (rows, scales) when layer 0 walks int8 rows) against
-    the oracle's search of the same variant on the same graph: every query
-    must walk the oracle's path (equal distance and expansion counts), its
-    id set must equal the oracle's up to near ties at the k-th score, and its
-    logits must agree with the exact scores."""
+    the oracle's search of the same variant on the same graph.  A query
+    walks the oracle's path when it expands the oracle's nodes in the
+    oracle's order (equal expansion records and counts); its id set must
+    then equal the oracle's up to near ties at the k-th score.  A query that
+    parts from the oracle's path must do so at a near tie: the first
+    expansion where the records differ is traced back to the comparison that
+    decided it, whose scores must lie within 1e-4 relative (an fp32 sum
+    against a float64 one can order such a pair either way); it is counted,
+    and its ids are not compared.  Every returned logit must agree with the
+    exact score of its id.  Returns (ids, stats, parted queries)."""
+    ef_eff = max(ef, k)
+    cap = ef_eff + 1024
     h = dev_tensor(vie, H, dtype)
-    ids, lg, st = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None)
+    ids, lg, st, tr = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None, trace_cap=cap)
     torch.cuda.synchronize()
-    ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
+    ids, lg, st, tr = (ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32),
+                       tr.cpu().numpy())
     if int8 is not None:
-        oid, olg, ost = parity.oracle_rows(O.hnsw_search_q, H, W, dtype, g, int8[0], int8[1], None, k, ef, width,
-                                           validate=False)
+        oid, olg, ost, otr = parity.oracle_rows(O.hnsw_search_q, H, W, dtype, g, int8[0], int8[1], None, k, ef,
+                                                width, validate=False, trace_cap=cap)
     elif width > 1:
-        oid, olg, ost = parity.oracle_rows(O.hnsw_search_multi, H, W, dtype, g, None, k, ef, width, validate=False)
+        oid, olg, ost, otr = parity.oracle_rows(O.hnsw_search_multi, H, W, dtype, g, None, k, ef, width,
+                                                validate=False, trace_cap=cap)
     else:
-        oid, olg, ost, _ = parity.oracle_rows(O.hnsw_search, H, W, dtype, g, None, k, ef, validate=False)
-    same = np.all(st == ost, axis=1)
-    ndiv = int((~same).sum())
-    assert ndiv == 0, "%s: %d traversal divergences (queries %s)" % (what, ndiv, np.nonzero(~same)[0][:8].tolist())
+        oid, olg, ost, _, otr = parity.oracle_rows(O.hnsw_search, H, W, dtype, g, None, k, ef, validate=False,
+                                                   trace_cap=cap)
+    assert st[:, 1].max() <= cap
+    parted = []
+    for q in range(len(H)):
+        if st[q].tolist() == ost[q].tolist() and np.array_equal(tr[q], otr[q]):
+            continue
+        try:
+            why = parity.first_divergence(W, dtype, g, H[q], tr[q], otr[q], ef_eff, int8=int8 is not None)
+        except AssertionError as e:
+            raise AssertionError("%s: query %d leaves the oracle's path, not at a near tie (counts %s vs %s): %s" %
+                                 (what, q, st[q].tolist(), ost[q].tolist(), e))
+        parted.append(q)
+        say("  %s: query %d parts from the oracle at expansion %d (layer %d: %s vs %s), a tie within %.2g" %
+            ((what, q) + tuple(why[:4]) + (why[4],)))
     parity.check_logits(W, dtype, H, ids, lg, what)
     valid = oid[:, -1] >= 0
     osk = np.where(valid, parity.exact_scores(W, dtype, H, np.where(oid >= 0, oid, 0))[:, -1], 0)
-    parity.check_id_sets(W, dtype, H, ids, oid, osk, what=what)
-    return ids, st, ndiv
+    keep = np.array([q for q in range(len(H)) if q not in parted], np.int64)
+    parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=keep, what=what)
+    return ids, st, len(parted)
 
 
 def _library_graph(ix, W, dtype, efC, seed):
@@ -278,17 +300,8 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
         # ef = 600: more than 256 entries past the first unexpanded one, so the
         # picks are found eight flags per lane until the span shortens
         for k, ef in [(10, 10), (50, 64), (50, 200), (50, 600)]:
-            h = dev_tensor(vie, H, synth.BF16)
-            ids, lg, st = ix.query(h, k, ef, stats=True, width=width)
-            torch.cuda.synchronize()
-            ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
-            oid, olg, ost = O.hnsw_search_multi(W, synth.BF16, g, H, k, ef, width, validate=False)
-            same = np.all(st == ost, axis=1)
             what = "multi width=%d k=%d ef=%d" % (width, k, ef)
-            parity.check_logits(W, synth.BF16, H, ids, lg, what)
-            osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
-            parity.check_id_sets(W, synth.BF16, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
-            assert int((~same).sum()) == 0, what
+            ids, st, _ = _compare_hnsw(vie, ix, W, synth.BF16, g, H, k, ef, what, width=width)
             say("  %s recall@k=%.3f mean n_dist=%.0f n_expand=%.1f" %
                 (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
 
@@ -364,16 +377,8 @@ def test_int8_search_matches_oracle(vie, width):
         q, sc = vie.quantize_rows(ix._W_dev, synth.BF16)
         ix.attach_int8(q, sc)
         for k, ef in [(10, 40), (50, 100), (50, 512)]:
-            ids, lg, st = ix.query(dev_tensor(vie, H, synth.BF16), k, ef, stats=True, width=width, int8=True)
-            torch.cuda.synchronize()
-            ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
-            oid, olg, ost = O.hnsw_search_q(W, synth.BF16, g, oq, osc, H, k, ef, width, validate=False)
             what = "int8 width=%d k=%d ef=%d" % (width, k, ef)
-            same = np.all(st == ost, axis=1)
-            assert int((~same).sum()) == 0, "%s: %d traversal divergences" % (what, int((~same).sum()))
-            parity.check_logits(W, synth.BF16, H, ids, lg, what)
-            osk = parity.exact_scores(W, synth.BF16, H, oid)[:, -1]
-            parity.check_id_sets(W, synth.BF16, H, ids, oid, osk, what=what)
+            ids, st, _ = _compare_hnsw(vie, ix, W, synth.BF16, g, H, k, ef, what, width=width, int8=(oq, osc))
             say("  %s recall@k=%.3f mean n_dist=%.0f" % (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean()))
 
 
@@ -514,19 +519,10 @@ def test_multi_and_int8_at_wide_rows(vie, d, dtype):
     # one expansion per step (hnsw_kernel at the same widths; 3000-byte rows
     # load 8 bytes per lane chunk)
     _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "hnsw d=%d" % d)
-    h = dev_tensor(vie, H, dtype)
     for width in (2, 4, 8):
-        ids, lg, st = ix.query(h, k, ef, stats=True, width=width)
-        torch.cuda.synchronize()
-        ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
-        oid, olg, ost = O.hnsw_search_multi(W, dtype, g, H, k, ef, width, validate=False)
-        same = np.all(st == ost, axis=1)
         what = "multi d=%d width=%d" % (d, width)
-        parity.check_logits(W, dtype, H, ids, lg, what)
-        osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
-        parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
-        assert int((~same).sum()) == 0, what
-        say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))
+        ids, st, _ = _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=width)
+        say("  %s mean n_dist=%.0f" % (what, st[:, 0].mean()))
     oq, osc = O.quantize_rows(W, dtype)
     q, sc = vie.quantize_rows(ix._W_dev, dtype)
     assert np.array_equal(q.cpu().numpy(), oq)
@@ -537,16 +533,8 @@ def test_multi_and_int8_at_wide_rows(vie, d, dtype):
         return
     ix.attach_int8(q, sc)
     for width in (1, 8):
-        ids, lg, st = ix.query(h, k, ef, stats=True, width=width, int8=True)
-        torch.cuda.synchronize()
-        ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
-        oid, olg, ost = O.hnsw_search_q(W, dtype, g, oq, osc, H, k, ef, width, validate=False)
         what = "int8 d=%d width=%d" % (d, width)
-        same = np.all(st == ost, axis=1)
-        assert int((~same).sum()) == 0, "%s: %d traversal divergences" % (what, int((~same).sum()))
-        parity.check_logits(W, dtype, H, ids, lg, what)
-        osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
-        parity.check_id_sets(W, dtype, H, ids, oid, osk, what=what)
+        ids, st, _ = _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=width, int8=(oq, osc))
         say("  %s mean n_dist=%.0f" % (what, st[:, 0].mean()))
 
 
@@ -564,17 +552,9 @@ def test_hnsw_narrow_loads_match_oracle(vie, V, d, dtype):
         ix = _load_on_gpu(vie, g, W, dtype, tmp)
         for k, ef in [(10, 50), (50, 128)]:
             _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, "hnsw d=%d k=%d ef=%d" % (d, k, ef))
-            ids, lg, st = ix.query(dev_tensor(vie, H, dtype), k, ef, stats=True, width=4)
-            torch.cuda.synchronize()
-            ids, lg, st = ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32)
-            oid, olg, ost = O.hnsw_search_multi(W, dtype, g, H, k, ef, 4, validate=False)
-            same = np.all(st == ost, axis=1)
             what = "multi d=%d k=%d ef=%d" % (d, k, ef)
-            parity.check_logits(W, dtype, H, ids, lg, what)
-            osk = parity.exact_scores(W, dtype, H, oid)[:, -1]
-            parity.check_id_sets(W, dtype, H, ids, oid, osk, queries=np.nonzero(same)[0], what=what)
-            assert int((~same).sum()) == 0, what
-            say("  %s divergent=%d mean n_dist=%.0f" % (what, int((~same).sum()), st[:, 0].mean()))
+            ids, st, _ = _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=4)
+            say("  %s mean n_dist=%.0f" % (what, st[:, 0].mean()))
 
 
 @pytest.mark.parametrize("V,d,dtype", [(3000, 2048, synth.BF16), (3000, 3072, synth.BF16), (3001, 37, synth.BF16),

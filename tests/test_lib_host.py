@@ -158,6 +158,8 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query_forced(ix._h, fake, 1, 10, 10, None, fake, 5, fake, fake, None, None) == vie.ESTATE
     prm = vie.SearchParams(1, 2)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # int8_rows
+    prm = vie.SearchParams(1, 0, fake, 0)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # trace_cap
     assert L.vie_index_attach_int8(ix._h, fake, fake) == vie.ESTATE  # not on a device
     assert L.vie_index_attach_int8(ix._h, fake, None) == vie.EINVAL
     assert L.vie_quantize_rows(fake, 0, 0, 8, fake, fake, None) == vie.EINVAL     # V

@@ -329,17 +329,31 @@ def _chain_case():
         if l[0] == "case":
             kv = dict(x.split("=") for x in l[1:])
             cases.append((int(kv["ef"]), int(kv["k"]), [int(x) for x in kv["ids"].split(",")],
-                          int(kv["n_dist"]), int(kv["n_expand"])))
+                          int(kv["n_dist"]), int(kv["n_expand"]), _steps(kv["expanded"])))
     return W, g, cases
+
+
+def _steps(text):
+    """'0|1,2|4' -> the trace entries of layer-0 expansions 0, 1, 2, 4 with
+    the first node of each step flagged (bit 26)."""
+    out = []
+    for step in text.split("|"):
+        for j, x in enumerate(step.split(",")):
+            out.append(int(x) | ((1 << 26) if j == 0 else 0))
+    return out
 
 
 def test_search_golden_chain_trace():
     W, g, cases = _chain_case()
     assert O.check_graph(g) == ""
-    for ef, k, ids, nd, ne in cases:
-        got, lg, st, _ = O.hnsw_search(W, synth.F32, g, np.ones((1, 1), np.float32), k, ef)
+    for ef, k, ids, nd, ne, order in cases:
+        got, lg, st, _, tr = O.hnsw_search(W, synth.F32, g, np.ones((1, 1), np.float32), k, ef, trace_cap=16)
         assert got[0].tolist() == ids, (ef, got)
         assert st[0].tolist() == [nd, ne], (ef, st)
+        assert tr[0][:ne].tolist() == order and np.all(tr[0][ne:] == -1), (ef, tr)
+        # a short record keeps the first expansions
+        _, _, _, _, tr2 = O.hnsw_search(W, synth.F32, g, np.ones((1, 1), np.float32), k, ef, trace_cap=2)
+        assert tr2[0].tolist() == order[:2]
 
 
 def _tree_case():
@@ -364,17 +378,18 @@ def _tree_case():
         if l[0] == "case":
             kv = dict(x.split("=") for x in l[1:])
             cases.append((int(kv["P"]), int(kv["ef"]), int(kv["k"]), [int(x) for x in kv["ids"].split(",")],
-                          int(kv["n_dist"]), int(kv["n_expand"])))
+                          int(kv["n_dist"]), int(kv["n_expand"]), _steps(kv["expanded"])))
     return W, g, cases
 
 
 def test_multi_expansion_golden_tree_trace():
     W, g, cases = _tree_case()
     assert O.check_graph(g) == ""
-    for P, ef, k, ids, nd, ne in cases:
-        got, lg, st = O.hnsw_search_multi(W, synth.F32, g, np.ones((1, 1), np.float32), k, ef, P)
+    for P, ef, k, ids, nd, ne, order in cases:
+        got, lg, st, tr = O.hnsw_search_multi(W, synth.F32, g, np.ones((1, 1), np.float32), k, ef, P, trace_cap=16)
         assert got[0].tolist() == ids, (P, ef, got)
         assert st[0].tolist() == [nd, ne], (P, ef, st)
+        assert tr[0][:ne].tolist() == order, (P, ef, tr)
 
 
 @pytest.mark.parametrize("seed", [4, 5])
@@ -383,10 +398,18 @@ def test_multi_expansion_with_width_one_is_the_search(seed):
     W = synth.make_w(V, d, synth.BF16, 60 + seed)
     H, _ = synth.make_queries(W, synth.BF16, 20, 70 + seed)
     g = O.hnsw_build(W, synth.BF16, 6, 30, seed)
-    a = O.hnsw_search(W, synth.BF16, g, H, 10, 40)
-    b = O.hnsw_search_multi(W, synth.BF16, g, H, 10, 40, 1)
-    for x, y in zip(a[:3], b):
+    a = O.hnsw_search(W, synth.BF16, g, H, 10, 40, trace_cap=512)
+    b = O.hnsw_search_multi(W, synth.BF16, g, H, 10, 40, 1, trace_cap=512)
+    for x, y in zip(a[:3] + a[4:], b):
         assert np.array_equal(x, y)
+    # the record tags each expansion with its layer: the upper layers first,
+    # then layer 0, as many as the counter says
+    for q in range(len(H)):
+        t = a[4][q][:a[2][q, 1]]
+        assert np.all((t >> 26) & 1 == 1)  # one node per step
+        lay = t >> 27
+        assert np.all(np.diff(lay) <= 0) and lay[-1] == 0 and lay[0] <= g.maxlevel
+        assert np.all(a[4][q][a[2][q, 1]:] == -1)
 
 
 @pytest.mark.parametrize("P", [2, 3, 8])

@@ -273,6 +273,20 @@ vie_status vie_dense_topk(const void *W_dev, vie_dtype dtype, int64_t V, int32_t
                           int32_t B, int32_t k, int32_t *ids_dev, float *logits_dev, void *workspace_dev,
                           size_t workspace_bytes, void *hip_stream);
 
+/* vie_dense_topk for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops, harnesses that forbid hipMalloc): the
+ * same kernels and results, with the workspace taken from a 16 MiB array
+ * that the library holds on each GPU until the process ends (set up on the
+ * first call on a device).  The call allocates nothing.  Calls on one GPU
+ * share that array, so calls that overlap in time on one GPU (other streams,
+ * other threads) race and must be ordered by the caller.  Limit:
+ * vie_dense_topk_workspace(V, d, B, k) <= 16 MiB (for example B <= 15 at
+ * V = 262144, B <= 30 at V = 128256); larger requests fail with
+ * VIE_EUNSUPPORTED before anything is enqueued.
+ * Errors: VIE_EINVAL, VIE_EUNSUPPORTED, VIE_EHIP. */
+vie_status vie_dense_topk_noalloc(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, const void *h_dev,
+                                  int32_t B, int32_t k, int32_t *ids_dev, float *logits_dev, void *hip_stream);
+
 /* Reconstructs full-vocabulary logits (Section 3): out_dev fp32[B][V] is -inf
  * everywhere except out[b][ids[b][j]] = logits[b][j].  Ids outside [0, V) are
  * skipped (so -1 padding is harmless); ids within a row must be distinct.

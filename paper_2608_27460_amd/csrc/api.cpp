@@ -406,6 +406,23 @@ vie_status vie_dense_topk(const void *W_dev, vie_dtype dtype, int64_t V, int32_t
                              static_cast<hipStream_t>(hip_stream));
 }
 
+vie_status vie_dense_topk_noalloc(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, const void *h_dev,
+                                  int32_t B, int32_t k, int32_t *ids_dev, float *logits_dev, void *hip_stream)
+{
+    g_last_error.clear();
+    if (!W_dev || !h_dev || !ids_dev || !logits_dev) return fail(VIE_EINVAL, "NULL argument");
+    if (vie_status s = check_dims(V, d, dtype)) return s;
+    if (vie_status s = check_k(k, V, B)) return s;
+    const size_t need = dense_workspace_bytes(V, d, B, k);
+    if (need > dense_scratch_bytes())
+        return fail(VIE_EUNSUPPORTED, "V = %lld, B = %d needs %zu bytes of workspace; the static one holds %zu",
+                    (long long)V, B, need, dense_scratch_bytes());
+    void *ws = nullptr;
+    if (vie_status s = dense_scratch(&ws)) return s;
+    return launch_dense_topk(W_dev, dtype, V, d, h_dev, B, k, ids_dev, logits_dev, ws,
+                             static_cast<hipStream_t>(hip_stream));
+}
+
 vie_status vie_scatter(const int32_t *ids_dev, const float *logits_dev, int32_t B, int32_t k, int64_t V,
                        float *out_dev, void *hip_stream)
 {

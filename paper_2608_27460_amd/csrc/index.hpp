@@ -101,6 +101,10 @@ vie_status launch_forced(const HnswLaunch &a, const int32_t *forced, int n, hipS
 size_t hnsw_lds_limit();
 
 size_t dense_workspace_bytes(int64_t V, int d, int B, int k);
+// The library's static per-GPU workspace of the dense head (kernels.hip):
+// its size, and its device address on the current device.
+size_t dense_scratch_bytes();
+vie_status dense_scratch(void **out);
 vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const void *h, int B, int k,
                              int32_t *ids, float *logits, void *ws, hipStream_t s);
 

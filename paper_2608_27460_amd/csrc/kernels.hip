@@ -22,6 +22,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <mutex>
 
 #include "index.hpp"
 #include "keys.hpp"
@@ -2359,6 +2360,46 @@ vie_status launch_dense_topk(const void *W, int dtype, int64_t V, int d, const v
             e = dense_launch_nb<2, true>(nb, W, V, row_bytes, hp, nq, k, p, zbuf, tops, ip, lp, s);
         if (e != hipSuccess) return launched(e, "dense top-k launch");
     }
+    return VIE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// the dense head's workspace for callers that cannot allocate
+// ---------------------------------------------------------------------------
+//
+// One array per GPU, held by the loaded library until the process ends.  On
+// the host its name is a stand-in, not a device address: host code passes
+// only the address hipGetSymbolAddress returns on each device.  Calls that
+// use it on one GPU share it and must not overlap in time.
+
+constexpr size_t kScratchBytes = size_t(16) << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kScratchDevices];  // device address of scratch, per device (set on first use)
+}  // namespace
+
+size_t dense_scratch_bytes() { return kScratchBytes; }
+
+vie_status dense_scratch(void **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(VIE_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kScratchDevices)
+        return fail(VIE_EUNSUPPORTED, "device %d: the static workspace serves devices 0..%d", dev,
+                    kScratchDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(VIE_EHIP, "hipGetSymbolAddress of the static workspace: %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
     return VIE_OK;
 }
 

@@ -68,6 +68,7 @@ def _load() -> C.CDLL:
         "vie_index_attach_int8": (st, [vp, vp, vp]),
         "vie_dense_topk_workspace": (st, [i64, i32, i32, i32, C.POINTER(sz)]),
         "vie_dense_topk": (st, [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp, sz, vp]),
+        "vie_dense_topk_noalloc": (st, [vp, i32, i64, i32, vp, i32, i32, vp, vp, vp]),
         "vie_scatter": (st, [vp, vp, i32, i32, i64, vp, vp]),
         "vie_status_string": (C.c_char_p, [st]),
         "vie_last_error": (C.c_char_p, []),
@@ -287,6 +288,18 @@ def dense_topk_into(W, h, k: int, ids, logits, workspace) -> None:
     _check(lib.vie_dense_topk(_dev_ptr(W, "W"), dt, V, d, _dev_ptr(h, "h"), h.shape[0], k, _dev_ptr(ids, "ids"),
                               _dev_ptr(logits, "logits"), _dev_ptr(workspace, "workspace"), workspace.numel(),
                               _stream(h)))
+
+
+def dense_topk_noalloc_into(W, h, k: int, ids, logits) -> None:
+    """dense_topk_into without a workspace argument: the library's static
+    per-GPU workspace (vie_dense_topk_noalloc); calls on one GPU must not
+    overlap."""
+    V, d = W.shape
+    dt = _dtype_of_tensor(W)
+    if _dtype_of_tensor(h) != dt:
+        raise TypeError("W and h must have the same dtype")
+    _check(lib.vie_dense_topk_noalloc(_dev_ptr(W, "W"), dt, V, d, _dev_ptr(h, "h"), h.shape[0], k,
+                                      _dev_ptr(ids, "ids"), _dev_ptr(logits, "logits"), _stream(h)))
 
 
 class DenseHead:

@@ -176,6 +176,10 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_dense_topk(fake, 2, 1000, 64, fake, 1, 50, fake, fake, ws, 1 << 30, None) == vie.EINVAL  # dtype
     assert L.vie_dense_topk(fake, 0, 1000, 0, fake, 1, 50, fake, fake, ws, 1 << 30, None) == vie.EINVAL  # d
     assert L.vie_dense_topk(fake, 0, 1000, 64, fake, 1, 1025, fake, fake, ws, 1 << 30, None) == vie.EINVAL
+    assert L.vie_dense_topk_noalloc(None, 1, 1000, 64, fake, 1, 50, fake, fake, None) == vie.EINVAL
+    assert L.vie_dense_topk_noalloc(fake, 1, 1000, 64, fake, 1, 1001, fake, fake, None) == vie.EINVAL  # k > V
+    assert L.vie_dense_topk_noalloc(fake, 1, 262144, 640, fake, 64, 50, fake, fake,
+                                    None) == vie.EUNSUPPORTED  # beyond the static workspace
     assert L.vie_scatter(fake, fake, 1, 0, 100, fake, None) == vie.EINVAL
     assert L.vie_scatter(fake, fake, 1, 5, 0, fake, None) == vie.EINVAL
     assert L.vie_scatter(None, fake, 1, 5, 100, fake, None) == vie.EINVAL

@@ -7,8 +7,8 @@ queries served one per call (B = 1), HNSW graph with M = 32 (M0 = 64),
 ef_construction = 200, built by the library on the host CPUs.
 
 The beam width is the one the method needs: for each traversal (the
-sequential search; 8 expansions per step; 8 per step on int8 rows with the
-exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
+sequential search; 8 or 32 expansions per step; 8, 16 or 32 per step on int8
+rows with the exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
 0.95 on the first 128 queries (recall against the exact dense head, itself
 parity-tested against the oracle).  The fastest of them at its ef is the
 headline traversal.
@@ -52,13 +52,19 @@ NODE_MASK = (1 << 26) - 1
 TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0)
     "sequential": (1, False),
     "width8": (8, False),
+    "width32": (32, False),
     "int8_width8": (8, True),
+    "int8_width16": (16, True),
+    "int8_width32": (32, True),
 }
-KERNEL_OF = {
-    "sequential": "hnsw_kernel",
-    "width8": "hnsw_multi_kernel (bf16 rows, 8 per step)",
-    "int8_width8": "hnsw_multi_kernel (int8 rows, 8 per step, exact re-rank)",
-}
+
+
+def kernel_of(trav):
+    width, int8 = TRAVERSALS[trav]
+    if width == 1 and not int8:
+        return "hnsw_kernel"
+    return "hnsw_multi_kernel (%s rows, %d per step%s)" % ("int8" if int8 else "stored", width,
+                                                          ", exact re-rank" if int8 else "")
 
 
 def measured_traffic(workload):
@@ -297,7 +303,7 @@ def main() -> int:
     if args.traversal:
         head_trav = args.traversal
     elif args.ef:
-        head_trav = "int8_width8" if "int8_width8" in travs else "width8"
+        head_trav = "int8_width32" if "int8_width32" in travs else "width32"
     else:
         head_trav = min(reachable, key=lambda t: calib[t]["tried"][str(chosen[t])]["us_per_query"])
     ef = chosen[head_trav]
@@ -340,7 +346,7 @@ def main() -> int:
                                     vie.scatter_into(iv[c], lv[c], wl.V, row)), nseq)
         seq = {"ef": ef_s, "queries": nseq, "us_per_query": pct(calls),
                "recall_at_k": round(recall(hi.cpu().numpy()[:nseq], exact_ids[:nseq]), 4),
-               "kernel": KERNEL_OF["sequential"]}
+               "kernel": kernel_of("sequential")}
 
     # ---- dense head: calls alternate between two copies of W_out -----------
     Wd2 = Wd.clone()
@@ -519,7 +525,7 @@ def main() -> int:
                    "recall_target": args.target_recall, "accumulate": "fp32",
                    "graph": {"maxlevel": info["maxlevel"], "entry": info["entry"],
                              "build_s_16_threads": None if cpu_build_s is None else round(cpu_build_s, 1)}},
-        "hnsw": {"traversal": head_trav, "ef": ef, "kernel": KERNEL_OF[head_trav],
+        "hnsw": {"traversal": head_trav, "ef": ef, "kernel": kernel_of(head_trav),
                  "us_per_query": round(h_ms * 1e3 / (SQ * args.steps), 2), "queries_per_s": round(h_qps, 1),
                  "per_call_us": pct(head_calls), "kernel_us": round(head_kernel_us, 2),
                  "recall_at_k": round(recall(head_ids, exact_ids), 4),
@@ -531,7 +537,7 @@ def main() -> int:
                   "per_call_us": pct(dense_calls), "kernel_us": round(d_kernel_us, 2), "W_copies": 2,
                   "wall_s": round(d_wall, 3)},
         "legs": legs,
-        "roofline": {"kernel": KERNEL_OF[head_trav], "bound": "hbm", "achieved": round(head_gbs, 2),
+        "roofline": {"kernel": kernel_of(head_trav), "bound": "hbm", "achieved": round(head_gbs, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(head_gbs / HBM_PEAK_GBS, 5),
                      "traffic": traffic.get(head_trav)},
         "roofline_dense": {"kernel": "dense_stream_kernel+dense_merge_kernel", "bound": "hbm",

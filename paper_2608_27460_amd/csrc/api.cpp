@@ -262,8 +262,8 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
 vie_status check_params(const vie_search_params *params)
 {
     if (!params) return VIE_OK;
-    if (params->expand_width < 1 || params->expand_width > 8)
-        return fail(VIE_EINVAL, "expand_width = %d outside 1..8", params->expand_width);
+    if (params->expand_width < 1 || params->expand_width > 32)
+        return fail(VIE_EINVAL, "expand_width = %d outside 1..32", params->expand_width);
     if (params->int8_rows != 0 && params->int8_rows != 1)
         return fail(VIE_EINVAL, "int8_rows = %d is neither 0 nor 1", params->int8_rows);
     if (params->trace_dev && params->trace_cap < 1)

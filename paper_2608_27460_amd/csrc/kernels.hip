@@ -1588,7 +1588,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 // of its lists there; the rest come from HBM.  Rows: each group keeps two
 // rows' loads in flight.
 
-constexpr int kMaxWidth = 8;        // widest expansion step
+constexpr int kMaxWidth = 32;       // widest expansion step
 constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
 
@@ -1700,6 +1700,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
     __shared__ int32_t lc_id[kMaxWidth];  // nodes whose lists sit in the cache
+    __shared__ int32_t s_pick[kMaxWidth];  // this step's picks (beam positions)
+    __shared__ int32_t s_np, s_after;
     __shared__ uint32_t s_hmax;           // Q8: bits of max |h|
     constexpr int kGroups = NT / G;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
@@ -1788,82 +1790,77 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     for (;;) {
         const uint32_t first = sh.first, nbeam = sh.nbeam;
         if (first >= nbeam) break;  // no unexpanded entry (first is ~0 then)
-        // the picks (up to width unexpanded entries from `first` on) and the
-        // next unexpanded entry after them, the same in every wave
-        int pick[kMaxWidth];
-#pragma unroll
-        for (int t = 0; t < kMaxWidth; ++t) pick[t] = -1;
-        int np = 0, after = -1;
-        if ((int)nbeam - (int)first <= kPickNarrowSpan) {
-            // a short span: one flag per lane, 64 entries per round
-            for (int i0 = (int)first; i0 < (int)nbeam && after < 0; i0 += kWave) {
-                uint64_t ball = __ballot(i0 + lane < (int)nbeam && !flag[i0 + lane]);
-#pragma unroll
-                for (int t = 0; t < kMaxWidth; ++t)
-                    if (t < width && pick[t] < 0 && ball) {
-                        pick[t] = i0 + __ffsll((long long)ball) - 1;
-                        ball &= ball - 1;
-                        ++np;
+        // the picks: up to width unexpanded entries from `first` on, in beam
+        // order, and the next unexpanded entry after them, found by wave 0
+        // (ballots over the expanded bits) and published in LDS
+        if (tid < kWave) {
+            int np = 0;
+            bool found_after = false;
+            if (lane == 0) s_after = -1;
+            if ((int)nbeam - (int)first <= kPickNarrowSpan) {
+                // a short span: one flag per lane, 64 entries per round
+                for (int i0 = (int)first; i0 < (int)nbeam && !found_after; i0 += kWave) {
+                    const int i = i0 + lane;
+                    const bool un = i < (int)nbeam && !(flag[i] & 1);
+                    const uint64_t ball = __ballot(un);
+                    const int rank = np + (int)__builtin_amdgcn_mbcnt_hi(
+                                              (uint32_t)(ball >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)ball, 0u));
+                    if (un && rank < width) s_pick[rank] = i;
+                    if (un && rank == width) s_after = i;
+                    found_after = np + __popcll(ball) > width;
+                    np = min(width, np + __popcll(ball));
+                }
+            } else {
+                // eight flags per lane (512 entries per round): bit 8 b of a
+                // lane's mask is set when entry 8 lane + b is unexpanded and in
+                // [first, nbeam); a lane's entries take the ranks after those of
+                // the lanes below it
+                for (int b0 = (int)first & ~7; b0 < (int)nbeam && !found_after; b0 += 8 * kWave) {
+                    const int i = b0 + 8 * lane;
+                    uint64_t m = 0ull;
+                    if (i < (int)nbeam) {
+                        m = ~*reinterpret_cast<const uint64_t *>(flag + i) & 0x0101010101010101ull;
+                        const int lo = (int)first - i, hi = (int)nbeam - i;
+                        if (lo >= 8) m = 0ull;
+                        else if (lo > 0) m &= ~0ull << (8 * lo);
+                        if (hi < 8) m &= (1ull << (8 * hi)) - 1ull;
                     }
-                if (np == width && ball && after < 0) after = i0 + __ffsll((long long)ball) - 1;
+                    const uint32_t cnt = (uint32_t)__popcll(m);
+                    const uint32_t incl = wave_incl_scan(cnt);
+                    int rank = np + (int)(incl - cnt);
+                    for (uint64_t mm = m; mm != 0ull && rank <= width; mm &= mm - 1ull, ++rank) {
+                        const int idx = i + (__ffsll((long long)mm) - 1) / 8;
+                        if (rank < width) s_pick[rank] = idx;
+                        else s_after = idx;
+                    }
+                    const int total = __builtin_amdgcn_readlane((int)incl, kWave - 1);
+                    found_after = np + total > width;
+                    np = min(width, np + total);
+                }
             }
-        } else {
-            // eight flags per lane (512 entries per round): bit 8 b of a lane's
-            // mask is set when entry 8 lane + b is unexpanded and in [first, nbeam);
-            // the lanes with such entries are then taken in order by ballot, and
-            // their entries by scalar bit scans, so every wave finds the same picks
-            for (int b0 = (int)first & ~7; b0 < (int)nbeam && after < 0; b0 += 8 * kWave) {
-                const int i = b0 + 8 * lane;
-                uint64_t m = 0ull;
-                if (i < (int)nbeam) {
-                    m = ~*reinterpret_cast<const uint64_t *>(flag + i) & 0x0101010101010101ull;
-                    const int lo = (int)first - i, hi = (int)nbeam - i;
-                    if (lo >= 8) m = 0ull;
-                    else if (lo > 0) m &= ~0ull << (8 * lo);
-                    if (hi < 8) m &= (1ull << (8 * hi)) - 1ull;
-                }
-                uint64_t lanes = __ballot(m != 0ull);
-                while (lanes != 0ull && after < 0) {
-                    const int L = __ffsll((long long)lanes) - 1;
-                    uint64_t ml = readlane64(m, L);
-                    while (ml != 0ull && after < 0) {
-                        const int idx = b0 + 8 * L + (__ffsll((long long)ml) - 1) / 8;
-                        if (np < width) {
-#pragma unroll
-                            for (int t = 0; t < kMaxWidth; ++t)
-                                if (t == np) pick[t] = idx;
-                            ++np;
-                        } else {
-                            after = idx;
-                        }
-                        ml &= ml - 1ull;
-                    }
-                    lanes &= lanes - 1ull;
-                }
+            if (lane == 0) {
+                s_np = np;
+                sh.nkeep = 0;  // last read before the previous merge
             }
         }
+        __syncthreads();
+        const int np = s_np;
         if (np == 0) break;
-        if (tid == 0) {
-            sh.nkeep = 0;  // last read before the previous merge
-            if (trace) {
-#pragma unroll
-                for (int t = 0; t < kMaxWidth; ++t)
-                    if (t < np) note_expand(trace, trace_cap, n_expand + t, 0, key_id(beam[pick[t]]), t == 0);
-            }
+        if (tid == 0 && trace) {
+            for (int t = 0; t < np; ++t) note_expand(trace, trace_cap, n_expand + t, 0, key_id(beam[s_pick[t]]), t == 0);
         }
         n_expand += np;
-        // claim the unseen neighbours of the picks (node t / M0, slot t % M0)
+        // claim the unseen neighbours of the picks (node t / M0, slot t % M0);
+        // a pick's list comes from the cache slot its flag names while the
+        // cache still holds that node's list, else from HBM.  The first slot
+        // of each pick marks it expanded (the other bits of its flag stay).
         for (int t = tid; t < np * M0; t += NT) {
             const int j = t / M0, slot = t - j * M0;
-            int pj = pick[0];
-#pragma unroll
-            for (int u = 1; u < kMaxWidth; ++u)
-                if (u == j) pj = pick[u];
+            const int pj = s_pick[j];
             const int32_t c = key_id(beam[pj]);
-            int src = -1;
-#pragma unroll
-            for (int u = 0; u < kMaxWidth; ++u)
-                if (u < width && lc_id[u] == c) src = u;
+            const int hint = (int)(flag[pj] >> 1) - 1;
+            const int src = hint >= 0 && lc_id[hint] == c ? hint : -1;
+            if (slot == 0) flag[pj] |= 1;
             // two guarded loads, not one through a selected pointer (that
             // would be a generic load, which waits on both memory counters)
             const int32_t ec = src >= 0 ? lcache[max(src, 0) * M0 + slot] : -1;
@@ -1981,19 +1978,19 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             const int pos = lo + above;
             if (pos < total) {
                 beam2[pos] = key;
-                flag2[pos] = 0;
+                // unexpanded; the best `width` kept keys name the cache slot
+                // that may hold their list
+                flag2[pos] = above < width ? (uint8_t)((above + 1) << 1) : (uint8_t)0;
                 if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
             }
         }
+        const int after = s_after;
         for (int i = (tid + NT / 2) % NT; i < (int)nbeam; i += NT) {  // the other half of the workgroup
             const uint64_t key = beam[i];
             const int pos = i + kept_above(key);
             if (pos < total) {
-                bool picked = false;
-#pragma unroll
-                for (int u = 0; u < kMaxWidth; ++u) picked |= pick[u] == i;
                 beam2[pos] = key;
-                flag2[pos] = picked ? 1 : flag[i];
+                flag2[pos] = flag[i] & 1;  // older cache slots are stale
                 if (i == after) atomicMin(&sh.first, (uint32_t)pos);
             }
         }

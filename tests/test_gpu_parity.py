@@ -286,7 +286,7 @@ def test_hnsw_matches_oracle_on_oracle_graph(vie, V, d, dtype, M, efC):
             assert np.array_equal(i1.cpu().numpy()[0], ids_b.cpu().numpy()[q])
 
 
-@pytest.mark.parametrize("width", [2, 3, 4, 8])
+@pytest.mark.parametrize("width", [2, 3, 4, 8, 13, 32])
 def test_hnsw_multi_expansion_matches_oracle(vie, width):
     """Several expansions per step follow the oracle's multi-expansion search
     (same visits and counts), with the list cache and ragged picks."""
@@ -628,7 +628,7 @@ def test_hnsw_batches_of_256_and_more(vie, dtype):
     ix = vie.Index.build(W, dtype, 16, 60, seed=1502, n_threads=16)
     g = _library_graph(ix, W, dtype, 60, 1502)
     ix.to_device(dev_tensor(vie, W, dtype))
-    _variants(vie, ix, W, dtype, g, H, 50, 128, "B=300")
+    _variants(vie, ix, W, dtype, g, H, 50, 128, "B=300", widths=(1, 8, 32))
 
 
 @pytest.mark.parametrize("d", [640, 1024, 2048, 3072])
@@ -645,7 +645,7 @@ def test_hnsw_degree_64_at_model_row_widths(vie, d):
     assert g.M0 == 64 and (g.adj0 >= 0).sum(axis=1).max() == 64
     ix.to_device(dev_tensor(vie, W, synth.BF16))
     for k, ef in [(50, 128), (50, 512)]:
-        _variants(vie, ix, W, synth.BF16, g, H, k, ef, "M0=64 d=%d ef=%d" % (d, ef))
+        _variants(vie, ix, W, synth.BF16, g, H, k, ef, "M0=64 d=%d ef=%d" % (d, ef), widths=(1, 8, 32))
 
 
 @pytest.mark.parametrize("d", [256, 2048])
@@ -677,4 +677,4 @@ def test_hnsw_full_size_gemma_graph(vie):
     say("gemma full: maxlevel %d entry %d" % (g.maxlevel, g.entry))
     ix.to_device(dev_tensor(vie, W, wl.dtype))
     for ef in (128, 2048):
-        _variants(vie, ix, W, wl.dtype, g, H, 50, ef, "gemma full ef=%d" % ef)
+        _variants(vie, ix, W, wl.dtype, g, H, 50, ef, "gemma full ef=%d" % ef, widths=(1, 8, 32))

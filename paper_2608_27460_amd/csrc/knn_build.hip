@@ -15,12 +15,10 @@
 //   5. entry point: the row of largest squared norm (ties: smaller id).
 //
 // Step 1 is a dense contraction: the Gram block S = W[rows] W^T of a chunk of
-// rows comes from a library GEMM (rocBLAS, fp32 accumulation), and one
-// workgroup per row selects its exact top K from S.  Steps 2-5 are this
-// file's kernels.  Scores are fp32 throughout; ties of equal scores are
+// rows comes from this file's matrix-core kernel (fp32 accumulation), and
+// one workgroup per row selects its exact top K from S.  Scores are fp32 throughout; ties of equal scores are
 // broken by id exactly as the oracle breaks them.
 #include <hip/hip_runtime.h>
-#include <rocblas/rocblas.h>
 
 #include <algorithm>
 #include <cstdint>
@@ -201,6 +199,135 @@ __device__ int block_topk(int64_t n, int K, KeyAt key_at, TopkShared &sh)
 // sort finishes; otherwise the exact radix select runs.  The sample only
 // decides the speed, never the result.
 constexpr int kSampleEvery = 8;
+
+// ---------------------------------------------------------------------------
+// Gram blocks on the matrix cores
+// ---------------------------------------------------------------------------
+//
+// S[c][j] = <w_{r0 + c}, w_j> for the rows c of a chunk and every row j, fp32
+// accumulation, written with row pitch ld.  A workgroup of four waves owns a
+// 128 x 128 tile (128 chunk rows c by 128 rows j); wave (wm, wn) computes its
+// 64 x 64 quarter as 4 x 4 tiles of 16 x 16 on the matrix cores
+// (v_mfma_f32_16x16x32_bf16 for bf16 rows, v_mfma_f32_16x16x4_f32 for fp32
+// rows).  The reduction over the row width runs in stages of kGramKC bytes
+// of each row: both 128-row slices of a stage are staged in LDS (padded
+// rows), the next stage loading into registers while the current one is
+// multiplied.  Lane (r, g) of a wave (r = lane % 16, g = lane / 16) feeds
+// row r of a 16-row operand with its g-th quarter of the k step, and ends
+// holding rows 4 g + i of column r of each 16 x 16 result.  Every score is
+// the same sequence of products and sums whichever tile computes it.
+
+constexpr int kGramTile = 128;                     // rows of c and of j per workgroup
+constexpr int kGramThreads = 256;                  // four waves, 2 x 2 quarters
+#ifndef VIE_GRAM_KC
+#define VIE_GRAM_KC 128
+#endif
+constexpr int kGramKC = VIE_GRAM_KC;               // bytes of a row per stage
+#ifndef VIE_GRAM_PAD
+#define VIE_GRAM_PAD 16
+#endif
+constexpr int kGramRowPitch = kGramKC + VIE_GRAM_PAD;  // LDS bytes per staged row (padded)
+constexpr int kGramStage = 2 * kGramTile * kGramRowPitch;  // A and B slices of one stage
+constexpr int kGramLoads = 2 * kGramTile * (kGramKC / 16) / kGramThreads;  // 16-byte loads per thread
+
+__device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kGramThreads) void knn_gram_kernel(const char *__restrict__ W, int64_t V, int row_bytes,
+                                                                int64_t r0, int64_t rows, float *__restrict__ S,
+                                                                int64_t ld)
+{
+    extern __shared__ __align__(16) char smem[];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int r = lane & 15, g = lane >> 4;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t c0 = (int64_t)blockIdx.y * kGramTile, j0 = (int64_t)blockIdx.x * kGramTile;
+    const int nstage = (row_bytes + kGramKC - 1) / kGramKC;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    // staging: load t of a thread covers staged row (L / 8) of A (L < 1024)
+    // or of B, 16 bytes at byte (L % 8) * 16 of the stage, L = t * 256 + tid
+    const char *src[kGramLoads];
+    int soff[kGramLoads], scol[kGramLoads];
+#pragma unroll
+    for (int t = 0; t < kGramLoads; ++t) {
+        const int L = t * kGramThreads + tid;
+        const int srow = L / (kGramKC / 16);  // 0..255: A rows then B rows
+        scol[t] = (L % (kGramKC / 16)) * 16;
+        const int64_t grow = srow < kGramTile ? r0 + min<int64_t>(c0 + srow, rows - 1)
+                                              : min<int64_t>(j0 + srow - kGramTile, V - 1);
+        src[t] = W + grow * (int64_t)row_bytes;
+        soff[t] = srow * kGramRowPitch + scol[t];
+    }
+    auto load_stage = [&](int st, u32x4(&buf)[kGramLoads]) {
+#pragma unroll
+        for (int t = 0; t < kGramLoads; ++t) {
+            const int c = st * kGramKC + scol[t];
+            buf[t] = c + 16 <= row_bytes ? *reinterpret_cast<const u32x4 *>(src[t] + c) : zero;
+        }
+    };
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    u32x4 pre[kGramLoads];
+    load_stage(0, pre);
+    for (int st = 0; st < nstage; ++st) {
+        char *buf = smem + (st & 1) * kGramStage;
+#pragma unroll
+        for (int t = 0; t < kGramLoads; ++t) *reinterpret_cast<u32x4 *>(buf + soff[t]) = pre[t];
+        if (st + 1 < nstage) load_stage(st + 1, pre);
+        __syncthreads();  // the stage is in LDS (and the stage before it is no longer read)
+        const char *A = buf + (wm * 64) * kGramRowPitch;
+        const char *B = buf + (kGramTile + wn * 64) * kGramRowPitch;
+        if constexpr (BF16) {
+#pragma unroll
+            for (int kk = 0; kk < kGramKC; kk += 64) {  // 32 bf16 per MFMA step
+                u32x4 a[4], b[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    a[m] = *reinterpret_cast<const u32x4 *>(A + (m * 16 + r) * kGramRowPitch + kk + 16 * g);
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    b[n] = *reinterpret_cast<const u32x4 *>(B + (n * 16 + r) * kGramRowPitch + kk + 16 * g);
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[m][n] = mfma_bf16(a[m], b[n], acc[m][n]);
+            }
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < kGramKC; kk += 16) {  // 4 floats per MFMA step
+                float a[4], b[4];
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    a[m] = *reinterpret_cast<const float *>(A + (m * 16 + r) * kGramRowPitch + kk + 4 * g);
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    b[n] = *reinterpret_cast<const float *>(B + (n * 16 + r) * kGramRowPitch + kk + 4 * g);
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[m][n] = mfma_f32(a[m], b[n], acc[m][n]);
+            }
+        }
+    }
+    // lane (r, g) holds chunk rows 16 m + 4 g + i of the quarter, column 16 n + r
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t c = c0 + wm * 64 + m * 16 + 4 * g + i;
+            if (c >= rows) continue;
+            float *out = S + c * ld + j0 + wn * 64;
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+                if (j0 + wn * 64 + n * 16 + r < V) out[n * 16 + r] = acc[m][n][i];
+        }
+}
 
 __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__restrict__ S, int64_t ld, int64_t r0,
                                                                 int64_t V, int K, int32_t *__restrict__ cand,
@@ -637,11 +764,6 @@ bool dalloc(T *&p, size_t bytes)
     return true;
 }
 
-vie_status blas_fail(rocblas_status st, const char *what)
-{
-    return fail(VIE_EHIP, "%s failed: %s", what, rocblas_status_to_string(st));
-}
-
 }  // namespace
 
 vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, int K, int M0, int64_t chunk_rows,
@@ -680,33 +802,21 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
         return st;
     };
 
-    rocblas_handle h = nullptr;
-    rocblas_status bs = rocblas_create_handle(&h);
-    if (bs != rocblas_status_success) return bail(blas_fail(bs, "rocblas_create_handle"));
-    bs = rocblas_set_stream(h, s);
-    const float one = 1.0f, zero = 0.0f;
-    for (int64_t r0 = 0; r0 < V && bs == rocblas_status_success; r0 += R) {
+    auto gram = dtype == VIE_BF16 ? knn_gram_kernel<true> : knn_gram_kernel<false>;
+    he = hipFuncSetAttribute((const void *)gram, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kGramStage);
+    if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
+    for (int64_t r0 = 0; r0 < V; r0 += R) {
         const int64_t rows = std::min(R, V - r0);
-        // column-major view: W^T is d x V (ld d); scores (V x rows, ld) = W[all] . W[chunk]^T
-        const char *Wc = static_cast<const char *>(W_dev) + r0 * row_bytes;
-        if (dtype == VIE_F32)
-            bs = rocblas_sgemm(h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)V,
-                               (rocblas_int)rows, d, &one, static_cast<const float *>(W_dev), d,
-                               reinterpret_cast<const float *>(Wc), d, &zero, b.S, (rocblas_int)ld);
-        else
-            bs = rocblas_gemm_ex(h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)V,
-                                 (rocblas_int)rows, d, &one, W_dev, rocblas_datatype_bf16_r, d, Wc,
-                                 rocblas_datatype_bf16_r, d, &zero, b.S, rocblas_datatype_f32_r, (rocblas_int)ld, b.S,
-                                 rocblas_datatype_f32_r, (rocblas_int)ld, rocblas_datatype_f32_r,
-                                 rocblas_gemm_algo_standard, 0, 0);
-        if (bs != rocblas_status_success) break;
+        const dim3 grid((unsigned)((V + kGramTile - 1) / kGramTile), (unsigned)((rows + kGramTile - 1) / kGramTile));
+        gram<<<grid, kGramThreads, 2 * kGramStage, s>>>(static_cast<const char *>(W_dev), V, row_bytes, r0, rows, b.S,
+                                                        ld);
+        he = hipGetLastError();
+        if (he != hipSuccess) break;
         knn_topk_kernel<<<(unsigned)rows, kTopkThreads, 0, s>>>(b.S, ld, r0, V, K, b.cand, b.cand_score);
         he = hipGetLastError();
         if (he != hipSuccess) break;
     }
-    (void)rocblas_destroy_handle(h);
-    if (bs != rocblas_status_success) return bail(blas_fail(bs, "GPU build: Gram GEMM"));
-    if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: top-k launch: %s", hipGetErrorString(he)));
+    if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: Gram / top-k launch: %s", hipGetErrorString(he)));
 
     sel<<<(unsigned)V, kSelectThreads, lds, s>>>(static_cast<const char *>(W_dev), row_bytes, K, M0, b.cand,
                                                  b.cand_score, b.fwd, b.fwd_score, b.nfwd);

@@ -211,8 +211,8 @@ constexpr int kSampleEvery = 8;
 // (v_mfma_f32_16x16x32_bf16 for bf16 rows, v_mfma_f32_16x16x4_f32 for fp32
 // rows).  The reduction over the row width runs in stages of kGramKC bytes
 // of each row: both 128-row slices of a stage are staged in LDS (padded
-// rows), the next stage loading into registers while the current one is
-// multiplied.  Lane (r, g) of a wave (r = lane % 16, g = lane / 16) feeds
+// rows), the stages two ahead loading into registers while the current one
+// is multiplied.  Lane (r, g) of a wave (r = lane % 16, g = lane / 16) feeds
 // row r of a 16-row operand with its g-th quarter of the k step, and ends
 // holding rows 4 g + i of column r of each 16 x 16 result.  Every score is
 // the same sequence of products and sums whichever tile computes it.
@@ -236,7 +236,7 @@ __device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 c)
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(kGramThreads) void knn_gram_kernel(const char *__restrict__ W, int64_t V, int row_bytes,
+__global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2))) void knn_gram_kernel(const char *__restrict__ W, int64_t V, int row_bytes,
                                                                 int64_t r0, int64_t rows, float *__restrict__ S,
                                                                 int64_t ld)
 {
@@ -244,7 +244,10 @@ __global__ __launch_bounds__(kGramThreads) void knn_gram_kernel(const char *__re
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t c0 = (int64_t)blockIdx.y * kGramTile, j0 = (int64_t)blockIdx.x * kGramTile;
+    // consecutive workgroups share a tile of rows j (and differ in c), so a
+    // tile of j is read from HBM once per chunk and the chunk's own rows stay
+    // in cache
+    const int64_t c0 = (int64_t)blockIdx.x * kGramTile, j0 = (int64_t)blockIdx.y * kGramTile;
     const int nstage = (row_bytes + kGramKC - 1) / kGramKC;
     const u32x4 zero = {0u, 0u, 0u, 0u};
     // staging: load t of a thread covers staged row (L / 8) of A (L < 1024)
@@ -273,45 +276,54 @@ __global__ __launch_bounds__(kGramThreads) void knn_gram_kernel(const char *__re
     for (int m = 0; m < 4; ++m)
 #pragma unroll
         for (int n = 0; n < 4; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    u32x4 pre[kGramLoads];
-    load_stage(0, pre);
-    for (int st = 0; st < nstage; ++st) {
-        char *buf = smem + (st & 1) * kGramStage;
+    // stages load two ahead: stage st's loads sit in register buffer st % 2
+    // (the loop is unrolled over the buffers, so no load in flight is ever
+    // copied) and in LDS buffer st % 2
+    u32x4 pre[2][kGramLoads];
+    load_stage(0, pre[0]);
+    if (nstage > 1) load_stage(1, pre[1]);
+    for (int st0 = 0; st0 < nstage; st0 += 2) {
 #pragma unroll
-        for (int t = 0; t < kGramLoads; ++t) *reinterpret_cast<u32x4 *>(buf + soff[t]) = pre[t];
-        if (st + 1 < nstage) load_stage(st + 1, pre);
-        __syncthreads();  // the stage is in LDS (and the stage before it is no longer read)
-        const char *A = buf + (wm * 64) * kGramRowPitch;
-        const char *B = buf + (kGramTile + wn * 64) * kGramRowPitch;
-        if constexpr (BF16) {
+        for (int pb = 0; pb < 2; ++pb) {
+            const int st = st0 + pb;
+            if (st >= nstage) break;  // uniform across the workgroup
+            char *buf = smem + pb * kGramStage;
 #pragma unroll
-            for (int kk = 0; kk < kGramKC; kk += 64) {  // 32 bf16 per MFMA step
-                u32x4 a[4], b[4];
+            for (int t = 0; t < kGramLoads; ++t) *reinterpret_cast<u32x4 *>(buf + soff[t]) = pre[pb][t];
+            if (st + 2 < nstage) load_stage(st + 2, pre[pb]);
+            __syncthreads();  // the stage is in LDS (and the stage before it is no longer read)
+            const char *A = buf + (wm * 64) * kGramRowPitch;
+            const char *B = buf + (kGramTile + wn * 64) * kGramRowPitch;
+            if constexpr (BF16) {
 #pragma unroll
-                for (int m = 0; m < 4; ++m)
-                    a[m] = *reinterpret_cast<const u32x4 *>(A + (m * 16 + r) * kGramRowPitch + kk + 16 * g);
+                for (int kk = 0; kk < kGramKC; kk += 64) {  // 32 bf16 per MFMA step
+                    u32x4 a[4], b[4];
 #pragma unroll
-                for (int n = 0; n < 4; ++n)
-                    b[n] = *reinterpret_cast<const u32x4 *>(B + (n * 16 + r) * kGramRowPitch + kk + 16 * g);
+                    for (int m = 0; m < 4; ++m)
+                        a[m] = *reinterpret_cast<const u32x4 *>(A + (m * 16 + r) * kGramRowPitch + kk + 16 * g);
 #pragma unroll
-                for (int m = 0; m < 4; ++m)
+                    for (int n = 0; n < 4; ++n)
+                        b[n] = *reinterpret_cast<const u32x4 *>(B + (n * 16 + r) * kGramRowPitch + kk + 16 * g);
 #pragma unroll
-                    for (int n = 0; n < 4; ++n) acc[m][n] = mfma_bf16(a[m], b[n], acc[m][n]);
-            }
-        } else {
+                    for (int m = 0; m < 4; ++m)
 #pragma unroll
-            for (int kk = 0; kk < kGramKC; kk += 16) {  // 4 floats per MFMA step
-                float a[4], b[4];
+                        for (int n = 0; n < 4; ++n) acc[m][n] = mfma_bf16(a[m], b[n], acc[m][n]);
+                }
+            } else {
 #pragma unroll
-                for (int m = 0; m < 4; ++m)
-                    a[m] = *reinterpret_cast<const float *>(A + (m * 16 + r) * kGramRowPitch + kk + 4 * g);
+                for (int kk = 0; kk < kGramKC; kk += 16) {  // 4 floats per MFMA step
+                    float a[4], b[4];
 #pragma unroll
-                for (int n = 0; n < 4; ++n)
-                    b[n] = *reinterpret_cast<const float *>(B + (n * 16 + r) * kGramRowPitch + kk + 4 * g);
+                    for (int m = 0; m < 4; ++m)
+                        a[m] = *reinterpret_cast<const float *>(A + (m * 16 + r) * kGramRowPitch + kk + 4 * g);
 #pragma unroll
-                for (int m = 0; m < 4; ++m)
+                    for (int n = 0; n < 4; ++n)
+                        b[n] = *reinterpret_cast<const float *>(B + (n * 16 + r) * kGramRowPitch + kk + 4 * g);
 #pragma unroll
-                    for (int n = 0; n < 4; ++n) acc[m][n] = mfma_f32(a[m], b[n], acc[m][n]);
+                    for (int m = 0; m < 4; ++m)
+#pragma unroll
+                        for (int n = 0; n < 4; ++n) acc[m][n] = mfma_f32(a[m], b[n], acc[m][n]);
+                }
             }
         }
     }
@@ -802,12 +814,14 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
         return st;
     };
 
+    if ((V + kGramTile - 1) / kGramTile > 65535)
+        return bail(fail(VIE_EUNSUPPORTED, "GPU build: V = %lld rows exceed the Gram grid", (long long)V));
     auto gram = dtype == VIE_BF16 ? knn_gram_kernel<true> : knn_gram_kernel<false>;
     he = hipFuncSetAttribute((const void *)gram, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kGramStage);
     if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
     for (int64_t r0 = 0; r0 < V; r0 += R) {
         const int64_t rows = std::min(R, V - r0);
-        const dim3 grid((unsigned)((V + kGramTile - 1) / kGramTile), (unsigned)((rows + kGramTile - 1) / kGramTile));
+        const dim3 grid((unsigned)((rows + kGramTile - 1) / kGramTile), (unsigned)((V + kGramTile - 1) / kGramTile));
         gram<<<grid, kGramThreads, 2 * kGramStage, s>>>(static_cast<const char *>(W_dev), V, row_bytes, r0, rows, b.S,
                                                         ld);
         he = hipGetLastError();

@@ -204,7 +204,34 @@ typedef struct {
                              Needs V < 2^26.  A diagnostic: it lets a
                              caller replay and compare a traversal. */
     int32_t trace_cap;    /* entries per query of trace_dev (>= 1 when set) */
+    int32_t team;         /* workgroups that search each query together,
+                             1..32 (0 counts as 1).  Each member keeps the
+                             whole search state and takes every decision
+                             itself, scores only the new nodes whose id
+                             modulo team is its member index, and passes the
+                             scores that can enter the beam to the others
+                             through workspace_dev, so the traversal, the
+                             results and stats are those of team = 1 (a
+                             query's distance evaluations are shared, its
+                             dependent steps are not).  All B * team
+                             workgroups must be resident on the device at
+                             once (else VIE_EUNSUPPORTED).  Should a member
+                             wait for another for seconds (the device kept
+                             busy by other work), the query's row holds
+                             ids -1, logits NaN and stats 0xFFFFFFFF. */
+    void *workspace_dev;  /* team > 1: device buffer of at least
+                             vie_query_workspace() bytes, 256-byte aligned,
+                             caller owned, no initialisation needed; calls
+                             that share it must not overlap in time.
+                             Ignored for team <= 1. */
+    size_t workspace_bytes;
 } vie_search_params;
+
+/* Bytes of device workspace that vie_query_ex / vie_query_forced need with
+ * these arguments (0 unless params->team > 1).
+ * Errors: VIE_EINVAL (as the query would report for its arguments). */
+vie_status vie_query_workspace(const vie_index *index, int32_t B, int32_t k, int32_t ef,
+                               const vie_search_params *params, size_t *bytes);
 
 /* vie_query with a layer-0 step that expands the expand_width best
  * unexpanded beam entries at once (their unvisited neighbours are scored

@@ -268,9 +268,37 @@ vie_status check_params(const vie_search_params *params)
         return fail(VIE_EINVAL, "int8_rows = %d is neither 0 nor 1", params->int8_rows);
     if (params->trace_dev && params->trace_cap < 1)
         return fail(VIE_EINVAL, "trace_cap = %d < 1 with a trace buffer", params->trace_cap);
+    if (params->team < 0 || params->team > kMaxTeam)
+        return fail(VIE_EINVAL, "team = %d outside 0..%d", params->team, kMaxTeam);
+    if (params->team > 1 && !params->workspace_dev) return fail(VIE_EINVAL, "a team search needs workspace_dev");
+    if (params->team > 1 && (uintptr_t)params->workspace_dev % 256)
+        return fail(VIE_EINVAL, "workspace_dev is not 256-byte aligned");
     return VIE_OK;
 }
+
+int team_of(const vie_search_params *params) { return params && params->team > 1 ? params->team : 1; }
 }  // namespace
+
+vie_status vie_query_workspace(const vie_index *ix, int32_t B, int32_t k, int32_t ef,
+                               const vie_search_params *params, size_t *bytes)
+{
+    g_last_error.clear();
+    if (!ix || !params || !bytes) return fail(VIE_EINVAL, "NULL argument");
+    if (params->expand_width < 1 || params->expand_width > 32)
+        return fail(VIE_EINVAL, "expand_width = %d outside 1..32", params->expand_width);
+    if (params->team < 0 || params->team > kMaxTeam)
+        return fail(VIE_EINVAL, "team = %d outside 0..%d", params->team, kMaxTeam);
+    if (vie_status s = check_k(k, ix->g.V, B)) return s;
+    if (ef < 1) return fail(VIE_EINVAL, "ef = %d < 1", ef);
+    HnswLaunch a{};
+    a.B = B;
+    a.M0 = ix->g.M0;
+    a.width = params->expand_width;
+    a.ef_eff = ef > k ? ef : k;
+    a.team = team_of(params);
+    *bytes = hnsw_team_workspace_bytes(a);
+    return VIE_OK;
+}
 
 vie_status vie_quantize_rows(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d, int8_t *q_dev,
                              float *scale_dev, void *hip_stream)
@@ -370,6 +398,14 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
     a.ldo = k + n_forced;
     a.trace = trace;
     a.trace_cap = trace ? params->trace_cap : 0;
+    a.team = team_of(params);
+    if (a.team > 1) {
+        const size_t need = hnsw_team_workspace_bytes(a);
+        if (params->workspace_bytes < need)
+            return fail(VIE_EINVAL, "workspace holds %zu bytes, a team of %d needs %zu", params->workspace_bytes,
+                        a.team, need);
+        a.team_ws = params->workspace_dev;
+    }
     if (int8_rows) {
         if (!ix->dev.q8) return fail(VIE_ESTATE, "no int8 rows attached (call vie_index_attach_int8)");
         a.q8 = ix->dev.q8;

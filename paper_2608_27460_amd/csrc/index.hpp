@@ -19,6 +19,7 @@ constexpr int kMaxK = 1024;       // largest k of any query
 constexpr int kMaxEf = 8192;      // largest beam of the HNSW kernel (LDS permitting)
 constexpr int kMaxD = 8192;       // largest row width
 constexpr int kMaxGpuBuildK = 128;  // candidates per node of the GPU batch build
+constexpr int kMaxTeam = 32;      // workgroups that may search one query together
 
 inline int elem_bytes(int dtype) { return dtype == VIE_F32 ? 4 : 2; }
 
@@ -90,7 +91,10 @@ struct HnswLaunch {
     uint32_t *stats;
     int32_t *trace = nullptr;  // [B][trace_cap] expansion record (nullptr: none)
     int trace_cap = 0;
+    int team = 1;              // workgroups per query (1: one)
+    void *team_ws = nullptr;   // team exchange workspace (hnsw_team_workspace_bytes)
 };
+size_t hnsw_team_workspace_bytes(const HnswLaunch &a);
 // Launchers return VIE_OK, VIE_EUNSUPPORTED for a shape they cannot serve, or
 // VIE_EHIP for a failed launch; the detail goes to set_error().
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s);

@@ -1166,7 +1166,35 @@ struct HnswShared {
     // hnsw_kernel's layer-0 loop: per step parity
     unsigned long long bestp[2];
     uint32_t nnewp[2], nkeepp[2], firstp[2];
+    // hnsw_multi_kernel in a team: new nodes scored by the other members,
+    // and a wait that gave up
+    uint32_t nother;
+    int team_err;
 };
+
+// A team: `size` workgroups search one query together (workgroup
+// q * size + m is member m of query q).  Every member keeps the whole search
+// state and takes every decision itself; each scores only the new nodes n
+// with n % size == m and passes its kept keys to the others through `keys`
+// ([query][3][member][slot] with `slot` entries each) and their number
+// through `tags` ([query][3][member], zero before the launch): at its e-th
+// exchange (from 1) a member publishes (e << 32) | count.  Everything the
+// members pass each other is written with device-scope stores (written
+// through to the device's coherence point) and read with device-scope loads,
+// and a member waits for its own stores to complete before it publishes the
+// count, so no cache needs to be written back or invalidated.
+struct TeamArgs {
+    int size;
+    int slot;
+    uint64_t *keys;
+    uint64_t *tags;
+};
+
+// Waits of a team member at an exchange are bounded (about two seconds):
+// members are launched only when all of them fit on the device at once, so
+// a wait that runs out means the members were not resident together, and
+// the search reports it in its results instead of waiting on.
+constexpr uint32_t kTeamSpin = 1u << 21;
 
 // p rounded up to 16 bytes past base (base 16-byte aligned), by pointer
 // arithmetic only: a pointer into LDS keeps its address space, so the
@@ -1695,7 +1723,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
     const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
     uint32_t *__restrict__ stats, const int8_t *__restrict__ q8, const float *__restrict__ q8scale,
-    int32_t *__restrict__ trace_all, int trace_cap)
+    int32_t *__restrict__ trace_all, int trace_cap, TeamArgs team)
 {
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
@@ -1703,9 +1731,12 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     __shared__ int32_t s_pick[kMaxWidth];  // this step's picks (beam positions)
     __shared__ int32_t s_np, s_after;
     __shared__ uint32_t s_hmax;           // Q8: bits of max |h|
+    __shared__ uint32_t s_xoff[kMaxTeam + 1];  // team exchange: where each member's keys go
     constexpr int kGroups = NT / G;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
-    const int q = blockIdx.x;
+    const int T = team.size;              // 1: one workgroup per query
+    const int q = blockIdx.x / T, mem = blockIdx.x - q * T;
+    uint32_t exchanges = 0;               // team exchanges so far
     const int hbytes = (row_bytes + 15) & ~15;
     const int vwords = (int)((V + 31) / 32);
     const int cap = width * M0;  // most nodes claimed in one step
@@ -1713,7 +1744,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     // list entries a group keeps per lane (as in hnsw_kernel: enough for
     // M0 = 64 at every group width)
     constexpr int PF = G >= 64 ? 1 : G >= 32 ? 2 : kPfbPerLane;
-    const bool cache_on = M0 <= PF * G;
+    const bool cache_on = M0 <= PF * G && T == 1;  // a member scores only its share of the rows
     const int d = row_bytes / (BF16 ? 2 : 4);
     const int d8 = Q8 ? (d + 15) & ~15 : 0;
     // LDS carve-up (sizes mirror hnsw_multi_lds_bytes)
@@ -1747,6 +1778,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     if (tid == 0) {
         sh.best = 0;
         s_hmax = 0;
+        sh.nother = 0;
+        sh.team_err = 0;
     }
     if (tid < kMaxWidth) lc_id[tid] = -1;
     __syncthreads();
@@ -1762,9 +1795,61 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int gl = tid % G;
     const int grp = tid / G;
     uint32_t n_dist = 0, n_expand = 0;
-    int32_t *trace = trace_all ? trace_all + (int64_t)q * trace_cap : nullptr;
+    int32_t *trace = trace_all && mem == 0 ? trace_all + (int64_t)q * trace_cap : nullptr;
     uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
                                                    vis, sh, n_dist, n_expand, trace, trace_cap);
+
+    // A team exchange: this member's `mine` keys (already in its slot of
+    // area `area`) meet the other members' keys, appended to dst after the
+    // `*n` already there.  Steps alternate between areas 0 and 1: a member
+    // can only be one exchange ahead of the slowest, so it never overwrites
+    // keys still being read.
+    auto exchange = [&](int area, uint32_t mine, uint64_t *dst, uint32_t *n) {
+        const int64_t base = ((int64_t)q * 3 + area) * T;
+        const uint32_t tag = ++exchanges;
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's key stores are complete
+        __syncthreads();
+        if (tid == 0)
+            __hip_atomic_store(team.tags + base + mem, ((uint64_t)tag << 32) | mine, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        // wave 0: lane o waits (bounded) for member o's count, then the
+        // running sums say where each member's keys go
+        if (tid < kWave) {
+            uint32_t c = 0u;
+            if (lane < T && lane != mem) {
+                uint32_t spins = 0;
+                for (;;) {
+                    const uint64_t w =
+                        __hip_atomic_load(team.tags + base + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if ((uint32_t)(w >> 32) == tag) {
+                        c = (uint32_t)w;
+                        break;
+                    }
+                    if (++spins > kTeamSpin) {
+                        sh.team_err = 1;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            const uint32_t incl = wave_incl_scan(c);
+            if (lane < T) s_xoff[lane + 1] = incl;
+            if (lane == 0) s_xoff[0] = 0;
+        }
+        __syncthreads();
+        if (sh.team_err) return;
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        const int total = (int)s_xoff[T];
+        for (int j = tid; j < total; j += NT) {
+            int o = 0;  // the member whose keys hold entry j
+            while ((int)s_xoff[o + 1] <= j) ++o;
+            const uint64_t *ok = team.keys + (base + o) * team.slot;
+            dst[mine + j] = __hip_atomic_load(ok + (j - (int)s_xoff[o]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (tid == 0) *n = mine + (uint32_t)total;
+        __syncthreads();
+    };
 
     if constexpr (Q8) {  // the layer-0 entry point scored again on its int8 row
         if (grp == 0) {
@@ -1866,11 +1951,16 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             const int32_t ec = src >= 0 ? lcache[max(src, 0) * M0 + slot] : -1;
             const int32_t eg = src < 0 ? adj0[(int64_t)c * M0 + slot] : -1;
             const int32_t e = src >= 0 ? ec : eg;
-            if (e >= 0 && claim(vis, e)) cid[atomicAdd(&sh.nnew, 1u)] = e;
+            if (e >= 0 && claim(vis, e)) {
+                if (e % T == mem) cid[atomicAdd(&sh.nnew, 1u)] = e;
+                else atomicAdd(&sh.nother, 1u);
+            }
         }
         __syncthreads();
-        const int nn = (int)sh.nnew;
-        n_dist += nn;
+        const int nn = (int)sh.nnew;  // this member's share of the new nodes
+        n_dist += nn + sh.nother;
+        const int area = (int)(exchanges & 1);
+        uint64_t *xk = T > 1 ? team.keys + (((int64_t)q * 3 + area) * T + mem) * team.slot : nullptr;
         const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
         // score the new rows, two per group at a time; keep the keys that
         // can enter the beam, and the lists of a group's first rows
@@ -1902,8 +1992,16 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 row_dot2<VEC, BF16, G>(W, ea, eb, row_bytes, hs, gl, sa, sb);
             }
             const uint64_t ka = make_key(sa, ea), kb = eb >= 0 ? make_key(sb, eb) : 0ull;
-            if (gl == 0 && ka > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = ka;
-            if (gl == 0 && eb >= 0 && kb > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = kb;
+            if (gl == 0 && ka > worst) {
+                const uint32_t slot = atomicAdd(&sh.nkeep, 1u);
+                ckey[slot] = ka;
+                if (xk) __hip_atomic_store(xk + slot, ka, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (gl == 0 && eb >= 0 && kb > worst) {
+                const uint32_t slot = atomicAdd(&sh.nkeep, 1u);
+                ckey[slot] = kb;
+                if (xk) __hip_atomic_store(xk + slot, kb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
 #pragma unroll
             for (int x = 0; x + 1 < kMultiHeld; x += 2)
                 if (x == r) {
@@ -1918,6 +2016,10 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         }
         if (tid == 0) sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
         __syncthreads();
+        if (T > 1) {  // the kept keys of the other members join this member's
+            exchange(area, sh.nkeep, ckey, &sh.nkeep);
+            if (sh.team_err) break;
+        }
         const int nk = (int)sh.nkeep;
         // with more than 64 kept keys, each wave sorts a run of 64 of them, so
         // that a key's rank among the kept keys is a sum of binary searches
@@ -1966,6 +2068,9 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         // merge the beam and the kept keys (as in the sequential kernel); the
         // picks are marked expanded, and the new first unexpanded entry is
         // the best kept key or the entry after the picks
+        // (the claimed ids are spent: cid[r] receives the beam position of
+        // the kept key of rank r, non-decreasing in r, so that a beam entry's
+        // count of larger kept keys is one binary search)
         const int total = min((int)nbeam + nk, ef);
         for (int j = tid; j < nk; j += NT) {
             const uint64_t key = ckey[j];
@@ -1975,6 +2080,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 const int mid = (lo + hi) >> 1;
                 if (beam[mid] > key) lo = mid + 1; else hi = mid;
             }
+            cid[above] = lo;
             const int pos = lo + above;
             if (pos < total) {
                 beam2[pos] = key;
@@ -1984,10 +2090,16 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
             }
         }
+        __syncthreads();
         const int after = s_after;
-        for (int i = (tid + NT / 2) % NT; i < (int)nbeam; i += NT) {  // the other half of the workgroup
+        for (int i = tid; i < (int)nbeam; i += NT) {
             const uint64_t key = beam[i];
-            const int pos = i + kept_above(key);
+            int lo = 0, hi = nk;  // kept keys whose beam position is <= i lie above beam[i]
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (cid[mid] <= i) lo = mid + 1; else hi = mid;
+            }
+            const int pos = i + lo;
             if (pos < total) {
                 beam2[pos] = key;
                 flag2[pos] = flag[i] & 1;  // older cache slots are stale
@@ -1997,6 +2109,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (tid == 0) {
             sh.nbeam = (uint32_t)total;
             sh.nnew = 0;  // read after the claim barrier only
+            sh.nother = 0;
         }
         __syncthreads();
         uint64_t *tb = beam;
@@ -2008,18 +2121,75 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     }
 
     const int nb = (int)sh.nbeam;
+    if (sh.team_err) {  // a team wait ran out: the results say so
+        if (mem == 0) {
+            for (int t = tid; t < k; t += NT) {
+                ids[(int64_t)q * ldo + t] = -1;
+                logits[(int64_t)q * ldo + t] = __builtin_nanf("");
+            }
+            if (stats && tid == 0) stats[2 * q] = stats[2 * q + 1] = 0xFFFFFFFFu;
+        }
+        return;
+    }
     if constexpr (Q8) {
-        // exact re-rank of the final beam: exact keys into beam2, then by rank
-        for (int j = grp; j < nb; j += kGroups) {
-            const int32_t e = key_id(beam[j]);
-            const float sc = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
-            if (gl == 0) beam2[j] = make_key(sc, e);
+        // exact re-rank of the final beam: exact keys into beam2, then by
+        // rank; in a team each member scores the entries of its share and
+        // the first member gathers all of them
+        if (T == 1) {
+            for (int j = grp; j < nb; j += kGroups) {
+                const int32_t e = key_id(beam[j]);
+                const float sc = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
+                if (gl == 0) beam2[j] = make_key(sc, e);
+            }
+        } else {
+            if (tid == 0) sh.nkeep = 0;
+            __syncthreads();
+            uint64_t *xr = team.keys + (((int64_t)q * 3 + 2) * T + mem) * team.slot;
+            for (int j = grp; j < nb; j += kGroups) {
+                const int32_t e = key_id(beam[j]);
+                if (e % T != mem) continue;
+                const float sc = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
+                if (gl == 0) {
+                    const uint32_t slot = atomicAdd(&sh.nkeep, 1u);
+                    beam2[slot] = make_key(sc, e);
+                    __hip_atomic_store(xr + slot, make_key(sc, e), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            __syncthreads();
+            exchange(2, sh.nkeep, beam2, &sh.nkeep);
+            if (mem != 0) return;
+            if (sh.team_err) {
+                for (int t = tid; t < k; t += NT) {
+                    ids[(int64_t)q * ldo + t] = -1;
+                    logits[(int64_t)q * ldo + t] = __builtin_nanf("");
+                }
+                if (stats && tid == 0) stats[2 * q] = stats[2 * q + 1] = 0xFFFFFFFFu;
+                return;
+            }
+        }
+        __syncthreads();
+        // rank the exact keys: each wave sorts runs of 64, a key's rank is
+        // the sum of its binary-search positions in the runs (stopped once
+        // it reaches k)
+        const int nrun = (nb + kWave - 1) / kWave;
+        for (int r = tid / kWave; r < nrun; r += NT / kWave) {
+            const int j = r * kWave + lane;
+            const uint64_t key = wave_sort_desc(j < nb ? beam2[j] : 0ull, lane);
+            if (j < nb) beam2[j] = key;  // the run's real keys are its largest
         }
         __syncthreads();
         for (int t = tid; t < nb; t += NT) {
             const uint64_t key = beam2[t];
             int rank = 0;
-            for (int j = 0; j < nb; ++j) rank += beam2[j] > key;
+            for (int r = 0; r < nrun && rank < k; ++r) {
+                const uint64_t *run = beam2 + r * kWave;
+                int lo = 0, hi = min(kWave, nb - r * kWave);
+                while (lo < hi) {
+                    const int mid = (lo + hi) >> 1;
+                    if (run[mid] > key) lo = mid + 1; else hi = mid;
+                }
+                rank += lo;
+            }
             if (rank < k) {
                 ids[(int64_t)q * ldo + rank] = key_id(key);
                 logits[(int64_t)q * ldo + rank] = key_logit(key);
@@ -2030,6 +2200,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             logits[(int64_t)q * ldo + t] = -__builtin_inff();
         }
     } else {
+        if (mem != 0) return;
         for (int t = tid; t < k; t += NT) {
             ids[(int64_t)q * ldo + t] = t < nb ? key_id(beam[t]) : -1;
             logits[(int64_t)q * ldo + t] = t < nb ? key_logit(beam[t]) : -__builtin_inff();
@@ -2432,20 +2603,71 @@ size_t hnsw_lds_limit()
 }
 
 namespace {
+__global__ void team_clear_kernel(uint64_t *__restrict__ tags, int n)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) tags[i] = 0ull;
+}
+
+// Keys a member passes at one exchange: the most new nodes of a step, or a
+// whole beam (the final re-rank).
+int team_slot(const HnswLaunch &a) { return std::max(a.width * a.M0, a.ef_eff); }
+
+size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// The team workspace: keys [B][3][team][slot] u64, then the published
+// counts [B][3][team] u64, each 256-byte aligned.
+TeamArgs team_layout(void *ws, int B, int team, int slot)
+{
+    char *p = static_cast<char *>(ws);
+    TeamArgs t;
+    t.size = team;
+    t.slot = slot;
+    t.keys = reinterpret_cast<uint64_t *>(p);
+    p += round256((size_t)B * 3 * team * slot * 8);
+    t.tags = reinterpret_cast<uint64_t *>(p);
+    return t;
+}
+}  // namespace
+
+size_t hnsw_team_workspace_bytes(const HnswLaunch &a)
+{
+    if (a.team <= 1) return 0;
+    const int slot = team_slot(a);
+    return round256((size_t)a.B * 3 * a.team * slot * 8) + round256((size_t)a.B * 3 * a.team * 8);
+}
+
+namespace {
 template <int NT, int VEC, bool BF16, int G>
 hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
 {
-    if (a.width > 1 || a.q8) {
+    if (a.width > 1 || a.q8 || a.team > 1) {
         auto kern = a.q8 ? hnsw_multi_kernel<NT, VEC, BF16, G, true> : hnsw_multi_kernel<NT, VEC, BF16, G, false>;
         if (lds > 64 * 1024) {
             hipError_t e =
                 hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
             if (e != hipSuccess) return e;
         }
-        kern<<<a.B, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0, a.M0,
-                                   a.upper_off, a.upper, a.M, a.maxlevel, a.entry, static_cast<const char *>(a.h),
-                                   a.k, a.ef_eff, a.width, a.ids, a.logits, a.ldo, a.stats, a.q8, a.q8scale,
-                                   a.trace, a.trace_cap);
+        TeamArgs team{1, 0, nullptr, nullptr};
+        if (a.team > 1) {
+            // every member of every query must be resident at once
+            int per = 0, dev = 0, cus = 0;
+            hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, NT, lds);
+            if (e == hipSuccess) e = hipGetDevice(&dev);
+            if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+            if (e != hipSuccess) return e;
+            if ((int64_t)per * cus < (int64_t)a.B * a.team) return hipErrorCooperativeLaunchTooLarge;
+            team = team_layout(a.team_ws, a.B, a.team, team_slot(a));
+            const int ntag = a.B * 3 * a.team;
+            team_clear_kernel<<<(ntag + 255) / 256, 256, 0, s>>>(team.tags, ntag);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        kern<<<a.B * team.size, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0,
+                                               a.M0, a.upper_off, a.upper, a.M, a.maxlevel, a.entry,
+                                               static_cast<const char *>(a.h), a.k, a.ef_eff, a.width, a.ids,
+                                               a.logits, a.ldo, a.stats, a.q8, a.q8scale, a.trace, a.trace_cap,
+                                               team);
         return hipGetLastError();
     }
     auto kern = hnsw_kernel<NT, VEC, BF16, G>;
@@ -2468,7 +2690,7 @@ hipError_t hnsw_launch_g(const HnswLaunch &a, size_t lds, hipStream_t s)
 {
     const int nchunk = a.d * elem_bytes(a.dtype) / VEC;
     constexpr int CPL = RowCpl<BF16>::value;
-    const bool wide = a.B < kHnswWideBatch;
+    const bool wide = (int64_t)a.B * a.team < kHnswWideBatch;
     if (nchunk <= 16 * CPL)
         return wide ? hnsw_launch<1024, VEC, BF16, 16>(a, lds, s) : hnsw_launch<256, VEC, BF16, 16>(a, lds, s);
     if (nchunk <= 32 * CPL)
@@ -2527,7 +2749,10 @@ vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
 {
     if (a.width < 1 || a.width > kMaxWidth)
         return fail(VIE_EUNSUPPORTED, "HNSW search: expansion width %d outside 1..%d", a.width, kMaxWidth);
-    const bool multi = a.width > 1 || a.q8;
+    if (a.team < 1 || a.team > kMaxTeam)
+        return fail(VIE_EUNSUPPORTED, "HNSW search: team of %d workgroups outside 1..%d", a.team, kMaxTeam);
+    if (a.team > 1 && !a.team_ws) return fail(VIE_EINVAL, "a team search needs its workspace");
+    const bool multi = a.width > 1 || a.q8 || a.team > 1;
     const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8)
                              : hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
     const size_t lim = hnsw_lds_limit();
@@ -2544,6 +2769,9 @@ vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
     else if (vec == 8) e = bf ? hnsw_launch_g<8, true>(a, lds, s) : hnsw_launch_g<8, false>(a, lds, s);
     else if (vec == 4) e = bf ? hnsw_launch_g<4, true>(a, lds, s) : hnsw_launch_g<4, false>(a, lds, s);
     else e = hnsw_launch_g<2, true>(a, lds, s);
+    if (e == hipErrorCooperativeLaunchTooLarge)
+        return fail(VIE_EUNSUPPORTED, "a team of %d workgroups for each of %d queries does not fit on the device at once",
+                    a.team, a.B);
     return launched(e, "HNSW search launch");
 }
 

@@ -27,7 +27,8 @@ class VieError(RuntimeError):
 
 class SearchParams(C.Structure):
     _fields_ = [("expand_width", C.c_int32), ("int8_rows", C.c_int32), ("trace_dev", C.c_void_p),
-                ("trace_cap", C.c_int32)]
+                ("trace_cap", C.c_int32), ("team", C.c_int32), ("workspace_dev", C.c_void_p),
+                ("workspace_bytes", C.c_size_t)]
 
 
 class BuildParams(C.Structure):
@@ -64,6 +65,7 @@ def _load() -> C.CDLL:
         "vie_query": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp]),
         "vie_query_ex": (st, [vp, vp, i32, i32, i32, vp, vp, vp, vp, vp]),
         "vie_query_forced": (st, [vp, vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, vp]),
+        "vie_query_workspace": (st, [vp, i32, i32, i32, vp, C.POINTER(sz)]),
         "vie_quantize_rows": (st, [vp, i32, i64, i32, vp, vp, vp]),
         "vie_index_attach_int8": (st, [vp, vp, vp]),
         "vie_dense_topk_workspace": (st, [i64, i32, i32, i32, C.POINTER(sz)]),
@@ -204,38 +206,53 @@ class Index:
         _check(lib.vie_index_attach_int8(self._h, _dev_ptr(q, "q"), _dev_ptr(scale, "scale")))
         self._q8 = (q, scale)
 
+    def _params(self, h, B: int, k: int, ef: int, width: int, int8: bool, trace, team: int) -> SearchParams:
+        prm = SearchParams(width, int(int8), None if trace is None else _dev_ptr(trace, "trace"),
+                           0 if trace is None else trace.shape[1], team, None, 0)
+        if team > 1:
+            n = C.c_size_t()
+            _check(lib.vie_query_workspace(self._h, B, k, ef, C.byref(prm), C.byref(n)))
+            ws = getattr(self, "_team_ws", None)
+            if ws is None or ws.numel() < n.value or ws.device != h.device:
+                ws = _torch().empty(n.value, dtype=_torch().uint8, device=h.device)
+                self._team_ws = ws
+            prm.workspace_dev = _dev_ptr(ws, "workspace")
+            prm.workspace_bytes = ws.numel()
+        return prm
+
     def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1, int8: bool = False,
-                   trace=None) -> None:
+                   trace=None, team: int = 1) -> None:
         """HNSW top-k of h [B, d] into preallocated ids int32 [B, k], logits fp32 [B, k]
         (and stats uint32-as-int32 [B, 2]) on the current stream; width > 1
         expands that many beam entries per layer-0 step, int8 walks layer 0 on
         the attached int8 rows, trace (int32 [B, cap]) receives each query's
-        expansions as (layer << 27) | node (vie_query_ex)."""
+        expansions as (layer << 27) | node, team > 1 searches each query with
+        that many workgroups (vie_query_ex; the index keeps the team
+        workspace, so team searches of one index must not overlap in time)."""
         B = h.shape[0]
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        if width == 1 and not int8 and trace is None:
+        if width == 1 and not int8 and trace is None and team <= 1:
             _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"),
                                  _dev_ptr(logits, "logits"), sp, _stream(h)))
         else:
-            prm = SearchParams(width, int(int8), None if trace is None else _dev_ptr(trace, "trace"),
-                               0 if trace is None else trace.shape[1])
+            prm = self._params(h, B, k, ef, width, int8, trace, team)
             _check(lib.vie_query_ex(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
     def query_forced_into(self, h, k: int, ef: int, forced, ids, logits, stats=None, width: int = 1,
-                          int8: bool = False) -> None:
+                          int8: bool = False, team: int = 1) -> None:
         """Search plus the forced-inclusion ids (int32 device tensor [n]):
         ids int32 [B, k + n], logits fp32 [B, k + n] (vie_query_forced)."""
         B = h.shape[0]
         n = int(forced.numel())
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        prm = SearchParams(width, int(int8), None, 0)
+        prm = self._params(h, B, k, ef, width, int8, None, team)
         fp = _dev_ptr(forced, "forced") if n else None
         _check(lib.vie_query_forced(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), fp, n, _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
     def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1, int8: bool = False,
-              trace_cap: int = 0):
+              trace_cap: int = 0, team: int = 1):
         """(ids, logits), plus stats if asked, plus the expansion trace
         [B, trace_cap] (-1 past the last expansion) if trace_cap > 0."""
         torch = _torch()
@@ -246,7 +263,7 @@ class Index:
         lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
         st = torch.empty((B, 2), dtype=torch.int32, device=h.device) if stats else None
         tr = torch.full((B, trace_cap), -1, dtype=torch.int32, device=h.device) if trace_cap > 0 else None
-        self.query_into(h, k, ef, ids, lg, st, width, int8, tr)
+        self.query_into(h, k, ef, ids, lg, st, width, int8, tr, team)
         out = (ids, lg) + ((st,) if stats else ())
         return out + (tr,) if tr is not None else out
 

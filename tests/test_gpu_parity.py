@@ -206,7 +206,7 @@ def _load_on_gpu(vie, g, W, dtype, tmp):
     return ix
 
 
-def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None):
+def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None, team=1):
     """One launch of the search variant (width expansions per layer-0 step;
     int8 = the oracle's (rows, scales) when layer 0 walks int8 rows) against
     the oracle's search of the same variant on the same graph.  A query
@@ -222,7 +222,7 @@ def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None):
     ef_eff = max(ef, k)
     cap = ef_eff + 1024
     h = dev_tensor(vie, H, dtype)
-    ids, lg, st, tr = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None, trace_cap=cap)
+    ids, lg, st, tr = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None, trace_cap=cap, team=team)
     torch.cuda.synchronize()
     ids, lg, st, tr = (ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32),
                        tr.cpu().numpy())
@@ -304,6 +304,58 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
             ids, st, _ = _compare_hnsw(vie, ix, W, synth.BF16, g, H, k, ef, what, width=width)
             say("  %s recall@k=%.3f mean n_dist=%.0f n_expand=%.1f" %
                 (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
+
+
+@pytest.mark.parametrize("team", [2, 3, 8])
+def test_hnsw_team_equals_one_workgroup(vie, team):
+    """A team of workgroups per query (each scoring its share of the new
+    nodes, all exchanging the keys that can enter the beam) walks the same
+    path as one workgroup: ids, logits, stats and expansion records are
+    bitwise those of team = 1, for the sequential and wide steps on bf16
+    and int8 rows, and the team's search matches the oracle."""
+    V, d = 6000, 96
+    W = synth.make_w(V, d, synth.BF16, 1880)
+    H, _ = synth.make_queries(W, synth.BF16, 24, 1881)
+    g = O.hnsw_build(W, synth.BF16, 8, 40, 5)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
+    h = dev_tensor(vie, H, synth.BF16)
+    oq, osc = O.quantize_rows(W, synth.BF16)
+    q8, sc = vie.quantize_rows(ix._W_dev, synth.BF16)
+    for int8 in (False, True):
+        ix.attach_int8(q8, sc) if int8 else ix.attach_int8(None, None)
+        for width in (1, 8, 32):
+            for k, ef in [(10, 10), (50, 200), (50, 600)]:
+                what = "team=%d int8=%d width=%d k=%d ef=%d" % (team, int8, width, k, ef)
+                say(what)
+                one = ix.query(h, k, ef, stats=True, width=width, int8=int8, trace_cap=ef + 1024)
+                many = ix.query(h, k, ef, stats=True, width=width, int8=int8, trace_cap=ef + 1024, team=team)
+                torch.cuda.synchronize()
+                for a, b, name in zip(one, many, ("ids", "logits", "stats", "trace")):
+                    a, b = a.cpu().numpy(), b.cpu().numpy()
+                    assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), "%s: %s differ" % (what, name)
+        _compare_hnsw(vie, ix, W, synth.BF16, g, H, 50, 200, "team=%d int8=%d vs oracle" % (team, int8), width=8,
+                      int8=(oq, osc) if int8 else None, team=team)
+    ix.attach_int8(None, None)
+    # one query after a batch: the arrival counters start again from zero
+    a = ix.query(h[:1], 10, 50, team=team)
+    b = ix.query(h[:1], 10, 50)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_hnsw_team_too_large_is_refused(vie):
+    """More team workgroups than the device holds at once: refused before
+    any launch (a member would otherwise wait for one never scheduled)."""
+    V, d = 3000, 64
+    W = synth.make_w(V, d, synth.BF16, 1890)
+    g = O.hnsw_build(W, synth.BF16, 8, 40, 5)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
+    H, _ = synth.make_queries(W, synth.BF16, 4096, 1891)
+    with pytest.raises(vie.VieError) as e:
+        ix.query(dev_tensor(vie, H, synth.BF16), 10, 50, team=32)
+    assert e.value.status == vie.EUNSUPPORTED
 
 
 @pytest.mark.parametrize("case", ["first64", "overlap", "max", "width4", "none"])

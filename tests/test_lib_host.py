@@ -160,6 +160,27 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # int8_rows
     prm = vie.SearchParams(1, 0, fake, 0)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # trace_cap
+    prm = vie.SearchParams(1, 0, None, 0, 33)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # team 33
+    prm = vie.SearchParams(1, 0, None, 0, 4)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # no workspace
+    prm = vie.SearchParams(1, 0, None, 0, 4, C.c_void_p(4096 + 8), 1 << 30)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # misaligned
+    n = C.c_size_t()
+    for team, want in [(0, 0), (1, 0), (4, None)]:
+        prm = vie.SearchParams(8, 0, None, 0, team)
+        assert L.vie_query_workspace(ix._h, 3, 10, 20, C.byref(prm), C.byref(n)) == vie.OK
+        if want is not None:
+            assert n.value == want
+        else:  # keys and published counts, each 256-byte aligned
+            slot = max(8 * ix.info()["M0"], 20)
+            up = lambda b: (b + 255) // 256 * 256  # noqa: E731
+            assert n.value == up(3 * 3 * 4 * slot * 8) + up(3 * 3 * 4 * 8)
+    prm = vie.SearchParams(1, 0, None, 0, 4, C.c_void_p(4096 * 16), 16)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.ESTATE
+    prm = vie.SearchParams(1, 0, None, 0, 40)
+    assert L.vie_query_workspace(ix._h, 3, 10, 20, C.byref(prm), C.byref(n)) == vie.EINVAL
+    assert L.vie_query_workspace(ix._h, 3, 10, 20, None, C.byref(n)) == vie.EINVAL
     assert L.vie_index_attach_int8(ix._h, fake, fake) == vie.ESTATE  # not on a device
     assert L.vie_index_attach_int8(ix._h, fake, None) == vie.EINVAL
     assert L.vie_quantize_rows(fake, 0, 0, 8, fake, fake, None) == vie.EINVAL     # V

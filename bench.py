@@ -7,10 +7,12 @@ queries served one per call (B = 1), HNSW graph with M = 32 (M0 = 64),
 ef_construction = 200, built by the library on the host CPUs.
 
 The beam width is the one the method needs: for each traversal (the
-sequential search; 8 or 32 expansions per step; 8, 16 or 32 per step on int8
-rows with the exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
+sequential search; 8 or 32 expansions per step; 8, 16, 32 or 64 per step on
+int8 rows with the exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
 0.95 on the first 128 queries (recall against the exact dense head, itself
-parity-tested against the oracle).  The fastest of them at its ef is the
+parity-tested against the oracle).  The team traversals (16 workgroups
+sharing each query's row scoring) walk exactly the path of their
+one-workgroup twin and take its ef.  The fastest of them at its ef is the
 headline traversal.
 
 A step is 128 queries, each a call of the head at B = 1 on one stream: the
@@ -49,22 +51,35 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SRC = os.path.join(ROOT, "paper_2608_27460_amd", "csrc", "kernels.hip")
 NODE_MASK = (1 << 26) - 1
 
-TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0)
-    "sequential": (1, False),
-    "width8": (8, False),
-    "width32": (32, False),
-    "int8_width8": (8, True),
-    "int8_width16": (16, True),
-    "int8_width32": (32, True),
+TEAM = 16  # workgroups per query of the team traversals
+TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0, workgroups per query)
+    "sequential": (1, False, 1),
+    "width8": (8, False, 1),
+    "width32": (32, False, 1),
+    "int8_width8": (8, True, 1),
+    "int8_width16": (16, True, 1),
+    "int8_width32": (32, True, 1),
+    "int8_width64": (64, True, 1),
+    "width32_team%d" % TEAM: (32, False, TEAM),
+    "int8_width16_team%d" % TEAM: (16, True, TEAM),
+    "int8_width32_team%d" % TEAM: (32, True, TEAM),
+    "int8_width64_team%d" % TEAM: (64, True, TEAM),
 }
 
 
+def solo_of(trav):
+    """The one-workgroup traversal a team traversal reproduces exactly."""
+    width, int8, _ = TRAVERSALS[trav]
+    return next(t for t, v in TRAVERSALS.items() if v == (width, int8, 1))
+
+
 def kernel_of(trav):
-    width, int8 = TRAVERSALS[trav]
-    if width == 1 and not int8:
+    width, int8, team = TRAVERSALS[trav]
+    if width == 1 and not int8 and team == 1:
         return "hnsw_kernel"
-    return "hnsw_multi_kernel (%s rows, %d per step%s)" % ("int8" if int8 else "stored", width,
-                                                          ", exact re-rank" if int8 else "")
+    return "hnsw_multi_kernel (%s rows, %d per step%s%s)" % (
+        "int8" if int8 else "stored", width, ", exact re-rank" if int8 else "",
+        ", %d workgroups per query" % team if team > 1 else "")
 
 
 def measured_traffic(workload):
@@ -271,8 +286,8 @@ def main() -> int:
     exact_ids = ex_ids.cpu().numpy()
 
     def search_into(index, trav, ef, q, ids_, lg_, st_=None, trace=None):
-        width, int8 = TRAVERSALS[trav]
-        index.query_into(hv[q], k, ef, ids_, lg_, st_, width, int8, trace)
+        width, int8, team = TRAVERSALS[trav]
+        index.query_into(hv[q], k, ef, ids_, lg_, st_, width, int8, trace, team)
 
     # ---- each traversal's beam width for the recall target ----------------
     nc = min(Q, args.calib_queries)
@@ -284,6 +299,16 @@ def main() -> int:
             chosen[trav] = args.ef
             continue
         tried = {}
+        if TRAVERSALS[trav][2] > 1:  # the same results as its one-workgroup twin: time it at that ef
+            ef = chosen.get(solo_of(trav))
+            if ef:
+                us = back_to_back(lambda c: search_into(ix, trav, ef, c, ci[c:c + 1], cl[c:c + 1]), nc)
+                r = recall(ci.cpu().numpy(), exact_ids[:nc])
+                tried[str(ef)] = {"us_per_query": round(us, 2), "recall_at_k": round(r, 4)}
+                chosen[trav] = ef
+            calib[trav] = {"ef": ef, "tried": tried, "same_results_as": solo_of(trav)}
+            log("[bench] %s: ef %s (as %s)" % (trav, ef, solo_of(trav)))
+            continue
         for ef in args.ef_ladder:
             if ef < k:
                 continue
@@ -303,7 +328,7 @@ def main() -> int:
     if args.traversal:
         head_trav = args.traversal
     elif args.ef:
-        head_trav = "int8_width32" if "int8_width32" in travs else "width32"
+        head_trav = "int8_width32_team%d" % TEAM if qrows is not None else "width32_team%d" % TEAM
     else:
         head_trav = min(reachable, key=lambda t: calib[t]["tried"][str(chosen[t])]["us_per_query"])
     ef = chosen[head_trav]
@@ -327,7 +352,7 @@ def main() -> int:
     cap = max(ef, k) + 1024
     trace = torch.full((Q, cap), -1, dtype=torch.int32, device=dev)
     for q0 in range(0, Q, 256):
-        width, int8 = TRAVERSALS[head_trav]
+        width, int8, _ = TRAVERSALS[head_trav]
         ix.query_into(Hd[q0:q0 + 256], k, ef, hi[q0:q0 + 256], hl[q0:q0 + 256], hs[q0:q0 + 256], width, int8,
                       trace[q0:q0 + 256])
     head_ids, head_lg = hi.cpu().numpy(), hl.cpu().numpy()
@@ -379,7 +404,7 @@ def main() -> int:
     up_exp, l0_exp, nd_up = lc[:, 0], lc[:, 1], lc[:, 2]
     assert np.array_equal(up_exp + l0_exp, ne), "expansion records disagree with the counters"
     lists = up_exp * M * 4 + l0_exp * M0 * 4
-    width, int8 = TRAVERSALS[head_trav]
+    width, int8, team = TRAVERSALS[head_trav]
     if int8:
         nd_l0 = nd - nd_up
         head_bytes = nd_up * wl.d * s + nd_l0 * (wl.d + 4) + np.minimum(max(ef, k), nd_l0) * wl.d * s + lists
@@ -414,9 +439,9 @@ def main() -> int:
                 q32, s32 = vie.quantize_rows(W32d, synth.F32)
                 ix32.attach_int8(q32, s32)
             f_i, f_l, _ = out_bufs(n32)
-            fw, f8 = TRAVERSALS[f_trav]
+            fw, f8, ft = TRAVERSALS[f_trav]
             hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None, fw,
-                                                        f8), n32)
+                                                        f8, None, ft), n32)
             legs["fp32_rows"] = {
                 "W_bytes": wl.V * wl.d * 4, "queries": n32, "dense_us_per_query": pct(dcalls),
                 "dense_hbm_frac": round(wl.V * wl.d * 4 / (np.median(dcalls) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
@@ -433,12 +458,14 @@ def main() -> int:
                 ncall = min(Q // Bc, 64)
                 bi, bl, _ = out_bufs(ncall * Bc)
                 hb = [Hd[c * Bc:(c + 1) * Bc] for c in range(ncall)]
-                w8, i8 = TRAVERSALS[head_trav]
+                w8, i8, tm = TRAVERSALS[head_trav]
+                tm = max(1, min(tm, 128 // Bc))  # the team shrinks as the batch grows (all resident at once)
                 h_call = back_to_back(lambda c: ix.query_into(hb[c], k, ef, bi[c * Bc:(c + 1) * Bc],
-                                                              bl[c * Bc:(c + 1) * Bc], None, w8, i8), ncall)
+                                                              bl[c * Bc:(c + 1) * Bc], None, w8, i8, None, tm),
+                                      ncall)
                 d_call = back_to_back(lambda c: vie.dense_topk_into(Wd, hb[c], k, bi[c * Bc:(c + 1) * Bc],
                                                                     bl[c * Bc:(c + 1) * Bc], dense.workspace), ncall)
-                bs[str(Bc)] = {"hnsw_us_per_call": round(h_call, 2), "dense_us_per_call": round(d_call, 2),
+                bs[str(Bc)] = {"team": tm, "hnsw_us_per_call": round(h_call, 2), "dense_us_per_call": round(d_call, 2),
                                "hnsw_queries_per_s": round(Bc * 1e6 / h_call, 1),
                                "dense_queries_per_s": round(Bc * 1e6 / d_call, 1),
                                "dense_hbm_frac": round(wl.V * wl.d * s / (d_call * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
@@ -448,7 +475,7 @@ def main() -> int:
         # ---- all queries in one launch --------------------------------------
         torch.cuda.synchronize()
         a, b = events(2)
-        w8, i8 = TRAVERSALS[head_trav]
+        w8, i8, _ = TRAVERSALS[head_trav]  # one workgroup per query: 1024 queries fill the device
         ix.query_into(Hd, k, ef, hi, hl, hs, w8, i8)
         a.record(stream)
         ix.query_into(Hd, k, ef, hi, hl, hs, w8, i8)
@@ -495,9 +522,9 @@ def main() -> int:
             fids = torch.arange(args.forced, dtype=torch.int32, device=dev)
             fi = torch.empty((nf, k + args.forced), dtype=torch.int32, device=dev)
             fl = torch.empty((nf, k + args.forced), dtype=torch.float32, device=dev)
-            w8, i8 = TRAVERSALS[head_trav]
+            w8, i8, tm = TRAVERSALS[head_trav]
             f_us = back_to_back(lambda c: ix.query_forced_into(hv[c], k, ef, fids, fi[c:c + 1], fl[c:c + 1], None, w8,
-                                                               i8), nf)
+                                                               i8, tm), nf)
             legs["forced"] = {"n": args.forced, "ids": "0..%d" % (args.forced - 1), "queries": nf,
                               "us_per_query": round(f_us, 2), "search_only_us_per_query": round(head_kernel_us, 2)}
 
@@ -567,7 +594,7 @@ def oracle_leg(args, wl, W, H, ix, graph, info, trav, ef, k, gids, glg, gst, gtr
 
     g = O.Graph(wl.V, wl.d, wl.dtype, info["M"], info["M0"], wl.efC, wl.seed_levels, info["maxlevel"],
                 info["entry"], graph["levels"], graph["adj0"], graph["upper_off"], graph["upper"])
-    width, int8 = TRAVERSALS[trav]
+    width, int8, _ = TRAVERSALS[trav]  # a team walks the one-workgroup path
     oq = osc = None
     if int8:
         oq, osc = O.quantize_rows(W, wl.dtype)

@@ -1616,7 +1616,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 // of its lists there; the rest come from HBM.  Rows: each group keeps two
 // rows' loads in flight.
 
-constexpr int kMaxWidth = 32;       // widest expansion step
+constexpr int kMaxWidth = 64;       // widest expansion step
 constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
 
@@ -1755,12 +1755,12 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)ef * 8;
     uint64_t *beam2 = reinterpret_cast<uint64_t *>(p);
     p += (size_t)ef * 8;
-    uint64_t *ckey = reinterpret_cast<uint64_t *>(p);
-    p += (size_t)cap * 8;
+    uint64_t *ckey = reinterpret_cast<uint64_t *>(p);  // padded to whole 64-key runs
+    p += (size_t)((cap + kWave - 1) & ~(kWave - 1)) * 8;
     int32_t *cid = reinterpret_cast<int32_t *>(p);
     p += (size_t)nid * 4;
-    int32_t *lcache = reinterpret_cast<int32_t *>(p);
-    p += (size_t)cap * 4;
+    int32_t *lcache = reinterpret_cast<int32_t *>(p);  // (none in a team)
+    p += T == 1 ? (size_t)cap * 4 : 0;
     // flag arrays 8-byte aligned and padded to 8 bytes: the picks scan reads
     // them eight flags per lane
     const int efp = (ef + 7) & ~7;
@@ -2027,8 +2027,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (nk > kWave) {
             for (int r = tid / kWave; r < nrun; r += NT / kWave) {
                 const int j = r * kWave + lane;
-                const uint64_t key = wave_sort_desc(j < nk ? ckey[j] : 0ull, lane);
-                if (j < nk) ckey[j] = key;  // the run's real keys are its largest
+                // the last run is padded with zero keys (below every real key)
+                ckey[j] = wave_sort_desc(j < nk ? ckey[j] : 0ull, lane);
             }
             __syncthreads();
         }
@@ -2038,14 +2038,28 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 for (int t = 0; t < nk; ++t) above += ckey[t] > key;
                 return above;
             }
-            for (int r = 0; r < nrun; ++r) {
-                const uint64_t *run = ckey + r * kWave;
-                int lo = 0, hi = min(kWave, nk - r * kWave);
-                while (lo < hi) {
-                    const int mid = (lo + hi) >> 1;
-                    if (run[mid] > key) lo = mid + 1; else hi = mid;
+            // fixed-step searches of 64-key runs, four runs at a time so that
+            // their LDS loads overlap
+            int r = 0;
+            for (; r + 4 <= nrun; r += 4) {
+                const uint64_t *a = ckey + r * kWave;
+                int p0 = 0, p1 = 0, p2 = 0, p3 = 0;
+#pragma unroll
+                for (int step = kWave / 2; step > 0; step >>= 1) {
+                    p0 += a[p0 + step - 1] > key ? step : 0;
+                    p1 += a[kWave + p1 + step - 1] > key ? step : 0;
+                    p2 += a[2 * kWave + p2 + step - 1] > key ? step : 0;
+                    p3 += a[3 * kWave + p3 + step - 1] > key ? step : 0;
                 }
-                above += lo;
+                above += p0 + (a[p0] > key) + p1 + (a[kWave + p1] > key) + p2 + (a[2 * kWave + p2] > key) + p3 +
+                         (a[3 * kWave + p3] > key);
+            }
+            for (; r < nrun; ++r) {
+                const uint64_t *a = ckey + r * kWave;
+                int p = 0;
+#pragma unroll
+                for (int step = kWave / 2; step > 0; step >>= 1) p += a[p + step - 1] > key ? step : 0;
+                above += p + (a[p] > key);
             }
             return above;
         };
@@ -2072,14 +2086,13 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         // the kept key of rank r, non-decreasing in r, so that a beam entry's
         // count of larger kept keys is one binary search)
         const int total = min((int)nbeam + nk, ef);
+        const int bstep = 1 << (31 - __builtin_clz(nbeam));  // nbeam >= 1
         for (int j = tid; j < nk; j += NT) {
             const uint64_t key = ckey[j];
+            int lo = 0;  // beam entries larger than key
+            for (int step = bstep; step > 0; step >>= 1)
+                if (lo + step <= (int)nbeam && beam[lo + step - 1] > key) lo += step;
             const int above = kept_above(key);
-            int lo = 0, hi = (int)nbeam;
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (beam[mid] > key) lo = mid + 1; else hi = mid;
-            }
             cid[above] = lo;
             const int pos = lo + above;
             if (pos < total) {
@@ -2092,13 +2105,12 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         }
         __syncthreads();
         const int after = s_after;
+        const int kstep = nk > 0 ? 1 << (31 - __builtin_clz(nk)) : 0;
         for (int i = tid; i < (int)nbeam; i += NT) {
             const uint64_t key = beam[i];
-            int lo = 0, hi = nk;  // kept keys whose beam position is <= i lie above beam[i]
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (cid[mid] <= i) lo = mid + 1; else hi = mid;
-            }
+            int lo = 0;  // kept keys whose beam position is <= i lie above beam[i]
+            for (int step = kstep; step > 0; step >>= 1)
+                if (lo + step <= nk && cid[lo + step - 1] <= i) lo += step;
             const int pos = i + lo;
             if (pos < total) {
                 beam2[pos] = key;
@@ -2581,12 +2593,13 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
-size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width, bool q8)
+size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width, bool q8, int team)
 {
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t cap = (size_t)width * M0, nid = cap > (size_t)M ? cap : (size_t)M;
-    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + cap * 8 + nid * 4 + cap * 4;
+    const size_t capk = (cap + 63) & ~(size_t)63;
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + capk * 8 + nid * 4 + (team == 1 ? cap * 4 : 0);
     n = ((n + 7) & ~(size_t)7) + 2 * (((size_t)ef_eff + 7) & ~(size_t)7);  // 8-aligned flag arrays
     n = (n + 15) & ~(size_t)15;
     if (q8) n += (size_t)((d + 15) & ~15);
@@ -2753,7 +2766,7 @@ vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
         return fail(VIE_EUNSUPPORTED, "HNSW search: team of %d workgroups outside 1..%d", a.team, kMaxTeam);
     if (a.team > 1 && !a.team_ws) return fail(VIE_EINVAL, "a team search needs its workspace");
     const bool multi = a.width > 1 || a.q8 || a.team > 1;
-    const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8)
+    const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8, a.team)
                              : hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
     const size_t lim = hnsw_lds_limit();
     if (lds > lim)

@@ -286,7 +286,7 @@ def test_hnsw_matches_oracle_on_oracle_graph(vie, V, d, dtype, M, efC):
             assert np.array_equal(i1.cpu().numpy()[0], ids_b.cpu().numpy()[q])
 
 
-@pytest.mark.parametrize("width", [2, 3, 4, 8, 13, 32])
+@pytest.mark.parametrize("width", [2, 3, 4, 8, 13, 32, 64])
 def test_hnsw_multi_expansion_matches_oracle(vie, width):
     """Several expansions per step follow the oracle's multi-expansion search
     (same visits and counts), with the list cache and ragged picks."""
@@ -324,7 +324,7 @@ def test_hnsw_team_equals_one_workgroup(vie, team):
     q8, sc = vie.quantize_rows(ix._W_dev, synth.BF16)
     for int8 in (False, True):
         ix.attach_int8(q8, sc) if int8 else ix.attach_int8(None, None)
-        for width in (1, 8, 32):
+        for width in (1, 8, 32, 64):
             for k, ef in [(10, 10), (50, 200), (50, 600)]:
                 what = "team=%d int8=%d width=%d k=%d ef=%d" % (team, int8, width, k, ef)
                 say(what)
@@ -414,7 +414,7 @@ def test_int8_rows_bitwise(vie, V, d, dtype):
     assert np.array_equal(sc.cpu().numpy().view(np.uint32), osc.view(np.uint32))
 
 
-@pytest.mark.parametrize("width", [1, 4, 8])
+@pytest.mark.parametrize("width", [1, 4, 8, 64])
 def test_int8_search_matches_oracle(vie, width):
     """Layer 0 on int8 scores (integer dot, fp32 scale products) walks exactly
     the oracle's path; the re-ranked result matches within the tolerances."""

@@ -7,10 +7,10 @@ queries served one per call (B = 1), HNSW graph with M = 32 (M0 = 64),
 ef_construction = 200, built by the library on the host CPUs.
 
 The beam width is the one the method needs: for each traversal (the
-sequential search; 8 or 32 expansions per step; 8, 16, 32 or 64 per step on
-int8 rows with the exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
+sequential search; 8, 32 or 64 expansions per step; 8, 16, 32 or 64 per step
+on int8 rows with the exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
 0.95 on the first 128 queries (recall against the exact dense head, itself
-parity-tested against the oracle).  The team traversals (16 workgroups
+parity-tested against the oracle).  The team traversals (32 workgroups
 sharing each query's row scoring) walk exactly the path of their
 one-workgroup twin and take its ef.  The fastest of them at its ef is the
 headline traversal.
@@ -51,17 +51,17 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SRC = os.path.join(ROOT, "paper_2608_27460_amd", "csrc", "kernels.hip")
 NODE_MASK = (1 << 26) - 1
 
-TEAM = 16  # workgroups per query of the team traversals
+TEAM = 32  # workgroups per query of the team traversals
 TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0, workgroups per query)
     "sequential": (1, False, 1),
     "width8": (8, False, 1),
     "width32": (32, False, 1),
+    "width64": (64, False, 1),
     "int8_width8": (8, True, 1),
     "int8_width16": (16, True, 1),
     "int8_width32": (32, True, 1),
     "int8_width64": (64, True, 1),
-    "width32_team%d" % TEAM: (32, False, TEAM),
-    "int8_width16_team%d" % TEAM: (16, True, TEAM),
+    "width64_team%d" % TEAM: (64, False, TEAM),
     "int8_width32_team%d" % TEAM: (32, True, TEAM),
     "int8_width64_team%d" % TEAM: (64, True, TEAM),
 }
@@ -328,7 +328,7 @@ def main() -> int:
     if args.traversal:
         head_trav = args.traversal
     elif args.ef:
-        head_trav = "int8_width32_team%d" % TEAM if qrows is not None else "width32_team%d" % TEAM
+        head_trav = "int8_width64_team%d" % TEAM if qrows is not None else "width64_team%d" % TEAM
     else:
         head_trav = min(reachable, key=lambda t: calib[t]["tried"][str(chosen[t])]["us_per_query"])
     ef = chosen[head_trav]
@@ -460,6 +460,7 @@ def main() -> int:
                 hb = [Hd[c * Bc:(c + 1) * Bc] for c in range(ncall)]
                 w8, i8, tm = TRAVERSALS[head_trav]
                 tm = max(1, min(tm, 128 // Bc))  # the team shrinks as the batch grows (all resident at once)
+                tm = 1 << (tm.bit_length() - 1)  # a power of two
                 h_call = back_to_back(lambda c: ix.query_into(hb[c], k, ef, bi[c * Bc:(c + 1) * Bc],
                                                               bl[c * Bc:(c + 1) * Bc], None, w8, i8, None, tm),
                                       ncall)

@@ -204,13 +204,14 @@ typedef struct {
                              Needs V < 2^26.  A diagnostic: it lets a
                              caller replay and compare a traversal. */
     int32_t trace_cap;    /* entries per query of trace_dev (>= 1 when set) */
-    int32_t team;         /* workgroups that search each query together,
-                             1..32 (0 counts as 1).  Each member keeps the
-                             whole search state and takes every decision
-                             itself, scores only the new nodes whose id
-                             modulo team is its member index, and passes the
-                             scores that can enter the beam to the others
-                             through workspace_dev, so the traversal, the
+    int32_t team;         /* workgroups that search each query together:
+                             1, 2, 4, 8, 16 or 32 (0 counts as 1).  Each
+                             member keeps the whole search state and takes
+                             every decision itself, scores only the new
+                             nodes whose id modulo team is its member
+                             index, and passes the scores that can enter
+                             the beam to the others through
+                             workspace_dev, so the traversal, the
                              results and stats are those of team = 1 (a
                              query's distance evaluations are shared, its
                              dependent steps are not).  All B * team

@@ -268,8 +268,8 @@ vie_status check_params(const vie_search_params *params)
         return fail(VIE_EINVAL, "int8_rows = %d is neither 0 nor 1", params->int8_rows);
     if (params->trace_dev && params->trace_cap < 1)
         return fail(VIE_EINVAL, "trace_cap = %d < 1 with a trace buffer", params->trace_cap);
-    if (params->team < 0 || params->team > kMaxTeam)
-        return fail(VIE_EINVAL, "team = %d outside 0..%d", params->team, kMaxTeam);
+    if (params->team < 0 || params->team > kMaxTeam || (params->team & (params->team - 1)))
+        return fail(VIE_EINVAL, "team = %d is neither 0 nor a power of two up to %d", params->team, kMaxTeam);
     if (params->team > 1 && !params->workspace_dev) return fail(VIE_EINVAL, "a team search needs workspace_dev");
     if (params->team > 1 && (uintptr_t)params->workspace_dev % 256)
         return fail(VIE_EINVAL, "workspace_dev is not 256-byte aligned");
@@ -286,8 +286,8 @@ vie_status vie_query_workspace(const vie_index *ix, int32_t B, int32_t k, int32_
     if (!ix || !params || !bytes) return fail(VIE_EINVAL, "NULL argument");
     if (params->expand_width < 1 || params->expand_width > 64)
         return fail(VIE_EINVAL, "expand_width = %d outside 1..64", params->expand_width);
-    if (params->team < 0 || params->team > kMaxTeam)
-        return fail(VIE_EINVAL, "team = %d outside 0..%d", params->team, kMaxTeam);
+    if (params->team < 0 || params->team > kMaxTeam || (params->team & (params->team - 1)))
+        return fail(VIE_EINVAL, "team = %d is neither 0 nor a power of two up to %d", params->team, kMaxTeam);
     if (vie_status s = check_k(k, ix->g.V, B)) return s;
     if (ef < 1) return fail(VIE_EINVAL, "ef = %d < 1", ef);
     HnswLaunch a{};

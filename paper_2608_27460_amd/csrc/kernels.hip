@@ -1172,10 +1172,10 @@ struct HnswShared {
     int team_err;
 };
 
-// A team: `size` workgroups search one query together (workgroup
-// q * size + m is member m of query q).  Every member keeps the whole search
-// state and takes every decision itself; each scores only the new nodes n
-// with n % size == m and passes its kept keys to the others through `keys`
+// A team: `size` workgroups (a power of two) search one query together
+// (workgroup q * size + m is member m of query q).  Every member keeps the
+// whole search state and takes every decision itself; each scores only the
+// new nodes n with n mod size == m and passes its kept keys to the others through `keys`
 // ([query][3][member][slot] with `slot` entries each) and their number
 // through `tags` ([query][3][member], zero before the launch): at its e-th
 // exchange (from 1) a member publishes (e << 32) | count.  Everything the
@@ -1740,6 +1740,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int hbytes = (row_bytes + 15) & ~15;
     const int vwords = (int)((V + 31) / 32);
     const int cap = width * M0;  // most nodes claimed in one step
+    // t / M0 for t < 2^15 (M0 <= 256) as a multiply-high by this magic number
+    const uint32_t m0_magic = (uint32_t)(((1ull << 32) + (uint32_t)M0 - 1u) / (uint32_t)M0);
     const int nid = cap > M ? cap : M;
     // list entries a group keeps per lane (as in hnsw_kernel: enough for
     // M0 = 64 at every group width)
@@ -1940,7 +1942,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         // cache still holds that node's list, else from HBM.  The first slot
         // of each pick marks it expanded (the other bits of its flag stay).
         for (int t = tid; t < np * M0; t += NT) {
-            const int j = t / M0, slot = t - j * M0;
+            const int j = (int)__umulhi((uint32_t)t, m0_magic), slot = t - j * M0;
             const int pj = s_pick[j];
             const int32_t c = key_id(beam[pj]);
             const int hint = (int)(flag[pj] >> 1) - 1;
@@ -1952,7 +1954,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             const int32_t eg = src < 0 ? adj0[(int64_t)c * M0 + slot] : -1;
             const int32_t e = src >= 0 ? ec : eg;
             if (e >= 0 && claim(vis, e)) {
-                if (e % T == mem) cid[atomicAdd(&sh.nnew, 1u)] = e;
+                if ((e & (T - 1)) == mem) cid[atomicAdd(&sh.nnew, 1u)] = e;
                 else atomicAdd(&sh.nother, 1u);
             }
         }
@@ -2159,7 +2161,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             uint64_t *xr = team.keys + (((int64_t)q * 3 + 2) * T + mem) * team.slot;
             for (int j = grp; j < nb; j += kGroups) {
                 const int32_t e = key_id(beam[j]);
-                if (e % T != mem) continue;
+                if ((e & (T - 1)) != mem) continue;
                 const float sc = row_dot<VEC, BF16, G>(W, e, row_bytes, hs, gl);
                 if (gl == 0) {
                     const uint32_t slot = atomicAdd(&sh.nkeep, 1u);
@@ -2762,8 +2764,9 @@ vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
 {
     if (a.width < 1 || a.width > kMaxWidth)
         return fail(VIE_EUNSUPPORTED, "HNSW search: expansion width %d outside 1..%d", a.width, kMaxWidth);
-    if (a.team < 1 || a.team > kMaxTeam)
-        return fail(VIE_EUNSUPPORTED, "HNSW search: team of %d workgroups outside 1..%d", a.team, kMaxTeam);
+    if (a.team < 1 || a.team > kMaxTeam || (a.team & (a.team - 1)))
+        return fail(VIE_EUNSUPPORTED, "HNSW search: team of %d workgroups is not a power of two in 1..%d", a.team,
+                    kMaxTeam);
     if (a.team > 1 && !a.team_ws) return fail(VIE_EINVAL, "a team search needs its workspace");
     const bool multi = a.width > 1 || a.q8 || a.team > 1;
     const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8, a.team)

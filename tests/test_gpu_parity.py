@@ -306,7 +306,7 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
                 (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
 
 
-@pytest.mark.parametrize("team", [2, 3, 8])
+@pytest.mark.parametrize("team", [2, 4, 32])
 def test_hnsw_team_equals_one_workgroup(vie, team):
     """A team of workgroups per query (each scoring its share of the new
     nodes, all exchanging the keys that can enter the beam) walks the same

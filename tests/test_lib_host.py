@@ -160,8 +160,9 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # int8_rows
     prm = vie.SearchParams(1, 0, fake, 0)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # trace_cap
-    prm = vie.SearchParams(1, 0, None, 0, 33)
-    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # team 33
+    for team in (33, 3, 12, -1):
+        prm = vie.SearchParams(1, 0, None, 0, team)
+        assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL, team
     prm = vie.SearchParams(1, 0, None, 0, 4)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # no workspace
     prm = vie.SearchParams(1, 0, None, 0, 4, C.c_void_p(4096 + 8), 1 << 30)

@@ -134,14 +134,19 @@ typedef struct {
  * bytes) and releases it before returning; it enqueues on hip_stream and
  * waits for it.
  * Errors: VIE_EINVAL (NULL, sizes, params), VIE_EUNSUPPORTED (rows not
- * 16-byte aligned), VIE_ENOMEM, VIE_EHIP (a HIP or rocBLAS call failed). */
+ * 16-byte aligned), VIE_ENOMEM, VIE_EHIP (a HIP call or launch failed). */
 vie_status vie_index_build_gpu(const void *W_dev, vie_dtype dtype, int64_t V, int32_t d,
                                const vie_gpu_build_params *params, void *hip_stream, vie_index **out);
 
-/* Writes the index file (format below).  Errors: VIE_EINVAL, VIE_EIO. */
+/* Writes the index file (format below).  Section 3: the index is built once,
+ * offline, and shipped with the model checkpoint; this file is that artifact
+ * (the graph plus a fingerprint of the W_out it was built on).
+ * Errors: VIE_EINVAL, VIE_EIO. */
 vie_status vie_index_save(const vie_index *index, const char *path);
 
-/* Reads and validates an index file (checksum, sizes, every id in range, no
+/* Loads the shipped index (Section 3: precomputed and distributed with the
+ * checkpoint, so inference never builds it).
+ * Reads and validates an index file (checksum, sizes, every id in range, no
  * self loops or duplicates, degree caps, nested levels, entry on the top
  * level).  If W_host is not NULL it must be the [V][d] matrix the index was
  * built on: its fingerprint is compared with the stored one.

@@ -394,8 +394,15 @@ def main() -> int:
     d_ms, d_wall = timed_steps(dense_step, args.steps, args.warmup)
     dense_calls = per_call(lambda c: dense_call(c), min(Q, 256))
     d_kernel_us = back_to_back(lambda c: dense_call(c, scatter=False), SQ)
-    assert np.array_equal(di.cpu().numpy()[:SQ], exact_ids[:SQ])  # both copies give the exact top k
-    del Wd2, Ws
+    # both copies give the same top k, bit for bit (the same kernels on equal bytes), and it is the exact top k
+    # of the 64-query passes up to the order of near ties (the passes sum in another order)
+    di2, dl2, _ = out_bufs(SQ)
+    for q in range(SQ):
+        vie.dense_topk_into(Ws[(q + 1) & 1], hv[q], k, di2[q:q + 1], dl2[q:q + 1], dhead.workspace)
+    assert np.array_equal(di.cpu().numpy()[:SQ], di2.cpu().numpy()) and \
+        np.array_equal(dl.cpu().numpy()[:SQ].view(np.uint32), dl2.cpu().numpy().view(np.uint32))
+    assert recall(di.cpu().numpy()[:SQ], exact_ids[:SQ]) >= 0.99
+    del Wd2, Ws, di2, dl2
 
     # ---- roofline figures --------------------------------------------------
     M, M0 = info["M"], info["M0"]

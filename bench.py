@@ -163,6 +163,8 @@ def main() -> int:
     ap.add_argument("--no-fp32", action="store_true")
     ap.add_argument("--forced", type=int, default=64,
                     help="forced-inclusion tokens of the forced leg (ids 0..n-1 stand in for special tokens)")
+    ap.add_argument("--share-groups", type=lambda x: [int(v) for v in x.split(",") if v], default=[2, 4],
+                    help="row-sharing group sizes of the one-launch leg (empty: skip the leg)")
     ap.add_argument("--batch-graph-k", type=int, default=128,
                     help="candidates per node of the GPU-built batch graph leg (0: skip the leg)")
     ap.add_argument("--cache", default=os.environ.get("VIE_CACHE", "/tmp/vie_cache"))
@@ -492,6 +494,29 @@ def main() -> int:
         one_launch_s = a.elapsed_time(b) * 1e-3
         legs["one_launch"] = {"queries": Q, "queries_per_s": round(Q / one_launch_s, 1),
                               "hbm_frac": round(float(head_bytes.sum()) / one_launch_s / 1e9 / HBM_PEAK_GBS, 4)}
+
+        # ---- row sharing between the queries of one launch ------------------
+        if args.share_groups:
+            rs = {}
+            w8, i8, _ = TRAVERSALS[head_trav]
+            for Bc in [b for b in (64, 256, 1024) if b <= Q]:
+                row, ref = {}, None
+                for sh in [1] + args.share_groups:
+                    def launch(_c, sh=sh, Bc=Bc):
+                        ix.query_into(Hd[:Bc], k, ef, hi[:Bc], hl[:Bc], hs[:Bc], w8, i8, None, 1, sh)
+                    try:
+                        ms = back_to_back(launch, 3) / 1e3
+                    except vie.VieError as e:  # a group's queries that do not fit in LDS
+                        row[str(sh)] = {"error": str(e)[:120]}
+                        continue
+                    out = (hi[:Bc].cpu().numpy(), hl[:Bc].cpu().numpy().view(np.uint32), hs[:Bc].cpu().numpy())
+                    if ref is None:
+                        ref = out
+                    row[str(sh)] = {"ms_per_launch": round(ms, 3), "queries_per_s": round(Bc / ms * 1e3, 1),
+                                    "same_results": all(np.array_equal(a, b) for a, b in zip(out, ref))}
+                rs[str(Bc)] = row
+            legs["row_sharing"] = {"traversal": "%s, one workgroup per query" % head_trav.split("_team")[0], "ef": ef,
+                                   "share": rs}
 
         # ---- batch graph built on the GPU, searched at B = 1 ----------------
         if args.batch_graph_k:

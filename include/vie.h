@@ -229,12 +229,30 @@ typedef struct {
                              vie_query_workspace() bytes, 256-byte aligned,
                              caller owned, no initialisation needed; calls
                              that share it must not overlap in time.
-                             Ignored for team <= 1. */
+                             Ignored for team <= 1 and share <= 1. */
     size_t workspace_bytes;
+    int32_t share;        /* row sharing between the call's queries: 1, 2,
+                             4, 8 or 16 (0 counts as 1) queries per group
+                             (query b is in group b / share).  The workgroup
+                             that fetches a row scores it for every query of
+                             its group and publishes the others' scores in
+                             workspace_dev; a query that later claims that
+                             node takes its score from there and reads no
+                             row.  Each score is computed by the same
+                             instructions the query's own workgroup would
+                             use, so results, stats and expansion records
+                             are those of share = 1; the rows read drop
+                             where the group's walks overlap.  Needs
+                             team <= 1 and workspace_dev (vie_query_workspace
+                             bytes, 256-byte aligned), which the library
+                             clears on its first use and then keeps valid
+                             across calls of any index; calls that share it
+                             must not overlap in time. */
 } vie_search_params;
 
 /* Bytes of device workspace that vie_query_ex / vie_query_forced need with
- * these arguments (0 unless params->team > 1).
+ * these arguments (0 unless params->team > 1 or params->share > 1; with
+ * share, about 8 V bytes per query).
  * Errors: VIE_EINVAL (as the query would report for its arguments). */
 vie_status vie_query_workspace(const vie_index *index, int32_t B, int32_t k, int32_t ef,
                                const vie_search_params *params, size_t *bytes);

@@ -270,13 +270,17 @@ vie_status check_params(const vie_search_params *params)
         return fail(VIE_EINVAL, "trace_cap = %d < 1 with a trace buffer", params->trace_cap);
     if (params->team < 0 || params->team > kMaxTeam || (params->team & (params->team - 1)))
         return fail(VIE_EINVAL, "team = %d is neither 0 nor a power of two up to %d", params->team, kMaxTeam);
-    if (params->team > 1 && !params->workspace_dev) return fail(VIE_EINVAL, "a team search needs workspace_dev");
-    if (params->team > 1 && (uintptr_t)params->workspace_dev % 256)
-        return fail(VIE_EINVAL, "workspace_dev is not 256-byte aligned");
+    if (params->share < 0 || params->share > kMaxShare || (params->share & (params->share - 1)))
+        return fail(VIE_EINVAL, "share = %d is neither 0 nor a power of two up to %d", params->share, kMaxShare);
+    if (params->team > 1 && params->share > 1) return fail(VIE_EINVAL, "team and share cannot be combined");
+    const bool ws = params->team > 1 || params->share > 1;
+    if (ws && !params->workspace_dev) return fail(VIE_EINVAL, "a team or row-sharing search needs workspace_dev");
+    if (ws && (uintptr_t)params->workspace_dev % 256) return fail(VIE_EINVAL, "workspace_dev is not 256-byte aligned");
     return VIE_OK;
 }
 
 int team_of(const vie_search_params *params) { return params && params->team > 1 ? params->team : 1; }
+int share_of(const vie_search_params *params) { return params && params->share > 1 ? params->share : 1; }
 }  // namespace
 
 vie_status vie_query_workspace(const vie_index *ix, int32_t B, int32_t k, int32_t ef,
@@ -288,6 +292,8 @@ vie_status vie_query_workspace(const vie_index *ix, int32_t B, int32_t k, int32_
         return fail(VIE_EINVAL, "expand_width = %d outside 1..64", params->expand_width);
     if (params->team < 0 || params->team > kMaxTeam || (params->team & (params->team - 1)))
         return fail(VIE_EINVAL, "team = %d is neither 0 nor a power of two up to %d", params->team, kMaxTeam);
+    if (params->share < 0 || params->share > kMaxShare || (params->share & (params->share - 1)))
+        return fail(VIE_EINVAL, "share = %d is neither 0 nor a power of two up to %d", params->share, kMaxShare);
     if (vie_status s = check_k(k, ix->g.V, B)) return s;
     if (ef < 1) return fail(VIE_EINVAL, "ef = %d < 1", ef);
     HnswLaunch a{};
@@ -296,7 +302,8 @@ vie_status vie_query_workspace(const vie_index *ix, int32_t B, int32_t k, int32_
     a.width = params->expand_width;
     a.ef_eff = ef > k ? ef : k;
     a.team = team_of(params);
-    *bytes = hnsw_team_workspace_bytes(a);
+    *bytes = hnsw_team_workspace_bytes(a) + hnsw_share_workspace_bytes(B, ix->g.V, ix->g.d, ix->g.dtype,
+                                                                        params->int8_rows != 0, share_of(params));
     return VIE_OK;
 }
 
@@ -410,6 +417,14 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
         if (!ix->dev.q8) return fail(VIE_ESTATE, "no int8 rows attached (call vie_index_attach_int8)");
         a.q8 = ix->dev.q8;
         a.q8scale = ix->dev.q8scale;
+    }
+    a.share = share_of(params);
+    if (a.share > 1) {
+        const size_t need = hnsw_share_workspace_bytes(a.B, a.V, a.d, a.dtype, a.q8 != nullptr, a.share);
+        if (params->workspace_bytes < need)
+            return fail(VIE_EINVAL, "workspace holds %zu bytes, row sharing in groups of %d needs %zu",
+                        params->workspace_bytes, a.share, need);
+        a.share_ws = params->workspace_dev;
     }
     hipStream_t st = static_cast<hipStream_t>(hip_stream);
     if (vie_status r = launch_hnsw_search(a, st)) return r;

@@ -20,6 +20,7 @@ constexpr int kMaxEf = 8192;      // largest beam of the HNSW kernel (LDS permit
 constexpr int kMaxD = 8192;       // largest row width
 constexpr int kMaxGpuBuildK = 128;  // candidates per node of the GPU batch build
 constexpr int kMaxTeam = 32;      // workgroups that may search one query together
+constexpr int kMaxShare = 16;     // queries per row-sharing group
 
 inline int elem_bytes(int dtype) { return dtype == VIE_F32 ? 4 : 2; }
 
@@ -93,8 +94,11 @@ struct HnswLaunch {
     int trace_cap = 0;
     int team = 1;              // workgroups per query (1: one)
     void *team_ws = nullptr;   // team exchange workspace (hnsw_team_workspace_bytes)
+    int share = 1;             // queries per row-sharing group (1: none)
+    void *share_ws = nullptr;  // row-sharing workspace (hnsw_share_workspace_bytes)
 };
 size_t hnsw_team_workspace_bytes(const HnswLaunch &a);
+size_t hnsw_share_workspace_bytes(int B, int64_t V, int d, int dtype, bool q8, int share);
 // Launchers return VIE_OK, VIE_EUNSUPPORTED for a shape they cannot serve, or
 // VIE_EHIP for a failed launch; the detail goes to set_error().
 vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s);

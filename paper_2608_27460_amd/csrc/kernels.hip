@@ -1170,6 +1170,7 @@ struct HnswShared {
     // and a wait that gave up
     uint32_t nother;
     int team_err;
+    uint32_t nfetch;  // hnsw_multi_kernel sharing rows: new nodes whose row is fetched
 };
 
 // A team: `size` workgroups (a power of two) search one query together
@@ -1195,6 +1196,24 @@ struct TeamArgs {
 // a wait that runs out means the members were not resident together, and
 // the search reports it in its results instead of waiting on.
 constexpr uint32_t kTeamSpin = 1u << 21;
+
+// Row sharing: the queries of one launch form groups of `size` (query q is
+// member q % size of group q / size).  A workgroup that fetches a row scores
+// it for every query of its group, with the same instructions the owner's
+// workgroup would use, and publishes the others' scores in `table`
+// ([query][V] words (epoch << 32) | ord(score)); a query that claims a node
+// whose word carries this launch's epoch takes the score from it and reads
+// no row.  `hq` holds the launch's queries in the kernel's layout (rows of
+// hbytes, zero padded), `hq8` / `hscale` their int8 form for int8 walks.
+struct ShareArgs {
+    int size;
+    int B;
+    uint64_t *table;
+    const uint32_t *epoch;
+    const char *hq;
+    const int8_t *hq8;
+    const float *hscale;
+};
 
 // p rounded up to 16 bytes past base (base 16-byte aligned), by pointer
 // arithmetic only: a pointer into LDS keeps its address space, so the
@@ -1709,6 +1728,79 @@ __device__ __forceinline__ void row_dot2_q8(const int8_t *__restrict__ Q, int64_
     ib = group_sum<G>(xb);
 }
 
+// row_dot2 for every query of a group (queries m = 0 .. qg - 1 at
+// hgroup + m * hbytes, in the kernel's query layout): the two rows' chunks
+// are loaded once, and each query's sums are taken with exactly row_dot2's
+// sequence of operations, so a query's scores are the bits its own
+// row_dot2 would give.  f(m, score_a, score_b) receives them in order.
+template <int VEC, bool BF16, int G, typename F>
+__device__ __forceinline__ void row_dot2_group(const char *__restrict__ W, int64_t ra, int64_t rb, int row_bytes,
+                                               const char *__restrict__ hgroup, int hbytes, int qg, int gl, F f)
+{
+    typedef typename Vec<VEC>::T T;
+    const T *wa = reinterpret_cast<const T *>(W + ra * (int64_t)row_bytes);
+    const T *wb = reinterpret_cast<const T *>(W + (rb >= 0 ? rb : ra) * (int64_t)row_bytes);
+    const int nchunk = row_bytes / VEC;
+    constexpr int CPL = RowCpl<BF16>::value;
+    T ba[CPL], bb[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        ba[i] = c < nchunk ? wa[c] : T{};
+        bb[i] = c < nchunk && rb >= 0 ? wb[c] : T{};
+    }
+    for (int m = 0; m < qg; ++m) {
+        const T *h = reinterpret_cast<const T *>(hgroup + (int64_t)m * hbytes);
+        typename AccOf<BF16>::T xa = 0, xb = 0;
+#pragma unroll
+        for (int i0 = 0; i0 < CPL; ++i0) {
+            const T hv = h[min(gl + i0 * G, nchunk - 1)];
+            xa = dot_vec<VEC, BF16>(ba[i0], hv, xa);
+            xb = dot_vec<VEC, BF16>(bb[i0], hv, xb);
+        }
+        for (int c = gl + CPL * G; c < nchunk; c += G) {
+            xa = dot_vec<VEC, BF16>(wa[c], h[c], xa);
+            if (rb >= 0) xb = dot_vec<VEC, BF16>(wb[c], h[c], xb);
+        }
+        f(m, (float)group_sum<G>(xa), (float)group_sum<G>(xb));
+    }
+}
+
+// row_dot2_q8 for every query of a group (int8 queries m at hgroup + m * d):
+// f(m, dot_a, dot_b) with the integer dots.
+template <int G, typename F>
+__device__ __forceinline__ void row_dot2_q8_group(const int8_t *__restrict__ Q, int64_t ra, int64_t rb, int d,
+                                                  const int8_t *__restrict__ hgroup, int qg, int gl, F f)
+{
+    const u32x4 *qa = reinterpret_cast<const u32x4 *>(Q + ra * (int64_t)d);
+    const u32x4 *qb = reinterpret_cast<const u32x4 *>(Q + (rb >= 0 ? rb : ra) * (int64_t)d);
+    const int nchunk = d / 16;
+    constexpr int CPL = 4;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 ba[CPL], bb[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = gl + i * G;
+        ba[i] = c < nchunk ? qa[c] : zero;
+        bb[i] = c < nchunk && rb >= 0 ? qb[c] : zero;
+    }
+    for (int m = 0; m < qg; ++m) {
+        const u32x4 *h = reinterpret_cast<const u32x4 *>(hgroup + (int64_t)m * d);
+        int xa = 0, xb = 0;
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+            const u32x4 hv = h[min(gl + i * G, nchunk - 1)];
+            xa = sdot16(ba[i], hv, xa);
+            xb = sdot16(bb[i], hv, xb);
+        }
+        for (int c = gl + CPL * G; c < nchunk; c += G) {
+            xa = sdot16(qa[c], h[c], xa);
+            if (rb >= 0) xb = sdot16(qb[c], h[c], xb);
+        }
+        f(m, group_sum<G>(xa), group_sum<G>(xb));
+    }
+}
+
 // Layer-0 score from int8 rows: fp32(integer dot) * row scale * query scale,
 // each product rounded to fp32 (no fused operations).
 __device__ __forceinline__ float q8_score(int acc, float row_scale, float query_scale)
@@ -1717,13 +1809,13 @@ __device__ __forceinline__ float q8_score(int acc, float row_scale, float query_
     return __fmul_rn(a, query_scale);
 }
 
-template <int NT, int VEC, bool BF16, int G, bool Q8>
+template <int NT, int VEC, bool BF16, int G, bool Q8, bool SHARE>
 __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const char *__restrict__ W, int64_t V, int row_bytes, const int32_t *__restrict__ adj0, int M0,
     const int32_t *__restrict__ upper_off, const int32_t *__restrict__ upper, int M, int maxlevel, int32_t entry,
     const char *__restrict__ hq, int k, int ef, int width, int32_t *__restrict__ ids, float *__restrict__ logits, int ldo,
     uint32_t *__restrict__ stats, const int8_t *__restrict__ q8, const float *__restrict__ q8scale,
-    int32_t *__restrict__ trace_all, int trace_cap, TeamArgs team)
+    int32_t *__restrict__ trace_all, int trace_cap, TeamArgs team, ShareArgs share)
 {
     extern __shared__ __align__(16) char smem[];
     __shared__ HnswShared sh;
@@ -1763,6 +1855,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)nid * 4;
     int32_t *lcache = reinterpret_cast<int32_t *>(p);  // (none in a team)
     p += T == 1 ? (size_t)cap * 4 : 0;
+    int32_t *fid = reinterpret_cast<int32_t *>(p);  // sharing rows: the new nodes whose rows are fetched
+    p += SHARE ? (size_t)cap * 4 : 0;
     // flag arrays 8-byte aligned and padded to 8 bytes: the picks scan reads
     // them eight flags per lane
     const int efp = (ef + 7) & ~7;
@@ -1773,6 +1867,11 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)efp;
     int8_t *hq8 = align16_past<int8_t>(smem, p);  // Q8: the int8 query
     p = reinterpret_cast<char *>(hq8) + d8;
+    // sharing rows: the group's queries (int8 rows of d8 bytes for Q8, else
+    // rows of hbytes)
+    const int gbytes = Q8 ? d8 : hbytes;
+    char *hgrp = reinterpret_cast<char *>(align16_past<int8_t>(smem, p));
+    p = hgrp + (SHARE ? (size_t)share.size * gbytes : 0);
     uint32_t *vis = align16_past<uint32_t>(smem, p);
 
     const char *h = hq + (int64_t)q * row_bytes;
@@ -1782,6 +1881,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         s_hmax = 0;
         sh.nother = 0;
         sh.team_err = 0;
+        sh.nfetch = 0;
     }
     if (tid < kMaxWidth) lc_id[tid] = -1;
     __syncthreads();
@@ -1798,6 +1898,17 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int grp = tid / G;
     uint32_t n_dist = 0, n_expand = 0;
     int32_t *trace = trace_all && mem == 0 ? trace_all + (int64_t)q * trace_cap : nullptr;
+    // sharing rows: this query's group (queries gq0 .. gq0 + qg - 1) and the launch's epoch
+    const int gq0 = SHARE ? q - q % share.size : q;
+    const int qg = SHARE ? min(share.size, share.B - gq0) : 1;
+    const uint32_t epoch = SHARE ? *share.epoch : 0u;
+    if constexpr (SHARE) {  // the group's queries into LDS, 16 bytes per thread at a time
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(Q8 ? reinterpret_cast<const char *>(share.hq8) + (int64_t)gq0 * d8
+                                                               : share.hq + (int64_t)gq0 * hbytes);
+        u32x4 *dst = reinterpret_cast<u32x4 *>(hgrp);
+        for (int i = tid; i < qg * gbytes / 16; i += NT) dst[i] = src[i];
+        __syncthreads();
+    }
     uint64_t cur = descend_upper<NT, VEC, BF16, G>(W, V, row_bytes, upper_off, upper, M, maxlevel, entry, hs, cid,
                                                    vis, sh, n_dist, n_expand, trace, trace_cap);
 
@@ -1964,6 +2075,27 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         const int area = (int)(exchanges & 1);
         uint64_t *xk = T > 1 ? team.keys + (((int64_t)q * 3 + area) * T + mem) * team.slot : nullptr;
         const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
+        // sharing rows: a new node whose score another query of the group
+        // published in this launch is kept or dropped on that score; the
+        // others go to the fetch list
+        const int32_t *lst = cid;
+        int nl = nn;
+        if constexpr (SHARE) {
+            for (int j = tid; j < nn; j += NT) {
+                const int32_t e = cid[j];
+                const uint64_t w = __hip_atomic_load(share.table + (int64_t)q * V + e, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                if ((uint32_t)(w >> 32) == epoch) {
+                    const uint64_t key = (w << 32) | (uint64_t)(~(uint32_t)e);
+                    if (key > worst) ckey[atomicAdd(&sh.nkeep, 1u)] = key;
+                } else {
+                    fid[atomicAdd(&sh.nfetch, 1u)] = e;
+                }
+            }
+            __syncthreads();
+            lst = fid;
+            nl = (int)sh.nfetch;
+        }
         // score the new rows, two per group at a time; keep the keys that
         // can enter the beam, and the lists of a group's first rows
         uint64_t rk[kMultiHeld];
@@ -1971,9 +2103,9 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
 #pragma unroll
         for (int r = 0; r < kMultiHeld; ++r) rk[r] = 0ull;
         int r = 0;
-        for (int j = grp; j < nn; j += 2 * kGroups, r += 2) {
-            const int32_t ea = cid[j];
-            const int32_t eb = j + kGroups < nn ? cid[j + kGroups] : -1;
+        for (int j = grp; j < nl; j += 2 * kGroups, r += 2) {
+            const int32_t ea = lst[j];
+            const int32_t eb = j + kGroups < nl ? lst[j + kGroups] : -1;
             int32_t la[PF], lb[PF];
             if (cache_on && r < kMultiHeld) {
 #pragma unroll
@@ -1984,7 +2116,33 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 }
             }
             float sa, sb;
-            if constexpr (Q8) {
+            if constexpr (SHARE) {
+                // every query of the group against the two rows; the others'
+                // scores published (one lane per row)
+                auto publish = [&](int m, float xa, float xb) {
+                    if (m == q - gq0) {
+                        sa = xa;
+                        sb = xb;
+                    } else if (gl == 0) {
+                        uint64_t *tm = share.table + (int64_t)(gq0 + m) * V;
+                        __hip_atomic_store(tm + ea, ((uint64_t)epoch << 32) | f2ord(xa), __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                        if (eb >= 0)
+                            __hip_atomic_store(tm + eb, ((uint64_t)epoch << 32) | f2ord(xb), __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                };
+                if constexpr (Q8) {
+                    const float ca = q8scale[ea], cb = eb >= 0 ? q8scale[eb] : 0.0f;
+                    row_dot2_q8_group<G>(q8, ea, eb, d, reinterpret_cast<const int8_t *>(hgrp), qg, gl,
+                                         [&](int m, int ia, int ib) {
+                                             const float hsc = share.hscale[gq0 + m];
+                                             publish(m, q8_score(ia, ca, hsc), q8_score(ib, cb, hsc));
+                                         });
+                } else {
+                    row_dot2_group<VEC, BF16, G>(W, ea, eb, row_bytes, hgrp, hbytes, qg, gl, publish);
+                }
+            } else if constexpr (Q8) {
                 const float ca = q8scale[ea], cb = eb >= 0 ? q8scale[eb] : 0.0f;
                 int ia, ib;
                 row_dot2_q8<G>(q8, ea, eb, d, hq8, gl, ia, ib);
@@ -2124,6 +2282,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             sh.nbeam = (uint32_t)total;
             sh.nnew = 0;  // read after the claim barrier only
             sh.nother = 0;
+            sh.nfetch = 0;
         }
         __syncthreads();
         uint64_t *tb = beam;
@@ -2595,16 +2754,19 @@ size_t hnsw_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M)
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
-size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width, bool q8, int team)
+size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int M, int width, bool q8, int team,
+                            int share)
 {
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t cap = (size_t)width * M0, nid = cap > (size_t)M ? cap : (size_t)M;
     const size_t capk = (cap + 63) & ~(size_t)63;
-    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + capk * 8 + nid * 4 + (team == 1 ? cap * 4 : 0);
+    size_t n = hbytes + (size_t)ef_eff * 8 * 2 + capk * 8 + nid * 4 + (team == 1 ? cap * 4 : 0) +
+               (share > 1 ? cap * 4 : 0);
     n = ((n + 7) & ~(size_t)7) + 2 * (((size_t)ef_eff + 7) & ~(size_t)7);  // 8-aligned flag arrays
     n = (n + 15) & ~(size_t)15;
     if (q8) n += (size_t)((d + 15) & ~15);
+    if (share > 1) n += (size_t)share * (q8 ? (size_t)((d + 15) & ~15) : hbytes);  // the group's queries
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
@@ -2653,11 +2815,110 @@ size_t hnsw_team_workspace_bytes(const HnswLaunch &a)
 }
 
 namespace {
+constexpr uint64_t kShareMagic = 0x5645534841524531ull;  // marks a row-sharing workspace as cleared
+
+// The row-sharing workspace: a 256-byte header (magic word, epoch), the
+// queries in the kernel's layout [B][hbytes], their int8 form [B][d] and
+// scales [B] (int8 walks), then the score table [B][V] u64, each part
+// 256-byte aligned.
+struct ShareLayout {
+    uint64_t *magic;
+    uint32_t *epoch;
+    char *hq;
+    int8_t *hq8;
+    float *hscale;
+    uint64_t *table;
+    size_t clear_bytes;  // from hq to the end
+};
+
+ShareLayout share_layout(void *ws, const HnswLaunch &a)
+{
+    char *p = static_cast<char *>(ws);
+    ShareLayout l;
+    l.magic = reinterpret_cast<uint64_t *>(p);
+    l.epoch = reinterpret_cast<uint32_t *>(p + 8);
+    p += 256;
+    const size_t hbytes = (size_t)((a.d * elem_bytes(a.dtype) + 15) & ~15);
+    l.hq = p;
+    p += round256((size_t)a.B * hbytes);
+    l.hq8 = reinterpret_cast<int8_t *>(p);
+    p += a.q8 ? round256((size_t)a.B * a.d) : 0;
+    l.hscale = reinterpret_cast<float *>(p);
+    p += a.q8 ? round256((size_t)a.B * 4) : 0;
+    l.table = reinterpret_cast<uint64_t *>(p);
+    p += round256((size_t)a.B * a.V * 8);
+    l.clear_bytes = (size_t)(p - l.hq);
+    return l;
+}
+
+// Zeroes the workspace (past the header) unless its magic word says a
+// previous call did; every workgroup reads the word first.
+__global__ void share_clear_kernel(const uint64_t *__restrict__ magic, uint4 *__restrict__ body, size_t n16)
+{
+    if (*magic == kShareMagic) return;
+    const uint4 z = {0u, 0u, 0u, 0u};
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+        body[i] = z;
+}
+
+// One thread: marks the workspace cleared and moves to the next epoch (an
+// epoch that wraps to 0 starts again at 1 and drops the mark, so that the
+// next call clears the table).
+__global__ void share_epoch_kernel(uint64_t *__restrict__ magic, uint32_t *__restrict__ epoch)
+{
+    uint32_t e = *magic == kShareMagic ? *epoch + 1u : 1u;
+    uint64_t m = kShareMagic;
+    if (e == 0u) {
+        e = 1u;
+        m = 0ull;
+    }
+    *epoch = e;
+    *magic = m;
+}
+
+// The queries in the kernel's layout (rows of hbytes, zero padded).
+__global__ void share_copy_kernel(const char *__restrict__ h, int row_bytes, int hbytes, char *__restrict__ hq)
+{
+    const int64_t b = blockIdx.x;
+    for (int i = threadIdx.x; i < hbytes; i += blockDim.x) hq[b * hbytes + i] = i < row_bytes ? h[b * row_bytes + i] : 0;
+}
+
+// The kernels that prepare a row-sharing search, on stream s.
+hipError_t share_prepare(const HnswLaunch &a, const ShareLayout &l, hipStream_t s)
+{
+    const size_t n16 = l.clear_bytes / 16;
+    share_clear_kernel<<<1024, 256, 0, s>>>(l.magic, reinterpret_cast<uint4 *>(l.hq), n16);
+    share_epoch_kernel<<<1, 1, 0, s>>>(l.magic, l.epoch);
+    const int row_bytes = a.d * elem_bytes(a.dtype);
+    share_copy_kernel<<<a.B, 256, 0, s>>>(static_cast<const char *>(a.h), row_bytes, (row_bytes + 15) & ~15, l.hq);
+    if (a.q8) {
+        const int grid = (a.B + kQuantWaves - 1) / kQuantWaves;
+        if (a.dtype == VIE_BF16)
+            quantize_kernel<true><<<grid, kQuantWaves * kWave, 0, s>>>(a.h, a.B, a.d, l.hq8, l.hscale);
+        else
+            quantize_kernel<false><<<grid, kQuantWaves * kWave, 0, s>>>(a.h, a.B, a.d, l.hq8, l.hscale);
+    }
+    return hipGetLastError();
+}
+}  // namespace
+
+size_t hnsw_share_workspace_bytes(int B, int64_t V, int d, int dtype, bool q8, int share)
+{
+    if (share <= 1) return 0;
+    const size_t hbytes = (size_t)((d * elem_bytes(dtype) + 15) & ~15);
+    return 256 + round256((size_t)B * hbytes) + (q8 ? round256((size_t)B * d) + round256((size_t)B * 4) : 0) +
+           round256((size_t)B * V * 8);
+}
+
+namespace {
 template <int NT, int VEC, bool BF16, int G>
 hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
 {
-    if (a.width > 1 || a.q8 || a.team > 1) {
-        auto kern = a.q8 ? hnsw_multi_kernel<NT, VEC, BF16, G, true> : hnsw_multi_kernel<NT, VEC, BF16, G, false>;
+    if (a.width > 1 || a.q8 || a.team > 1 || a.share > 1) {
+        auto kern = a.share > 1 ? (a.q8 ? hnsw_multi_kernel<NT, VEC, BF16, G, true, true>
+                                        : hnsw_multi_kernel<NT, VEC, BF16, G, false, true>)
+                                : (a.q8 ? hnsw_multi_kernel<NT, VEC, BF16, G, true, false>
+                                        : hnsw_multi_kernel<NT, VEC, BF16, G, false, false>);
         if (lds > 64 * 1024) {
             hipError_t e =
                 hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -2678,11 +2939,18 @@ hipError_t hnsw_launch(const HnswLaunch &a, size_t lds, hipStream_t s)
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
+        ShareArgs share{1, a.B, nullptr, nullptr, nullptr, nullptr, nullptr};
+        if (a.share > 1) {
+            const ShareLayout l = share_layout(a.share_ws, a);
+            hipError_t e = share_prepare(a, l, s);
+            if (e != hipSuccess) return e;
+            share = ShareArgs{a.share, a.B, l.table, l.epoch, l.hq, l.hq8, l.hscale};
+        }
         kern<<<a.B * team.size, NT, lds, s>>>(static_cast<const char *>(a.W), a.V, a.d * elem_bytes(a.dtype), a.adj0,
                                                a.M0, a.upper_off, a.upper, a.M, a.maxlevel, a.entry,
                                                static_cast<const char *>(a.h), a.k, a.ef_eff, a.width, a.ids,
                                                a.logits, a.ldo, a.stats, a.q8, a.q8scale, a.trace, a.trace_cap,
-                                               team);
+                                               team, share);
         return hipGetLastError();
     }
     auto kern = hnsw_kernel<NT, VEC, BF16, G>;
@@ -2768,8 +3036,13 @@ vie_status launch_hnsw_search(const HnswLaunch &a, hipStream_t s)
         return fail(VIE_EUNSUPPORTED, "HNSW search: team of %d workgroups is not a power of two in 1..%d", a.team,
                     kMaxTeam);
     if (a.team > 1 && !a.team_ws) return fail(VIE_EINVAL, "a team search needs its workspace");
-    const bool multi = a.width > 1 || a.q8 || a.team > 1;
-    const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8, a.team)
+    if (a.share < 1 || a.share > kMaxShare || (a.share & (a.share - 1)))
+        return fail(VIE_EUNSUPPORTED, "HNSW search: row-sharing groups of %d queries (not a power of two up to %d)",
+                    a.share, kMaxShare);
+    if (a.share > 1 && (a.team > 1 || !a.share_ws))
+        return fail(VIE_EINVAL, "row sharing needs its workspace and one workgroup per query");
+    const bool multi = a.width > 1 || a.q8 || a.team > 1 || a.share > 1;
+    const size_t lds = multi ? hnsw_multi_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M, a.width, a.q8, a.team, a.share)
                              : hnsw_lds_bytes(a.V, a.d, a.dtype, a.ef_eff, a.M0, a.M);
     const size_t lim = hnsw_lds_limit();
     if (lds > lim)

@@ -28,7 +28,7 @@ class VieError(RuntimeError):
 class SearchParams(C.Structure):
     _fields_ = [("expand_width", C.c_int32), ("int8_rows", C.c_int32), ("trace_dev", C.c_void_p),
                 ("trace_cap", C.c_int32), ("team", C.c_int32), ("workspace_dev", C.c_void_p),
-                ("workspace_bytes", C.c_size_t)]
+                ("workspace_bytes", C.c_size_t), ("share", C.c_int32)]
 
 
 class BuildParams(C.Structure):
@@ -206,36 +206,38 @@ class Index:
         _check(lib.vie_index_attach_int8(self._h, _dev_ptr(q, "q"), _dev_ptr(scale, "scale")))
         self._q8 = (q, scale)
 
-    def _params(self, h, B: int, k: int, ef: int, width: int, int8: bool, trace, team: int) -> SearchParams:
+    def _params(self, h, B: int, k: int, ef: int, width: int, int8: bool, trace, team: int,
+                share: int = 1) -> SearchParams:
         prm = SearchParams(width, int(int8), None if trace is None else _dev_ptr(trace, "trace"),
-                           0 if trace is None else trace.shape[1], team, None, 0)
-        if team > 1:
+                           0 if trace is None else trace.shape[1], team, None, 0, share)
+        if team > 1 or share > 1:
             n = C.c_size_t()
             _check(lib.vie_query_workspace(self._h, B, k, ef, C.byref(prm), C.byref(n)))
-            ws = getattr(self, "_team_ws", None)
+            ws = getattr(self, "_ws", None)
             if ws is None or ws.numel() < n.value or ws.device != h.device:
                 ws = _torch().empty(n.value, dtype=_torch().uint8, device=h.device)
-                self._team_ws = ws
+                self._ws = ws
             prm.workspace_dev = _dev_ptr(ws, "workspace")
             prm.workspace_bytes = ws.numel()
         return prm
 
     def query_into(self, h, k: int, ef: int, ids, logits, stats=None, width: int = 1, int8: bool = False,
-                   trace=None, team: int = 1) -> None:
+                   trace=None, team: int = 1, share: int = 1) -> None:
         """HNSW top-k of h [B, d] into preallocated ids int32 [B, k], logits fp32 [B, k]
         (and stats uint32-as-int32 [B, 2]) on the current stream; width > 1
         expands that many beam entries per layer-0 step, int8 walks layer 0 on
         the attached int8 rows, trace (int32 [B, cap]) receives each query's
         expansions as (layer << 27) | node, team > 1 searches each query with
-        that many workgroups (vie_query_ex; the index keeps the team
-        workspace, so team searches of one index must not overlap in time)."""
+        that many workgroups, share > 1 lets groups of that many queries
+        share the rows they fetch (vie_query_ex; the index keeps the
+        workspace, so such searches of one index must not overlap in time)."""
         B = h.shape[0]
         sp = None if stats is None else _dev_ptr(stats, "stats")
-        if width == 1 and not int8 and trace is None and team <= 1:
+        if width == 1 and not int8 and trace is None and team <= 1 and share <= 1:
             _check(lib.vie_query(self._h, _dev_ptr(h, "h"), B, k, ef, _dev_ptr(ids, "ids"),
                                  _dev_ptr(logits, "logits"), sp, _stream(h)))
         else:
-            prm = self._params(h, B, k, ef, width, int8, trace, team)
+            prm = self._params(h, B, k, ef, width, int8, trace, team, share)
             _check(lib.vie_query_ex(self._h, _dev_ptr(h, "h"), B, k, ef, C.byref(prm), _dev_ptr(ids, "ids"),
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
@@ -252,7 +254,7 @@ class Index:
                                     _dev_ptr(logits, "logits"), sp, _stream(h)))
 
     def query(self, h, k: int, ef: int, stats: bool = False, width: int = 1, int8: bool = False,
-              trace_cap: int = 0, team: int = 1):
+              trace_cap: int = 0, team: int = 1, share: int = 1):
         """(ids, logits), plus stats if asked, plus the expansion trace
         [B, trace_cap] (-1 past the last expansion) if trace_cap > 0."""
         torch = _torch()
@@ -263,7 +265,7 @@ class Index:
         lg = torch.empty((B, k), dtype=torch.float32, device=h.device)
         st = torch.empty((B, 2), dtype=torch.int32, device=h.device) if stats else None
         tr = torch.full((B, trace_cap), -1, dtype=torch.int32, device=h.device) if trace_cap > 0 else None
-        self.query_into(h, k, ef, ids, lg, st, width, int8, tr, team)
+        self.query_into(h, k, ef, ids, lg, st, width, int8, tr, team, share)
         out = (ids, lg) + ((st,) if stats else ())
         return out + (tr,) if tr is not None else out
 

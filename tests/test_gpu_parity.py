@@ -206,7 +206,7 @@ def _load_on_gpu(vie, g, W, dtype, tmp):
     return ix
 
 
-def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None, team=1):
+def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None, team=1, share=1):
     """One launch of the search variant (width expansions per layer-0 step;
     int8 = the oracle's (rows, scales) when layer 0 walks int8 rows) against
     the oracle's search of the same variant on the same graph.  A query
@@ -222,7 +222,8 @@ def _compare_hnsw(vie, ix, W, dtype, g, H, k, ef, what, width=1, int8=None, team
     ef_eff = max(ef, k)
     cap = ef_eff + 1024
     h = dev_tensor(vie, H, dtype)
-    ids, lg, st, tr = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None, trace_cap=cap, team=team)
+    ids, lg, st, tr = ix.query(h, k, ef, stats=True, width=width, int8=int8 is not None, trace_cap=cap, team=team,
+                               share=share)
     torch.cuda.synchronize()
     ids, lg, st, tr = (ids.cpu().numpy(), lg.cpu().numpy(), st.cpu().numpy().astype(np.uint32),
                        tr.cpu().numpy())
@@ -342,6 +343,41 @@ def test_hnsw_team_equals_one_workgroup(vie, team):
     b = ix.query(h[:1], 10, 50)
     torch.cuda.synchronize()
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("dtype,d", [(synth.BF16, 96), (synth.F32, 64)])
+def test_hnsw_row_sharing_equals_independent(vie, dtype, d):
+    """Queries that share fetched rows in groups (a row fetched for one query
+    is scored for every query of its group, the others' scores published in
+    the workspace) walk exactly the paths of independent workgroups: ids,
+    logits, stats and expansion records bitwise equal to share = 1, for
+    groups of 2, 4 and 16 with a partial last group, on stored and int8
+    rows, across calls that reuse the workspace; and against the oracle."""
+    V = 6000
+    W = synth.make_w(V, d, dtype, 1900 + d)
+    H, _ = synth.make_queries(W, dtype, 23, 1901 + d)
+    g = O.hnsw_build(W, dtype, 8, 40, 5)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, dtype, tmp)
+    h = dev_tensor(vie, H, dtype)
+    oq, osc = O.quantize_rows(W, dtype)
+    q8, sc = vie.quantize_rows(ix._W_dev, dtype)
+    for int8 in (False, True):
+        ix.attach_int8(q8, sc) if int8 else ix.attach_int8(None, None)
+        for width in (1, 8, 64):
+            for k, ef in [(10, 10), (50, 200), (50, 600)]:
+                one = ix.query(h, k, ef, stats=True, width=width, int8=int8, trace_cap=ef + 1024)
+                for share in (2, 4, 16):
+                    what = "share=%d int8=%d width=%d k=%d ef=%d" % (share, int8, width, k, ef)
+                    many = ix.query(h, k, ef, stats=True, width=width, int8=int8, trace_cap=ef + 1024, share=share)
+                    torch.cuda.synchronize()
+                    for a, b, name in zip(one, many, ("ids", "logits", "stats", "trace")):
+                        a, b = a.cpu().numpy(), b.cpu().numpy()
+                        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), "%s: %s differ" % (what, name)
+            say("  share int8=%d width=%d equal to independent workgroups" % (int8, width))
+        _compare_hnsw(vie, ix, W, dtype, g, H, 50, 200, "share=4 int8=%d vs oracle" % int8, width=8,
+                      int8=(oq, osc) if int8 else None, share=4)
+    ix.attach_int8(None, None)
 
 
 def test_hnsw_team_too_large_is_refused(vie):

@@ -179,6 +179,17 @@ def test_calls_fail_synchronously_before_any_hip_call():
             assert n.value == up(3 * 3 * 4 * slot * 8) + up(3 * 3 * 4 * 8)
     prm = vie.SearchParams(1, 0, None, 0, 4, C.c_void_p(4096 * 16), 16)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.ESTATE
+    for share, team, ws, want in [(3, 0, 4096 * 16, vie.EINVAL), (32, 0, 4096 * 16, vie.EINVAL),
+                                  (-2, 0, 4096 * 16, vie.EINVAL), (2, 2, 4096 * 16, vie.EINVAL),
+                                  (2, 0, 0, vie.EINVAL), (2, 0, 4096 + 8, vie.EINVAL), (2, 1, 4096 * 16, vie.ESTATE)]:
+        prm = vie.SearchParams(1, 0, None, 0, team, C.c_void_p(ws) if ws else None, 1 << 30, share)
+        assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == want, (share, team)
+    up = lambda b: (b + 255) // 256 * 256  # noqa: E731
+    for int8 in (0, 1):  # header, queries (rows of 16-byte multiples), int8 queries and scales, score table
+        prm = vie.SearchParams(8, int8, None, 0, 0, None, 0, 4)
+        assert L.vie_query_workspace(ix._h, 5, 10, 20, C.byref(prm), C.byref(n)) == vie.OK
+        want = 256 + up(5 * 32) + (up(5 * 8) + up(5 * 4) if int8 else 0) + up(5 * 300 * 8)
+        assert n.value == want, (int8, n.value, want)
     prm = vie.SearchParams(1, 0, None, 0, 40)
     assert L.vie_query_workspace(ix._h, 3, 10, 20, C.byref(prm), C.byref(n)) == vie.EINVAL
     assert L.vie_query_workspace(ix._h, 3, 10, 20, None, C.byref(n)) == vie.EINVAL

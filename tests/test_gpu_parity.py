@@ -313,10 +313,12 @@ def test_hnsw_team_equals_one_workgroup(vie, team):
     nodes, all exchanging the keys that can enter the beam) walks the same
     path as one workgroup: ids, logits, stats and expansion records are
     bitwise those of team = 1, for the sequential and wide steps on bf16
-    and int8 rows, and the team's search matches the oracle."""
+    and int8 rows, and the team's search matches the oracle.  (All B x team
+    workgroups must be resident at once: at most two 1024-thread workgroups
+    per CU, so the batch shrinks as the team grows.)"""
     V, d = 6000, 96
     W = synth.make_w(V, d, synth.BF16, 1880)
-    H, _ = synth.make_queries(W, synth.BF16, 24, 1881)
+    H, _ = synth.make_queries(W, synth.BF16, min(24, 256 // team), 1881)
     g = O.hnsw_build(W, synth.BF16, 8, 40, 5)
     with tempfile.TemporaryDirectory() as tmp:
         ix = _load_on_gpu(vie, g, W, synth.BF16, tmp)
@@ -707,8 +709,9 @@ def _variants(vie, ix, W, dtype, g, H, k, ef, what, widths=(1, 8), int8=True):
 
 @pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
 def test_hnsw_batches_of_256_and_more(vie, dtype):
-    """300 queries in one launch take the 256-thread workgroups of every
-    search variant; each query still walks the oracle's path."""
+    """300 queries in one launch (more workgroups than the device holds at
+    once) in every search variant; each query still walks the oracle's
+    path."""
     say("hnsw B=300", dtype)
     V, d, B = 8000, 256, 300
     W = synth.make_w(V, d, dtype, 1500)
@@ -717,6 +720,19 @@ def test_hnsw_batches_of_256_and_more(vie, dtype):
     g = _library_graph(ix, W, dtype, 60, 1502)
     ix.to_device(dev_tensor(vie, W, dtype))
     _variants(vie, ix, W, dtype, g, H, 50, 128, "B=300", widths=(1, 8, 32))
+
+
+def test_hnsw_large_batches_with_wide_beams(vie):
+    """260 queries whose beams take more than half of a CU's LDS (one
+    workgroup per CU at a time); every variant still walks the oracle's
+    path."""
+    V, d, B = 8000, 128, 260
+    W = synth.make_w(V, d, synth.BF16, 1700)
+    H, _ = synth.make_queries(W, synth.BF16, B, 1701)
+    ix = vie.Index.build(W, synth.BF16, 16, 60, seed=1702, n_threads=16)
+    g = _library_graph(ix, W, synth.BF16, 60, 1702)
+    ix.to_device(dev_tensor(vie, W, synth.BF16))
+    _variants(vie, ix, W, synth.BF16, g, H, 50, 5000, "B=260 ef=5000", widths=(1, 8))
 
 
 @pytest.mark.parametrize("d", [640, 1024, 2048, 3072])

@@ -8,7 +8,7 @@ ef_construction = 200, built by the library on the host CPUs.
 
 The beam width is the one the method needs: for each traversal (the
 sequential search; 8, 32 or 64 expansions per step; 8, 16, 32 or 64 per step
-on int8 rows with the exact re-rank) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
+on int8 rows with the exact re-rank; 128 per step in teams only) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
 0.95 on the first 128 queries (recall against the exact dense head, itself
 parity-tested against the oracle).  The team traversals (32 workgroups
 sharing each query's row scoring) walk exactly the path of their
@@ -62,15 +62,18 @@ TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0, w
     "int8_width32": (32, True, 1),
     "int8_width64": (64, True, 1),
     "width64_team%d" % TEAM: (64, False, TEAM),
+    "width128_team%d" % TEAM: (128, False, TEAM),
     "int8_width32_team%d" % TEAM: (32, True, TEAM),
     "int8_width64_team%d" % TEAM: (64, True, TEAM),
+    "int8_width128_team%d" % TEAM: (128, True, TEAM),
 }
 
 
 def solo_of(trav):
-    """The one-workgroup traversal a team traversal reproduces exactly."""
+    """The one-workgroup traversal a team traversal reproduces exactly (None
+    when there is none: 128 per step needs a team's smaller LDS)."""
     width, int8, _ = TRAVERSALS[trav]
-    return next(t for t, v in TRAVERSALS.items() if v == (width, int8, 1))
+    return next((t for t, v in TRAVERSALS.items() if v == (width, int8, 1)), None)
 
 
 def kernel_of(trav):
@@ -301,7 +304,7 @@ def main() -> int:
             chosen[trav] = args.ef
             continue
         tried = {}
-        if TRAVERSALS[trav][2] > 1:  # the same results as its one-workgroup twin: time it at that ef
+        if TRAVERSALS[trav][2] > 1 and solo_of(trav):  # the results of its one-workgroup twin: time it at that ef
             ef = chosen.get(solo_of(trav))
             if ef:
                 us = back_to_back(lambda c: search_into(ix, trav, ef, c, ci[c:c + 1], cl[c:c + 1]), nc)
@@ -330,7 +333,7 @@ def main() -> int:
     if args.traversal:
         head_trav = args.traversal
     elif args.ef:
-        head_trav = "int8_width64_team%d" % TEAM if qrows is not None else "width64_team%d" % TEAM
+        head_trav = "int8_width128_team%d" % TEAM if qrows is not None else "width128_team%d" % TEAM
     else:
         head_trav = min(reachable, key=lambda t: calib[t]["tried"][str(chosen[t])]["us_per_query"])
     ef = chosen[head_trav]
@@ -353,10 +356,11 @@ def main() -> int:
     # every query once (untimed) for recall, counts and expansion records
     cap = max(ef, k) + 1024
     trace = torch.full((Q, cap), -1, dtype=torch.int32, device=dev)
-    for q0 in range(0, Q, 256):
-        width, int8, _ = TRAVERSALS[head_trav]
-        ix.query_into(Hd[q0:q0 + 256], k, ef, hi[q0:q0 + 256], hl[q0:q0 + 256], hs[q0:q0 + 256], width, int8,
-                      trace[q0:q0 + 256])
+    width, int8, team = TRAVERSALS[head_trav]
+    tb = max(1, 256 // team)  # queries per launch: every team member resident at once
+    for q0 in range(0, Q, tb):
+        ix.query_into(Hd[q0:q0 + tb], k, ef, hi[q0:q0 + tb], hl[q0:q0 + tb], hs[q0:q0 + tb], width, int8,
+                      trace[q0:q0 + tb], team)
     head_ids, head_lg = hi.cpu().numpy(), hl.cpu().numpy()
     head_st = hs.cpu().numpy().astype(np.int64)
     head_tr = trace.cpu().numpy()
@@ -449,12 +453,17 @@ def main() -> int:
                 ix32.attach_int8(q32, s32)
             f_i, f_l, _ = out_bufs(n32)
             fw, f8, ft = TRAVERSALS[f_trav]
-            hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None, fw,
-                                                        f8, None, ft), n32)
+            try:
+                hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None,
+                                                            fw, f8, None, ft), n32)
+            except vie.VieError:  # fp32 queries take twice the LDS: 64 per step then
+                fw = 64
+                hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None,
+                                                            fw, f8, None, ft), n32)
             legs["fp32_rows"] = {
                 "W_bytes": wl.V * wl.d * 4, "queries": n32, "dense_us_per_query": pct(dcalls),
                 "dense_hbm_frac": round(wl.V * wl.d * 4 / (np.median(dcalls) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-                "hnsw": {"traversal": f_trav, "ef": ef, "us_per_query": pct(hcalls),
+                "hnsw": {"traversal": f_trav, "expansions_per_step": fw, "ef": ef, "us_per_query": pct(hcalls),
                          "recall_at_k": round(recall(f_i.cpu().numpy(), ex32), 4)},
                 "graph_build_s": None if b32 is None else round(b32, 1)}
             del ix32, W32d, H32d, h32
@@ -486,19 +495,23 @@ def main() -> int:
         torch.cuda.synchronize()
         a, b = events(2)
         w8, i8, _ = TRAVERSALS[head_trav]  # one workgroup per query: 1024 queries fill the device
+        w8 = min(w8, 64)  # (128 per step fits only a team's LDS)
         ix.query_into(Hd, k, ef, hi, hl, hs, w8, i8)
         a.record(stream)
         ix.query_into(Hd, k, ef, hi, hl, hs, w8, i8)
         b.record(stream)
         torch.cuda.synchronize()
         one_launch_s = a.elapsed_time(b) * 1e-3
-        legs["one_launch"] = {"queries": Q, "queries_per_s": round(Q / one_launch_s, 1),
-                              "hbm_frac": round(float(head_bytes.sum()) / one_launch_s / 1e9 / HBM_PEAK_GBS, 4)}
+        # its algorithmic bytes: the headline's, scaled by this walk's distance evaluations
+        ol_bytes = float(head_bytes.sum()) * float(hs[:, 0].double().mean()) / float(nd.mean())
+        legs["one_launch"] = {"queries": Q, "expansions_per_step": w8, "queries_per_s": round(Q / one_launch_s, 1),
+                              "hbm_frac": round(ol_bytes / one_launch_s / 1e9 / HBM_PEAK_GBS, 4)}
 
         # ---- row sharing between the queries of one launch ------------------
         if args.share_groups:
             rs = {}
             w8, i8, _ = TRAVERSALS[head_trav]
+            w8 = min(w8, 64)
             for Bc in [b for b in (64, 256, 1024) if b <= Q]:
                 row, ref = {}, None
                 for sh in [1] + args.share_groups:
@@ -515,8 +528,8 @@ def main() -> int:
                     row[str(sh)] = {"ms_per_launch": round(ms, 3), "queries_per_s": round(Bc / ms * 1e3, 1),
                                     "same_results": all(np.array_equal(a, b) for a, b in zip(out, ref))}
                 rs[str(Bc)] = row
-            legs["row_sharing"] = {"traversal": "%s, one workgroup per query" % head_trav.split("_team")[0], "ef": ef,
-                                   "share": rs}
+            legs["row_sharing"] = {"traversal": "%swidth%d, one workgroup per query" % ("int8_" if i8 else "", w8),
+                                   "ef": ef, "share": rs}
 
         # ---- batch graph built on the GPU, searched at B = 1 ----------------
         if args.batch_graph_k:

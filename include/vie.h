@@ -193,7 +193,7 @@ vie_status vie_query(const vie_index *index, const void *h_dev, int32_t B, int32
 
 /* Options of vie_query_ex and vie_query_forced. */
 typedef struct {
-    int32_t expand_width; /* beam entries expanded per layer-0 step, 1..64 */
+    int32_t expand_width; /* beam entries expanded per layer-0 step, 1..128 */
     int32_t int8_rows;    /* 1: layer-0 scores from the int8 rows attached with
                              vie_index_attach_int8, final beam re-ranked on
                              the stored rows; 0: stored rows throughout */
@@ -268,7 +268,7 @@ vie_status vie_query_workspace(const vie_index *index, int32_t B, int32_t k, int
  * it independently.  Limits as vie_query, and LDS must also hold about
  * 16 bytes per claimed neighbour (expand_width * M0 of them).
  * Errors: as vie_query; VIE_EINVAL also for params NULL or expand_width
- * outside 1..64. */
+ * outside 1..128. */
 vie_status vie_query_ex(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,
                         const vie_search_params *params, int32_t *ids_dev, float *logits_dev,
                         uint32_t *stats_dev, void *hip_stream);

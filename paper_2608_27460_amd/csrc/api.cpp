@@ -262,8 +262,8 @@ vie_status query_impl(const vie_index *ix, const void *h_dev, int32_t B, int32_t
 vie_status check_params(const vie_search_params *params)
 {
     if (!params) return VIE_OK;
-    if (params->expand_width < 1 || params->expand_width > 64)
-        return fail(VIE_EINVAL, "expand_width = %d outside 1..64", params->expand_width);
+    if (params->expand_width < 1 || params->expand_width > 128)
+        return fail(VIE_EINVAL, "expand_width = %d outside 1..128", params->expand_width);
     if (params->int8_rows != 0 && params->int8_rows != 1)
         return fail(VIE_EINVAL, "int8_rows = %d is neither 0 nor 1", params->int8_rows);
     if (params->trace_dev && params->trace_cap < 1)
@@ -288,8 +288,8 @@ vie_status vie_query_workspace(const vie_index *ix, int32_t B, int32_t k, int32_
 {
     g_last_error.clear();
     if (!ix || !params || !bytes) return fail(VIE_EINVAL, "NULL argument");
-    if (params->expand_width < 1 || params->expand_width > 64)
-        return fail(VIE_EINVAL, "expand_width = %d outside 1..64", params->expand_width);
+    if (params->expand_width < 1 || params->expand_width > 128)
+        return fail(VIE_EINVAL, "expand_width = %d outside 1..128", params->expand_width);
     if (params->team < 0 || params->team > kMaxTeam || (params->team & (params->team - 1)))
         return fail(VIE_EINVAL, "team = %d is neither 0 nor a power of two up to %d", params->team, kMaxTeam);
     if (params->share < 0 || params->share > kMaxShare || (params->share & (params->share - 1)))

@@ -1635,7 +1635,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 // of its lists there; the rest come from HBM.  Rows: each group keeps two
 // rows' loads in flight.
 
-constexpr int kMaxWidth = 64;       // widest expansion step
+constexpr int kMaxWidth = 128;      // widest expansion step
 constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
 
@@ -1832,6 +1832,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int hbytes = (row_bytes + 15) & ~15;
     const int vwords = (int)((V + 31) / 32);
     const int cap = width * M0;  // most nodes claimed in one step
+    // cache slots a flag byte can name (slot + 1 in its upper seven bits)
+    const int hints = width < 127 ? width : 127;
     // t / M0 for t < 2^15 (M0 <= 256) as a multiply-high by this magic number
     const uint32_t m0_magic = (uint32_t)(((1ull << 32) + (uint32_t)M0 - 1u) / (uint32_t)M0);
     const int nid = cap > M ? cap : M;
@@ -2229,7 +2231,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             for (int x = 0; x < kMultiHeld; ++x)
                 if (rk[x] != 0ull) {
                     const int above = kept_above(rk[x]);
-                    if (above < width) {
+                    if (above < hints) {
 #pragma unroll
                         for (int u = 0; u < PF; ++u) {
                             const int t = gl + u * G;
@@ -2259,7 +2261,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 beam2[pos] = key;
                 // unexpanded; the best `width` kept keys name the cache slot
                 // that may hold their list
-                flag2[pos] = above < width ? (uint8_t)((above + 1) << 1) : (uint8_t)0;
+                flag2[pos] = above < hints ? (uint8_t)((above + 1) << 1) : (uint8_t)0;
                 if (above == 0) atomicMin(&sh.first, (uint32_t)pos);
             }
         }

@@ -287,7 +287,7 @@ def test_hnsw_matches_oracle_on_oracle_graph(vie, V, d, dtype, M, efC):
             assert np.array_equal(i1.cpu().numpy()[0], ids_b.cpu().numpy()[q])
 
 
-@pytest.mark.parametrize("width", [2, 3, 4, 8, 13, 32, 64])
+@pytest.mark.parametrize("width", [2, 3, 4, 8, 13, 32, 64, 128])
 def test_hnsw_multi_expansion_matches_oracle(vie, width):
     """Several expansions per step follow the oracle's multi-expansion search
     (same visits and counts), with the list cache and ragged picks."""
@@ -327,7 +327,7 @@ def test_hnsw_team_equals_one_workgroup(vie, team):
     q8, sc = vie.quantize_rows(ix._W_dev, synth.BF16)
     for int8 in (False, True):
         ix.attach_int8(q8, sc) if int8 else ix.attach_int8(None, None)
-        for width in (1, 8, 32, 64):
+        for width in (1, 8, 64, 128):
             for k, ef in [(10, 10), (50, 200), (50, 600)]:
                 what = "team=%d int8=%d width=%d k=%d ef=%d" % (team, int8, width, k, ef)
                 say(what)

@@ -147,8 +147,8 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query(None, fake, 1, 10, 10, fake, fake, None, None) == vie.EINVAL
     prm = vie.SearchParams(0)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # width 0
-    prm = vie.SearchParams(65)
-    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # width 65
+    prm = vie.SearchParams(129)
+    assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # width 129
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, None, fake, fake, None, None) == vie.EINVAL
     prm = vie.SearchParams(4)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.ESTATE

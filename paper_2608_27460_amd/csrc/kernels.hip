@@ -1957,8 +1957,9 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         const int total = (int)s_xoff[T];
         for (int j = tid; j < total; j += NT) {
-            int o = 0;  // the member whose keys hold entry j
-            while ((int)s_xoff[o + 1] <= j) ++o;
+            int o = 0;  // the member whose keys hold entry j: the last with s_xoff[o] <= j
+            for (int step = kMaxTeam / 2; step > 0; step >>= 1)
+                if (o + step < T && (int)s_xoff[o + step] <= j) o += step;
             const uint64_t *ok = team.keys + (base + o) * team.slot;
             dst[mine + j] = __hip_atomic_load(ok + (j - (int)s_xoff[o]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
@@ -2772,13 +2773,17 @@ size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int
     return n + (size_t)((V + 31) / 32) * 4;
 }
 
+// LDS a search workgroup may take for its dynamic carve-up: the device's
+// per-block limit less a reserve for the kernels' static variables (about
+// 1.4 KB in hnsw_multi_kernel: shared counters, picks, cache ids, team offsets).
 size_t hnsw_lds_limit()
 {
+    constexpr int kStaticReserve = 2048;
     int dev = 0, v = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 64 * 1024;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
-        return 64 * 1024;
-    return (size_t)v;
+    if (hipGetDevice(&dev) != hipSuccess) return 64 * 1024 - kStaticReserve;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= kStaticReserve)
+        return 64 * 1024 - kStaticReserve;
+    return (size_t)(v - kStaticReserve);
 }
 
 namespace {

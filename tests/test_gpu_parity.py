@@ -307,7 +307,7 @@ def test_hnsw_multi_expansion_matches_oracle(vie, width):
                 (what, parity.recall(ids, exact[:, :k]), st[:, 0].mean(), st[:, 1].mean()))
 
 
-@pytest.mark.parametrize("team", [2, 4, 32])
+@pytest.mark.parametrize("team", [2, 4, 32, 64])
 def test_hnsw_team_equals_one_workgroup(vie, team):
     """A team of workgroups per query (each scoring its share of the new
     nodes, all exchanging the keys that can enter the beam) walks the same
@@ -380,6 +380,31 @@ def test_hnsw_row_sharing_equals_independent(vie, dtype, d):
         _compare_hnsw(vie, ix, W, dtype, g, H, 50, 200, "share=4 int8=%d vs oracle" % int8, width=8,
                       int8=(oq, osc) if int8 else None, share=4)
     ix.attach_int8(None, None)
+
+
+def test_hnsw_lds_at_the_limit_is_refused_cleanly(vie):
+    """Beams whose LDS carve-up lands within a couple of KB of the per-block
+    limit (where the kernels' static variables no longer fit beside it):
+    every call either runs or is refused with VIE_EUNSUPPORTED before any
+    launch, never a failed launch."""
+    V, d = 3000, 3072
+    W = synth.make_w(V, d, synth.F32, 1910)
+    H, _ = synth.make_queries(W, synth.F32, 2, 1911)
+    g = O.hnsw_build(W, synth.F32, 32, 40, 5)
+    with tempfile.TemporaryDirectory() as tmp:
+        ix = _load_on_gpu(vie, g, W, synth.F32, tmp)
+    h = dev_tensor(vie, H, synth.F32)
+    seen = set()
+    for ef in range(2800, 3000, 8):
+        try:
+            ids, _ = ix.query(h, 10, ef, width=128, team=2)
+            torch.cuda.synchronize()
+            assert (ids.cpu().numpy() >= 0).all()
+            seen.add("ok")
+        except vie.VieError as e:
+            assert e.status == vie.EUNSUPPORTED, (ef, str(e))
+            seen.add("refused")
+    assert seen == {"ok", "refused"}, seen  # the sweep crosses the limit
 
 
 def test_hnsw_team_too_large_is_refused(vie):

@@ -1638,6 +1638,7 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 constexpr int kMaxWidth = 128;      // widest expansion step
 constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
+constexpr int kClaimBatch = 4;      // list entries a thread claims together
 
 // <row a, h> and <row b, h> (b < 0: only a) with both rows' chunks loaded
 // before either is used (chunks past the row's end read as zeros), the
@@ -1899,6 +1900,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     const int gl = tid % G;
     const int grp = tid / G;
     uint32_t n_dist = 0, n_expand = 0;
+    uint32_t n_other = 0;  // in a team: this thread's claims of nodes another member scores
     int32_t *trace = trace_all && mem == 0 ? trace_all + (int64_t)q * trace_cap : nullptr;
     // sharing rows: this query's group (queries gq0 .. gq0 + qg - 1) and the launch's epoch
     const int gq0 = SHARE ? q - q % share.size : q;
@@ -2055,26 +2057,47 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         // a pick's list comes from the cache slot its flag names while the
         // cache still holds that node's list, else from HBM.  The first slot
         // of each pick marks it expanded (the other bits of its flag stay).
-        for (int t = tid; t < np * M0; t += NT) {
-            const int j = (int)__umulhi((uint32_t)t, m0_magic), slot = t - j * M0;
-            const int pj = s_pick[j];
-            const int32_t c = key_id(beam[pj]);
-            const int hint = (int)(flag[pj] >> 1) - 1;
-            const int src = hint >= 0 && lc_id[hint] == c ? hint : -1;
-            if (slot == 0) flag[pj] |= 1;
-            // two guarded loads, not one through a selected pointer (that
-            // would be a generic load, which waits on both memory counters)
-            const int32_t ec = src >= 0 ? lcache[max(src, 0) * M0 + slot] : -1;
-            const int32_t eg = src < 0 ? adj0[(int64_t)c * M0 + slot] : -1;
-            const int32_t e = src >= 0 ? ec : eg;
-            if (e >= 0 && claim(vis, e)) {
-                if ((e & (T - 1)) == mem) cid[atomicAdd(&sh.nnew, 1u)] = e;
-                else atomicAdd(&sh.nother, 1u);
+        // A thread loads its kClaimBatch list entries, marks the picks it
+        // meets expanded, issues all its bitmap claims (an OR of zero where
+        // there is no entry), then appends its new nodes: no claim waits
+        // behind another.
+        const int ncl = np * M0;
+        for (int t0 = tid; t0 < ncl; t0 += kClaimBatch * NT) {
+            int32_t ev[kClaimBatch];
+#pragma unroll
+            for (int u = 0; u < kClaimBatch; ++u) {
+                const int t = min(t0 + u * NT, ncl - 1);
+                const int j = (int)__umulhi((uint32_t)t, m0_magic), slot = t - j * M0;
+                const int pj = s_pick[j];
+                const int32_t c = key_id(beam[pj]);
+                const int hint = (int)(flag[pj] >> 1) - 1;
+                const int src = hint >= 0 && lc_id[hint] == c ? hint : -1;
+                // two guarded loads, not one through a selected pointer (that
+                // would be a generic load, which waits on both memory counters)
+                const int32_t ec = src >= 0 ? lcache[max(src, 0) * M0 + slot] : -1;
+                const int32_t eg = src < 0 ? adj0[(int64_t)c * M0 + slot] : -1;
+                ev[u] = t0 + u * NT < ncl ? (src >= 0 ? ec : eg) : -1;
             }
+#pragma unroll
+            for (int u = 0; u < kClaimBatch; ++u) {
+                const int t = t0 + u * NT;
+                const int j = (int)__umulhi((uint32_t)t, m0_magic);
+                if (t < ncl && t == j * M0) flag[s_pick[j]] |= 1;
+            }
+            uint32_t old[kClaimBatch];
+#pragma unroll
+            for (int u = 0; u < kClaimBatch; ++u)
+                old[u] = atomicOr(&vis[max(ev[u], 0) >> 5], ev[u] >= 0 ? 1u << (ev[u] & 31) : 0u);
+#pragma unroll
+            for (int u = 0; u < kClaimBatch; ++u)
+                if (ev[u] >= 0 && !(old[u] & (1u << (ev[u] & 31)))) {
+                    if ((ev[u] & (T - 1)) == mem) cid[atomicAdd(&sh.nnew, 1u)] = ev[u];
+                    else ++n_other;
+                }
         }
         __syncthreads();
         const int nn = (int)sh.nnew;  // this member's share of the new nodes
-        n_dist += nn + sh.nother;
+        n_dist += nn;
         const int area = (int)(exchanges & 1);
         uint64_t *xk = T > 1 ? team.keys + (((int64_t)q * 3 + area) * T + mem) * team.slot : nullptr;
         const uint64_t worst = nbeam == (uint32_t)ef ? beam[nbeam - 1] : 0ull;
@@ -2284,7 +2307,6 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (tid == 0) {
             sh.nbeam = (uint32_t)total;
             sh.nnew = 0;  // read after the claim barrier only
-            sh.nother = 0;
             sh.nfetch = 0;
         }
         __syncthreads();
@@ -2296,6 +2318,12 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         flag2 = tf;
     }
 
+    if (T > 1) {  // the other members' new nodes count as distance evaluations too (one add per wave)
+        const uint32_t incl = wave_incl_scan(n_other);
+        if (lane == kWave - 1) atomicAdd(&sh.nother, incl);
+        __syncthreads();
+        n_dist += sh.nother;
+    }
     const int nb = (int)sh.nbeam;
     if (sh.team_err) {  // a team wait ran out: the results say so
         if (mem == 0) {

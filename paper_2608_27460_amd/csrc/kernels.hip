@@ -545,6 +545,13 @@ __device__ __forceinline__ uint64_t wave_bitonic_merge_desc(uint64_t key, int la
     return key;
 }
 
+// The key of lane 63 - lane.
+__device__ __forceinline__ uint64_t lane_reverse(uint64_t v, int lane)
+{
+    const int src = kWave - 1 - lane;
+    return ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(v >> 32), src) << 32) | (uint32_t)__shfl((int)(uint32_t)v, src);
+}
+
 // Adds the keys >= T of rows [row0, row0 + nrows) (clamped to V) of zq to
 // gat; the whole workgroup takes part, kGatherBatch loads in flight per
 // thread.  Element i is row i % rows_per of listed slab i / rows_per.
@@ -1852,8 +1859,8 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
     p += (size_t)ef * 8;
     uint64_t *beam2 = reinterpret_cast<uint64_t *>(p);
     p += (size_t)ef * 8;
-    uint64_t *ckey = reinterpret_cast<uint64_t *>(p);  // padded to whole 64-key runs
-    p += (size_t)((cap + kWave - 1) & ~(kWave - 1)) * 8;
+    uint64_t *ckey = reinterpret_cast<uint64_t *>(p);  // padded to whole 128-key runs
+    p += (size_t)((cap + 2 * kWave - 1) & ~(2 * kWave - 1)) * 8;
     int32_t *cid = reinterpret_cast<int32_t *>(p);
     p += (size_t)nid * 4;
     int32_t *lcache = reinterpret_cast<int32_t *>(p);  // (none in a team)
@@ -2207,14 +2214,21 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             if (sh.team_err) break;
         }
         const int nk = (int)sh.nkeep;
-        // with more than 64 kept keys, each wave sorts a run of 64 of them, so
-        // that a key's rank among the kept keys is a sum of binary searches
-        const int nrun = (nk + kWave - 1) / kWave;
+        // with more than 64 kept keys, each wave sorts runs of 128 of them
+        // (two sorted halves of 64, the second reversed so that the pair is
+        // bitonic, half-cleaned and merged in registers), so that a key's rank
+        // among the kept keys is a sum of binary searches.  (Runs of 256, four
+        // halves per wave, measured slower: the sort outweighs the searches.)
+        constexpr int kRun = 2 * kWave;
+        const int nrun = (nk + kRun - 1) / kRun;
         if (nk > kWave) {
             for (int r = tid / kWave; r < nrun; r += NT / kWave) {
-                const int j = r * kWave + lane;
+                const int j0 = r * kRun + lane, j1 = j0 + kWave;
                 // the last run is padded with zero keys (below every real key)
-                ckey[j] = wave_sort_desc(j < nk ? ckey[j] : 0ull, lane);
+                const uint64_t a = wave_sort_desc(j0 < nk ? ckey[j0] : 0ull, lane);
+                const uint64_t br = lane_reverse(wave_sort_desc(j1 < nk ? ckey[j1] : 0ull, lane), lane);
+                ckey[j0] = wave_bitonic_merge_desc(a > br ? a : br, lane);
+                ckey[j1] = wave_bitonic_merge_desc(a > br ? br : a, lane);
             }
             __syncthreads();
         }
@@ -2224,27 +2238,27 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 for (int t = 0; t < nk; ++t) above += ckey[t] > key;
                 return above;
             }
-            // fixed-step searches of 64-key runs, four runs at a time so that
-            // their LDS loads overlap
+            // fixed-step searches of the 128-key runs, four runs at a time so
+            // that their LDS loads overlap
             int r = 0;
             for (; r + 4 <= nrun; r += 4) {
-                const uint64_t *a = ckey + r * kWave;
+                const uint64_t *a = ckey + r * kRun;
                 int p0 = 0, p1 = 0, p2 = 0, p3 = 0;
 #pragma unroll
-                for (int step = kWave / 2; step > 0; step >>= 1) {
+                for (int step = kRun / 2; step > 0; step >>= 1) {
                     p0 += a[p0 + step - 1] > key ? step : 0;
-                    p1 += a[kWave + p1 + step - 1] > key ? step : 0;
-                    p2 += a[2 * kWave + p2 + step - 1] > key ? step : 0;
-                    p3 += a[3 * kWave + p3 + step - 1] > key ? step : 0;
+                    p1 += a[kRun + p1 + step - 1] > key ? step : 0;
+                    p2 += a[2 * kRun + p2 + step - 1] > key ? step : 0;
+                    p3 += a[3 * kRun + p3 + step - 1] > key ? step : 0;
                 }
-                above += p0 + (a[p0] > key) + p1 + (a[kWave + p1] > key) + p2 + (a[2 * kWave + p2] > key) + p3 +
-                         (a[3 * kWave + p3] > key);
+                above += p0 + (a[p0] > key) + p1 + (a[kRun + p1] > key) + p2 + (a[2 * kRun + p2] > key) + p3 +
+                         (a[3 * kRun + p3] > key);
             }
             for (; r < nrun; ++r) {
-                const uint64_t *a = ckey + r * kWave;
+                const uint64_t *a = ckey + r * kRun;
                 int p = 0;
 #pragma unroll
-                for (int step = kWave / 2; step > 0; step >>= 1) p += a[p + step - 1] > key ? step : 0;
+                for (int step = kRun / 2; step > 0; step >>= 1) p += a[p + step - 1] > key ? step : 0;
                 above += p + (a[p] > key);
             }
             return above;
@@ -2791,7 +2805,7 @@ size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int
     const int row_bytes = d * elem_bytes(dtype);
     const size_t hbytes = (size_t)((row_bytes + 15) & ~15);
     const size_t cap = (size_t)width * M0, nid = cap > (size_t)M ? cap : (size_t)M;
-    const size_t capk = (cap + 63) & ~(size_t)63;
+    const size_t capk = (cap + 127) & ~(size_t)127;
     size_t n = hbytes + (size_t)ef_eff * 8 * 2 + capk * 8 + nid * 4 + (team == 1 ? cap * 4 : 0) +
                (share > 1 ? cap * 4 : 0);
     n = ((n + 7) & ~(size_t)7) + 2 * (((size_t)ef_eff + 7) & ~(size_t)7);  // 8-aligned flag arrays

@@ -225,11 +225,12 @@ typedef struct {
                              wait for another for seconds (the device kept
                              busy by other work), the query's row holds
                              ids -1, logits NaN and stats 0xFFFFFFFF. */
-    void *workspace_dev;  /* team > 1: device buffer of at least
-                             vie_query_workspace() bytes, 256-byte aligned,
-                             caller owned, no initialisation needed; calls
-                             that share it must not overlap in time.
-                             Ignored for team <= 1 and share <= 1. */
+    void *workspace_dev;  /* team > 1 or share > 1: device buffer of at
+                             least vie_query_workspace() bytes, 256-byte
+                             aligned, caller owned, no initialisation
+                             needed; calls that share it must not overlap
+                             in time.  Ignored for team <= 1 and
+                             share <= 1. */
     size_t workspace_bytes;
     int32_t share;        /* row sharing between the call's queries: 1, 2,
                              4, 8 or 16 (0 counts as 1) queries per group
@@ -247,7 +248,9 @@ typedef struct {
                              bytes, 256-byte aligned), which the library
                              clears on its first use and then keeps valid
                              across calls of any index; calls that share it
-                             must not overlap in time. */
+                             must not overlap in time.  Each workgroup also
+                             holds its group's queries in LDS (share times
+                             the query's size). */
 } vie_search_params;
 
 /* Bytes of device workspace that vie_query_ex / vie_query_forced need with
@@ -266,7 +269,11 @@ vie_status vie_query_workspace(const vie_index *index, int32_t B, int32_t k, int
  * sequential traversal as the obstacle to GPU execution, Section 5).  The
  * results follow the same rule on any hardware; the test oracle implements
  * it independently.  Limits as vie_query, and LDS must also hold about
- * 16 bytes per claimed neighbour (expand_width * M0 of them).
+ * 16 bytes per claimed neighbour (expand_width * M0 of them; 12 in a team,
+ * which keeps no list cache): a shape that does not fit is refused with
+ * VIE_EUNSUPPORTED before any launch (on gfx950, 128 per step at
+ * ef_eff = 2048 fits a 128256-row head with bf16 queries of 3072 values
+ * only in a team).
  * Errors: as vie_query; VIE_EINVAL also for params NULL or expand_width
  * outside 1..128. */
 vie_status vie_query_ex(const vie_index *index, const void *h_dev, int32_t B, int32_t k, int32_t ef,

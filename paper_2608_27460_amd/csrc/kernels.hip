@@ -9,10 +9,18 @@
 //                        slabs' candidate lists.
 //   hnsw_kernel          HNSW k-NN search (Sections 2-3; Malkov & Yashunin
 //                        Algorithms 2 and 5), one workgroup per query.
-//   hnsw_multi_kernel    the same search expanding several beam entries per
-//                        layer-0 step, optionally on int8 rows (Section 5's
-//                        open problems: sequential traversal, quantization).
-//   quantize_kernel      per-row scaled int8 copy of W_out.
+//   hnsw_multi_kernel    the same search expanding up to 128 beam entries
+//                        per layer-0 step, optionally on int8 rows, in a
+//                        team of up to 64 workgroups per query that divide
+//                        each step's row scoring, or with the rows a launch's
+//                        queries fetch shared within groups of queries
+//                        (Section 5's open problems: sequential traversal,
+//                        quantization).
+//   team_clear_kernel,   set-up of a team search (published counts zeroed)
+//   share_*_kernel       and of row sharing (workspace cleared once, epoch,
+//                        queries copied).
+//   quantize_kernel      per-row scaled int8 copy of W_out (and of a
+//                        launch's queries for row sharing).
 //   forced_kernel        search result joined with explicitly scored ids
 //                        (Section 3's forced-inclusion tokens).
 //
@@ -1634,13 +1642,20 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 // algorithm), trading a few more distance evaluations for width times fewer
 // dependent steps.
 //
-// Picks: every wave finds the same picks on its own (ballots over the
-// expanded flags, from the best unexpanded entry on), so no barrier publishes
-// them; the picked entries are marked expanded when the beam is merged into
-// its other buffer.  Lists: the groups that score the best `width` new rows
-// keep those rows' lists in a small LDS cache, so the next step reads most
-// of its lists there; the rest come from HBM.  Rows: each group keeps two
-// rows' loads in flight.
+// A step: wave 0 finds the picks (ballots over the expanded flags, from the
+// best unexpanded entry on) and publishes them in LDS behind one barrier;
+// the threads that claim a pick's list mark it expanded; the new rows are
+// scored two per group at a time; the keys that can enter the beam are
+// sorted into runs of 128 and ranked, and beam and kept keys are merged into
+// the other beam buffer.  Lists: the groups that score the best `width` new
+// rows keep those rows' lists in a small LDS cache (one workgroup per query
+// only), so the next step reads most of its lists there; the rest come from
+// HBM.
+//
+// A team (TeamArgs) runs this on several workgroups per query that divide
+// only the scoring and pass each other the kept keys every step; row sharing
+// (ShareArgs) lets the queries of a group reuse each other's scores.  Both
+// leave every decision, and so the traversal, exactly as above.
 
 constexpr int kMaxWidth = 128;      // widest expansion step
 constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first

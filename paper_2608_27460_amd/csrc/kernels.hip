@@ -874,18 +874,27 @@ __global__ __launch_bounds__(kMergeThreads) void dense_merge_kernel(const float 
 // (NQT 16-query tiles) and walks the row width in stages of KC columns.
 //
 // The operand layout of the instruction wants 16 different rows per load,
-// which scatters a wave's accesses over 16 rows; streamed that way W_out
-// reaches barely half of the HBM bandwidth.  So each wave stages its rows
-// through its own slice of LDS: a stage is read with non-temporal loads that
-// cover whole contiguous row segments (the next one or two stages are loaded
-// while the current one is multiplied), written to LDS and read back in operand
-// layout.  The reduction index is free to permute, so lane (r, g) =
-// (lane % 16, lane / 16) takes columns 32 t + 8 g .. + 7 of step t for its
-// row r and the same columns of its query.  The queries' columns of a stage
-// are staged in LDS once for the four waves (read with the row stage, one
-// stage ahead), which keeps the registers for loads in flight.  The slab's
-// logits and two largest keys per query go to the workspace in the layout
-// of the single-query path, and dense_merge_kernel selects the top k.
+// which scatters a wave's accesses over 16 rows (64 bytes of each); loaded
+// that way straight into the operand registers, a 128256 x 3072 bf16 W_out
+// streamed at 3.7-4.8 TB/s per call on MI355X (64 to 4 queries), against
+// 5.0-6.1 TB/s staged.  So each wave stages its rows through its own slice of
+// LDS: a stage is read with non-temporal loads that cover whole contiguous
+// row segments (the next one or two stages are loaded while the current one
+// is multiplied), written to LDS and read back in operand layout: lane
+// (r, g) = (lane % 16, lane / 16) takes columns 32 t + 8 g .. + 7 of step t
+// for its row r and the same columns of its query.  The queries' columns of
+// a stage are staged in LDS once for the four waves (read with the row
+// stage, one stage ahead), which keeps the registers for loads in flight.
+// The slab's logits (16-byte stores) and its kTopR largest keys per query go
+// to the workspace in the layout of the single-query path, and
+// dense_merge_kernel selects the top k.
+//
+// Staged rows are padded by 32 bytes.  A 16-byte LDS read of 64 lanes takes
+// four cycles on gfx950 when no bank is over-used; measured with the LDS
+// counters, the operand read (16 rows, four 16-byte pieces each) takes four
+// cycles when the row pitch is 32 bytes more than a multiple of 64 and eight
+// cycles (half of them bank conflicts) when it is 16 or 48 more, while the
+// stage writes take eight cycles at any of these pitches.
 
 #ifndef VIE_MFMA_MIN_B
 #define VIE_MFMA_MIN_B 3
@@ -924,7 +933,7 @@ constexpr int kMfmaRowsPerIter = kMfmaWaves * kMfmaRowsPerWave;
 static_assert(kMfmaMaxWgs <= kMergeThreads, "the merge gives every slab maximum a thread");
 
 #ifndef VIE_MFMA_PAD
-#define VIE_MFMA_PAD 16
+#define VIE_MFMA_PAD 32
 #endif
 constexpr int mfma_pitch(int KC) { return KC * 2 + VIE_MFMA_PAD; }  // LDS bytes per staged row (padded)
 constexpr size_t mfma_lds(int NQT, int KC)
@@ -964,6 +973,9 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int nrows = (int)max<int64_t>(0, min<int64_t>(rows_per_wg, V - r0));
     const int nstage = (d + KC - 1) / KC;
     const u32x4 zero = {0u, 0u, 0u, 0u};
+    // slab starts are multiples of 128 rows, so with V % 4 == 0 every group
+    // of four rows of a query's logits is 16-byte aligned
+    const bool zvec = (V & 3) == 0 && ((uintptr_t)zout & 15) == 0;
     // W staging: load j of a lane covers row kRowsPerLoad j + srow, 16 bytes
     // at column scol of the stage
     const int srow = lane / kLanesPerRow, scol = 8 * (lane % kLanesPerRow);
@@ -987,100 +999,136 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
         for (int i = 0; i < kTopR; ++i) best[n][i] = 0ull;
 
-    // every wave runs the same number of iterations (the workgroup barriers
-    // need it); rows past the slab are clamped and discarded
-    for (int rb0 = 0; rb0 < nrows; rb0 += kMfmaRowsPerIter) {
-        const int rb = rb0 + wave * kMfmaRowsPerWave;
-        const uint16_t *wrow[kLoads];
+    // The slab's row blocks (kMfmaRowsPerIter rows each) and their stages run
+    // as one sequence of nblk * nstage stages, so the loads of the next
+    // block's first stages are in flight while a block finishes and writes
+    // its logits.  Every wave runs every stage (the workgroup barriers need
+    // it); rows past the slab are clamped and discarded.  W stages run LA
+    // ahead: stage s's loads sit in buffer s % LA (the loop is unrolled over
+    // the buffers, so no in-flight load is ever copied); the query stage runs
+    // one ahead.  Every stage issues the same loads with no branch around
+    // them, in the order they are consumed (columns past the row are clamped
+    // to its last piece and replaced by zeros when staged; the loads past
+    // the last stage re-read one cache line): the compiler then counts the
+    // loads in flight exactly and waits only for the stage being staged, not
+    // for the ones still ahead.
+    const int nblk = (nrows + kMfmaRowsPerIter - 1) / kMfmaRowsPerIter;
+    const int ntot = nblk * nstage;
+    // W load j of a lane reads row wrow[j] of the block being loaded; past
+    // the last block every load reads the first piece of the slab's last
+    // row (one cache line, no HBM traffic to speak of)
+    const int wr = wave * kMfmaRowsPerWave + srow;
+    int la = 0, la_st = 0, la_rb = 0;  // sequence number, stage and block row of the next W stage to load
+    const uint16_t *wrow[kLoads];
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) wrow[j] = W + (r0 + min(wr + kRowsPerLoad * j, nrows - 1)) * (int64_t)d;
+    auto next_w_stage = [&]() {
+        ++la;
+        if (++la_st == nstage) {
+            la_st = 0;
+            la_rb += kMfmaRowsPerIter;
+            const int base = la < ntot ? la_rb + wr : nrows - 1;
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j)
+                wrow[j] = W + (r0 + min(base + kRowsPerLoad * j, nrows - 1)) * (int64_t)d;
+        }
+    };
+    u32x4 pre[LA][kLoads];
+    u32x4 hpre[kHLoads];
+#pragma unroll
+    for (int b = 0; b < LA; ++b) {
+        const int col = la < ntot ? min(la_st * KC + scol, d - 8) : 0;
 #pragma unroll
         for (int j = 0; j < kLoads; ++j)
-            wrow[j] = W + (r0 + min(rb + kRowsPerLoad * j + srow, nrows - 1)) * (int64_t)d;
-        // W stages run LA ahead: stage st's loads sit in buffer st % LA
-        // (the loop is unrolled over the buffers, so no in-flight load is
-        // ever copied); the query stage runs one ahead
-        u32x4 pre[LA][kLoads];
+            pre[b][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + col));
+        next_w_stage();
+        __builtin_amdgcn_sched_barrier(0);  // keep the issue order
+        if (b == 0) {
 #pragma unroll
-        for (int b = 0; b < LA; ++b)
+            for (int j = 0; j < kHLoads; ++j)
+                hpre[j] = *reinterpret_cast<const u32x4 *>(hrowp[j] + min(hcol[j], d - 8));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    f32x4 acc[2][NQT];
 #pragma unroll
-            for (int j = 0; j < kLoads; ++j) {
-                const int c = b * KC + scol;
-                pre[b][j] = b < nstage && c + 8 <= d
-                                ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + c))
-                                : zero;
-            }
-        u32x4 hpre[kHLoads];
+    for (int m = 0; m < 2; ++m)
 #pragma unroll
-        for (int j = 0; j < kHLoads; ++j)
-            hpre[j] = hcol[j] + 8 <= d ? *reinterpret_cast<const u32x4 *>(hrowp[j] + hcol[j]) : zero;
-        f32x4 acc[2][NQT];
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-            for (int n = 0; n < NQT; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int n = 0; n < NQT; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-        for (int st0 = 0; st0 < nstage; st0 += LA) {
+    int st = 0, rbb = 0;  // the current stage within its block, the block's first row
+    for (int s0 = 0; s0 < ntot; s0 += LA) {
 #pragma unroll
-            for (int b = 0; b < LA; ++b) {
-                const int st = st0 + b;
-                if (st >= nstage) break;  // uniform across the workgroup
-                const int c0 = st * KC;
-                __syncthreads();  // every wave is done with the previous query stage
-                // this stage into LDS, then the loads of stage st + LA (W) and st + 1 (queries)
+        for (int b = 0; b < LA; ++b) {
+            if (s0 + b >= ntot) break;  // uniform across the workgroup
+            const int c0 = st * KC;
+            __syncthreads();  // every wave is done with the previous stage
+            // this stage into LDS, then the loads of the next query stage
+            // and of the W stage LA ahead
+            const bool win = c0 + scol + 8 <= d;
 #pragma unroll
-                for (int j = 0; j < kLoads; ++j)
-                    *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) = pre[b][j];
+            for (int j = 0; j < kLoads; ++j)
+                *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) =
+                    win ? pre[b][j] : zero;
 #pragma unroll
-                for (int j = 0; j < kHLoads; ++j) *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = hpre[j];
-                if (st + LA < nstage) {
-                    const int c = c0 + LA * KC + scol;
+            for (int j = 0; j < kHLoads; ++j)
+                *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = c0 + hcol[j] + 8 <= d ? hpre[j] : zero;
+            const int cn = st + 1 < nstage ? c0 + KC : 0;
 #pragma unroll
-                    for (int j = 0; j < kLoads; ++j)
-                        pre[b][j] = c + 8 <= d
-                                        ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + c))
-                                        : zero;
+            for (int j = 0; j < kHLoads; ++j)
+                hpre[j] = *reinterpret_cast<const u32x4 *>(hrowp[j] + min(cn + hcol[j], d - 8));
+            __builtin_amdgcn_sched_barrier(0);
+            const int col = la < ntot ? min(la_st * KC + scol, d - 8) : 0;
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j)
+                pre[b][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + col));
+            next_w_stage();
+            __syncthreads();  // the stage is complete
+#pragma unroll
+            for (int t = 0; t < kSteps; ++t) {
+                u32x4 a[2];
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+                    a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                for (int n = 0; n < NQT; ++n) {
+                    const u32x4 bv =
+                        *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                    for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
                 }
-                if (st + 1 < nstage) {
+            }
+            __builtin_amdgcn_wave_barrier();
+            if (++st == nstage) {
+                // the block's last stage: lane (r, g) holds rows 4 g + i of
+                // each 16-row tile for query 16 n + r; one 16-byte store
+                // where the four rows exist and are 16-byte aligned
+                const int rb = rbb + wave * kMfmaRowsPerWave;
 #pragma unroll
-                    for (int j = 0; j < kHLoads; ++j) {
-                        const int ch = c0 + KC + hcol[j];
-                        hpre[j] = ch + 8 <= d ? *reinterpret_cast<const u32x4 *>(hrowp[j] + ch) : zero;
-                    }
-                }
-                __syncthreads();  // the query stage is complete
-#pragma unroll
-                for (int t = 0; t < kSteps; ++t) {
-                    u32x4 a[2];
-#pragma unroll
-                    for (int m = 0; m < 2; ++m)
-                        a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+                for (int m = 0; m < 2; ++m)
 #pragma unroll
                     for (int n = 0; n < NQT; ++n) {
-                        const u32x4 bv =
-                            *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+                        const int q = n * 16 + r;
+                        const int lr = rb + m * 16 + 4 * g;
+                        if (q < nq) {
+                            float *zp = zout + (int64_t)q * V + r0 + lr;
+                            if (zvec && lr + 3 < nrows)
+                                __builtin_nontemporal_store(acc[m][n], reinterpret_cast<f32x4 *>(zp));
+                            else
 #pragma unroll
-                        for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
+                                for (int i = 0; i < 4; ++i)
+                                    if (lr + i < nrows) zp[i] = acc[m][n][i];
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                if (lr + i < nrows)
+                                    topr_insert(make_key(acc[m][n][i], (int32_t)(r0 + lr + i)), best[n]);
+                        }
+                        acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
                     }
-                }
-                __builtin_amdgcn_wave_barrier();
+                st = 0;
+                rbb += kMfmaRowsPerIter;
             }
         }
-        // lane (r, g) holds rows 4 g + i of each 16-row tile for query 16 n + r
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-            for (int n = 0; n < NQT; ++n) {
-                const int q = n * 16 + r;
-                const int lr = rb + m * 16 + 4 * g;
-                if (q < nq) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        if (lr + i < nrows) {
-                            const float z = acc[m][n][i];
-                            zout[(int64_t)q * V + r0 + lr + i] = z;
-                            topr_insert(make_key(z, (int32_t)(r0 + lr + i)), best[n]);
-                        }
-                }
-            }
     }
     // per query: the kTopR largest over the four lane groups, then over the waves
 #pragma unroll

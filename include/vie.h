@@ -126,9 +126,13 @@ typedef struct {
  * with inner product as the similarity; construction on the GPU is the
  * future work of Section 5, and this batch form (one layer, maxlevel 0) is
  * the library's own.  The graph searches with vie_query like any index: the
- * greedy upper layers are empty.  On return the graph is complete, on the
- * device (as after vie_index_to_device with W_dev, which must stay allocated)
- * and on the host (save, export); the index reports M = max(2, M0 / 2)
+ * greedy upper layers are empty.  On return the graph is complete and on the
+ * device (as after vie_index_to_device with W_dev, which must stay allocated);
+ * its layer-0 lists reach the host when a call first needs them there
+ * (vie_index_save, vie_index_export, vie_index_to_device copy them from the
+ * device, so these may also fail with VIE_EHIP for such an index; the first
+ * of them should not race with another on the same index).  The index
+ * reports M = max(2, M0 / 2)
  * (capped at M0), ef_construction = K, seed 0.  The call allocates device
  * scratch (chunk_rows x V x 4 bytes of scores plus about V (8K + 16 M0)
  * bytes) and releases it before returning; it enqueues on hip_stream and
@@ -141,7 +145,8 @@ vie_status vie_index_build_gpu(const void *W_dev, vie_dtype dtype, int64_t V, in
 /* Writes the index file (format below).  Section 3: the index is built once,
  * offline, and shipped with the model checkpoint; this file is that artifact
  * (the graph plus a fingerprint of the W_out it was built on).
- * Errors: VIE_EINVAL, VIE_EIO. */
+ * Errors: VIE_EINVAL, VIE_EIO, VIE_EHIP (a GPU-built index whose lists could
+ * not be copied from the device). */
 vie_status vie_index_save(const vie_index *index, const char *path);
 
 /* Loads the shipped index (Section 3: precomputed and distributed with the
@@ -164,7 +169,8 @@ vie_status vie_index_info(const vie_index *index, vie_index_desc *out);
 
 /* Copies the graph into caller arrays: levels uint8[V], adj0 int32[V][M0],
  * upper_off int32[V], upper int32[n_upper_blocks][M] (layout as in the file).
- * Any pointer may be NULL to skip that array.  Errors: VIE_EINVAL. */
+ * Any pointer may be NULL to skip that array.  Errors: VIE_EINVAL, VIE_EHIP
+ * (a GPU-built index whose lists could not be copied from the device). */
 vie_status vie_index_export(const vie_index *index, uint8_t *levels, int32_t *adj0,
                             int32_t *upper_off, int32_t *upper);
 

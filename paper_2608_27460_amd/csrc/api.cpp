@@ -5,8 +5,10 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "index.hpp"
 #include "vie.h"
@@ -14,6 +16,11 @@
 struct vie_index {
     vie::Graph g;
     vie::DeviceGraph dev;
+    // A GPU-built index keeps its layer-0 lists on the device only until a
+    // host-side call needs them (save, export, moving the index); the first
+    // such call copies them into g.adj0.
+    bool adj0_device_only = false;
+    std::mutex host_mu;
 };
 
 namespace vie {
@@ -62,6 +69,24 @@ vie_status check_k(int32_t k, int64_t V, int32_t B)
 {
     if (B < 1 || B > 65535) return fail(VIE_EINVAL, "B = %d out of range [1, 65535]", B);
     if (k < 1 || k > kMaxK || k > V) return fail(VIE_EINVAL, "k = %d out of range [1, min(V, %d)]", k, kMaxK);
+    return VIE_OK;
+}
+
+// The host copy of a GPU-built index's layer-0 lists (see vie_index).
+vie_status fetch_host_adjacency(vie_index *ix)
+{
+    std::lock_guard<std::mutex> lock(ix->host_mu);
+    if (!ix->adj0_device_only) return VIE_OK;
+    Graph &g = ix->g;
+    std::vector<int32_t> adj((size_t)g.V * g.M0);
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess) e = hipSetDevice(ix->dev.device);
+    if (e == hipSuccess) e = hipMemcpy(adj.data(), ix->dev.adj0, adj.size() * 4, hipMemcpyDeviceToHost);
+    (void)hipSetDevice(cur);
+    if (e != hipSuccess) return hip_fail(e, "copying the graph to the host");
+    g.adj0.swap(adj);
+    ix->adj0_device_only = false;
     return VIE_OK;
 }
 
@@ -150,6 +175,7 @@ vie_status vie_index_build_gpu(const void *W_dev, vie_dtype dtype, int64_t V, in
         delete ix;
         return s;
     }
+    ix->adj0_device_only = true;
     *out = ix;
     return VIE_OK;
 }
@@ -158,6 +184,7 @@ vie_status vie_index_save(const vie_index *ix, const char *path)
 {
     g_last_error.clear();
     if (!ix || !path) return fail(VIE_EINVAL, "NULL argument");
+    if (vie_status s = fetch_host_adjacency(const_cast<vie_index *>(ix))) return s;
     return save_graph(ix->g, path);
 }
 
@@ -187,6 +214,7 @@ vie_status vie_index_to_device(vie_index *ix, const void *W_dev, void *hip_strea
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (vie_status s = fetch_host_adjacency(ix)) return s;
     free_device(ix->dev);
     const Graph &g = ix->g;
     DeviceGraph d;
@@ -239,6 +267,7 @@ vie_status vie_index_export(const vie_index *ix, uint8_t *levels, int32_t *adj0,
 {
     g_last_error.clear();
     if (!ix) return fail(VIE_EINVAL, "NULL index");
+    if (vie_status s = fetch_host_adjacency(const_cast<vie_index *>(ix))) return s;
     const Graph &g = ix->g;
     if (levels) std::memcpy(levels, g.levels.data(), g.levels.size());
     if (adj0) std::memcpy(adj0, g.adj0.data(), g.adj0.size() * 4);

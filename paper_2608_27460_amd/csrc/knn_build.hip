@@ -23,6 +23,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <type_traits>
 #include <vector>
 
 #include "index.hpp"
@@ -210,12 +211,22 @@ constexpr int kSampleEvery = 8;
 // 64 x 64 quarter as 4 x 4 tiles of 16 x 16 on the matrix cores
 // (v_mfma_f32_16x16x32_bf16 for bf16 rows, v_mfma_f32_16x16x4_f32 for fp32
 // rows).  The reduction over the row width runs in stages of kGramKC bytes
-// of each row: both 128-row slices of a stage are staged in LDS (padded
-// rows), the stages two ahead loading into registers while the current one
-// is multiplied.  Lane (r, g) of a wave (r = lane % 16, g = lane / 16) feeds
-// row r of a 16-row operand with its g-th quarter of the k step, and ends
-// holding rows 4 g + i of column r of each 16 x 16 result.  Every score is
-// the same sequence of products and sums whichever tile computes it.
+// of each row: both 128-row slices of a stage are staged in LDS, the stages
+// two ahead loading into registers while the current one is multiplied.
+// Lane (r, g) of a wave (r = lane % 16, g = lane / 16) feeds row r of a
+// 16-row operand with its g-th quarter of the k step, and ends holding rows
+// 4 g + i of column r of each 16 x 16 result.  Every score is the same
+// sequence of products and sums whichever tile computes it.
+//
+// Staged rows are not padded: the 16-byte piece p of staged row x sits at
+// piece p ^ ((x >> 1) & 7) of the row.  Measured with the LDS counters on
+// gfx950, the operand reads (16 rows, four consecutive pieces or four
+// consecutive floats each) then use every bank once per cycle, where rows
+// padded by 16 bytes took twice the cycles (half of them bank conflicts),
+// and the two stages fit twice per CU.  Every load of a stage is issued with
+// no branch around it (pieces past the row are clamped to its last piece and
+// replaced by zeros when staged), in the order they are consumed, so the
+// compiler waits only for the stage being staged.
 
 constexpr int kGramTile = 128;                     // rows of c and of j per workgroup
 constexpr int kGramThreads = 256;                  // four waves, 2 x 2 quarters
@@ -223,11 +234,12 @@ constexpr int kGramThreads = 256;                  // four waves, 2 x 2 quarters
 #define VIE_GRAM_KC 128
 #endif
 constexpr int kGramKC = VIE_GRAM_KC;               // bytes of a row per stage
-#ifndef VIE_GRAM_PAD
-#define VIE_GRAM_PAD 16
-#endif
-constexpr int kGramRowPitch = kGramKC + VIE_GRAM_PAD;  // LDS bytes per staged row (padded)
+static_assert(kGramKC == 128, "the piece swizzle is laid out for 8 pieces a staged row");
+constexpr int kGramRowPitch = kGramKC;                 // LDS bytes per staged row
 constexpr int kGramStage = 2 * kGramTile * kGramRowPitch;  // A and B slices of one stage
+
+// byte offset of 16-byte piece p of staged row x
+__device__ __forceinline__ int gram_piece(int x, int p) { return x * kGramRowPitch + ((p ^ ((x >> 1) & 7)) << 4); }
 constexpr int kGramLoads = 2 * kGramTile * (kGramKC / 16) / kGramThreads;  // 16-byte loads per thread
 
 __device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 c)
@@ -262,14 +274,13 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
         const int64_t grow = srow < kGramTile ? r0 + min<int64_t>(c0 + srow, rows - 1)
                                               : min<int64_t>(j0 + srow - kGramTile, V - 1);
         src[t] = W + grow * (int64_t)row_bytes;
-        soff[t] = srow * kGramRowPitch + scol[t];
+        soff[t] = gram_piece(srow, scol[t] >> 4);
     }
     auto load_stage = [&](int st, u32x4(&buf)[kGramLoads]) {
 #pragma unroll
-        for (int t = 0; t < kGramLoads; ++t) {
-            const int c = st * kGramKC + scol[t];
-            buf[t] = c + 16 <= row_bytes ? *reinterpret_cast<const u32x4 *>(src[t] + c) : zero;
-        }
+        for (int t = 0; t < kGramLoads; ++t)
+            buf[t] = *reinterpret_cast<const u32x4 *>(src[t] + min(st * kGramKC + scol[t], row_bytes - 16));
+        __builtin_amdgcn_sched_barrier(0);  // keep the issue order
     };
     f32x4 acc[4][4];
 #pragma unroll
@@ -277,56 +288,65 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
         for (int n = 0; n < 4; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     // stages load two ahead: stage st's loads sit in register buffer st % 2
-    // (the loop is unrolled over the buffers, so no load in flight is ever
-    // copied) and in LDS buffer st % 2
+    // (the stage pairs are written out over the buffers, so no load in
+    // flight is ever copied) and in LDS buffer st % 2
     u32x4 pre[2][kGramLoads];
     load_stage(0, pre[0]);
-    if (nstage > 1) load_stage(1, pre[1]);
-    for (int st0 = 0; st0 < nstage; st0 += 2) {
+    load_stage(min(1, nstage - 1), pre[1]);
+    // one stage: into LDS buffer PB from register buffer PB, the loads of the
+    // stage two ahead into that register buffer, then the products.  The
+    // stage pairs run in a loop without any branch inside (so the compiler
+    // keeps the loads of the next stage in flight across it) and an odd last
+    // stage after it.
+    auto run_stage = [&](auto pbc, int st) {
+        constexpr int pb = decltype(pbc)::value;
+        char *buf = smem + pb * kGramStage;
 #pragma unroll
-        for (int pb = 0; pb < 2; ++pb) {
-            const int st = st0 + pb;
-            if (st >= nstage) break;  // uniform across the workgroup
-            char *buf = smem + pb * kGramStage;
+        for (int t = 0; t < kGramLoads; ++t)
+            *reinterpret_cast<u32x4 *>(buf + soff[t]) = st * kGramKC + scol[t] + 16 <= row_bytes ? pre[pb][t] : zero;
+        __builtin_amdgcn_sched_barrier(0);
+        load_stage(min(st + 2, nstage - 1), pre[pb]);  // past the end: the last stage again (cached)
+        __syncthreads();  // the stage is in LDS (and the stage before it is no longer read)
+        const char *A = buf + (wm * 64) * kGramRowPitch;
+        const char *B = buf + (kGramTile + wn * 64) * kGramRowPitch;
+        if constexpr (BF16) {
 #pragma unroll
-            for (int t = 0; t < kGramLoads; ++t) *reinterpret_cast<u32x4 *>(buf + soff[t]) = pre[pb][t];
-            if (st + 2 < nstage) load_stage(st + 2, pre[pb]);
-            __syncthreads();  // the stage is in LDS (and the stage before it is no longer read)
-            const char *A = buf + (wm * 64) * kGramRowPitch;
-            const char *B = buf + (kGramTile + wn * 64) * kGramRowPitch;
-            if constexpr (BF16) {
+            for (int kk = 0; kk < kGramKC; kk += 64) {  // 32 bf16 per MFMA step
+                u32x4 a[4], b[4];
 #pragma unroll
-                for (int kk = 0; kk < kGramKC; kk += 64) {  // 32 bf16 per MFMA step
-                    u32x4 a[4], b[4];
+                for (int m = 0; m < 4; ++m)
+                    a[m] = *reinterpret_cast<const u32x4 *>(A + gram_piece(m * 16 + r, kk / 16 + g));
 #pragma unroll
-                    for (int m = 0; m < 4; ++m)
-                        a[m] = *reinterpret_cast<const u32x4 *>(A + (m * 16 + r) * kGramRowPitch + kk + 16 * g);
+                for (int n = 0; n < 4; ++n)
+                    b[n] = *reinterpret_cast<const u32x4 *>(B + gram_piece(n * 16 + r, kk / 16 + g));
 #pragma unroll
-                    for (int n = 0; n < 4; ++n)
-                        b[n] = *reinterpret_cast<const u32x4 *>(B + (n * 16 + r) * kGramRowPitch + kk + 16 * g);
+                for (int m = 0; m < 4; ++m)
 #pragma unroll
-                    for (int m = 0; m < 4; ++m)
+                    for (int n = 0; n < 4; ++n) acc[m][n] = mfma_bf16(a[m], b[n], acc[m][n]);
+            }
+        } else {
 #pragma unroll
-                        for (int n = 0; n < 4; ++n) acc[m][n] = mfma_bf16(a[m], b[n], acc[m][n]);
-                }
-            } else {
+            for (int kk = 0; kk < kGramKC; kk += 16) {  // 4 floats per MFMA step
+                float a[4], b[4];
 #pragma unroll
-                for (int kk = 0; kk < kGramKC; kk += 16) {  // 4 floats per MFMA step
-                    float a[4], b[4];
+                for (int m = 0; m < 4; ++m)
+                    a[m] = *reinterpret_cast<const float *>(A + gram_piece(m * 16 + r, kk / 16) + 4 * g);
 #pragma unroll
-                    for (int m = 0; m < 4; ++m)
-                        a[m] = *reinterpret_cast<const float *>(A + (m * 16 + r) * kGramRowPitch + kk + 4 * g);
+                for (int n = 0; n < 4; ++n)
+                    b[n] = *reinterpret_cast<const float *>(B + gram_piece(n * 16 + r, kk / 16) + 4 * g);
 #pragma unroll
-                    for (int n = 0; n < 4; ++n)
-                        b[n] = *reinterpret_cast<const float *>(B + (n * 16 + r) * kGramRowPitch + kk + 4 * g);
+                for (int m = 0; m < 4; ++m)
 #pragma unroll
-                    for (int m = 0; m < 4; ++m)
-#pragma unroll
-                        for (int n = 0; n < 4; ++n) acc[m][n] = mfma_f32(a[m], b[n], acc[m][n]);
-                }
+                    for (int n = 0; n < 4; ++n) acc[m][n] = mfma_f32(a[m], b[n], acc[m][n]);
             }
         }
+    };
+    int st = 0;
+    for (; st + 1 < nstage; st += 2) {
+        run_stage(std::integral_constant<int, 0>(), st);
+        run_stage(std::integral_constant<int, 1>(), st + 1);
     }
+    if (st < nstage) run_stage(std::integral_constant<int, 0>(), st);
     // lane (r, g) holds chunk rows 16 m + 4 g + i of the quarter, column 16 n + r
 #pragma unroll
     for (int m = 0; m < 4; ++m)
@@ -742,9 +762,10 @@ struct Buffers {
     int64_t *roff = nullptr;
     uint64_t *rev = nullptr;
     unsigned long long *best = nullptr;
+    char *sample = nullptr;  // the rows of W_out the fingerprint samples, gathered
     void release()
     {
-        void *p[] = {S, cand, fwd, nfwd, cand_score, fwd_score, count, roff, rev, best};
+        void *p[] = {S, cand, fwd, nfwd, cand_score, fwd_score, count, roff, rev, best, sample};
         for (void *q : p)
             if (q) (void)hipFree(q);
         S = nullptr;
@@ -754,6 +775,7 @@ struct Buffers {
         roff = nullptr;
         rev = nullptr;
         best = nullptr;
+        sample = nullptr;
     }
     void release_graph()
     {
@@ -796,12 +818,16 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
 
     Buffers b;
     const int64_t edges = V * M0;
+    // the rows the W_out fingerprint samples: every step-th row, then the last
+    const int64_t step = V / 1024 > 1 ? V / 1024 : 1;
+    const int64_t nreg = (V + step - 1) / step;
     if (!dalloc(b.S, (size_t)R * ld * 4) || !dalloc(b.cand, (size_t)V * K * 4) ||
         !dalloc(b.cand_score, (size_t)V * K * 4) || !dalloc(b.fwd, (size_t)edges * 4) ||
         !dalloc(b.fwd_score, (size_t)edges * 4) || !dalloc(b.nfwd, (size_t)V * 4) ||
         !dalloc(b.count, (size_t)V * 4) || !dalloc(b.roff, (size_t)(V + 1) * 8) ||
         !dalloc(b.rev, (size_t)edges * 8) || !dalloc(b.best, 8) || !dalloc(b.adj0, (size_t)edges * 4) ||
-        !dalloc(b.upper_off, (size_t)V * 4) || !dalloc(b.upper, 4)) {
+        !dalloc(b.upper_off, (size_t)V * 4) || !dalloc(b.upper, 4) ||
+        !dalloc(b.sample, (size_t)(nreg + 1) * row_bytes)) {
         b.release();
         b.release_graph();
         return fail(VIE_ENOMEM, "GPU build: device allocation failed (V = %lld, chunk of %lld rows)", (long long)V,
@@ -868,24 +894,26 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
     g.seed = 0;
     g.maxlevel = 0;
     g.levels.assign((size_t)V, 0);
-    g.adj0.resize((size_t)edges);
     g.upper_off.assign((size_t)V, -1);
+    // (the layer-0 lists stay on the device: the index copies them to the
+    // host when a host-side call first needs them)
     unsigned long long best = 0;
-    he = hipMemcpyAsync(g.adj0.data(), b.adj0, (size_t)edges * 4, hipMemcpyDeviceToHost, s);
-    if (he == hipSuccess) he = hipMemcpyAsync(&best, b.best, 8, hipMemcpyDeviceToHost, s);
-    // the rows the W_out fingerprint samples
-    const int64_t step = V / 1024 > 1 ? V / 1024 : 1;
-    std::vector<int64_t> rows;
-    for (int64_t r = 0; r < V; r += step) rows.push_back(r);
-    rows.push_back(V - 1);
-    std::vector<char> sample(rows.size() * (size_t)row_bytes);
-    for (size_t t = 0; t < rows.size() && he == hipSuccess; ++t)
-        he = hipMemcpyAsync(sample.data() + t * row_bytes, static_cast<const char *>(W_dev) + rows[t] * row_bytes,
-                            row_bytes, hipMemcpyDeviceToHost, s);
+    he = hipMemcpyAsync(&best, b.best, 8, hipMemcpyDeviceToHost, s);
+    // the sampled rows of W_out gathered on the device (one strided copy
+    // and the last row), then one copy to the host: a copy per row, or a
+    // strided copy straight to host memory, took 7-15 ms of host time
+    std::vector<char> sample((size_t)(nreg + 1) * row_bytes);
+    if (he == hipSuccess)
+        he = hipMemcpy2DAsync(b.sample, (size_t)row_bytes, W_dev, (size_t)step * row_bytes, (size_t)row_bytes,
+                              (size_t)nreg, hipMemcpyDeviceToDevice, s);
+    if (he == hipSuccess)
+        he = hipMemcpyAsync(b.sample + nreg * row_bytes, static_cast<const char *>(W_dev) + (V - 1) * row_bytes,
+                            row_bytes, hipMemcpyDeviceToDevice, s);
+    if (he == hipSuccess) he = hipMemcpyAsync(sample.data(), b.sample, sample.size(), hipMemcpyDeviceToHost, s);
     if (he == hipSuccess) he = hipStreamSynchronize(s);
     if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
     g.entry = (int32_t)(~(uint32_t)best);
-    g.fingerprint = w_fingerprint_rows(sample.data(), dtype, V, d, (int64_t)rows.size());
+    g.fingerprint = w_fingerprint_rows(sample.data(), dtype, V, d, nreg + 1);
     b.release();
 
     dg = DeviceGraph();

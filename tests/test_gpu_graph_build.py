@@ -83,7 +83,16 @@ def test_integer_hub_rows_with_large_reverse_lists(vie):
     # collects thousands of reverse edges (more than one selection round holds)
     V, d, K, M0 = 6000, 32, 32, 16
     W = integer_rows(V, d, synth.BF16, 5, hubs=[(np.arange(5) * 1000 + 7, 10.0)])
-    ix, g, _ = build_both(vie, W, synth.BF16, K, M0)
+    ix, g, Wd = build_both(vie, W, synth.BF16, K, M0)
+    # the lists stay on the device until a host-side call needs them: moving
+    # the index first copies them to the host, then uploads them again, and
+    # the search does not change
+    H = Wd[:8].contiguous()
+    ids0, lg0 = ix.query(H, 10, 32)
+    ix.to_device(Wd)
+    ids1, lg1 = ix.query(H, 10, 32)
+    torch.cuda.synchronize()
+    assert torch.equal(ids0, ids1) and torch.equal(lg0, lg1)
     ex = ix.export()
     assert ix.info()["entry"] == g.entry
     assert np.array_equal(ex["adj0"], g.adj0)

@@ -41,7 +41,7 @@ constexpr int kGatherCap = 2048;             // keys a selection sorts in LDS
 constexpr int kSelectThreads = 256;
 constexpr int kSelectRows = 128;             // candidate rows of one Gram block (K <= 128)
 constexpr int kChunkBytes = 256;             // bytes of a row per staged chunk
-constexpr int kChunkPitch = kChunkBytes + 16;
+constexpr int kChunkPitch = kChunkBytes + 32;  // padded: the matrix-core operand reads hit every LDS bank once
 constexpr int kGramPitch = kSelectRows + 1;  // floats per Gram row in LDS
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));

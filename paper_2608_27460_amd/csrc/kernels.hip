@@ -999,136 +999,110 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
         for (int i = 0; i < kTopR; ++i) best[n][i] = 0ull;
 
-    // The slab's row blocks (kMfmaRowsPerIter rows each) and their stages run
-    // as one sequence of nblk * nstage stages, so the loads of the next
-    // block's first stages are in flight while a block finishes and writes
-    // its logits.  Every wave runs every stage (the workgroup barriers need
-    // it); rows past the slab are clamped and discarded.  W stages run LA
-    // ahead: stage s's loads sit in buffer s % LA (the loop is unrolled over
-    // the buffers, so no in-flight load is ever copied); the query stage runs
-    // one ahead.  Every stage issues the same loads with no branch around
-    // them, in the order they are consumed (columns past the row are clamped
-    // to its last piece and replaced by zeros when staged; the loads past
-    // the last stage re-read one cache line): the compiler then counts the
+    // Every wave runs the same number of iterations (the workgroup barriers
+    // need it); rows past the slab are clamped and discarded.  W stages run
+    // LA ahead: stage st's loads sit in buffer st % LA (the loop is unrolled
+    // over the buffers, so no in-flight load is ever copied); the query stage
+    // runs one ahead.  Every stage issues the same loads with no branch
+    // around them, in the order they are consumed (columns past the row are
+    // clamped to its last piece and replaced by zeros when staged; the loads
+    // of stages past the end re-read a query piece, which stays in L2), with
+    // scheduling barriers keeping that order: the compiler then counts the
     // loads in flight exactly and waits only for the stage being staged, not
     // for the ones still ahead.
-    const int nblk = (nrows + kMfmaRowsPerIter - 1) / kMfmaRowsPerIter;
-    const int ntot = nblk * nstage;
-    // W load j of a lane reads row wrow[j] of the block being loaded; past
-    // the last block every load reads the first piece of the slab's last
-    // row (one cache line, no HBM traffic to speak of)
-    const int wr = wave * kMfmaRowsPerWave + srow;
-    int la = 0, la_st = 0, la_rb = 0;  // sequence number, stage and block row of the next W stage to load
-    const uint16_t *wrow[kLoads];
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) wrow[j] = W + (r0 + min(wr + kRowsPerLoad * j, nrows - 1)) * (int64_t)d;
-    auto next_w_stage = [&]() {
-        ++la;
-        if (++la_st == nstage) {
-            la_st = 0;
-            la_rb += kMfmaRowsPerIter;
-            const int base = la < ntot ? la_rb + wr : nrows - 1;
-#pragma unroll
-            for (int j = 0; j < kLoads; ++j)
-                wrow[j] = W + (r0 + min(base + kRowsPerLoad * j, nrows - 1)) * (int64_t)d;
-        }
-    };
-    u32x4 pre[LA][kLoads];
-    u32x4 hpre[kHLoads];
-#pragma unroll
-    for (int b = 0; b < LA; ++b) {
-        const int col = la < ntot ? min(la_st * KC + scol, d - 8) : 0;
+    for (int rb0 = 0; rb0 < nrows; rb0 += kMfmaRowsPerIter) {
+        const int rb = rb0 + wave * kMfmaRowsPerWave;
+        const uint16_t *wrow[kLoads];
 #pragma unroll
         for (int j = 0; j < kLoads; ++j)
-            pre[b][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + col));
-        next_w_stage();
-        __builtin_amdgcn_sched_barrier(0);  // keep the issue order
-        if (b == 0) {
-#pragma unroll
-            for (int j = 0; j < kHLoads; ++j)
-                hpre[j] = *reinterpret_cast<const u32x4 *>(hrowp[j] + min(hcol[j], d - 8));
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    }
-    f32x4 acc[2][NQT];
-#pragma unroll
-    for (int m = 0; m < 2; ++m)
-#pragma unroll
-        for (int n = 0; n < NQT; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-
-    int st = 0, rbb = 0;  // the current stage within its block, the block's first row
-    for (int s0 = 0; s0 < ntot; s0 += LA) {
+            wrow[j] = W + (r0 + min(rb + kRowsPerLoad * j + srow, nrows - 1)) * (int64_t)d;
+        u32x4 pre[LA][kLoads];
+        u32x4 hpre[kHLoads];
 #pragma unroll
         for (int b = 0; b < LA; ++b) {
-            if (s0 + b >= ntot) break;  // uniform across the workgroup
-            const int c0 = st * KC;
-            __syncthreads();  // every wave is done with the previous stage
-            // this stage into LDS, then the loads of the next query stage
-            // and of the W stage LA ahead
-            const bool win = c0 + scol + 8 <= d;
 #pragma unroll
             for (int j = 0; j < kLoads; ++j)
-                *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) =
-                    win ? pre[b][j] : zero;
+                pre[b][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(
+                    b < nstage ? wrow[j] + min(b * KC + scol, d - 8) : hrowp[0]));
+            __builtin_amdgcn_sched_barrier(0);  // keep the issue order
+            if (b == 0) {
 #pragma unroll
-            for (int j = 0; j < kHLoads; ++j)
-                *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = c0 + hcol[j] + 8 <= d ? hpre[j] : zero;
-            const int cn = st + 1 < nstage ? c0 + KC : 0;
-#pragma unroll
-            for (int j = 0; j < kHLoads; ++j)
-                hpre[j] = *reinterpret_cast<const u32x4 *>(hrowp[j] + min(cn + hcol[j], d - 8));
-            __builtin_amdgcn_sched_barrier(0);
-            const int col = la < ntot ? min(la_st * KC + scol, d - 8) : 0;
-#pragma unroll
-            for (int j = 0; j < kLoads; ++j)
-                pre[b][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[j] + col));
-            next_w_stage();
-            __syncthreads();  // the stage is complete
-#pragma unroll
-            for (int t = 0; t < kSteps; ++t) {
-                u32x4 a[2];
-#pragma unroll
-                for (int m = 0; m < 2; ++m)
-                    a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
-#pragma unroll
-                for (int n = 0; n < NQT; ++n) {
-                    const u32x4 bv =
-                        *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
-#pragma unroll
-                    for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
-                }
-            }
-            __builtin_amdgcn_wave_barrier();
-            if (++st == nstage) {
-                // the block's last stage: lane (r, g) holds rows 4 g + i of
-                // each 16-row tile for query 16 n + r; one 16-byte store
-                // where the four rows exist and are 16-byte aligned
-                const int rb = rbb + wave * kMfmaRowsPerWave;
-#pragma unroll
-                for (int m = 0; m < 2; ++m)
-#pragma unroll
-                    for (int n = 0; n < NQT; ++n) {
-                        const int q = n * 16 + r;
-                        const int lr = rb + m * 16 + 4 * g;
-                        if (q < nq) {
-                            float *zp = zout + (int64_t)q * V + r0 + lr;
-                            if (zvec && lr + 3 < nrows)
-                                __builtin_nontemporal_store(acc[m][n], reinterpret_cast<f32x4 *>(zp));
-                            else
-#pragma unroll
-                                for (int i = 0; i < 4; ++i)
-                                    if (lr + i < nrows) zp[i] = acc[m][n][i];
-#pragma unroll
-                            for (int i = 0; i < 4; ++i)
-                                if (lr + i < nrows)
-                                    topr_insert(make_key(acc[m][n][i], (int32_t)(r0 + lr + i)), best[n]);
-                        }
-                        acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                    }
-                st = 0;
-                rbb += kMfmaRowsPerIter;
+                for (int j = 0; j < kHLoads; ++j)
+                    hpre[j] = *reinterpret_cast<const u32x4 *>(hrowp[j] + min(hcol[j], d - 8));
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+        f32x4 acc[2][NQT];
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int n = 0; n < NQT; ++n) acc[m][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        for (int st0 = 0; st0 < nstage; st0 += LA) {
+#pragma unroll
+            for (int b = 0; b < LA; ++b) {
+                const int st = st0 + b;
+                if (st >= nstage) break;  // uniform across the workgroup
+                const int c0 = st * KC;
+                __syncthreads();  // every wave is done with the previous query stage
+                // this stage into LDS, then the loads of stage st + 1 (queries)
+                // and st + LA (W)
+                const bool win = c0 + scol + 8 <= d;
+#pragma unroll
+                for (int j = 0; j < kLoads; ++j)
+                    *reinterpret_cast<u32x4 *>(slice + (kRowsPerLoad * j + srow) * kPitch + scol * 2) =
+                        win ? pre[b][j] : zero;
+#pragma unroll
+                for (int j = 0; j < kHLoads; ++j)
+                    *reinterpret_cast<u32x4 *>(hsl + hoff[j]) = c0 + hcol[j] + 8 <= d ? hpre[j] : zero;
+#pragma unroll
+                for (int j = 0; j < kHLoads; ++j)
+                    hpre[j] = *reinterpret_cast<const u32x4 *>(hrowp[j] + min(c0 + KC + hcol[j], d - 8));
+                __builtin_amdgcn_sched_barrier(0);
+                const bool ahead = st + LA < nstage;
+#pragma unroll
+                for (int j = 0; j < kLoads; ++j)
+                    pre[b][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(
+                        ahead ? wrow[j] + min(c0 + LA * KC + scol, d - 8) : hrowp[0]));
+                __syncthreads();  // the query stage is complete
+#pragma unroll
+                for (int t = 0; t < kSteps; ++t) {
+                    u32x4 a[2];
+#pragma unroll
+                    for (int m = 0; m < 2; ++m)
+                        a[m] = *reinterpret_cast<const u32x4 *>(slice + (m * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                    for (int n = 0; n < NQT; ++n) {
+                        const u32x4 bv =
+                            *reinterpret_cast<const u32x4 *>(hsl + (n * 16 + r) * kPitch + (32 * t + 8 * g) * 2);
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) acc[m][n] = mfma_bf16(a[m], bv, acc[m][n]);
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
+        }
+        // lane (r, g) holds rows 4 g + i of each 16-row tile for query 16 n + r:
+        // one 16-byte store where the four rows exist and are 16-byte aligned
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int n = 0; n < NQT; ++n) {
+                const int q = n * 16 + r;
+                const int lr = rb + m * 16 + 4 * g;
+                if (q < nq) {
+                    float *zp = zout + (int64_t)q * V + r0 + lr;
+                    if (zvec && lr + 3 < nrows)
+                        __builtin_nontemporal_store(acc[m][n], reinterpret_cast<f32x4 *>(zp));
+                    else
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (lr + i < nrows) zp[i] = acc[m][n][i];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (lr + i < nrows) topr_insert(make_key(acc[m][n][i], (int32_t)(r0 + lr + i)), best[n]);
+                }
+            }
     }
     // per query: the kTopR largest over the four lane groups, then over the waves
 #pragma unroll

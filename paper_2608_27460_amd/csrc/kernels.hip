@@ -1084,6 +1084,8 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(2)
         }
         // lane (r, g) holds rows 4 g + i of each 16-row tile for query 16 n + r:
         // one 16-byte store where the four rows exist and are 16-byte aligned
+        // (non-temporal from 32 queries on; measured: a 16-query pass is
+        // faster with ordinary stores, a 32-query pass with non-temporal ones)
 #pragma unroll
         for (int m = 0; m < 2; ++m)
 #pragma unroll
@@ -1092,9 +1094,12 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(2)
                 const int lr = rb + m * 16 + 4 * g;
                 if (q < nq) {
                     float *zp = zout + (int64_t)q * V + r0 + lr;
-                    if (zvec && lr + 3 < nrows)
-                        __builtin_nontemporal_store(acc[m][n], reinterpret_cast<f32x4 *>(zp));
-                    else
+                    if (zvec && lr + 3 < nrows) {
+                        if constexpr (NQT == 1)
+                            *reinterpret_cast<f32x4 *>(zp) = acc[m][n];
+                        else
+                            __builtin_nontemporal_store(acc[m][n], reinterpret_cast<f32x4 *>(zp));
+                    } else
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
                             if (lr + i < nrows) zp[i] = acc[m][n][i];

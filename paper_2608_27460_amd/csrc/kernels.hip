@@ -454,8 +454,14 @@ dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const ch
 #endif
 template <int CPL> struct StreamRows { static constexpr int value = CPL >= 4 ? 1 : CPL == 2 ? VIE_STREAM_ROWS2 : 4 / CPL; };
 
+// Occupancy hints: rows of 12 chunks per lane at two waves per SIMD, fp32
+// rows of 2 to 8 chunks at three, so that no single-query variant spills
+// registers (measured on MI355X: with 8 chunks at four waves the fp32 variant
+// spilled and streamed a 128256 x 2048 fp32 head at 57% of the HBM peak,
+// against 83% without the spill).
+
 template <bool BF16, int NB, int CPL>
-__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 && CPL <= 2 && CPL * StreamRows<CPL>::value <= 4 ? 8 : 4))) void
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(CPL >= 12 ? 2 : !BF16 && CPL >= 2 ? 3 : !BF16 ? 4 : NB == 1 && CPL <= 2 && CPL * StreamRows<CPL>::value <= 4 ? 8 : 4))) void
 dense_stream_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
                     int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ tops)
 {
@@ -2603,7 +2609,7 @@ bool dense_plan(int64_t V, int row_bytes, DensePlan &p)
 int stream_cpl(int row_bytes, int nb)
 {
     const int c = (row_bytes / 16 + kWave - 1) / kWave;
-    const int cpl = c <= 1 ? 1 : c <= 2 ? 2 : c <= 4 ? 4 : c <= 8 ? 8 : 0;
+    const int cpl = c <= 1 ? 1 : c <= 2 ? 2 : c <= 4 ? 4 : c <= 8 ? 8 : c <= 12 ? 12 : 0;
     return nb == 2 && cpl > 4 ? 0 : cpl;
 }
 
@@ -2634,7 +2640,8 @@ hipError_t stream_launch_cpl(int cpl, int nb, const void *W, int64_t V, int row_
         case 1: return stream_launch<BF16, 1, 1>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
         case 2: return stream_launch<BF16, 1, 2>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
         case 4: return stream_launch<BF16, 1, 4>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
-        default: return stream_launch<BF16, 1, 8>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+        case 8: return stream_launch<BF16, 1, 8>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
+        default: return stream_launch<BF16, 1, 12>(W, V, row_bytes, h, nq, k, p, zbuf, tops, ids, logits, s);
         }
     }
     switch (cpl) {

@@ -81,6 +81,11 @@ DENSE_CASES = [
     (7001, 2048, synth.BF16, 2, 50),   # two queries, 4 chunks per lane
     (5003, 3072, synth.BF16, 2, 10),   # two queries, rows too long for it: the slab kernel
     (8000, 1000, synth.F32, 1, 30),    # fp32, 250 chunks
+    (3000, 3072, synth.F32, 1, 50),    # fp32 rows of 768 chunks: 12 of 12 per lane
+    (2000, 2560, synth.F32, 1, 20),    # fp32, 10 of 12 chunks per lane
+    (2500, 5120, synth.BF16, 1, 40),   # bf16 rows of 10 KB: 10 of 12 chunks per lane
+    (1200, 6144, synth.BF16, 1, 50),   # bf16, 12 of 12 chunks per lane
+    (1500, 3328, synth.F32, 1, 10),    # 13 chunks per lane: the slab kernel
     (4000, 256, synth.F32, 2, 40),     # fp32, two queries, one chunk per lane
     # fewer slabs than k over more rows than the merge holds in LDS: every
     # row is a candidate and the merge bisects the whole key space

@@ -385,8 +385,12 @@ __device__ __forceinline__ void slab_epilogue(const float *z, int zpitch, int nq
     }
 }
 
+// (occupancy hints: the fp32 variants of one and four queries had spilled
+// registers at eight and four waves per SIMD; measured per call on MI355X,
+// 100000 x 4096 fp32 at B = 1 280 -> 265 us, 128256 x 3072 fp32 at B = 4
+// 426 -> 407 us)
 template <int VEC, bool BF16, int NB>
-__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 8 : 4))) void
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(NB == 1 ? (BF16 ? 8 : 6) : !BF16 && NB == 4 ? (VEC == 16 ? 2 : 3) : 4))) void
 dense_slab_kernel(const char *__restrict__ W, int64_t V, int row_bytes, const char *__restrict__ hq, int nq,
                   int rows_per_wg, float *__restrict__ zout, uint64_t *__restrict__ tops)
 {

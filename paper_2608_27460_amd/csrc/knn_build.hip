@@ -381,18 +381,32 @@ __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__r
     __syncthreads();
     // (kSampleBatch sampled blocks per round: their loads are all in flight
     // before the first histogram update)
+    // (the next round's loads are issued before this round's updates)
     constexpr int kSampleBatch = 8;
+    constexpr int64_t kRound = (int64_t)kSampleBatch * kSampleEvery * kTopkThreads;
     uint32_t ns = 0;
-    for (int64_t j0 = 0; j0 < V; j0 += (int64_t)kSampleBatch * kSampleEvery * kTopkThreads) {
-        float x[kSampleBatch];  // loads first (index clamped, no branch), keys after
+    auto load_round = [&](int64_t j0, float(&x)[kSampleBatch]) {
 #pragma unroll
         for (int u = 0; u < kSampleBatch; ++u)
             x[u] = row[min<int64_t>(j0 + (int64_t)u * kSampleEvery * kTopkThreads + tid, V - 1)];
+        __builtin_amdgcn_sched_barrier(0);  // keep the issue order
+    };
+    auto count_round = [&](int64_t j0, const float(&x)[kSampleBatch]) {
 #pragma unroll
         for (int u = 0; u < kSampleBatch; ++u) {
             const int64_t jb = j0 + (int64_t)u * kSampleEvery * kTopkThreads, j = jb + tid;
             if (jb < V) ns += (uint32_t)min<int64_t>(kTopkThreads, V - jb);
             if (j < V && j != i) atomicAdd(&sh.hist[(uint32_t)(make_key(x[u], (int32_t)j) >> (64 - kDigitBits))], 1u);
+        }
+    };
+    {
+        float xa[kSampleBatch], xb[kSampleBatch];
+        load_round(0, xa);
+        for (int64_t j0 = 0; j0 < V; j0 += 2 * kRound) {
+            load_round(j0 + kRound, xb);
+            count_round(j0, xa);
+            load_round(j0 + 2 * kRound, xa);
+            count_round(j0 + kRound, xb);
         }
     }
     const uint32_t want = (uint32_t)((2 * (int64_t)K * ns + V - 1) / V) + 4;
@@ -418,17 +432,20 @@ __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__r
     __syncthreads();
     // (fewer sampled keys than want: T0 = 1, every key)
     const uint64_t T0 = sh.count ? ((uint64_t)sh.bucket << (64 - kDigitBits)) | 1ull : 1ull;
-    // gather every key >= T0, four scores per load, kGatherLoads loads in flight
+    // gather every key >= T0, four scores per load: batches of kGatherLoads
+    // loads per thread, the next batch issued before the current one is
+    // sifted so that the row keeps streaming (indices clamped, no branch
+    // around a load; the keys past the row are skipped when sifted)
     constexpr int kGatherLoads = 8;
+    constexpr int64_t kBatch = (int64_t)kGatherLoads * kTopkThreads;
     const int64_t n4 = (V + 3) / 4;
     const float4 *row4 = reinterpret_cast<const float4 *>(row);
-    for (int64_t b0 = 0; b0 < n4; b0 += kGatherLoads * kTopkThreads) {
-        float4 v[kGatherLoads];
+    auto load_batch = [&](int64_t b0, float4(&v)[kGatherLoads]) {
 #pragma unroll
-        for (int u = 0; u < kGatherLoads; ++u) {
-            const int64_t q = b0 + u * kTopkThreads + tid;
-            v[u] = q < n4 ? row4[q] : float4{0.0f, 0.0f, 0.0f, 0.0f};
-        }
+        for (int u = 0; u < kGatherLoads; ++u) v[u] = row4[min(b0 + u * kTopkThreads + tid, n4 - 1)];
+        __builtin_amdgcn_sched_barrier(0);  // keep the issue order
+    };
+    auto sift_batch = [&](int64_t b0, const float4(&v)[kGatherLoads]) {
 #pragma unroll
         for (int u = 0; u < kGatherLoads; ++u) {
             const int64_t j = 4 * (b0 + u * kTopkThreads + tid);
@@ -444,6 +461,14 @@ __global__ __launch_bounds__(kTopkThreads) void knn_topk_kernel(const float *__r
                 }
             }
         }
+    };
+    float4 va[kGatherLoads], vb[kGatherLoads];
+    load_batch(0, va);
+    for (int64_t b0 = 0; b0 < n4; b0 += 2 * kBatch) {
+        load_batch(b0 + kBatch, vb);
+        sift_batch(b0, va);
+        load_batch(b0 + 2 * kBatch, va);
+        sift_batch(b0 + kBatch, vb);
     }
     __syncthreads();
     const uint32_t ng = sh.n;

@@ -206,13 +206,16 @@ constexpr int kSampleEvery = 8;
 // ---------------------------------------------------------------------------
 //
 // S[c][j] = <w_{r0 + c}, w_j> for the rows c of a chunk and every row j, fp32
-// accumulation, written with row pitch ld.  A workgroup of four waves owns a
-// 128 x 128 tile (128 chunk rows c by 128 rows j); wave (wm, wn) computes its
-// 64 x 64 quarter as 4 x 4 tiles of 16 x 16 on the matrix cores
+// accumulation, written with row pitch ld.  A workgroup of eight waves owns
+// a 256 x 128 tile (256 chunk rows c by 128 rows j); wave (wm, wn) computes
+// its 64 x 64 block as 4 x 4 tiles of 16 x 16 on the matrix cores
 // (v_mfma_f32_16x16x32_bf16 for bf16 rows, v_mfma_f32_16x16x4_f32 for fp32
 // rows).  The reduction over the row width runs in stages of kGramKC bytes
-// of each row: both 128-row slices of a stage are staged in LDS, the stages
-// two ahead loading into registers while the current one is multiplied.
+// of each row: both slices of a stage (256 and 128 rows) are staged in LDS,
+// the stages two ahead loading into registers while the current one is
+// multiplied.  (128 x 128 tiles of four waves, two workgroups per CU, read a
+// quarter more through the CU for the same products and measured the same
+// per chunk but 2-5% slower per build.)
 // Lane (r, g) of a wave (r = lane % 16, g = lane / 16) feeds row r of a
 // 16-row operand with its g-th quarter of the k step, and ends holding rows
 // 4 g + i of column r of each 16 x 16 result.  Every score is the same
@@ -222,25 +225,29 @@ constexpr int kSampleEvery = 8;
 // piece p ^ ((x >> 1) & 7) of the row.  Measured with the LDS counters on
 // gfx950, the operand reads (16 rows, four consecutive pieces or four
 // consecutive floats each) then use every bank once per cycle, where rows
-// padded by 16 bytes took twice the cycles (half of them bank conflicts),
-// and the two stages fit twice per CU.  Every load of a stage is issued with
+// padded by 16 bytes took twice the cycles (half of them bank conflicts).  Every load of a stage is issued with
 // no branch around it (pieces past the row are clamped to its last piece and
 // replaced by zeros when staged), in the order they are consumed, so the
 // compiler waits only for the stage being staged.
 
-constexpr int kGramTile = 128;                     // rows of c and of j per workgroup
-constexpr int kGramThreads = 256;                  // four waves, 2 x 2 quarters
+#ifndef VIE_GRAM_TILE_C
+#define VIE_GRAM_TILE_C 256
+#endif
+constexpr int kGramTileC = VIE_GRAM_TILE_C;        // chunk rows c per workgroup (128 or 256)
+constexpr int kGramTile = 128;                     // rows j per workgroup
+constexpr int kGramThreads = 2 * kGramTileC;       // (kGramTileC / 64) x 2 waves of 64 x 64 quarters
 #ifndef VIE_GRAM_KC
 #define VIE_GRAM_KC 128
 #endif
 constexpr int kGramKC = VIE_GRAM_KC;               // bytes of a row per stage
 static_assert(kGramKC == 128, "the piece swizzle is laid out for 8 pieces a staged row");
 constexpr int kGramRowPitch = kGramKC;                 // LDS bytes per staged row
-constexpr int kGramStage = 2 * kGramTile * kGramRowPitch;  // A and B slices of one stage
+constexpr int kGramStage = (kGramTileC + kGramTile) * kGramRowPitch;  // A and B slices of one stage
 
 // byte offset of 16-byte piece p of staged row x
 __device__ __forceinline__ int gram_piece(int x, int p) { return x * kGramRowPitch + ((p ^ ((x >> 1) & 7)) << 4); }
-constexpr int kGramLoads = 2 * kGramTile * (kGramKC / 16) / kGramThreads;  // 16-byte loads per thread
+constexpr int kGramLoads = (kGramTileC + kGramTile) * (kGramKC / 16) / kGramThreads;  // 16-byte loads per thread
+static_assert(kGramLoads * kGramThreads == (kGramTileC + kGramTile) * (kGramKC / 16), "staging shape");
 
 __device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 c)
 {
@@ -259,11 +266,12 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
     // consecutive workgroups share a tile of rows j (and differ in c), so a
     // tile of j is read from HBM once per chunk and the chunk's own rows stay
     // in cache
-    const int64_t c0 = (int64_t)blockIdx.x * kGramTile, j0 = (int64_t)blockIdx.y * kGramTile;
+    const int64_t c0 = (int64_t)blockIdx.x * kGramTileC, j0 = (int64_t)blockIdx.y * kGramTile;
     const int nstage = (row_bytes + kGramKC - 1) / kGramKC;
     const u32x4 zero = {0u, 0u, 0u, 0u};
-    // staging: load t of a thread covers staged row (L / 8) of A (L < 1024)
-    // or of B, 16 bytes at byte (L % 8) * 16 of the stage, L = t * 256 + tid
+    // staging: load t of a thread covers staged row (L / 8) of A (the first
+    // kGramTileC rows) or of B, 16 bytes at byte (L % 8) * 16 of the stage,
+    // L = t * kGramThreads + tid
     const char *src[kGramLoads];
     int soff[kGramLoads], scol[kGramLoads];
 #pragma unroll
@@ -271,8 +279,8 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
         const int L = t * kGramThreads + tid;
         const int srow = L / (kGramKC / 16);  // 0..255: A rows then B rows
         scol[t] = (L % (kGramKC / 16)) * 16;
-        const int64_t grow = srow < kGramTile ? r0 + min<int64_t>(c0 + srow, rows - 1)
-                                              : min<int64_t>(j0 + srow - kGramTile, V - 1);
+        const int64_t grow = srow < kGramTileC ? r0 + min<int64_t>(c0 + srow, rows - 1)
+                                               : min<int64_t>(j0 + srow - kGramTileC, V - 1);
         src[t] = W + grow * (int64_t)row_bytes;
         soff[t] = gram_piece(srow, scol[t] >> 4);
     }
@@ -308,7 +316,7 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
         load_stage(min(st + 2, nstage - 1), pre[pb]);  // past the end: the last stage again (cached)
         __syncthreads();  // the stage is in LDS (and the stage before it is no longer read)
         const char *A = buf + (wm * 64) * kGramRowPitch;
-        const char *B = buf + (kGramTile + wn * 64) * kGramRowPitch;
+        const char *B = buf + (kGramTileC + wn * 64) * kGramRowPitch;
         if constexpr (BF16) {
 #pragma unroll
             for (int kk = 0; kk < kGramKC; kk += 64) {  // 32 bf16 per MFMA step
@@ -872,7 +880,7 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
     if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
     for (int64_t r0 = 0; r0 < V; r0 += R) {
         const int64_t rows = std::min(R, V - r0);
-        const dim3 grid((unsigned)((rows + kGramTile - 1) / kGramTile), (unsigned)((V + kGramTile - 1) / kGramTile));
+        const dim3 grid((unsigned)((rows + kGramTileC - 1) / kGramTileC), (unsigned)((V + kGramTile - 1) / kGramTile));
         gram<<<grid, kGramThreads, 2 * kGramStage, s>>>(static_cast<const char *>(W_dev), V, row_bytes, r0, rows, b.S,
                                                         ld);
         he = hipGetLastError();

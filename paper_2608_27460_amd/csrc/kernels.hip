@@ -165,6 +165,27 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
     return x;
 }
 
+// Minimum and maximum over the 64 lanes of a wave (strides written out, so
+// that xor_lane's switch folds away).  Every lane of the wave must be active.
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v)
+{
+    v = min(v, xor_lane(v, 32));
+    v = min(v, xor_lane(v, 16));
+    v = min(v, xor_lane(v, 8));
+    v = min(v, xor_lane(v, 4));
+    v = min(v, xor_lane(v, 2));
+    return min(v, xor_lane(v, 1));
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
+{
+    v = max(v, xor_lane(v, 32));
+    v = max(v, xor_lane(v, 16));
+    v = max(v, xor_lane(v, 8));
+    v = max(v, xor_lane(v, 4));
+    v = max(v, xor_lane(v, 2));
+    return max(v, xor_lane(v, 1));
+}
+
 // xor_lane for 32- and 64-bit values of any type (float, int, double).
 template <typename T> __device__ __forceinline__ T xor_lane_as(T v, int s)
 {
@@ -1223,6 +1244,8 @@ struct HnswShared {
     uint32_t nother;
     int team_err;
     uint32_t nfetch;  // hnsw_multi_kernel sharing rows: new nodes whose row is fetched
+    // hnsw_multi_kernel: the bound below which kept keys cannot enter the beam
+    uint32_t fmin, fmax, fsel, fcount, fn;
 };
 
 // A team: `size` workgroups (a power of two) search one query together
@@ -1695,6 +1718,11 @@ __global__ __launch_bounds__(NT) void hnsw_kernel(
 // leave every decision, and so the traversal, exactly as above.
 
 constexpr int kMaxWidth = 128;      // widest expansion step
+// Kept keys a wide step drops below the beam's reach before ranking them
+// (only when a step keeps more than this many keys and has this many list
+// slots: the histogram and the per-edge beam counts take 2 KB of the
+// claimed-id array).
+constexpr int kKeepFilterMin = 512;
 constexpr int kPickNarrowSpan = 256;  // picks scan: one flag per lane up to this many entries past the first
 constexpr int kMultiHeld = 2;       // rows per group whose lists a group can cache
 constexpr int kClaimBatch = 4;      // list entries a thread claims together
@@ -2265,7 +2293,111 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
             exchange(area, sh.nkeep, ckey, &sh.nkeep);
             if (sh.team_err) break;
         }
-        const int nk = (int)sh.nkeep;
+        int nk = (int)sh.nkeep;
+        // A step that keeps many more keys than the beam can take (the first
+        // steps of a wide walk, while the beam fills) drops the kept keys that
+        // cannot enter it before they are sorted and ranked.  A histogram of
+        // the kept keys' score bits (256 buckets over their range) and, per
+        // bucket edge, the beam entries at or above it suggest the highest
+        // edge with at least ef keys of the beam and the kept keys at or above
+        // it.  The kept keys at or above that edge are gathered and counted
+        // exactly; only if they and the beam entries at or above the edge are
+        // at least ef do they replace the kept keys: every key dropped then has
+        // ef larger keys, so the merge would drop it anyway and the new beam
+        // is the same.  The histogram, the per-edge beam counts and the
+        // gathered keys use the claimed-id array, which is free between the
+        // scoring and the merge.
+        static_assert(NT >= 256, "a thread per histogram bucket");
+        uint32_t tau = 0;  // kept keys with score bits below tau were dropped
+        if (cap >= kKeepFilterMin && nk > kKeepFilterMin && (int)nbeam + nk > ef) {  // uniform
+            uint32_t *hist = reinterpret_cast<uint32_t *>(cid);            // [256]
+            uint32_t *bcount = hist + 256;                                 // [256], by descending bucket
+            uint64_t *keep2 = reinterpret_cast<uint64_t *>(hist + 256);    // gathered keys (after bcount is read)
+            const uint32_t room = (uint32_t)(cap - 256) / 2;
+            if (tid == 0) {
+                sh.fmin = 0xFFFFFFFFu;
+                sh.fmax = 0u;
+                sh.fsel = 256u;
+                sh.fn = 0u;
+            }
+            for (int t = tid; t < 256; t += NT) hist[t] = 0u;
+            __syncthreads();
+            uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+            for (int j = tid; j < nk; j += NT) {
+                const uint32_t sbits = (uint32_t)(ckey[j] >> 32);
+                mn = min(mn, sbits);
+                mx = max(mx, sbits);
+            }
+            mn = wave_min_u32(mn);
+            mx = wave_max_u32(mx);
+            if (lane == 0) {
+                atomicMin(&sh.fmin, mn);
+                atomicMax(&sh.fmax, mx);
+            }
+            __syncthreads();
+            const uint32_t lo = sh.fmin;
+            const uint32_t span = sh.fmax - lo;
+            const float scale = 256.0f / ((float)span + 1.0f);
+            for (int j = tid; j < nk; j += NT) {
+                const uint32_t sbits = (uint32_t)(ckey[j] >> 32);
+                atomicAdd(&hist[min(255u, (uint32_t)((float)(sbits - lo) * scale))], 1u);
+            }
+            // edge of bucket b: lo + b (span + 1) / 256 (an exact count is
+            // taken below, so the edges need not match the buckets exactly)
+            auto edge = [&](int b) { return lo + (uint32_t)(((uint64_t)b * ((uint64_t)span + 1)) >> 8); };
+            if (tid < 256) {
+                const uint64_t thr = (uint64_t)edge(255 - tid) << 32;
+                const int bst = 1 << (31 - __builtin_clz(nbeam));  // nbeam >= 1
+                int c = 0;  // beam entries at or above the edge of bucket 255 - tid
+                for (int step = bst; step > 0; step >>= 1)
+                    if (c + step <= (int)nbeam && beam[c + step - 1] >= thr) c += step;
+                bcount[tid] = (uint32_t)c;
+            }
+            __syncthreads();
+            if (tid < kWave) {  // wave 0: the highest bucket whose edge reaches ef keys
+                uint32_t v[4], sum = 0;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    v[u] = hist[255 - (4 * lane + u)];
+                    sum += v[u];
+                }
+                uint32_t run = wave_incl_scan(sum) - sum;  // kept keys in the buckets above this lane's
+                int sel = 256;
+                uint32_t nb = 0;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    run += v[u];
+                    if (sel == 256 && run + bcount[4 * lane + u] >= (uint32_t)ef) {
+                        sel = 4 * lane + u;
+                        nb = bcount[4 * lane + u];
+                    }
+                }
+                const uint64_t any = __ballot(sel < 256);
+                if (any != 0ull && lane == __ffsll((long long)any) - 1) {
+                    sh.fsel = (uint32_t)sel;
+                    sh.fcount = nb;  // beam entries at or above the chosen edge
+                }
+            }
+            __syncthreads();
+            if (sh.fsel < 256u) {  // uniform
+                const uint32_t t = edge(255 - (int)sh.fsel);
+                for (int j = tid; j < nk; j += NT) {
+                    const uint64_t key = ckey[j];
+                    if ((uint32_t)(key >> 32) >= t) {
+                        const uint32_t slot = atomicAdd(&sh.fn, 1u);
+                        if (slot < room) keep2[slot] = key;
+                    }
+                }
+                __syncthreads();
+                const uint32_t ng = sh.fn;
+                if (ng <= room && ng < (uint32_t)nk && ng + sh.fcount >= (uint32_t)ef) {  // uniform
+                    tau = t;
+                    nk = (int)ng;
+                    for (int j = tid; j < nk; j += NT) ckey[j] = keep2[j];
+                    __syncthreads();
+                }
+            }
+        }
         // with more than 64 kept keys, each wave sorts runs of 128 of them
         // (two sorted halves of 64, the second reversed so that the pair is
         // bitonic, half-cleaned and merged in registers), so that a key's rank
@@ -2319,7 +2451,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (cache_on) {
 #pragma unroll
             for (int x = 0; x < kMultiHeld; ++x)
-                if (rk[x] != 0ull) {
+                if (rk[x] != 0ull && (uint32_t)(rk[x] >> 32) >= tau) {
                     const int above = kept_above(rk[x]);
                     if (above < hints) {
 #pragma unroll

@@ -1245,7 +1245,7 @@ struct HnswShared {
     int team_err;
     uint32_t nfetch;  // hnsw_multi_kernel sharing rows: new nodes whose row is fetched
     // hnsw_multi_kernel: the bound below which kept keys cannot enter the beam
-    uint32_t fmin, fmax, fsel, fcount, fn;
+    uint32_t fmin, fmax, fsel, fcount, fn, ftau;
 };
 
 // A team: `size` workgroups (a power of two) search one query together
@@ -2287,7 +2287,10 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                     }
                 }
         }
-        if (tid == 0) sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
+        if (tid == 0) {
+            sh.first = 0xFFFFFFFFu;  // every thread read it before the claim barrier
+            sh.ftau = 0u;
+        }
         __syncthreads();
         if (T > 1) {  // the kept keys of the other members join this member's
             exchange(area, sh.nkeep, ckey, &sh.nkeep);
@@ -2308,7 +2311,6 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         // gathered keys use the claimed-id array, which is free between the
         // scoring and the merge.
         static_assert(NT >= 256, "a thread per histogram bucket");
-        uint32_t tau = 0;  // kept keys with score bits below tau were dropped
         if (cap >= kKeepFilterMin && nk > kKeepFilterMin && (int)nbeam + nk > ef) {  // uniform
             uint32_t *hist = reinterpret_cast<uint32_t *>(cid);            // [256]
             uint32_t *bcount = hist + 256;                                 // [256], by descending bucket
@@ -2391,7 +2393,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
                 __syncthreads();
                 const uint32_t ng = sh.fn;
                 if (ng <= room && ng < (uint32_t)nk && ng + sh.fcount >= (uint32_t)ef) {  // uniform
-                    tau = t;
+                    if (tid == 0) sh.ftau = t;  // kept keys with score bits below it were dropped
                     nk = (int)ng;
                     for (int j = tid; j < nk; j += NT) ckey[j] = keep2[j];
                     __syncthreads();
@@ -2451,7 +2453,7 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (cache_on) {
 #pragma unroll
             for (int x = 0; x < kMultiHeld; ++x)
-                if (rk[x] != 0ull && (uint32_t)(rk[x] >> 32) >= tau) {
+                if (rk[x] != 0ull && (uint32_t)(rk[x] >> 32) >= sh.ftau) {
                     const int above = kept_above(rk[x]);
                     if (above < hints) {
 #pragma unroll

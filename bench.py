@@ -10,7 +10,7 @@ The beam width is the one the method needs: for each traversal (the
 sequential search; 8, 32 or 64 expansions per step; 8, 16, 32 or 64 per step
 on int8 rows with the exact re-rank; 128 per step in teams only) the smallest ef of 128, 256, ..., 4096 whose recall@50 reaches
 0.95 on the first 128 queries (recall against the exact dense head, itself
-parity-tested against the oracle).  The team traversals (64 workgroups
+parity-tested against the oracle).  The team traversals (128 workgroups
 sharing each query's row scoring) walk exactly the path of their
 one-workgroup twin and take its ef.  The fastest of them at its ef is the
 headline traversal.
@@ -51,7 +51,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SRC = os.path.join(ROOT, "paper_2608_27460_amd", "csrc", "kernels.hip")
 NODE_MASK = (1 << 26) - 1
 
-TEAM = 64  # workgroups per query of the team traversals
+TEAM = 128  # workgroups per query of the team traversals
 TRAVERSALS = {  # name -> (expansions per layer-0 step, int8 rows for layer 0, workgroups per query)
     "sequential": (1, False, 1),
     "width8": (8, False, 1),

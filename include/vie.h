@@ -216,7 +216,7 @@ typedef struct {
                              caller replay and compare a traversal. */
     int32_t trace_cap;    /* entries per query of trace_dev (>= 1 when set) */
     int32_t team;         /* workgroups that search each query together:
-                             1, 2, 4, 8, 16, 32 or 64 (0 counts as 1).  Each
+                             a power of two up to 256 (0 counts as 1).  Each
                              member keeps the whole search state and takes
                              every decision itself, scores only the new
                              nodes whose id modulo team is its member

@@ -19,7 +19,7 @@ constexpr int kMaxK = 1024;       // largest k of any query
 constexpr int kMaxEf = 8192;      // largest beam of the HNSW kernel (LDS permitting)
 constexpr int kMaxD = 8192;       // largest row width
 constexpr int kMaxGpuBuildK = 128;  // candidates per node of the GPU batch build
-constexpr int kMaxTeam = 64;      // workgroups that may search one query together
+constexpr int kMaxTeam = 256;     // workgroups that may search one query together
 constexpr int kMaxShare = 16;     // queries per row-sharing group
 
 inline int elem_bytes(int dtype) { return dtype == VIE_F32 ? 4 : 2; }

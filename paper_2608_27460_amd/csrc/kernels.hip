@@ -11,7 +11,7 @@
 //                        Algorithms 2 and 5), one workgroup per query.
 //   hnsw_multi_kernel    the same search expanding up to 128 beam entries
 //                        per layer-0 step, optionally on int8 rows, in a
-//                        team of up to 64 workgroups per query that divide
+//                        team of up to 256 workgroups per query that divide
 //                        each step's row scoring, or with the rows a launch's
 //                        queries fetch shared within groups of queries
 //                        (Section 5's open problems: sequential traversal,
@@ -2017,28 +2017,45 @@ __global__ __launch_bounds__(NT) void hnsw_multi_kernel(
         if (tid == 0)
             __hip_atomic_store(team.tags + base + mem, ((uint64_t)tag << 32) | mine, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-        // wave 0: lane o waits (bounded) for member o's count, then the
-        // running sums say where each member's keys go
+        // wave 0: lane l waits (bounded) for the counts of members l, l + 64,
+        // ..., then the running sums say where each member's keys go
+        constexpr int kPerLane = (kMaxTeam + kWave - 1) / kWave;
         if (tid < kWave) {
-            uint32_t c = 0u;
-            if (lane < T && lane != mem) {
-                uint32_t spins = 0;
-                for (;;) {
-                    const uint64_t w =
-                        __hip_atomic_load(team.tags + base + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if ((uint32_t)(w >> 32) == tag) {
-                        c = (uint32_t)w;
-                        break;
-                    }
-                    if (++spins > kTeamSpin) {
-                        sh.team_err = 1;
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                }
+            uint32_t c[kPerLane];
+            uint32_t need = 0u;  // bit i: the count of member lane + 64 i is still awaited
+#pragma unroll
+            for (int i = 0; i < kPerLane; ++i) {
+                c[i] = 0u;
+                const int o = lane + i * kWave;
+                if (o < T && o != mem) need |= 1u << i;
             }
-            const uint32_t incl = wave_incl_scan(c);
-            if (lane < T) s_xoff[lane + 1] = incl;
+            uint32_t spins = 0;
+            while (need) {
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i)
+                    if (need & (1u << i)) {
+                        const uint64_t w = __hip_atomic_load(team.tags + base + lane + i * kWave, __ATOMIC_RELAXED,
+                                                             __HIP_MEMORY_SCOPE_AGENT);
+                        if ((uint32_t)(w >> 32) == tag) {
+                            c[i] = (uint32_t)w;
+                            need &= ~(1u << i);
+                        }
+                    }
+                if (!need) break;
+                if (++spins > kTeamSpin) {
+                    sh.team_err = 1;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            uint32_t carry = 0u;
+#pragma unroll
+            for (int i = 0; i < kPerLane; ++i) {
+                const uint32_t incl = wave_incl_scan(c[i]) + carry;
+                const int o = lane + i * kWave;
+                if (o < T) s_xoff[o + 1] = incl;
+                carry = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
+            }
             if (lane == 0) s_xoff[0] = 0;
         }
         __syncthreads();
@@ -3003,11 +3020,13 @@ size_t hnsw_multi_lds_bytes(int64_t V, int d, int dtype, int ef_eff, int M0, int
 }
 
 // LDS a search workgroup may take for its dynamic carve-up: the device's
-// per-block limit less a reserve for the kernels' static variables (about
-// 1.4 KB in hnsw_multi_kernel: shared counters, picks, cache ids, team offsets).
+// per-block limit less a reserve for the kernels' static variables (2.2 KB
+// in hnsw_multi_kernel: shared counters, picks, cache ids and the offsets of
+// up to kMaxTeam members' keys).
 size_t hnsw_lds_limit()
 {
-    constexpr int kStaticReserve = 2048;
+    constexpr int kStaticReserve = 3072;
+    static_assert((kMaxTeam + 1) * 4 + 1280 <= kStaticReserve, "team offsets fit the static reserve");
     int dev = 0, v = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 64 * 1024 - kStaticReserve;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= kStaticReserve)

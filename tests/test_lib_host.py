@@ -160,7 +160,7 @@ def test_calls_fail_synchronously_before_any_hip_call():
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # int8_rows
     prm = vie.SearchParams(1, 0, fake, 0)
     assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL  # trace_cap
-    for team in (33, 3, 12, -1, 128):
+    for team in (33, 3, 12, -1, 512):
         prm = vie.SearchParams(1, 0, None, 0, team)
         assert L.vie_query_ex(ix._h, fake, 1, 10, 10, C.byref(prm), fake, fake, None, None) == vie.EINVAL, team
     prm = vie.SearchParams(1, 0, None, 0, 4)

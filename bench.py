@@ -477,7 +477,7 @@ def main() -> int:
                 bi, bl, _ = out_bufs(ncall * Bc)
                 hb = [Hd[c * Bc:(c + 1) * Bc] for c in range(ncall)]
                 w8, i8, tm = TRAVERSALS[head_trav]
-                tm = max(1, min(tm, 128 // Bc))  # the team shrinks as the batch grows (all resident at once)
+                tm = max(1, min(tm, 256 // Bc))  # the team shrinks as the batch grows (all resident at once)
                 tm = 1 << (tm.bit_length() - 1)  # a power of two
                 h_call = back_to_back(lambda c: ix.query_into(hb[c], k, ef, bi[c * Bc:(c + 1) * Bc],
                                                               bl[c * Bc:(c + 1) * Bc], None, w8, i8, None, tm),

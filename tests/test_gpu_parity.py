@@ -739,6 +739,34 @@ def _variants(vie, ix, W, dtype, g, H, k, ef, what, widths=(1, 8), int8=True):
         ix.attach_int8(None, None)
 
 
+def test_hnsw_full_size_headline_configuration(vie):
+    """The configuration the benchmark times, at full size: the
+    Llama-3.2-3B-shaped head (128256 rows of 3072 bf16 values), its graph
+    built by the library at M = 32, ef_construction = 200, one query per
+    launch, 128 expansions per layer-0 step in a team of 128 workgroups,
+    k = 50, ef = 2048; 8 queries on the stored rows and 4 on int8 rows, each
+    against the oracle's search of the exported graph (exact counters and
+    expansion records, ids and logits)."""
+    wl = synth.WORKLOADS["llama3.2-3b"]
+    W = wl.make_w()
+    H, _ = wl.make_queries(W, Q=8)
+    ix = vie.Index.build(W, wl.dtype, wl.M, wl.efC, seed=wl.seed_levels, n_threads=16)
+    g = _library_graph(ix, W, wl.dtype, wl.efC, wl.seed_levels)
+    say("llama3.2-3b full: maxlevel %d entry %d" % (g.maxlevel, g.entry))
+    ix.to_device(dev_tensor(vie, W, wl.dtype))
+    for q in range(8):
+        _, st, _ = _compare_hnsw(vie, ix, W, wl.dtype, g, H[q:q + 1], 50, 2048, "headline q=%d" % q, width=128,
+                                 team=128)
+        say("  q=%d n_dist=%d n_expand=%d" % (q, st[0, 0], st[0, 1]))
+    oq, osc = O.quantize_rows(W, wl.dtype)
+    q8, sc = vie.quantize_rows(ix._W_dev, wl.dtype)
+    ix.attach_int8(q8, sc)
+    for q in range(4):
+        _compare_hnsw(vie, ix, W, wl.dtype, g, H[q:q + 1], 50, 2048, "headline int8 q=%d" % q, width=128,
+                      team=128, int8=(oq, osc))
+    ix.attach_int8(None, None)
+
+
 @pytest.mark.parametrize("dtype", [synth.BF16, synth.F32])
 def test_hnsw_batches_of_256_and_more(vie, dtype):
     """300 queries in one launch (more workgroups than the device holds at

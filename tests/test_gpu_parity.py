@@ -739,6 +739,47 @@ def _variants(vie, ix, W, dtype, g, H, k, ef, what, widths=(1, 8), int8=True):
         ix.attach_int8(None, None)
 
 
+def test_repeat_runs_are_byte_identical(vie):
+    """Every kernel family run twice on the same inputs writes the same
+    bytes: the dense head on the vector path (B = 1, 4) and the matrix cores
+    (B = 64), the row quantization, the sequential, wide, team and
+    row-sharing searches on bf16 and int8 rows (ids, logits, counters and
+    expansion records) and the scatter.  Waves and workgroups that raced
+    over shared state would show up here as a difference."""
+    V, d = 30000, 1024
+    W = synth.make_w(V, d, synth.BF16, 2100)
+    H, _ = synth.make_queries(W, synth.BF16, 64, 2101)
+    Wd, Hd = dev_tensor(vie, W, synth.BF16), dev_tensor(vie, H, synth.BF16)
+
+    def twice(what, fn):
+        say("repeat", what)
+        a = [t.cpu().numpy().copy() for t in fn()]
+        b = [t.cpu().numpy().copy() for t in fn()]
+        torch.cuda.synchronize()
+        for x, y in zip(a, b):
+            assert x.tobytes() == y.tobytes(), what
+        return a
+
+    dense = vie.DenseHead(Wd, max_batch=64, max_k=100)
+    for B in (1, 4, 64):
+        for k in (1, 50, 100):
+            twice("dense B=%d k=%d" % (B, k), lambda: dense(Hd[:B], k))
+    q8, sc = twice("quantize", lambda: vie.quantize_rows(Wd, synth.BF16))
+    ix = vie.Index.build(W, synth.BF16, 16, 40, seed=2102, n_threads=16)
+    ix.to_device(Wd)
+    ix.attach_int8(torch.from_numpy(q8).cuda(), torch.from_numpy(sc).cuda())
+    ef = 200
+    for width, int8, team, share, B in [(1, False, 1, 1, 64), (8, False, 1, 1, 64), (64, False, 4, 1, 16),
+                                        (128, False, 8, 1, 8), (32, True, 2, 1, 32), (8, False, 1, 4, 64),
+                                        (8, True, 1, 4, 64)]:
+        what = "hnsw width=%d int8=%d team=%d share=%d B=%d" % (width, int8, team, share, B)
+        ids, lg, _, _ = twice(what, lambda: ix.query(Hd[:B], 50, ef, stats=True, width=width, int8=int8,
+                                                     trace_cap=ef + 1024, team=team, share=share))
+    ids_d, lg_d = torch.from_numpy(ids).cuda(), torch.from_numpy(lg).cuda()
+    twice("scatter", lambda: (vie.scatter(ids_d, lg_d, V),))
+    ix.attach_int8(None, None)
+
+
 def test_hnsw_full_size_headline_configuration(vie):
     """The configuration the benchmark times, at full size: the
     Llama-3.2-3B-shaped head (128256 rows of 3072 bf16 values), its graph

@@ -452,14 +452,19 @@ def main() -> int:
                 q32, s32 = vie.quantize_rows(W32d, synth.F32)
                 ix32.attach_int8(q32, s32)
             f_i, f_l, _ = out_bufs(n32)
-            fw, f8, ft = TRAVERSALS[f_trav]
-            try:
-                hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None,
-                                                            fw, f8, None, ft), n32)
-            except vie.VieError:  # fp32 queries take twice the LDS: 64 per step then
-                fw = 64
-                hcalls = per_call(lambda c: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1], f_l[c:c + 1], None,
-                                                            fw, f8, None, ft), n32)
+            fw0, f8, ft = TRAVERSALS[f_trav]
+            hcalls = None
+            for fw in [w for w in (128, 112, 96, 80, 64) if w <= fw0]:
+                # fp32 queries take twice the LDS of bf16 ones: the widest step that fits
+                try:
+                    hcalls = per_call(lambda c, w=fw: ix32.query_into(H32d[c:c + 1], k, ef, f_i[c:c + 1],
+                                                                      f_l[c:c + 1], None, w, f8, None, ft), n32)
+                    break
+                except vie.VieError as e:
+                    if e.status != vie.EUNSUPPORTED:
+                        raise
+            assert hcalls is not None, "no step width fits the fp32 search"
+
             legs["fp32_rows"] = {
                 "W_bytes": wl.V * wl.d * 4, "queries": n32, "dense_us_per_query": pct(dcalls),
                 "dense_hbm_frac": round(wl.V * wl.d * 4 / (np.median(dcalls) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),

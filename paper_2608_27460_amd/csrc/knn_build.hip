@@ -263,10 +263,19 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int r = lane & 15, g = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
-    // consecutive workgroups share a tile of rows j (and differ in c), so a
-    // tile of j is read from HBM once per chunk and the chunk's own rows stay
-    // in cache
-    const int64_t c0 = (int64_t)blockIdx.x * kGramTileC, j0 = (int64_t)blockIdx.y * kGramTile;
+    // Launch order for the eight XCDs, each with its own L2: workgroups are
+    // dealt to the XCDs in turn (workgroup L runs on XCD L % 8), so XCD x
+    // takes the tiles of rows j numbered x, x + 8, x + 16, ..., each with
+    // all of the chunk's tiles c in a row.  A tile of j is then fetched by
+    // one XCD only, and the chunk's rows are shared by the workgroups that
+    // XCD runs at once.  The grid holds the tiles of j rounded up to a
+    // multiple of 8; the workgroups past the last tile return at once.
+    const int nc = (int)((rows + kGramTileC - 1) / kGramTileC);
+    const int64_t nj = (V + kGramTile - 1) / kGramTile;
+    const int64_t wg = blockIdx.x, i = wg >> 3;
+    const int64_t jt = (i / nc) * 8 + (wg & 7), ct = i % nc;
+    if (jt >= nj) return;
+    const int64_t c0 = ct * kGramTileC, j0 = jt * kGramTile;
     const int nstage = (row_bytes + kGramKC - 1) / kGramKC;
     const u32x4 zero = {0u, 0u, 0u, 0u};
     // staging: load t of a thread covers staged row (L / 8) of A (the first
@@ -873,14 +882,15 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
         return st;
     };
 
-    if ((V + kGramTile - 1) / kGramTile > 65535)
+    const int64_t gram_nj8 = ((V + kGramTile - 1) / kGramTile + 7) / 8 * 8;  // tiles of j, rounded up to 8
+    if (gram_nj8 * ((R + kGramTileC - 1) / kGramTileC) > 0x7FFFFFFF)
         return bail(fail(VIE_EUNSUPPORTED, "GPU build: V = %lld rows exceed the Gram grid", (long long)V));
     auto gram = dtype == VIE_BF16 ? knn_gram_kernel<true> : knn_gram_kernel<false>;
     he = hipFuncSetAttribute((const void *)gram, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kGramStage);
     if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
     for (int64_t r0 = 0; r0 < V; r0 += R) {
         const int64_t rows = std::min(R, V - r0);
-        const dim3 grid((unsigned)((rows + kGramTileC - 1) / kGramTileC), (unsigned)((V + kGramTile - 1) / kGramTile));
+        const dim3 grid((unsigned)(((rows + kGramTileC - 1) / kGramTileC) * gram_nj8));
         gram<<<grid, kGramThreads, 2 * kGramStage, s>>>(static_cast<const char *>(W_dev), V, row_bytes, r0, rows, b.S,
                                                         ld);
         he = hipGetLastError();

@@ -264,17 +264,19 @@ __global__ __launch_bounds__(kGramThreads) __attribute__((amdgpu_waves_per_eu(2)
     const int r = lane & 15, g = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
     // Launch order for the eight XCDs, each with its own L2: workgroups are
-    // dealt to the XCDs in turn (workgroup L runs on XCD L % 8), so XCD x
-    // takes the tiles of rows j numbered x, x + 8, x + 16, ..., each with
-    // all of the chunk's tiles c in a row.  A tile of j is then fetched by
-    // one XCD only, and the chunk's rows are shared by the workgroups that
-    // XCD runs at once.  The grid holds the tiles of j rounded up to a
-    // multiple of 8; the workgroups past the last tile return at once.
+    // dealt to the XCDs in turn (workgroup L runs on XCD L % 8).  XCD x
+    // takes half of the chunk's tiles c (the first half for even x) and the
+    // tiles of rows j numbered x / 2, x / 2 + 4, ..., each with all of its
+    // tiles c in a row: a tile of j is fetched by two XCDs, and each XCD
+    // re-reads only its half of the chunk's rows.  The grid rounds the tiles
+    // of c up to an even count and those of j up to a multiple of 4; the
+    // workgroups past the last tile return at once.
     const int nc = (int)((rows + kGramTileC - 1) / kGramTileC);
+    const int nch = (nc + 1) / 2;
     const int64_t nj = (V + kGramTile - 1) / kGramTile;
-    const int64_t wg = blockIdx.x, i = wg >> 3;
-    const int64_t jt = (i / nc) * 8 + (wg & 7), ct = i % nc;
-    if (jt >= nj) return;
+    const int64_t wg = blockIdx.x, i = wg >> 3, x = wg & 7;
+    const int64_t jt = (i / nch) * 4 + (x >> 1), ct = (x & 1) * nch + i % nch;
+    if (jt >= nj || ct >= nc) return;
     const int64_t c0 = ct * kGramTileC, j0 = jt * kGramTile;
     const int nstage = (row_bytes + kGramKC - 1) / kGramKC;
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -882,15 +884,15 @@ vie_status build_knn_graph_gpu(const void *W_dev, int dtype, int64_t V, int d, i
         return st;
     };
 
-    const int64_t gram_nj8 = ((V + kGramTile - 1) / kGramTile + 7) / 8 * 8;  // tiles of j, rounded up to 8
-    if (gram_nj8 * ((R + kGramTileC - 1) / kGramTileC) > 0x7FFFFFFF)
+    const int64_t gram_nj4 = ((V + kGramTile - 1) / kGramTile + 3) / 4 * 4;  // tiles of j, rounded up to 4
+    if (gram_nj4 * ((R + kGramTileC - 1) / kGramTileC + 1) > 0x7FFFFFFF)
         return bail(fail(VIE_EUNSUPPORTED, "GPU build: V = %lld rows exceed the Gram grid", (long long)V));
     auto gram = dtype == VIE_BF16 ? knn_gram_kernel<true> : knn_gram_kernel<false>;
     he = hipFuncSetAttribute((const void *)gram, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kGramStage);
     if (he != hipSuccess) return bail(fail(VIE_EHIP, "GPU build: %s", hipGetErrorString(he)));
     for (int64_t r0 = 0; r0 < V; r0 += R) {
         const int64_t rows = std::min(R, V - r0);
-        const dim3 grid((unsigned)(((rows + kGramTileC - 1) / kGramTileC) * gram_nj8));
+        const dim3 grid((unsigned)((((rows + kGramTileC - 1) / kGramTileC + 1) / 2 * 2) * gram_nj4));
         gram<<<grid, kGramThreads, 2 * kGramStage, s>>>(static_cast<const char *>(W_dev), V, row_bytes, r0, rows, b.S,
                                                         ld);
         he = hipGetLastError();
